@@ -1,0 +1,244 @@
+#!/usr/bin/env python3
+"""Attention forward+backward throughput on one MI355X.
+
+One step = the whole hot path on one batch of synthetic token-major input:
+fbl_attn_fwd (O, LSE) then the three backward launches (row statistic and
+dQ-accumulator reset, main pass, dQ conversion), all through the C ABI on
+torch's current stream.  Inputs, outputs and the workspace are resident in
+HBM before the timed region; nothing is allocated inside it.
+
+Prints one JSON line.  `value` is algorithmic TFLOP/s of fwd+bwd: 14*d FLOPs
+per (query, key) pair the mask allows, per query head (4*d forward: QK^T and
+PV; 10*d backward: the QK^T recompute, dO V^T, P^T dO, dS^T Q and dS K).
+
+  python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+"""
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2516.6   # dense MFMA, 256 CU x 4096 flop/clk x 2.4 GHz
+PEAK_F32_TFLOPS = 157.3
+PEAK_HBM_GBS = 8000.0
+
+
+def allowed_pairs(w, kv_len) -> int:
+    """Number of (query, key) pairs the mask allows, summed over batch and query heads."""
+    S = w.S
+    total = 0
+    for b in range(w.B):
+        L = S if kv_len is None else int(min(max(int(kv_len[b]), 0), S))
+        if w.mask & 1:
+            # query i sees keys j <= i, j < L
+            total += sum(min(i + 1, L) for i in range(S)) if L < S else S * (S + 1) // 2
+        else:
+            total += S * L
+    return total * w.Hq
+
+
+def algorithmic_bytes(w, es: int) -> dict:
+    """Minimum HBM traffic: fwd reads Q,K,V and writes O,LSE; bwd reads
+    Q,K,V,O,dO,LSE and writes dQ,dK,dV (workspace excluded)."""
+    nq = w.B * w.S * w.Hq * w.d * es
+    nk = w.B * w.S * w.Hkv * w.d * es
+    lse = w.B * w.Hq * w.S * 4
+    return {"fwd": nq + 2 * nk + nq + lse, "bwd_main": nq + 2 * nk + nq + lse + 2 * nk,
+            "total": (nq + 2 * nk + nq + lse) + (nq + 2 * nk + 2 * nq + lse + nq + 2 * nk)}
+
+
+def cpu_baseline(w, inp, budget_s: float):
+    """The fp64 oracle on a bounded sample of the same workload: whole heads of
+    batch 0 (full sequence), one at a time, until `budget_s` seconds pass."""
+    import numpy as np
+
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
+    except Exception:  # pragma: no cover
+        threads = os.cpu_count()
+    d, G = w.d, w.Hq // w.Hkv
+    scale = 1.0 / math.sqrt(d)
+    kv = inp["kv_len"]
+    done_pairs = 0
+    heads = 0
+    t0 = time.perf_counter()
+    for g in range(w.Hkv):
+        qh = list(range(g * G, (g + 1) * G))
+        qcols = np.concatenate([np.arange(h * d, (h + 1) * d) for h in qh])
+        kcols = np.arange(g * d, (g + 1) * d)
+        q = inp["q"][:1, :, qcols]
+        do = inp["do"][:1, :, qcols]
+        k = inp["k"][:1, :, kcols]
+        v = inp["v"][:1, :, kcols]
+        kl = None if kv is None else kv[:1]
+        oracle.attn_fwd(q, k, v, G, 1, scale, bool(w.mask & 1), kl)
+        oracle.attn_bwd(q, k, v, do, G, 1, scale, bool(w.mask & 1), kl)
+        heads += G
+        sub = type(w)(w.name, B=1, S=w.S, Hq=G, Hkv=1, d=d, dtype=w.dtype, mask=w.mask)
+        done_pairs += allowed_pairs(sub, kl)
+        if time.perf_counter() - t0 >= budget_s:
+            break
+    dt = time.perf_counter() - t0
+    flops = 14 * d * done_pairs
+    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"batch 0, query heads 0..{heads - 1} of {w.Hq} (full S={w.S}), fp64 numpy fwd+bwd, "
+                      f"{dt:.1f} s, {flops / 1e9:.1f} GFLOP algorithmic",
+            "seconds": dt, "host_cpus": os.cpu_count()}
+
+
+def dispatched_kernels(step):
+    """Kernel names dispatched by one step (torch profiler; None if unavailable)."""
+    try:
+        import torch
+        from torch.profiler import ProfilerActivity, profile
+        with profile(activities=[ProfilerActivity.CUDA]) as prof:
+            step()
+            torch.cuda.synchronize()
+        names = sorted({e.key for e in prof.key_averages() if e.device_time_total > 0})
+        return names or None
+    except Exception:
+        return None
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="llama7b_causal")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle work for cpu_baseline")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py measures one GPU only: the attention path has no multi-GPU mode in this build "
+              f"(asked for --gpus {args.gpus}, WORLD_SIZE {world}).", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2607_21624_amd as fbl
+    import synth
+
+    w = synth.WORKLOADS[args.workload]
+    inp = synth.make_inputs(w)
+    dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+    dev = lambda x: torch.from_numpy(x).to("cuda").to(dt)
+    q, k, v, do = dev(inp["q"]), dev(inp["k"]), dev(inp["v"]), dev(inp["do"])
+    kv_len = None if inp["kv_len"] is None else torch.from_numpy(inp["kv_len"]).to("cuda")
+    causal = bool(w.mask & synth.MASK_CAUSAL)
+    scale = 1.0 / math.sqrt(w.d)
+    o = torch.empty_like(q)
+    lse = torch.empty((w.B, w.Hq, w.S), dtype=torch.float32, device="cuda")
+    dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+    ws = torch.empty(fbl.fbl_attn_bwd_workspace(fbl.layout_of(q, w.Hq), fbl.layout_of(k, w.Hkv)),
+                     dtype=torch.uint8, device="cuda")
+    stream = torch.cuda.current_stream()
+
+    def bwd(phases):
+        fbl.attn_bwd(q, k, v, o, do, lse, w.Hq, w.Hkv, scale, causal, kv_len, dq=dq, dk=dk, dv=dv, workspace=ws,
+                     phases=phases)
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record(stream)
+        fbl.attn_fwd(q, k, v, w.Hq, w.Hkv, scale, causal, kv_len, out=o, lse=lse)
+        if ev is not None:
+            ev[1].record(stream)
+        bwd(fbl.FBL_BWD_PREP)
+        if ev is not None:
+            ev[2].record(stream)
+        bwd(fbl.FBL_BWD_MAIN)
+        if ev is not None:
+            ev[3].record(stream)
+        bwd(fbl.FBL_BWD_DQ)
+        if ev is not None:
+            ev[4].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    mem_before = torch.cuda.memory_allocated()
+
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record(stream)
+    for i in range(args.steps):
+        step(evs[i])
+    stop.record(stream)
+    torch.cuda.synchronize()
+    total_ms = start.elapsed_time(stop)
+    ms_per_step = total_ms / args.steps
+    k_fwd = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
+    k_pre = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
+    k_main = float(np.mean([e[2].elapsed_time(e[3]) for e in evs]))
+    k_dq = float(np.mean([e[3].elapsed_time(e[4]) for e in evs]))
+    assert torch.cuda.memory_allocated() == mem_before, "the timed steps allocated device memory"
+
+    pairs = allowed_pairs(w, inp["kv_len"])
+    flops = 14 * w.d * pairs
+    tflops = flops / (ms_per_step * 1e-3) / 1e12
+    peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
+    fwd_tf = 4 * w.d * pairs / (k_fwd * 1e-3) / 1e12
+    main_tf = 10 * w.d * pairs / (k_main * 1e-3) / 1e12
+    if k_main >= k_fwd:
+        dom = {"kernel": "attn_bwd_main", "achieved": main_tf, "flops_per_launch": 10 * w.d * pairs,
+               "avg_ms": k_main}
+    else:
+        dom = {"kernel": "attn_fwd_kernel", "achieved": fwd_tf, "flops_per_launch": 4 * w.d * pairs, "avg_ms": k_fwd}
+    roofline = {"bound": "mfma", "achieved": round(dom["achieved"], 2), "peak": peak, "unit": "TFLOP/s",
+                "frac": round(dom["achieved"] / peak, 4), "traffic": None, "kernel": dom["kernel"],
+                "avg_launch_ms": round(dom["avg_ms"], 4), "flops_per_launch": dom["flops_per_launch"]}
+
+    kernels = dispatched_kernels(step)
+    foreign = None
+    if kernels is not None:
+        foreign = [n for n in kernels if not any(t in n for t in ("attn_fwd", "attn_bwd"))]
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(w, inp, args.cpu_budget)
+
+    es = 2 if w.dtype == "bf16" else 4
+    line = {
+        "metric": "attn fwd+bwd TFLOP/s & % bf16 MFMA peak at 1 GPU; layout-copy bytes (=0)",
+        "value": round(tflops, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic (seeded N(0,1) token-major Q,K,V,dO)",
+        "config": {"workload": w.name, "B": w.B, "S": w.S, "Hq": w.Hq, "Hkv": w.Hkv, "d": w.d,
+                   "mask": {0: "none", 1: "causal", 2: "key_padding", 3: "causal+key_padding"}[w.mask],
+                   "layout": "token-major [B,S,H*d]", "parallelism": "single GPU"},
+        "pct_peak": round(100 * tflops / peak, 2),
+        "layout_copy_bytes": 0 if foreign == [] else None,
+        "dispatched_kernels": kernels,
+        "kernel_ms": {"attn_fwd": round(k_fwd, 4), "attn_bwd_pre": round(k_pre, 4), "attn_bwd_main": round(k_main, 4),
+                      "attn_bwd_dq": round(k_dq, 4)},
+        "kernel_tflops": {"attn_fwd": round(fwd_tf, 2), "attn_bwd_main": round(main_tf, 2)},
+        "algorithmic_gflop": round(flops / 1e9, 3),
+        "algorithmic_bytes": algorithmic_bytes(w, es)["total"],
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

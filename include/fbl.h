@@ -1,0 +1,201 @@
+/*
+ * fbl.h -- C ABI of the layout-copy-free attention forward/backward library
+ * for AMD Instinct MI355X (gfx950).
+ *
+ * What it computes.  Multi-head attention forward and backward of a
+ * fine-tuning step, directly on token-major activations [B, S, H*d] as a QKV
+ * projection writes them.  The paper's attention module (section 2.2, the
+ * LoRA fine-tuning example) forms P = softmax(Q K^T) and multiplies by V; the
+ * head split (reshape (B,S,D) -> (B,S,H,HD)) and the transpose to
+ * (B,H,S,HD) (section 4.3.1, the multi-head attention chain) are not carried
+ * out as copies: they are folded into one affine index map per tensor
+ * (section 4.3.2, the composed tile-index function f3 o f2 o f1), which the
+ * kernels apply when they stage (tile_s x d) row tiles -- the R-Tile of
+ * section 4.2 -- into LDS.  No layout-conversion kernel is ever launched.
+ *
+ * Conventions shared by every entry point.
+ *  - Element (b, h, s, i) of a tensor described by an fbl_layout L is at
+ *    element offset  b*L.sb + s*L.ss + h*L.sh + i*L.sd  from its base pointer.
+ *  - Q, O, dO, dQ have Hq heads; K, V, dK, dV have Hkv heads; query head h
+ *    reads key/value head h / (Hq/Hkv) (grouped-query attention with
+ *    contiguous groups).  Self-attention: all tensors share B and S.
+ *  - Scores are  scale * q_i . k_j ; key j is allowed for query i iff
+ *    (!causal || j <= i) && (!key_padding || j < kv_len[b]).  Disallowed
+ *    scores are -inf.  A query row with no allowed key gets O = 0,
+ *    LSE = -inf and contributes no gradient.
+ *  - LSE is float32 [B, Hq, S], contiguous, natural-log log-sum-exp of the
+ *    scaled masked scores.
+ *  - Storage type of Q, K, V, O, dO, dQ, dK, dV is one fbl_dtype for the whole
+ *    call (fp32 or bf16); accumulation is fp32.
+ *  - Ownership: the caller owns every buffer (device memory for tensors,
+ *    host memory for descriptors).  The library never allocates, frees or
+ *    synchronises.  Inputs are read-only; outputs are fully overwritten
+ *    (no accumulate semantics) and must not alias inputs.
+ *  - Errors: every check runs on the host before the first launch, so an
+ *    error return means nothing was enqueued.  Return codes are the only
+ *    error channel; nothing aborts or throws across the ABI.
+ *  - Streams: `stream` is a hipStream_t (NULL = the null stream).  On FBL_OK
+ *    the work is enqueued on it and the call returns without waiting.
+ */
+#ifndef FBL_H
+#define FBL_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    FBL_OK = 0,
+    FBL_ERR_NULL = 1,        /* a required pointer is NULL                          */
+    FBL_ERR_SHAPE = 2,       /* non-positive or mutually inconsistent extents       */
+    FBL_ERR_DTYPE = 3,       /* unknown dtype, or dtypes differ between tensors     */
+    FBL_ERR_LAYOUT = 4,      /* a tile-legality check failed (strides, tile shape)  */
+    FBL_ERR_ALIGN = 5,       /* base pointer or row stride not 16-byte aligned      */
+    FBL_ERR_UNSUPPORTED = 6, /* head dim / mask combination not implemented         */
+    FBL_ERR_WORKSPACE = 7,   /* workspace NULL or smaller than fbl_attn_bwd_workspace */
+    FBL_ERR_HIP = 8,         /* the HIP runtime reported an error at launch         */
+    FBL_ERR_ARG = 9          /* other invalid argument (non-finite scale, aliasing) */
+} fbl_status;
+
+typedef enum { FBL_F32 = 0, FBL_BF16 = 1 } fbl_dtype;
+
+/*
+ * Layout descriptor of one tensor with logical dims (B, H, S, D) -- the
+ * "logical dimensions S(t) and physical layout L(t)" of the paper's problem
+ * statement (section 3.1) -- plus the R-Tile the kernels stage it in.
+ *
+ * Strides are in elements.  Token-major defaults: sd = 1, sh = D,
+ * ss = H*D (row stride), sb = S*ss.  A row stride larger than H*D describes a
+ * view into a wider packed projection output without copying it.
+ * tile_s x tile_d is the R-Tile: tile_s token rows by tile_d head-dim
+ * columns.  tile_d divides D (tile boundary preservation, section 4.3.1) and
+ * sd == 1 (intra-tile continuity, section 4.3.1).
+ */
+typedef struct {
+    int32_t dtype;    /* fbl_dtype                                   */
+    int32_t tile_s;   /* R-Tile rows (tokens); set by fbl_layout_desc */
+    int32_t tile_d;   /* R-Tile columns (head-dim elements)          */
+    int32_t reserved; /* zero                                        */
+    int64_t B, S, H, D;
+    int64_t sb, ss, sh, sd;
+} fbl_layout;
+
+#define FBL_MASK_CAUSAL 1u      /* key j allowed only for queries i >= j        */
+#define FBL_MASK_KEY_PADDING 2u /* key j allowed only if j < kv_len[b]           */
+
+typedef struct {
+    uint32_t kind;          /* OR of FBL_MASK_* bits                             */
+    uint32_t reserved;      /* zero                                              */
+    const int32_t* kv_len;  /* device pointer, int32 [B]; required with KEY_PADDING;
+                               values are clamped to [0, S]                     */
+} fbl_mask;
+
+/*
+ * Fill *out with the token-major descriptor of a tensor with B batches, S
+ * tokens, H heads of D elements, and run the tile-legality checks of the
+ * paper's tile propagation (section 4.3.1): the R-Tile column count tile_d
+ * must divide the head dim (tile boundary preservation), the innermost
+ * stride is 1 (intra-tile continuity), and rows and heads must not overlap.
+ *
+ *   dtype        FBL_F32 or FBL_BF16.
+ *   row_stride   elements between consecutive tokens; 0 means H*D.
+ *                Must be >= H*D.
+ *   batch_stride elements between consecutive batches; 0 means S*row_stride.
+ *                Must be >= S*row_stride when B > 1.
+ *   tile_d       R-Tile width in head-dim elements; 0 means D.  Must divide D
+ *                and span a multiple of 16 bytes.
+ * tile_s is set from the library's tile table for (D, dtype).
+ * Returns FBL_ERR_NULL, FBL_ERR_SHAPE, FBL_ERR_DTYPE or FBL_ERR_LAYOUT on
+ * failure (then *out is left zeroed).  Pure host function.
+ */
+fbl_status fbl_layout_desc(fbl_layout* out, int32_t dtype, int64_t B, int64_t S, int64_t H, int64_t D,
+                           int64_t row_stride, int64_t batch_stride, int64_t tile_d);
+
+/*
+ * Host evaluation of the index map: element offset of logical (b, h, s, i),
+ * or -1 when the descriptor is NULL or an index is out of range.
+ */
+int64_t fbl_layout_offset(const fbl_layout* l, int64_t b, int64_t h, int64_t s, int64_t i);
+
+/*
+ * Diagnostic: evaluate the index map on the GPU with the same device code the
+ * attention kernels use to address tensors, writing out[((b*H + h)*S + s)*D + i]
+ * = offset(b, h, s, i) as int64 into the device buffer `out` of
+ * B*H*S*D elements.  Enqueued on `stream`.
+ */
+fbl_status fbl_layout_map_device(const fbl_layout* l, int64_t* out, void* stream);
+
+/*
+ * Attention forward.
+ *   lq/q     queries, Hq heads.       lk/k, lv/v  keys and values, Hkv heads.
+ *   lo/o     output, same extents as q.
+ *   lse      float32 [B, Hq, S] contiguous, written (saved for the backward).
+ *   scale    softmax scale (finite), e.g. 1/sqrt(D).
+ *   mask     see fbl_mask.
+ * Supported: D in {32, 64, 128}; Hq % Hkv == 0; S up to 2^30.
+ * Checks: non-NULL pointers; one dtype; lq.B == lk.B == lv.B == lo.B;
+ * lq.S == lk.S == lv.S == lo.S; lk and lv extents equal; lq.D == lk.D;
+ * lo extents equal lq's; sd == 1; tile_d divides D; base pointers and
+ * row strides 16-byte aligned; kv_len given with KEY_PADDING; o and lse do
+ * not overlap any input.
+ */
+fbl_status fbl_attn_fwd(const fbl_layout* lq, const void* q, const fbl_layout* lk, const void* k,
+                        const fbl_layout* lv, const void* v, const fbl_layout* lo, void* o, float* lse,
+                        float scale, fbl_mask mask, void* stream);
+
+/*
+ * Bytes of device workspace fbl_attn_bwd needs for these shapes: an fp32
+ * dQ accumulator [B, S, Hq*D] and the fp32 row statistic
+ * D_i = sum_k dO_ik O_ik, [B, Hq, S], 256-byte aligned sections.
+ */
+fbl_status fbl_attn_bwd_workspace(const fbl_layout* lq, const fbl_layout* lk, size_t* bytes);
+
+/*
+ * Attention backward of L = sum(O * dO): writes dQ (Hq heads), dK and dV
+ * (Hkv heads; each the sum over the query heads of its group).  The softmax
+ * probabilities are recomputed from q, k and the saved lse; nothing of size
+ * S x S is stored.  o and lse must be the forward's outputs for q, k, v.
+ *   ws/ws_bytes  device workspace of at least fbl_attn_bwd_workspace bytes,
+ *                256-byte aligned; its contents on entry do not matter.
+ * Same checks as fbl_attn_fwd for the shared arguments, plus: ldo/ldq
+ * extents equal lq's, ldk/ldv extents equal lk's, outputs do not overlap
+ * inputs or the workspace.
+ */
+fbl_status fbl_attn_bwd(const fbl_layout* lq, const void* q, const fbl_layout* lk, const void* k,
+                        const fbl_layout* lv, const void* v, const fbl_layout* lo, const void* o,
+                        const fbl_layout* ldo, const void* dO, const float* lse, float scale, fbl_mask mask,
+                        const fbl_layout* ldq, void* dq, const fbl_layout* ldk, void* dk,
+                        const fbl_layout* ldv, void* dv, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * The three launches of fbl_attn_bwd, selectable one by one (same arguments
+ * and checks as fbl_attn_bwd; `phases` is an OR of the bits below, enqueued
+ * in the order listed).  fbl_attn_bwd(...) equals
+ * fbl_attn_bwd_phases(FBL_BWD_ALL, ...).  Running the phases as separate calls
+ * on one stream gives the same result; a later phase reads what an earlier
+ * one left in the workspace, so the same workspace must be passed to all.
+ *   FBL_BWD_PREP  row statistic D_i = sum_k dO_ik O_ik and zeroed dQ accumulator
+ *   FBL_BWD_MAIN  recompute P; dK, dV; dQ accumulated in fp32
+ *   FBL_BWD_DQ    dQ = storage type of scale * accumulator
+ */
+#define FBL_BWD_PREP 1u
+#define FBL_BWD_MAIN 2u
+#define FBL_BWD_DQ 4u
+#define FBL_BWD_ALL 7u
+fbl_status fbl_attn_bwd_phases(uint32_t phases, const fbl_layout* lq, const void* q, const fbl_layout* lk,
+                               const void* k, const fbl_layout* lv, const void* v, const fbl_layout* lo,
+                               const void* o, const fbl_layout* ldo, const void* dO, const float* lse, float scale,
+                               fbl_mask mask, const fbl_layout* ldq, void* dq, const fbl_layout* ldk, void* dk,
+                               const fbl_layout* ldv, void* dv, void* ws, size_t ws_bytes, void* stream);
+
+/* Static, human-readable name of a status code. */
+const char* fbl_status_str(fbl_status s);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FBL_H */

@@ -1,0 +1,309 @@
+// api.cpp -- the C ABI: layout descriptors, validation and kernel dispatch.
+//
+// Every check runs on the host before the first launch; an error return
+// means nothing was enqueued.  The library holds no mutable global state
+// (the per-kernel LDS attribute is set once, thread-safely, by a function-
+// local static) and never allocates, frees or synchronises.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+
+#include "../../include/fbl.h"
+#include "kernels.hpp"
+#include "tiles.hpp"
+
+using fbl::bf16;
+
+namespace {
+
+int64_t elem_size(int32_t dt) { return dt == FBL_BF16 ? 2 : (dt == FBL_F32 ? 4 : 0); }
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// Tile-legality of one descriptor (paper section 4.3.1 checks): intra-tile
+// continuity (sd == 1), tile boundary preservation (tile_d divides D), rows
+// that hold whole heads, and 16-byte aligned rows.
+fbl_status check_layout(const fbl_layout* l) {
+    if (!l) return FBL_ERR_NULL;
+    const int64_t es = elem_size(l->dtype);
+    if (es == 0) return FBL_ERR_DTYPE;
+    if (l->B <= 0 || l->S <= 0 || l->H <= 0 || l->D <= 0) return FBL_ERR_SHAPE;
+    if (l->B > INT32_MAX || l->S > (1 << 30) || l->H > 65535) return FBL_ERR_SHAPE;
+    if (l->sd != 1) return FBL_ERR_LAYOUT;
+    if (l->tile_d <= 0 || l->D % l->tile_d != 0 || (l->tile_d * es) % 16 != 0) return FBL_ERR_LAYOUT;
+    if (l->sh < l->D) return FBL_ERR_LAYOUT;
+    if (l->ss < (l->H - 1) * l->sh + l->D) return FBL_ERR_LAYOUT;
+    if (l->B > 1 && l->sb < (l->S - 1) * l->ss + (l->H - 1) * l->sh + l->D) return FBL_ERR_LAYOUT;
+    if (l->sb < 0) return FBL_ERR_LAYOUT;
+    if ((l->ss * es) % 16 != 0 || (l->sh * es) % 16 != 0 || (l->sb * es) % 16 != 0) return FBL_ERR_ALIGN;
+    return FBL_OK;
+}
+
+bool same_extents(const fbl_layout* a, const fbl_layout* b) {
+    return a->B == b->B && a->S == b->S && a->H == b->H && a->D == b->D && a->dtype == b->dtype;
+}
+
+// Bytes spanned by a tensor from its base pointer (last element + 1).
+int64_t span_bytes(const fbl_layout* l) {
+    const int64_t last = (l->B - 1) * l->sb + (l->S - 1) * l->ss + (l->H - 1) * l->sh + (l->D - 1);
+    return (last + 1) * elem_size(l->dtype);
+}
+
+bool overlaps(const void* a, int64_t na, const void* b, int64_t nb) {
+    const uintptr_t pa = reinterpret_cast<uintptr_t>(a), pb = reinterpret_cast<uintptr_t>(b);
+    return pa < pb + (uintptr_t)nb && pb < pa + (uintptr_t)na;
+}
+
+fbl::TokMap tokmap(const fbl_layout* l) { return fbl::TokMap{l->sb, l->ss, l->sh}; }
+
+fbl::MaskArgs mask_args(const fbl_mask& m) {
+    return fbl::MaskArgs{(m.kind & FBL_MASK_CAUSAL) ? 1 : 0,
+                         (m.kind & FBL_MASK_KEY_PADDING) ? m.kv_len : nullptr};
+}
+
+// Checks shared by forward and backward: q/k/v consistency, mask, scale.
+fbl_status check_qkv(const fbl_layout* lq, const void* q, const fbl_layout* lk, const void* k, const fbl_layout* lv,
+                     const void* v, float scale, const fbl_mask& mask) {
+    if (!lq || !lk || !lv || !q || !k || !v) return FBL_ERR_NULL;
+    fbl_status st;
+    if ((st = check_layout(lq)) != FBL_OK) return st;
+    if ((st = check_layout(lk)) != FBL_OK) return st;
+    if ((st = check_layout(lv)) != FBL_OK) return st;
+    if (lq->dtype != lk->dtype || lq->dtype != lv->dtype) return FBL_ERR_DTYPE;
+    if (lq->B != lk->B || lq->B != lv->B || lq->S != lk->S || lq->S != lv->S) return FBL_ERR_SHAPE;
+    if (!same_extents(lk, lv)) return FBL_ERR_SHAPE;
+    if (lq->D != lk->D) return FBL_ERR_SHAPE;
+    if (lq->H % lk->H != 0) return FBL_ERR_SHAPE;
+    if (lq->D != 32 && lq->D != 64 && lq->D != 128) return FBL_ERR_UNSUPPORTED;
+    if (!aligned16(q) || !aligned16(k) || !aligned16(v)) return FBL_ERR_ALIGN;
+    if (mask.kind & ~(FBL_MASK_CAUSAL | FBL_MASK_KEY_PADDING)) return FBL_ERR_ARG;
+    if ((mask.kind & FBL_MASK_KEY_PADDING) && !mask.kv_len) return FBL_ERR_NULL;
+    if (!std::isfinite(scale)) return FBL_ERR_ARG;
+    return FBL_OK;
+}
+
+template <typename T>
+hipError_t dispatch_fwd(int D, const fbl::FwdArgs& a, hipStream_t s) {
+    switch (D) {
+        case 32: return fbl::launch_attn_fwd<T, 32>(a, s);
+        case 64: return fbl::launch_attn_fwd<T, 64>(a, s);
+        default: return fbl::launch_attn_fwd<T, 128>(a, s);
+    }
+}
+
+template <typename T>
+hipError_t dispatch_bwd(int D, const fbl::BwdArgs& a, unsigned phases, hipStream_t s) {
+    switch (D) {
+        case 32: return fbl::launch_attn_bwd<T, 32>(a, phases, s);
+        case 64: return fbl::launch_attn_bwd<T, 64>(a, phases, s);
+        default: return fbl::launch_attn_bwd<T, 128>(a, phases, s);
+    }
+}
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+struct WsLayout {
+    size_t dq_acc, drow, total;
+};
+
+WsLayout ws_layout(const fbl_layout* lq) {
+    WsLayout w;
+    w.dq_acc = 0;
+    const size_t n_dq = (size_t)lq->B * lq->S * lq->H * lq->D * sizeof(float);
+    w.drow = align256(n_dq);
+    const size_t n_dr = (size_t)lq->B * lq->H * lq->S * sizeof(float);
+    w.total = align256(w.drow + n_dr);
+    return w;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* fbl_status_str(fbl_status s) {
+    switch (s) {
+        case FBL_OK: return "FBL_OK";
+        case FBL_ERR_NULL: return "FBL_ERR_NULL: a required pointer is NULL";
+        case FBL_ERR_SHAPE: return "FBL_ERR_SHAPE: non-positive or inconsistent extents";
+        case FBL_ERR_DTYPE: return "FBL_ERR_DTYPE: unknown or mismatched dtype";
+        case FBL_ERR_LAYOUT: return "FBL_ERR_LAYOUT: tile-legality check failed";
+        case FBL_ERR_ALIGN: return "FBL_ERR_ALIGN: pointer or stride not 16-byte aligned";
+        case FBL_ERR_UNSUPPORTED: return "FBL_ERR_UNSUPPORTED: head dim or mask not implemented";
+        case FBL_ERR_WORKSPACE: return "FBL_ERR_WORKSPACE: workspace missing or too small";
+        case FBL_ERR_HIP: return "FBL_ERR_HIP: HIP runtime error at launch";
+        case FBL_ERR_ARG: return "FBL_ERR_ARG: invalid argument";
+    }
+    return "FBL_ERR_UNKNOWN";
+}
+
+fbl_status fbl_layout_desc(fbl_layout* out, int32_t dtype, int64_t B, int64_t S, int64_t H, int64_t D,
+                           int64_t row_stride, int64_t batch_stride, int64_t tile_d) {
+    if (!out) return FBL_ERR_NULL;
+    std::memset(out, 0, sizeof(*out));
+    if (elem_size(dtype) == 0) return FBL_ERR_DTYPE;
+    if (B <= 0 || S <= 0 || H <= 0 || D <= 0 || row_stride < 0 || batch_stride < 0 || tile_d < 0) return FBL_ERR_SHAPE;
+    fbl_layout l;
+    std::memset(&l, 0, sizeof(l));
+    l.dtype = dtype;
+    l.B = B;
+    l.S = S;
+    l.H = H;
+    l.D = D;
+    l.sd = 1;
+    l.sh = D;
+    l.ss = row_stride ? row_stride : H * D;
+    l.sb = batch_stride ? batch_stride : S * l.ss;
+    if (tile_d > INT32_MAX) return FBL_ERR_LAYOUT;
+    l.tile_d = (int32_t)(tile_d ? tile_d : D);
+    l.tile_s = fbl::tile_rows(D, dtype);
+    const fbl_status st = check_layout(&l);
+    if (st != FBL_OK) return st;
+    *out = l;
+    return FBL_OK;
+}
+
+int64_t fbl_layout_offset(const fbl_layout* l, int64_t b, int64_t h, int64_t s, int64_t i) {
+    if (!l) return -1;
+    if (b < 0 || b >= l->B || h < 0 || h >= l->H || s < 0 || s >= l->S || i < 0 || i >= l->D) return -1;
+    return b * l->sb + s * l->ss + h * l->sh + i * l->sd;
+}
+
+fbl_status fbl_layout_map_device(const fbl_layout* l, int64_t* out, void* stream) {
+    if (!l || !out) return FBL_ERR_NULL;
+    const fbl_status st = check_layout(l);
+    if (st != FBL_OK) return st;
+    const hipError_t e = fbl::launch_layout_map(tokmap(l), (int)l->B, (int)l->H, (int)l->S, (int)l->D, out,
+                                                static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? FBL_OK : FBL_ERR_HIP;
+}
+
+fbl_status fbl_attn_fwd(const fbl_layout* lq, const void* q, const fbl_layout* lk, const void* k,
+                        const fbl_layout* lv, const void* v, const fbl_layout* lo, void* o, float* lse, float scale,
+                        fbl_mask mask, void* stream) {
+    fbl_status st = check_qkv(lq, q, lk, k, lv, v, scale, mask);
+    if (st != FBL_OK) return st;
+    if (!lo || !o || !lse) return FBL_ERR_NULL;
+    if ((st = check_layout(lo)) != FBL_OK) return st;
+    if (!same_extents(lo, lq)) return lo->dtype != lq->dtype ? FBL_ERR_DTYPE : FBL_ERR_SHAPE;
+    if (!aligned16(o) || !aligned16(lse)) return FBL_ERR_ALIGN;
+    const int64_t lse_bytes = lq->B * lq->H * lq->S * 4;
+    const void* ins[3] = {q, k, v};
+    const int64_t in_bytes[3] = {span_bytes(lq), span_bytes(lk), span_bytes(lv)};
+    for (int i = 0; i < 3; ++i) {
+        if (overlaps(o, span_bytes(lo), ins[i], in_bytes[i])) return FBL_ERR_ARG;
+        if (overlaps(lse, lse_bytes, ins[i], in_bytes[i])) return FBL_ERR_ARG;
+    }
+    if (overlaps(o, span_bytes(lo), lse, lse_bytes)) return FBL_ERR_ARG;
+
+    fbl::FwdArgs a;
+    a.q = q;
+    a.k = k;
+    a.v = v;
+    a.o = o;
+    a.lse = lse;
+    a.mq = tokmap(lq);
+    a.mk = tokmap(lk);
+    a.mv = tokmap(lv);
+    a.mo = tokmap(lo);
+    a.B = (int)lq->B;
+    a.S = (int)lq->S;
+    a.Hq = (int)lq->H;
+    a.Hkv = (int)lk->H;
+    a.scale_log2 = scale * 1.4426950408889634f;
+    a.mask = mask_args(mask);
+    const hipStream_t s = static_cast<hipStream_t>(stream);
+    const hipError_t e = lq->dtype == FBL_BF16 ? dispatch_fwd<bf16>((int)lq->D, a, s)
+                                               : dispatch_fwd<float>((int)lq->D, a, s);
+    return e == hipSuccess ? FBL_OK : FBL_ERR_HIP;
+}
+
+fbl_status fbl_attn_bwd_workspace(const fbl_layout* lq, const fbl_layout* lk, size_t* bytes) {
+    if (!lq || !lk || !bytes) return FBL_ERR_NULL;
+    fbl_status st;
+    if ((st = check_layout(lq)) != FBL_OK) return st;
+    if ((st = check_layout(lk)) != FBL_OK) return st;
+    *bytes = ws_layout(lq).total;
+    return FBL_OK;
+}
+
+fbl_status fbl_attn_bwd_phases(uint32_t phases, const fbl_layout* lq, const void* q, const fbl_layout* lk,
+                               const void* k, const fbl_layout* lv, const void* v, const fbl_layout* lo,
+                               const void* o, const fbl_layout* ldo, const void* dO, const float* lse, float scale,
+                               fbl_mask mask, const fbl_layout* ldq, void* dq, const fbl_layout* ldk, void* dk,
+                               const fbl_layout* ldv, void* dv, void* ws, size_t ws_bytes, void* stream) {
+    if (phases == 0 || (phases & ~FBL_BWD_ALL)) return FBL_ERR_ARG;
+    fbl_status st = check_qkv(lq, q, lk, k, lv, v, scale, mask);
+    if (st != FBL_OK) return st;
+    if (!lo || !o || !ldo || !dO || !lse || !ldq || !dq || !ldk || !dk || !ldv || !dv) return FBL_ERR_NULL;
+    const fbl_layout* all[5] = {lo, ldo, ldq, ldk, ldv};
+    for (const fbl_layout* l : all)
+        if ((st = check_layout(l)) != FBL_OK) return st;
+    for (const fbl_layout* l : {lo, ldo, ldq})
+        if (!same_extents(l, lq)) return l->dtype != lq->dtype ? FBL_ERR_DTYPE : FBL_ERR_SHAPE;
+    for (const fbl_layout* l : {ldk, ldv})
+        if (!same_extents(l, lk)) return l->dtype != lq->dtype ? FBL_ERR_DTYPE : FBL_ERR_SHAPE;
+    if (!aligned16(o) || !aligned16(dO) || !aligned16(lse) || !aligned16(dq) || !aligned16(dk) || !aligned16(dv))
+        return FBL_ERR_ALIGN;
+    if (!ws) return FBL_ERR_WORKSPACE;
+    const WsLayout w = ws_layout(lq);
+    if (ws_bytes < w.total) return FBL_ERR_WORKSPACE;
+    if ((reinterpret_cast<uintptr_t>(ws) & 255u) != 0) return FBL_ERR_ALIGN;
+
+    const int64_t lse_bytes = lq->B * lq->H * lq->S * 4;
+    const void* ins[7] = {q, k, v, o, dO, lse, ws};
+    const int64_t in_bytes[7] = {span_bytes(lq),  span_bytes(lk), span_bytes(lv),      span_bytes(lo),
+                                 span_bytes(ldo), lse_bytes,      (int64_t)ws_bytes};
+    void* outs[3] = {dq, dk, dv};
+    const int64_t out_bytes[3] = {span_bytes(ldq), span_bytes(ldk), span_bytes(ldv)};
+    for (int i = 0; i < 3; ++i) {
+        for (int j = 0; j < 7; ++j)
+            if (overlaps(outs[i], out_bytes[i], ins[j], in_bytes[j])) return FBL_ERR_ARG;
+        for (int j = i + 1; j < 3; ++j)
+            if (overlaps(outs[i], out_bytes[i], outs[j], out_bytes[j])) return FBL_ERR_ARG;
+    }
+
+    fbl::BwdArgs a;
+    a.q = q;
+    a.k = k;
+    a.v = v;
+    a.o = o;
+    a.dout = dO;
+    a.lse = lse;
+    a.dq = dq;
+    a.dk = dk;
+    a.dv = dv;
+    a.dq_acc = reinterpret_cast<float*>(static_cast<unsigned char*>(ws) + w.dq_acc);
+    a.drow = reinterpret_cast<float*>(static_cast<unsigned char*>(ws) + w.drow);
+    a.mq = tokmap(lq);
+    a.mk = tokmap(lk);
+    a.mv = tokmap(lv);
+    a.mo = tokmap(lo);
+    a.mdo = tokmap(ldo);
+    a.mdq = tokmap(ldq);
+    a.mdk = tokmap(ldk);
+    a.mdv = tokmap(ldv);
+    a.B = (int)lq->B;
+    a.S = (int)lq->S;
+    a.Hq = (int)lq->H;
+    a.Hkv = (int)lk->H;
+    a.scale = scale;
+    a.scale_log2 = scale * 1.4426950408889634f;
+    a.mask = mask_args(mask);
+    const hipStream_t s = static_cast<hipStream_t>(stream);
+    const hipError_t e = lq->dtype == FBL_BF16 ? dispatch_bwd<bf16>((int)lq->D, a, phases, s)
+                                               : dispatch_bwd<float>((int)lq->D, a, phases, s);
+    return e == hipSuccess ? FBL_OK : FBL_ERR_HIP;
+}
+
+fbl_status fbl_attn_bwd(const fbl_layout* lq, const void* q, const fbl_layout* lk, const void* k,
+                        const fbl_layout* lv, const void* v, const fbl_layout* lo, const void* o,
+                        const fbl_layout* ldo, const void* dO, const float* lse, float scale, fbl_mask mask,
+                        const fbl_layout* ldq, void* dq, const fbl_layout* ldk, void* dk, const fbl_layout* ldv,
+                        void* dv, void* ws, size_t ws_bytes, void* stream) {
+    return fbl_attn_bwd_phases(FBL_BWD_ALL, lq, q, lk, k, lv, v, lo, o, ldo, dO, lse, scale, mask, ldq, dq, ldk, dk,
+                               ldv, dv, ws, ws_bytes, stream);
+}
+
+}  // extern "C"

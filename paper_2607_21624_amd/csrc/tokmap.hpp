@@ -1,0 +1,63 @@
+// tokmap.hpp -- the device side of the token-major index map.
+//
+// The reshape (B,S,D) -> (B,S,H,HD) and transpose -> (B,H,S,HD) of the
+// multi-head attention chain (paper section 4.3.1) only move whole head-dim
+// rows, so their composition (section 4.3.2, f3 o f2 o f1) is one affine map
+//   offset(b, h, s, i) = b*sb + s*ss + h*sh + i        (sd == 1)
+// evaluated once per tile origin; rows of a staged tile then sit ss elements
+// apart.  The strides arrive as kernel arguments, already validated on the
+// host (sd == 1, head-aligned tiles, 16-byte aligned rows).
+#pragma once
+
+#include <stdint.h>
+
+namespace fbl {
+
+struct TokMap {
+    int64_t sb, ss, sh;
+
+    __device__ __host__ __forceinline__ int64_t head_base(int b, int h) const {
+        return (int64_t)b * sb + (int64_t)h * sh;
+    }
+    __device__ __host__ __forceinline__ int64_t offset(int b, int h, int s, int i) const {
+        return (int64_t)b * sb + (int64_t)s * ss + (int64_t)h * sh + i;
+    }
+};
+
+struct MaskArgs {
+    int causal;             // key j allowed only for query i >= j
+    const int32_t* kv_len;  // nullptr, or device [B]: key j allowed only if j < kv_len[b]
+};
+
+struct FwdArgs {
+    const void* q;
+    const void* k;
+    const void* v;
+    void* o;
+    float* lse;
+    TokMap mq, mk, mv, mo;
+    int B, S, Hq, Hkv;
+    float scale_log2;  // softmax scale times log2(e)
+    MaskArgs mask;
+};
+
+struct BwdArgs {
+    const void* q;
+    const void* k;
+    const void* v;
+    const void* o;
+    const void* dout;
+    const float* lse;
+    void* dq;
+    void* dk;
+    void* dv;
+    float* dq_acc;   // fp32 [B, S, Hq*D] token-major workspace
+    float* drow;     // fp32 [B, Hq, S] workspace: sum_i dO * O per query row
+    TokMap mq, mk, mv, mo, mdo, mdq, mdk, mdv;
+    int B, S, Hq, Hkv;
+    float scale;       // softmax scale
+    float scale_log2;  // scale * log2(e)
+    MaskArgs mask;
+};
+
+}  // namespace fbl

@@ -1,0 +1,245 @@
+"""ctypes binding of libfbl.so (the C ABI in include/fbl.h).
+
+Argument marshalling only: every step of the attention path runs in the HIP
+kernels behind the C ABI.  torch is used for device memory (allocating outputs
+and the workspace) and for the current stream.  If libfbl.so is missing the
+import fails; there is no fallback implementation.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+from typing import Optional, Tuple
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libfbl.so")
+
+FBL_OK = 0
+FBL_ERR_NULL = 1
+FBL_ERR_SHAPE = 2
+FBL_ERR_DTYPE = 3
+FBL_ERR_LAYOUT = 4
+FBL_ERR_ALIGN = 5
+FBL_ERR_UNSUPPORTED = 6
+FBL_ERR_WORKSPACE = 7
+FBL_ERR_HIP = 8
+FBL_ERR_ARG = 9
+
+FBL_F32 = 0
+FBL_BF16 = 1
+FBL_MASK_CAUSAL = 1
+FBL_MASK_KEY_PADDING = 2
+
+FBL_BWD_PREP = 1
+FBL_BWD_MAIN = 2
+FBL_BWD_DQ = 4
+FBL_BWD_ALL = 7
+
+EXPORTED = ("fbl_layout_desc", "fbl_layout_offset", "fbl_layout_map_device", "fbl_attn_fwd",
+            "fbl_attn_bwd_workspace", "fbl_attn_bwd", "fbl_attn_bwd_phases", "fbl_status_str")
+
+
+class Layout(ctypes.Structure):
+    """Mirror of fbl_layout."""
+    _fields_ = [("dtype", ctypes.c_int32), ("tile_s", ctypes.c_int32), ("tile_d", ctypes.c_int32),
+                ("reserved", ctypes.c_int32),
+                ("B", ctypes.c_int64), ("S", ctypes.c_int64), ("H", ctypes.c_int64), ("D", ctypes.c_int64),
+                ("sb", ctypes.c_int64), ("ss", ctypes.c_int64), ("sh", ctypes.c_int64), ("sd", ctypes.c_int64)]
+
+    def __repr__(self):
+        return (f"Layout(dtype={self.dtype}, B={self.B}, S={self.S}, H={self.H}, D={self.D}, "
+                f"sb={self.sb}, ss={self.ss}, sh={self.sh}, sd={self.sd}, tile=({self.tile_s}x{self.tile_d}))")
+
+
+class Mask(ctypes.Structure):
+    """Mirror of fbl_mask."""
+    _fields_ = [("kind", ctypes.c_uint32), ("reserved", ctypes.c_uint32), ("kv_len", ctypes.c_void_p)]
+
+
+class FblError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {status_str(status)} (status {status})")
+
+
+def _load() -> ctypes.CDLL:
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"libfbl.so not built at {LIB_PATH}; run __graft_entry__.build() "
+                          "or python paper_2607_21624_amd/build.py")
+    lib = ctypes.CDLL(LIB_PATH)
+    P = ctypes.POINTER
+    vp = ctypes.c_void_p
+    lib.fbl_layout_desc.argtypes = [P(Layout), ctypes.c_int32] + [ctypes.c_int64] * 7
+    lib.fbl_layout_desc.restype = ctypes.c_int
+    lib.fbl_layout_offset.argtypes = [P(Layout)] + [ctypes.c_int64] * 4
+    lib.fbl_layout_offset.restype = ctypes.c_int64
+    lib.fbl_layout_map_device.argtypes = [P(Layout), vp, vp]
+    lib.fbl_layout_map_device.restype = ctypes.c_int
+    lib.fbl_attn_fwd.argtypes = [P(Layout), vp, P(Layout), vp, P(Layout), vp, P(Layout), vp, vp,
+                                 ctypes.c_float, Mask, vp]
+    lib.fbl_attn_fwd.restype = ctypes.c_int
+    lib.fbl_attn_bwd_workspace.argtypes = [P(Layout), P(Layout), P(ctypes.c_size_t)]
+    lib.fbl_attn_bwd_workspace.restype = ctypes.c_int
+    lib.fbl_attn_bwd.argtypes = [P(Layout), vp, P(Layout), vp, P(Layout), vp, P(Layout), vp, P(Layout), vp,
+                                 vp, ctypes.c_float, Mask, P(Layout), vp, P(Layout), vp, P(Layout), vp,
+                                 vp, ctypes.c_size_t, vp]
+    lib.fbl_attn_bwd.restype = ctypes.c_int
+    lib.fbl_attn_bwd_phases.argtypes = [ctypes.c_uint32] + lib.fbl_attn_bwd.argtypes
+    lib.fbl_attn_bwd_phases.restype = ctypes.c_int
+    lib.fbl_status_str.argtypes = [ctypes.c_int]
+    lib.fbl_status_str.restype = ctypes.c_char_p
+    return lib
+
+
+LIB = _load()
+
+
+def status_str(status: int) -> str:
+    return LIB.fbl_status_str(int(status)).decode()
+
+
+def _check(status: int, where: str) -> None:
+    if status != FBL_OK:
+        raise FblError(status, where)
+
+
+# ------------------------------------------------------------------ layouts
+def fbl_layout_desc(dtype: int, B: int, S: int, H: int, D: int, row_stride: int = 0, batch_stride: int = 0,
+                    tile_d: int = 0) -> Layout:
+    out = Layout()
+    _check(LIB.fbl_layout_desc(ctypes.byref(out), dtype, B, S, H, D, row_stride, batch_stride, tile_d),
+           "fbl_layout_desc")
+    return out
+
+
+def fbl_layout_desc_status(dtype: int, B: int, S: int, H: int, D: int, row_stride: int = 0,
+                           batch_stride: int = 0, tile_d: int = 0) -> Tuple[int, Layout]:
+    """Like fbl_layout_desc but returns (status, layout) instead of raising."""
+    out = Layout()
+    st = LIB.fbl_layout_desc(ctypes.byref(out), dtype, B, S, H, D, row_stride, batch_stride, tile_d)
+    return st, out
+
+
+def fbl_layout_offset(l: Layout, b: int, h: int, s: int, i: int) -> int:
+    return LIB.fbl_layout_offset(ctypes.byref(l), b, h, s, i)
+
+
+def _ptr(x) -> Optional[int]:
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    return x.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def fbl_layout_map_device(l: Layout, out, stream=None) -> None:
+    _check(LIB.fbl_layout_map_device(ctypes.byref(l), _ptr(out), _stream(stream)), "fbl_layout_map_device")
+
+
+def _mask(causal: bool, kv_len) -> Mask:
+    kind = (FBL_MASK_CAUSAL if causal else 0) | (FBL_MASK_KEY_PADDING if kv_len is not None else 0)
+    return Mask(kind, 0, _ptr(kv_len))
+
+
+def fbl_attn_fwd_raw(lq, q, lk, k, lv, v, lo, o, lse, scale, mask: Mask, stream=None) -> int:
+    """Direct call; returns the status code (for boundary tests)."""
+    return LIB.fbl_attn_fwd(ctypes.byref(lq) if lq is not None else None, _ptr(q),
+                            ctypes.byref(lk) if lk is not None else None, _ptr(k),
+                            ctypes.byref(lv) if lv is not None else None, _ptr(v),
+                            ctypes.byref(lo) if lo is not None else None, _ptr(o), _ptr(lse), float(scale),
+                            mask, _stream(stream) if stream != 0 else None)
+
+
+def fbl_attn_bwd_workspace(lq: Layout, lk: Layout) -> int:
+    n = ctypes.c_size_t(0)
+    _check(LIB.fbl_attn_bwd_workspace(ctypes.byref(lq), ctypes.byref(lk), ctypes.byref(n)), "fbl_attn_bwd_workspace")
+    return int(n.value)
+
+
+def fbl_attn_bwd_raw(lq, q, lk, k, lv, v, lo, o, ldo, do, lse, scale, mask: Mask, ldq, dq, ldk, dk, ldv, dv,
+                     ws, ws_bytes, stream=None, phases: int = FBL_BWD_ALL) -> int:
+    """Direct call of fbl_attn_bwd (phases == FBL_BWD_ALL) or fbl_attn_bwd_phases; returns the status."""
+    ref = lambda l: ctypes.byref(l) if l is not None else None
+    args = (ref(lq), _ptr(q), ref(lk), _ptr(k), ref(lv), _ptr(v), ref(lo), _ptr(o), ref(ldo), _ptr(do), _ptr(lse),
+            float(scale), mask, ref(ldq), _ptr(dq), ref(ldk), _ptr(dk), ref(ldv), _ptr(dv), _ptr(ws), int(ws_bytes),
+            _stream(stream) if stream != 0 else None)
+    if phases == FBL_BWD_ALL:
+        return LIB.fbl_attn_bwd(*args)
+    return LIB.fbl_attn_bwd_phases(phases, *args)
+
+
+# ------------------------------------------------------- torch-tensor helpers
+def _dtype_code(t) -> int:
+    import torch
+    if t.dtype == torch.bfloat16:
+        return FBL_BF16
+    if t.dtype == torch.float32:
+        return FBL_F32
+    raise FblError(FBL_ERR_DTYPE, f"unsupported tensor dtype {t.dtype}")
+
+
+def layout_of(t, H: int) -> Layout:
+    """Descriptor of a token-major [B, S, H*D] tensor (or a strided view of one:
+    inner stride 1, arbitrary row and batch strides).  No data is touched."""
+    if t.dim() != 3:
+        raise FblError(FBL_ERR_SHAPE, "expected a [B, S, H*D] tensor")
+    B, S, HD = t.shape
+    if HD % H:
+        raise FblError(FBL_ERR_SHAPE, f"last dim {HD} not divisible by heads {H}")
+    if t.stride(2) != 1:
+        raise FblError(FBL_ERR_LAYOUT, "innermost stride must be 1")
+    return fbl_layout_desc(_dtype_code(t), B, S, H, HD // H, row_stride=t.stride(1),
+                           batch_stride=t.stride(0) if B > 1 else 0)
+
+
+def attn_fwd(q, k, v, Hq: int, Hkv: int, scale: Optional[float] = None, causal: bool = False, kv_len=None,
+             out=None, lse=None, stream=None):
+    """Forward on token-major tensors.  Returns (O, LSE); O has q's shape and dtype
+    (allocated contiguous unless `out` is given), LSE is float32 [B, Hq, S]."""
+    import torch
+    lq, lk, lv = layout_of(q, Hq), layout_of(k, Hkv), layout_of(v, Hkv)
+    if scale is None:
+        scale = 1.0 / math.sqrt(lq.D)
+    B, S = q.shape[0], q.shape[1]
+    if out is None:
+        out = torch.empty((B, S, q.shape[2]), dtype=q.dtype, device=q.device)
+    if lse is None:
+        lse = torch.empty((B, Hq, S), dtype=torch.float32, device=q.device)
+    lo = layout_of(out, Hq)
+    _check(fbl_attn_fwd_raw(lq, q, lk, k, lv, v, lo, out, lse, scale, _mask(causal, kv_len), stream),
+           "fbl_attn_fwd")
+    return out, lse
+
+
+def attn_bwd(q, k, v, o, do, lse, Hq: int, Hkv: int, scale: Optional[float] = None, causal: bool = False,
+             kv_len=None, dq=None, dk=None, dv=None, workspace=None, stream=None, phases: int = FBL_BWD_ALL):
+    """Backward.  Returns (dQ, dK, dV) with the shapes/dtypes of q, k, v."""
+    import torch
+    lq, lk, lv = layout_of(q, Hq), layout_of(k, Hkv), layout_of(v, Hkv)
+    lo, ldo = layout_of(o, Hq), layout_of(do, Hq)
+    if scale is None:
+        scale = 1.0 / math.sqrt(lq.D)
+    if dq is None:
+        dq = torch.empty(q.shape, dtype=q.dtype, device=q.device)
+    if dk is None:
+        dk = torch.empty(k.shape, dtype=k.dtype, device=k.device)
+    if dv is None:
+        dv = torch.empty(v.shape, dtype=v.dtype, device=v.device)
+    need = fbl_attn_bwd_workspace(lq, lk)
+    if workspace is None:
+        workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
+    ldq, ldk, ldv = layout_of(dq, Hq), layout_of(dk, Hkv), layout_of(dv, Hkv)
+    _check(fbl_attn_bwd_raw(lq, q, lk, k, lv, v, lo, o, ldo, do, lse, scale, _mask(causal, kv_len), ldq, dq, ldk,
+                            dk, ldv, dv, workspace, workspace.numel() * workspace.element_size(), stream,
+                            phases), "fbl_attn_bwd")
+    return dq, dk, dv

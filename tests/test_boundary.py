@@ -1,0 +1,236 @@
+"""The C ABI boundary on the CPU: the library loads, exports what include/fbl.h
+declares, and rejects every invalid call before any launch.
+
+No test here ever passes validation with made-up pointers: each call carries
+exactly one defect, so nothing reaches a GPU launch.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2607_21624_amd as fbl
+from paper_2607_21624_amd import fbl as F
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "fbl.h")
+
+FAKE = 1 << 20          # 16-byte aligned made-up device addresses (never dereferenced)
+BF16, F32 = fbl.FBL_BF16, fbl.FBL_F32
+
+
+def header_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(fbl_[a-z_]+)\s*\(", text)))
+
+
+def test_header_symbols_exported():
+    names = header_functions()
+    assert set(names) == set(fbl.EXPORTED)
+    lib = ctypes.CDLL(fbl.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_status_strings():
+    for s in range(10):
+        assert fbl.status_str(s).startswith("FBL_")
+    assert "UNKNOWN" in fbl.status_str(99)
+
+
+# ------------------------------------------------------------- descriptors
+def test_layout_desc_defaults_and_tile():
+    l = fbl.fbl_layout_desc(BF16, 4, 1024, 16, 64)
+    assert (l.sd, l.sh, l.ss, l.sb) == (1, 64, 1024, 1024 * 1024)
+    assert l.tile_d == 64 and l.tile_s in (32, 64)
+
+
+@pytest.mark.parametrize("args,status", [
+    ((7, 1, 4, 2, 64), F.FBL_ERR_DTYPE),
+    ((BF16, 0, 4, 2, 64), F.FBL_ERR_SHAPE),
+    ((BF16, 1, 0, 2, 64), F.FBL_ERR_SHAPE),
+    ((BF16, 1, 4, 0, 64), F.FBL_ERR_SHAPE),
+    ((BF16, 1, 4, 2, -64), F.FBL_ERR_SHAPE),
+])
+def test_layout_desc_rejects(args, status):
+    st, l = fbl.fbl_layout_desc_status(*args)
+    assert st == status
+    assert l.B == 0 and l.D == 0  # left zeroed
+
+
+def test_layout_desc_row_stride_checks():
+    # rows overlapping the previous row's heads
+    st, _ = fbl.fbl_layout_desc_status(BF16, 2, 8, 4, 64, row_stride=4 * 64 - 8)
+    assert st == F.FBL_ERR_LAYOUT
+    # batches overlapping
+    st, _ = fbl.fbl_layout_desc_status(BF16, 2, 8, 4, 64, row_stride=256, batch_stride=256 * 7)
+    assert st == F.FBL_ERR_LAYOUT
+    # 16-byte alignment of rows: 4*64 + 4 bf16 elements = 520 bytes
+    st, _ = fbl.fbl_layout_desc_status(BF16, 2, 8, 4, 64, row_stride=260)
+    assert st == F.FBL_ERR_ALIGN
+    # a packed QKV row (12 query heads + 2*4 kv heads) is a legal view
+    st, l = fbl.fbl_layout_desc_status(BF16, 2, 8, 4, 64, row_stride=(12 + 8) * 64)
+    assert st == F.FBL_OK and l.ss == 20 * 64
+
+
+def test_paper_tile_boundary_examples():
+    import json
+    cases = json.load(open(os.path.join(ROOT, "tests", "golden", "layout_cases.json")))["head_split_examples"]
+    for c in cases:
+        st, _ = fbl.fbl_layout_desc_status(BF16, 1, 16, c["heads"], c["head_dim"], tile_d=c["tile_d"])
+        assert (st == F.FBL_OK) == c["legal"], c["cite"]
+        assert c["heads"] * c["head_dim"] == c["hidden"]
+
+
+def test_layout_offset_matches_oracle_bit_exact():
+    import numpy as np
+    import oracle
+    for (B, S, H, D) in [(1, 64, 2, 32), (8, 128, 12, 64), (2, 37, 3, 128)]:
+        l = fbl.fbl_layout_desc(BF16, B, S, H, D)
+        want = oracle.token_major_offsets(B, S, H, D)
+        got = np.empty_like(want)
+        for b in range(B):
+            for h in range(H):
+                for s in range(S):
+                    base = fbl.fbl_layout_offset(l, b, h, s, 0)
+                    got[b, h, s, :] = base + np.arange(D)
+                    assert fbl.fbl_layout_offset(l, b, h, s, D - 1) == base + D - 1
+        assert np.array_equal(got, want)
+
+
+def test_layout_offset_strided_view_matches_oracle():
+    import numpy as np
+    import oracle
+    B, S, H, D, row = 2, 9, 4, 32, 10 * 32
+    l = fbl.fbl_layout_desc(F32, B, S, H, D, row_stride=row)
+    want = oracle.head_split_offsets(B, S, H, D, row_stride=row, batch_stride=S * row)
+    got = np.array([[[[fbl.fbl_layout_offset(l, b, h, s, i) for i in range(D)] for s in range(S)]
+                     for h in range(H)] for b in range(B)])
+    assert np.array_equal(got, want)
+
+
+def test_layout_offset_out_of_range():
+    l = fbl.fbl_layout_desc(BF16, 2, 4, 3, 32)
+    assert fbl.fbl_layout_offset(l, 2, 0, 0, 0) == -1
+    assert fbl.fbl_layout_offset(l, 0, 3, 0, 0) == -1
+    assert fbl.fbl_layout_offset(l, 0, 0, 4, 0) == -1
+    assert fbl.fbl_layout_offset(l, 0, 0, 0, 32) == -1
+    assert fbl.fbl_layout_offset(l, -1, 0, 0, 0) == -1
+    assert F.LIB.fbl_layout_offset(None, 0, 0, 0, 0) == -1
+
+
+# ------------------------------------------------------------ attention calls
+def _fwd_setup(dtype=BF16, B=2, S=16, Hq=4, Hkv=2, D=64):
+    lq = fbl.fbl_layout_desc(dtype, B, S, Hq, D)
+    lk = fbl.fbl_layout_desc(dtype, B, S, Hkv, D)
+    lv = fbl.fbl_layout_desc(dtype, B, S, Hkv, D)
+    lo = fbl.fbl_layout_desc(dtype, B, S, Hq, D)
+    es = 2 if dtype == BF16 else 4
+    nq = B * S * Hq * D * es
+    nk = B * S * Hkv * D * es
+    ptr = {"q": FAKE, "k": FAKE + nq + 4096, "v": FAKE + nq + nk + 8192, "o": FAKE + nq + 2 * nk + 12288}
+    ptr["lse"] = ptr["o"] + nq + 4096
+    return lq, lk, lv, lo, ptr
+
+
+def _fwd(lq, lk, lv, lo, p, scale=0.125, kind=0, kv_len=None):
+    return fbl.fbl_attn_fwd_raw(lq, p["q"], lk, p["k"], lv, p["v"], lo, p["o"], p["lse"], scale,
+                                F.Mask(kind, 0, kv_len), stream=0)
+
+
+def _copy(l, **kw):
+    n = F.Layout()
+    ctypes.memmove(ctypes.byref(n), ctypes.byref(l), ctypes.sizeof(l))
+    for k, v in kw.items():
+        setattr(n, k, v)
+    return n
+
+
+def test_fwd_rejections():
+    lq, lk, lv, lo, p = _fwd_setup()
+    E = F
+    assert _fwd(None, lk, lv, lo, p) == E.FBL_ERR_NULL
+    assert _fwd(lq, lk, lv, lo, dict(p, q=None)) == E.FBL_ERR_NULL
+    assert _fwd(lq, lk, lv, lo, dict(p, lse=None)) == E.FBL_ERR_NULL
+    assert _fwd(lq, lk, _copy(lv, dtype=F32), lo, p) == E.FBL_ERR_DTYPE
+    assert _fwd(lq, lk, lv, _copy(lo, dtype=F32), p) == E.FBL_ERR_DTYPE
+    assert _fwd(lq, _copy(lk, S=8, sb=8 * 128), lv, lo, p) == E.FBL_ERR_SHAPE
+    assert _fwd(lq, _copy(lk, H=3, ss=3 * 64, sb=16 * 192), _copy(lv, H=3, ss=3 * 64, sb=16 * 192), lo, p) \
+        == E.FBL_ERR_SHAPE  # Hq % Hkv != 0
+    assert _fwd(lq, lk, lv, _copy(lo, H=2, ss=128, sb=16 * 128), p) == E.FBL_ERR_SHAPE
+    # unsupported head dim (legal layout, no kernel)
+    lq2, lk2, lv2, lo2, p2 = _fwd_setup(D=48)
+    assert _fwd(lq2, lk2, lv2, lo2, p2) == E.FBL_ERR_UNSUPPORTED
+    # intra-tile continuity and tile boundary
+    assert _fwd(_copy(lq, sd=2), lk, lv, lo, p) == E.FBL_ERR_LAYOUT
+    assert _fwd(_copy(lq, tile_d=48), lk, lv, lo, p) == E.FBL_ERR_LAYOUT
+    # alignment
+    assert _fwd(lq, lk, lv, lo, dict(p, k=p["k"] + 2)) == E.FBL_ERR_ALIGN
+    # mask
+    assert _fwd(lq, lk, lv, lo, p, kind=F.FBL_MASK_KEY_PADDING, kv_len=None) == E.FBL_ERR_NULL
+    assert _fwd(lq, lk, lv, lo, p, kind=8) == E.FBL_ERR_ARG
+    # scale
+    assert _fwd(lq, lk, lv, lo, p, scale=float("nan")) == E.FBL_ERR_ARG
+    assert _fwd(lq, lk, lv, lo, p, scale=float("inf")) == E.FBL_ERR_ARG
+    # output aliasing an input
+    assert _fwd(lq, lk, lv, lo, dict(p, o=p["q"])) == E.FBL_ERR_ARG
+    assert _fwd(lq, lk, lv, lo, dict(p, lse=p["v"] + 64)) == E.FBL_ERR_ARG
+
+
+def _bwd_setup(D=64, dtype=BF16):
+    lq, lk, lv, lo, p = _fwd_setup(dtype=dtype, D=D)
+    B, S, Hq, Hkv = 2, 16, 4, 2
+    es = 2 if dtype == BF16 else 4
+    nq = B * S * Hq * D * es
+    nk = B * S * Hkv * D * es
+    base = p["lse"] + 4096 * 4
+    p.update({"do": base, "dq": base + nq + 4096, "dk": base + 2 * nq + 8192, "dv": base + 2 * nq + nk + 12288})
+    p["ws"] = p["dv"] + nk + 4096
+    p["ws"] = (p["ws"] + 255) // 256 * 256
+    ws_bytes = fbl.fbl_attn_bwd_workspace(lq, lk)
+    return lq, lk, lv, lo, p, ws_bytes
+
+
+def _bwd(lq, lk, lv, lo, p, ws_bytes, ldo=None, ldq=None, ldk=None, ldv=None, kind=0, kv_len=None, scale=0.1):
+    ldo = ldo or lo
+    ldq = ldq or lq
+    ldk = ldk or lk
+    ldv = ldv or lv
+    return fbl.fbl_attn_bwd_raw(lq, p["q"], lk, p["k"], lv, p["v"], lo, p["o"], ldo, p["do"], p["lse"], scale,
+                                F.Mask(kind, 0, kv_len), ldq, p["dq"], ldk, p["dk"], ldv, p["dv"], p["ws"],
+                                ws_bytes, stream=0)
+
+
+def test_bwd_workspace_size():
+    lq = fbl.fbl_layout_desc(BF16, 2, 16, 4, 64)
+    lk = fbl.fbl_layout_desc(BF16, 2, 16, 2, 64)
+    n = fbl.fbl_attn_bwd_workspace(lq, lk)
+    assert n >= 2 * 16 * 4 * 64 * 4 + 2 * 4 * 16 * 4
+    assert n % 256 == 0
+
+
+def test_bwd_rejections():
+    lq, lk, lv, lo, p, ws = _bwd_setup()
+    E = F
+    assert _bwd(lq, lk, lv, lo, dict(p, do=None), ws) == E.FBL_ERR_NULL
+    assert _bwd(lq, lk, lv, lo, dict(p, dk=None), ws) == E.FBL_ERR_NULL
+    assert _bwd(lq, lk, lv, lo, dict(p, ws=None), ws) == E.FBL_ERR_WORKSPACE
+    assert _bwd(lq, lk, lv, lo, p, ws - 256) == E.FBL_ERR_WORKSPACE
+    assert _bwd(lq, lk, lv, lo, dict(p, ws=p["ws"] + 16), ws) == E.FBL_ERR_ALIGN
+    assert _bwd(lq, lk, lv, lo, p, ws, ldq=_copy(lq, dtype=F32)) == E.FBL_ERR_DTYPE
+    assert _bwd(lq, lk, lv, lo, p, ws, ldk=_copy(lq)) == E.FBL_ERR_SHAPE
+    assert _bwd(lq, lk, lv, lo, p, ws, ldv=_copy(lv, sd=3)) == E.FBL_ERR_LAYOUT
+    assert _bwd(lq, lk, lv, lo, dict(p, dq=p["do"]), ws) == E.FBL_ERR_ARG      # output aliases input
+    assert _bwd(lq, lk, lv, lo, dict(p, dv=p["dk"]), ws) == E.FBL_ERR_ARG      # outputs alias each other
+    assert _bwd(lq, lk, lv, lo, dict(p, dq=p["ws"]), ws) == E.FBL_ERR_ARG      # output aliases workspace
+    assert _bwd(lq, lk, lv, lo, p, ws, kind=F.FBL_MASK_KEY_PADDING) == E.FBL_ERR_NULL
+    assert _bwd(lq, lk, lv, lo, p, ws, scale=float("nan")) == E.FBL_ERR_ARG
+    assert _bwd(lq, lk, lv, lo, dict(p, lse=p["lse"] + 4), ws) == E.FBL_ERR_ALIGN
+
+
+def test_layout_map_device_rejects_null():
+    l = fbl.fbl_layout_desc(BF16, 1, 4, 2, 32)
+    assert F.LIB.fbl_layout_map_device(ctypes.byref(l), None, None) == F.FBL_ERR_NULL
+    assert F.LIB.fbl_layout_map_device(None, FAKE, None) == F.FBL_ERR_NULL

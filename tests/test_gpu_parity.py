@@ -1,0 +1,221 @@
+"""GPU parity: the HIP path (through the C ABI) against the fp64 oracle on the
+same seeded inputs.
+
+Tolerance per output tensor T in {O, LSE, dQ, dK, dV}:
+max|T_gpu - T_ref| / max|T_ref| <= 1e-4 for fp32 storage, <= 2e-2 for bf16
+storage (over all elements, padded rows included; -inf LSE entries must
+match exactly).  Index maps are compared bit-exactly.
+"""
+import math
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from parity_util import (TOL, compare, gpu_fwd_bwd, note, oracle_fwd_bwd, rel_err, select_heads, to_dev,
+                         to_np)
+
+pytestmark = pytest.mark.gpu
+
+
+def _lib():
+    import paper_2607_21624_amd as fbl
+    return fbl
+
+
+# ----------------------------------------------------------------- index map
+@pytest.mark.parametrize("B,S,H,D,row", [(1, 64, 2, 32, 0), (8, 128, 12, 64, 0), (2, 33, 3, 128, 0),
+                                          (2, 9, 4, 64, 10 * 64)])
+def test_device_index_map_bit_exact(B, S, H, D, row):
+    import torch
+    fbl = _lib()
+    note(f"index map B={B} S={S} H={H} D={D} row={row}")
+    l = fbl.fbl_layout_desc(fbl.FBL_BF16, B, S, H, D, row_stride=row)
+    out = torch.full((B * H * S * D,), -7, dtype=torch.int64, device="cuda")
+    fbl.fbl_layout_map_device(l, out)
+    torch.cuda.synchronize()
+    got = out.cpu().numpy().reshape(B, H, S, D)
+    if row:
+        want = oracle.head_split_offsets(B, S, H, D, row_stride=row, batch_stride=S * row)
+    else:
+        want = oracle.token_major_offsets(B, S, H, D)
+    assert np.array_equal(got, want)
+
+
+# ---------------------------------------------------------- named workloads
+def _check_workload(name, kv_heads=None, seed=None):
+    w = synth.WORKLOADS[name]
+    inp = synth.make_inputs(w, seed=seed)
+    note(f"{name} seed={inp['seed']} B={w.B} S={w.S} Hq={w.Hq} Hkv={w.Hkv} d={w.d} {w.dtype} mask={w.mask}")
+    got = select_heads(gpu_fwd_bwd(inp), w, kv_heads)
+    ref = oracle_fwd_bwd(inp, kv_heads)
+    errs, bad = compare(got, ref, w.dtype)
+    note(f"{name} rel errs {errs}")
+    assert not bad, f"{name}: {bad} (tol {TOL[w.dtype]})"
+
+
+def test_tiny_mha_f32():
+    _check_workload("tiny_mha_f32")
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_bert_base_keypad(seed):
+    _check_workload("bert_base_keypad", seed=seed)
+
+
+def test_gpt2_medium_causal():
+    _check_workload("gpt2_medium_causal")
+
+
+def test_llama32_1b_gqa_sampled_groups():
+    # full-size launch; the oracle checks two of the eight key/value groups
+    _check_workload("llama32_1b_gqa", kv_heads=[0, 5])
+
+
+def test_llama7b_causal_sampled_heads():
+    # full-size launch; the oracle checks three of the 32 heads
+    _check_workload("llama7b_causal", kv_heads=[0, 17, 31])
+
+
+# ------------------------------------------------------- random small shapes
+RANDOM_CASES = []
+for _d in (32, 64, 128):
+    for _dt in ("f32", "bf16"):
+        for _i in range(3):
+            RANDOM_CASES.append((_d, _dt, 100 * _d + 10 * (_dt == "bf16") + _i))
+
+
+@pytest.mark.parametrize("d,dt,seed", RANDOM_CASES)
+def test_random_shapes(d, dt, seed):
+    rng = np.random.default_rng(seed)
+    w = synth.random_workload(rng, dtype=dt, d=d, max_s=300, name=f"rand{seed}")
+    inp = synth.make_inputs(w)
+    note(f"random seed={seed} B={w.B} S={w.S} Hq={w.Hq} Hkv={w.Hkv} d={d} {dt} mask={w.mask} kv_len={inp['kv_len']}")
+    errs, bad = compare(gpu_fwd_bwd(inp), oracle_fwd_bwd(inp), dt)
+    assert not bad, f"{w}: {bad}"
+
+
+@pytest.mark.parametrize("S", [1, 2, 31, 32, 33, 64, 65, 127, 128, 129, 191, 257])
+@pytest.mark.parametrize("d", [64, 128])
+def test_ragged_lengths_causal_gqa(S, d):
+    w = synth.Workload(f"ragged{S}", B=2, S=S, Hq=4, Hkv=2, d=d, dtype="bf16", mask=synth.MASK_CAUSAL,
+                       seed=S + d)
+    inp = synth.make_inputs(w)
+    note(f"ragged S={S} d={d}")
+    errs, bad = compare(gpu_fwd_bwd(inp), oracle_fwd_bwd(inp), "bf16")
+    assert not bad, f"S={S} d={d}: {bad}"
+
+
+# ------------------------------------------------------------- edge cases
+def test_zero_and_overlong_key_lengths():
+    import torch
+    fbl = _lib()
+    w = synth.Workload("edge", B=3, S=70, Hq=2, Hkv=1, d=64, dtype="bf16", mask=synth.MASK_KEY_PADDING,
+                       len_lo=0, len_hi=0, seed=5)
+    inp = synth.make_inputs(w)
+    inp["kv_len"] = np.array([0, 70, 1000], dtype=np.int32)  # empty, exact, clamped to S
+    note("kv_len 0 / S / >S")
+    got = gpu_fwd_bwd(inp)
+    ref_in = dict(inp, kv_len=np.array([0, 70, 70], dtype=np.int32))
+    ref = oracle_fwd_bwd(ref_in)
+    assert np.all(np.isneginf(got["lse"][0])) and np.all(got["o"][0] == 0)
+    assert np.all(got["dq"][0] == 0) and np.all(got["dk"][0] == 0) and np.all(got["dv"][0] == 0)
+    errs, bad = compare(got, ref, "bf16")
+    assert not bad, bad
+
+
+def test_backward_alone_from_oracle_forward():
+    """Feed the oracle's O and LSE (cast to storage) to the GPU backward."""
+    import torch
+    fbl = _lib()
+    w = synth.WORKLOADS["gpt2_medium_causal"]
+    w = synth.Workload("bwd_only", B=2, S=384, Hq=8, Hkv=2, d=128, dtype="bf16", mask=synth.MASK_CAUSAL, seed=3)
+    inp = synth.make_inputs(w)
+    ref = oracle_fwd_bwd(inp)
+    scale = 1.0 / math.sqrt(w.d)
+    note("bwd only")
+    q, k, v, do = (to_dev(inp[n], "bf16") for n in ("q", "k", "v", "do"))
+    o = to_dev(synth.round_to_bf16(ref["o"]), "bf16")
+    lse = torch.from_numpy(ref["lse"].astype(np.float32)).cuda()
+    dq, dk, dv = fbl.attn_bwd(q, k, v, o, do, lse, w.Hq, w.Hkv, scale, True, None)
+    torch.cuda.synchronize()
+    for n, t in (("dq", dq), ("dk", dk), ("dv", dv)):
+        assert rel_err(to_np(t), ref[n]) <= TOL["bf16"], n
+
+
+def test_strided_views_of_packed_projection():
+    """Q, K, V read as column views of one packed [B, S, (Hq+2Hkv)d] tensor and
+    dQ/dK/dV written into views of a packed gradient tensor: no copies."""
+    import torch
+    fbl = _lib()
+    B, S, Hq, Hkv, d = 2, 200, 8, 2, 64
+    w = synth.Workload("packed", B=B, S=S, Hq=Hq, Hkv=Hkv, d=d, dtype="bf16", mask=synth.MASK_CAUSAL, seed=9)
+    inp = synth.make_inputs(w)
+    note("packed views")
+    packed = to_dev(np.concatenate([inp["q"], inp["k"], inp["v"]], axis=2), "bf16")
+    q = packed[:, :, :Hq * d]
+    k = packed[:, :, Hq * d:(Hq + Hkv) * d]
+    v = packed[:, :, (Hq + Hkv) * d:]
+    do = to_dev(inp["do"], "bf16")
+    gpacked = torch.zeros_like(packed)
+    scale = 1.0 / math.sqrt(d)
+    ptrs = [t.data_ptr() for t in (q, k, v)]
+    o, lse = fbl.attn_fwd(q, k, v, Hq, Hkv, scale, True)
+    dq, dk, dv = fbl.attn_bwd(q, k, v, o, do, lse, Hq, Hkv, scale, True, None,
+                              dq=gpacked[:, :, :Hq * d], dk=gpacked[:, :, Hq * d:(Hq + Hkv) * d],
+                              dv=gpacked[:, :, (Hq + Hkv) * d:])
+    torch.cuda.synchronize()
+    assert [t.data_ptr() for t in (q, k, v)] == ptrs
+    ref = oracle_fwd_bwd(inp)
+    got = {"o": to_np(o), "lse": to_np(lse), "dq": to_np(gpacked[:, :, :Hq * d]),
+           "dk": to_np(gpacked[:, :, Hq * d:(Hq + Hkv) * d]), "dv": to_np(gpacked[:, :, (Hq + Hkv) * d:])}
+    errs, bad = compare(got, ref, "bf16")
+    assert not bad, bad
+
+
+def test_repeatability_and_no_allocation():
+    """fwd and dK/dV are bitwise repeatable; dQ (fp32 atomics) within tolerance;
+    the calls allocate no device memory when outputs and workspace are given."""
+    import torch
+    fbl = _lib()
+    w = synth.Workload("rep", B=2, S=512, Hq=8, Hkv=4, d=128, dtype="bf16", mask=synth.MASK_CAUSAL, seed=4)
+    inp = synth.make_inputs(w)
+    note("repeatability")
+    q, k, v, do = (to_dev(inp[n], "bf16") for n in ("q", "k", "v", "do"))
+    scale = 1.0 / math.sqrt(w.d)
+    o = torch.empty_like(q)
+    lse = torch.empty((w.B, w.Hq, w.S), dtype=torch.float32, device="cuda")
+    dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+    lq, lk = fbl.layout_of(q, w.Hq), fbl.layout_of(k, w.Hkv)
+    ws = torch.empty(fbl.fbl_attn_bwd_workspace(lq, lk), dtype=torch.uint8, device="cuda")
+    runs = []
+    for _ in range(3):
+        torch.cuda.synchronize()
+        before = torch.cuda.memory_allocated()
+        fbl.attn_fwd(q, k, v, w.Hq, w.Hkv, scale, True, None, out=o, lse=lse)
+        fbl.attn_bwd(q, k, v, o, do, lse, w.Hq, w.Hkv, scale, True, None, dq=dq, dk=dk, dv=dv, workspace=ws)
+        torch.cuda.synchronize()
+        assert torch.cuda.memory_allocated() == before
+        runs.append([t.clone() for t in (o, lse, dq, dk, dv)])
+    for r in runs[1:]:
+        assert torch.equal(r[0], runs[0][0]) and torch.equal(r[1], runs[0][1])
+        assert torch.equal(r[3], runs[0][3]) and torch.equal(r[4], runs[0][4])
+        assert rel_err(to_np(r[2]), to_np(runs[0][2])) < 1e-2
+
+
+def test_gradient_invariants_on_gpu_outputs():
+    """sum_j dK_j = 0 and sum_j dV_j = sum_i dO_i per (batch, kv head), within
+    the bf16 tolerance scaled by the number of summed rows."""
+    w = synth.Workload("inv", B=2, S=256, Hq=8, Hkv=2, d=64, dtype="bf16", mask=synth.MASK_CAUSAL, seed=6)
+    inp = synth.make_inputs(w)
+    note("invariants")
+    got = gpu_fwd_bwd(inp)
+    d, G = w.d, w.Hq // w.Hkv
+    for b in range(w.B):
+        for g in range(w.Hkv):
+            dk = got["dk"][b, :, g * d:(g + 1) * d]
+            dv = got["dv"][b, :, g * d:(g + 1) * d]
+            want = sum(inp["do"][b, :, h * d:(h + 1) * d].sum(axis=0) for h in range(g * G, (g + 1) * G))
+            assert np.max(np.abs(dk.sum(axis=0))) <= 2e-2 * np.max(np.abs(dk)) * math.sqrt(w.S)
+            assert np.max(np.abs(dv.sum(axis=0) - want)) <= 2e-2 * np.max(np.abs(want))
