@@ -56,6 +56,25 @@ bool overlaps(const void* a, int64_t na, const void* b, int64_t nb) {
     return pa < pb + (uintptr_t)nb && pb < pa + (uintptr_t)na;
 }
 
+// Whether two described tensors share any byte.  Exact for the common case of
+// column views into one packed projection output (same row and batch strides,
+// rows of one view falling between the columns of the other); otherwise the
+// byte ranges decide (conservative).
+bool views_overlap(const void* pa, const fbl_layout* la, const void* pb, const fbl_layout* lb) {
+    const int64_t na = span_bytes(la), nb = span_bytes(lb);
+    if (!overlaps(pa, na, pb, nb)) return false;
+    const int64_t es = elem_size(la->dtype);
+    if (es != elem_size(lb->dtype) || la->ss != lb->ss || la->B != lb->B || la->S != lb->S) return true;
+    if (la->B > 1 && (la->sb != lb->sb || la->sb % la->ss != 0)) return true;
+    const int64_t dbytes = (int64_t)(reinterpret_cast<uintptr_t>(pb) - reinterpret_cast<uintptr_t>(pa));
+    if (dbytes % es != 0) return true;
+    const int64_t delta = dbytes / es;
+    const int64_t wa = (la->H - 1) * la->sh + la->D;  // columns a row of each view covers
+    const int64_t wb = (lb->H - 1) * lb->sh + lb->D;
+    if (delta >= 0) return !(delta >= wa && delta + wb <= la->ss);
+    return !(-delta >= wb && -delta + wa <= la->ss);
+}
+
 fbl::TokMap tokmap(const fbl_layout* l) { return fbl::TokMap{l->sb, l->ss, l->sh}; }
 
 fbl::MaskArgs mask_args(const fbl_mask& m) {
@@ -190,10 +209,10 @@ fbl_status fbl_attn_fwd(const fbl_layout* lq, const void* q, const fbl_layout* l
     if (!aligned16(o) || !aligned16(lse)) return FBL_ERR_ALIGN;
     const int64_t lse_bytes = lq->B * lq->H * lq->S * 4;
     const void* ins[3] = {q, k, v};
-    const int64_t in_bytes[3] = {span_bytes(lq), span_bytes(lk), span_bytes(lv)};
+    const fbl_layout* in_l[3] = {lq, lk, lv};
     for (int i = 0; i < 3; ++i) {
-        if (overlaps(o, span_bytes(lo), ins[i], in_bytes[i])) return FBL_ERR_ARG;
-        if (overlaps(lse, lse_bytes, ins[i], in_bytes[i])) return FBL_ERR_ARG;
+        if (views_overlap(o, lo, ins[i], in_l[i])) return FBL_ERR_ARG;
+        if (overlaps(lse, lse_bytes, ins[i], span_bytes(in_l[i]))) return FBL_ERR_ARG;
     }
     if (overlaps(o, span_bytes(lo), lse, lse_bytes)) return FBL_ERR_ARG;
 
@@ -252,16 +271,17 @@ fbl_status fbl_attn_bwd_phases(uint32_t phases, const fbl_layout* lq, const void
     if ((reinterpret_cast<uintptr_t>(ws) & 255u) != 0) return FBL_ERR_ALIGN;
 
     const int64_t lse_bytes = lq->B * lq->H * lq->S * 4;
-    const void* ins[7] = {q, k, v, o, dO, lse, ws};
-    const int64_t in_bytes[7] = {span_bytes(lq),  span_bytes(lk), span_bytes(lv),      span_bytes(lo),
-                                 span_bytes(ldo), lse_bytes,      (int64_t)ws_bytes};
+    const void* ins[5] = {q, k, v, o, dO};
+    const fbl_layout* in_l[5] = {lq, lk, lv, lo, ldo};
     void* outs[3] = {dq, dk, dv};
-    const int64_t out_bytes[3] = {span_bytes(ldq), span_bytes(ldk), span_bytes(ldv)};
+    const fbl_layout* out_l[3] = {ldq, ldk, ldv};
     for (int i = 0; i < 3; ++i) {
-        for (int j = 0; j < 7; ++j)
-            if (overlaps(outs[i], out_bytes[i], ins[j], in_bytes[j])) return FBL_ERR_ARG;
+        for (int j = 0; j < 5; ++j)
+            if (views_overlap(outs[i], out_l[i], ins[j], in_l[j])) return FBL_ERR_ARG;
+        if (overlaps(outs[i], span_bytes(out_l[i]), lse, lse_bytes)) return FBL_ERR_ARG;
+        if (overlaps(outs[i], span_bytes(out_l[i]), ws, (int64_t)ws_bytes)) return FBL_ERR_ARG;
         for (int j = i + 1; j < 3; ++j)
-            if (overlaps(outs[i], out_bytes[i], outs[j], out_bytes[j])) return FBL_ERR_ARG;
+            if (views_overlap(outs[i], out_l[i], outs[j], out_l[j])) return FBL_ERR_ARG;
     }
 
     fbl::BwdArgs a;

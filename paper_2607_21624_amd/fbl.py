@@ -64,6 +64,11 @@ class FblError(RuntimeError):
 
 
 def _load() -> ctypes.CDLL:
+    # torch bundles its own HIP runtime (soname libamdhip64.so.7).  Loading it
+    # first makes libfbl.so bind to that same runtime instead of pulling in a
+    # second copy from /opt/rocm: one runtime owns the device memory and the
+    # streams that torch hands over.
+    import torch  # noqa: F401
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"libfbl.so not built at {LIB_PATH}; run __graft_entry__.build() "
                           "or python paper_2607_21624_amd/build.py")

@@ -234,3 +234,21 @@ def test_layout_map_device_rejects_null():
     l = fbl.fbl_layout_desc(BF16, 1, 4, 2, 32)
     assert F.LIB.fbl_layout_map_device(ctypes.byref(l), None, None) == F.FBL_ERR_NULL
     assert F.LIB.fbl_layout_map_device(None, FAKE, None) == F.FBL_ERR_NULL
+
+
+def test_bwd_rejects_overlapping_packed_views():
+    """Column views of one packed gradient buffer: interleaved but disjoint views
+    are legal (exercised on the GPU); views sharing columns are rejected here."""
+    lq, lk, lv, lo, p, ws = _bwd_setup()
+    B, S, Hq, Hkv, D = 2, 16, 4, 2, 64
+    row = (Hq + 2 * Hkv) * D
+    ldq = fbl.fbl_layout_desc(BF16, B, S, Hq, D, row_stride=row)
+    ldk = fbl.fbl_layout_desc(BF16, B, S, Hkv, D, row_stride=row)
+    ldv = fbl.fbl_layout_desc(BF16, B, S, Hkv, D, row_stride=row)
+    base = p["ws"] + ws + 4096 * 16
+    # dk starts one head early: shares dq's last head columns
+    bad = dict(p, dq=base, dk=base + (Hq - 1) * D * 2, dv=base + (Hq + Hkv) * D * 2)
+    assert _bwd(lq, lk, lv, lo, bad, ws, ldq=ldq, ldk=ldk, ldv=ldv) == F.FBL_ERR_ARG
+    # dv starts inside dk's columns
+    bad = dict(p, dq=base, dk=base + Hq * D * 2, dv=base + (Hq + 1) * D * 2)
+    assert _bwd(lq, lk, lv, lo, bad, ws, ldq=ldq, ldk=ldk, ldv=ldv) == F.FBL_ERR_ARG
