@@ -115,6 +115,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="llama7b_causal")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-kernel-list", action="store_true",
+                    help="skip the torch-profiler dispatch listing (use under rocprofv3)")
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle work for cpu_baseline")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -200,7 +202,7 @@ def main():
                 "frac": round(dom["achieved"] / peak, 4), "traffic": None, "kernel": dom["kernel"],
                 "avg_launch_ms": round(dom["avg_ms"], 4), "flops_per_launch": dom["flops_per_launch"]}
 
-    kernels = dispatched_kernels(step)
+    kernels = None if args.no_kernel_list else dispatched_kernels(step)
     foreign = None
     if kernels is not None:
         foreign = [n for n in kernels if not any(t in n for t in ("attn_fwd", "attn_bwd"))]

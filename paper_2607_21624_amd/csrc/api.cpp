@@ -96,6 +96,9 @@ fbl_status check_qkv(const fbl_layout* lq, const void* q, const fbl_layout* lk, 
     if (lq->D != lk->D) return FBL_ERR_SHAPE;
     if (lq->H % lk->H != 0) return FBL_ERR_SHAPE;
     if (lq->D != 32 && lq->D != 64 && lq->D != 128) return FBL_ERR_UNSUPPORTED;
+    // tiles are fetched through 32-bit buffer offsets from each (batch, head) base
+    for (const fbl_layout* l : {lq, lk, lv})
+        if (((l->S - 1) * l->ss + l->D) * elem_size(l->dtype) >= ((int64_t)1 << 31)) return FBL_ERR_UNSUPPORTED;
     if (!aligned16(q) || !aligned16(k) || !aligned16(v)) return FBL_ERR_ALIGN;
     if (mask.kind & ~(FBL_MASK_CAUSAL | FBL_MASK_KEY_PADDING)) return FBL_ERR_ARG;
     if ((mask.kind & FBL_MASK_KEY_PADDING) && !mask.kv_len) return FBL_ERR_NULL;

@@ -1,27 +1,33 @@
 // attn_fwd.hip -- attention forward on token-major Q/K/V, gfx950.
 //
 // One workgroup = 4 wavefronts = 128 queries of one (batch, query head); each
-// wavefront owns 32 queries.  The loop streams key/value tiles of 64 rows
-// (the R-Tile, section 4.2) from the token-major tensors straight into LDS:
-// row r of the tile is row (k0 + r) of the projection output, read at
-// base + b*sb + (k0+r)*ss + hk*sh, so the head split and transpose of the
-// multi-head attention chain (section 4.3.1) never materialise.
+// wavefront owns 32 queries.  Key/value tiles of 64 rows (the R-Tile, paper
+// section 4.2) stream from the token-major tensors into LDS: row r of a tile
+// is token (k0 + r) of head hk, read at base + b*sb + (k0+r)*ss + hk*sh, so
+// the head split and transpose of the multi-head attention chain (section
+// 4.3.1) are a change of base address, never a copy.  Tiles are double
+// buffered and filled by LDS DMA, so tile j+1 is in flight while tile j is
+// consumed; one barrier per tile.
 //
 // The products are arranged so that no operand needs a physical transpose
-// (the tile invariance of section 4.2: the same staged tile serves both
-// reduction directions):
-//   S^T = K Q^T   A = K rows (LDS row reads), B = Q rows (registers);
-//                 the accumulator puts one query per lane column, so the
-//                 softmax row max/sum over keys is an in-lane reduction plus
-//                 one exchange between the two 32-lane halves;
+// (the tile invariance of section 4.2: one staged tile serves both reduction
+// directions):
+//   S^T = K Q^T     A = K rows (LDS row reads), B = Q rows (registers); the
+//                   accumulator holds one query per lane column, so the
+//                   softmax row max/sum over keys is an in-lane reduction
+//                   plus one exchange between the two 32-lane halves;
 //   O^T += V^T P^T  A = V^T via LDS transposed reads (ds_read_b64_tr_b16),
-//                 B = P^T taken straight from the S^T accumulator registers.
+//                   B = P^T straight from the S^T accumulator registers.
 // QK^T followed by PV is the consecutive matrix-product pair of section 4.4.2;
-// here both share one tile configuration inside one kernel.
-// Online softmax in base 2 with scale*log2(e) folded into the scores; the
-// saved LSE is converted to natural log at the store.
+// both share one tile configuration inside one kernel.
+// Online softmax in base 2 with scale*log2(e) folded into one FMA per score.
+// The running maximum is raised only when a tile exceeds it by more than
+// 2^8 (a stale maximum leaves every probability <= 256 and cancels in O/l),
+// which skips almost all rescales of the O accumulator.  The saved LSE is
+// converted to natural log at the store.
 #include "cdna4.hpp"
 #include "kernels.hpp"
+#include "stage.hpp"
 #include "tokmap.hpp"
 
 namespace fbl {
@@ -31,35 +37,16 @@ namespace {
 constexpr int kFwdWaves = 4;
 constexpr int kFwdBM = 32 * kFwdWaves;  // queries per workgroup
 constexpr int kFwdBN = 64;              // keys per tile
+constexpr float kRescaleSlack = 8.0f;   // log2 of the largest unnormalised probability
 
 template <typename T, int D>
-struct FwdTile {
-    static constexpr int PITCH = D + 16 / (int)sizeof(T);  // LDS row pitch (elements), 16-byte pad
-    static constexpr int CPR = D * (int)sizeof(T) / 16;    // 16-byte chunks per row
-};
-
-template <typename T, int D>
-__device__ __forceinline__ void stage_rows(T* dst, const T* src, int64_t ss, int row0, int nrows_valid) {
-    using TL = FwdTile<T, D>;
-    constexpr int NCH = kFwdBN * TL::CPR;
-    constexpr int EPC = 16 / (int)sizeof(T);
-#pragma unroll
-    for (int i = threadIdx.x; i < NCH; i += kFwdWaves * 64) {
-        const int r = i / TL::CPR, cc = i % TL::CPR;
-        uint4 x = {0u, 0u, 0u, 0u};
-        if (r < nrows_valid) x = load16(src + (int64_t)(row0 + r) * ss + cc * EPC);
-        *reinterpret_cast<uint4*>(dst + r * TL::PITCH + cc * EPC) = x;
-    }
-}
-
-template <typename T, int D>
-__global__ __launch_bounds__(256) void attn_fwd_kernel(FwdArgs a) {
-    using TL = FwdTile<T, D>;
+__global__ __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) void attn_fwd_kernel(FwdArgs a) {
+    using G = TileGeom<T, D>;
     constexpr int NC = D / 16;  // k-chunks over the head dim
     constexpr int ND = D / 32;  // 32-wide output column blocks
-    constexpr int PITCH = TL::PITCH;
-    __shared__ __attribute__((aligned(16))) T sK[kFwdBN * PITCH];
-    __shared__ __attribute__((aligned(16))) T sV[kFwdBN * PITCH];
+    constexpr int TILE = kFwdBN * D;
+    extern __shared__ __attribute__((aligned(1024))) unsigned char fwd_smem[];
+    T* smem = reinterpret_cast<T*>(fwd_smem);  // K0 K1 V0 V1, TILE elements each
 
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
@@ -67,10 +54,13 @@ __global__ __launch_bounds__(256) void attn_fwd_kernel(FwdArgs a) {
     const int c32 = lane & 31;
     const int S = a.S;
     const int nqb = (S + kFwdBM - 1) / kFwdBM;
-    // causal: the last query blocks see the most keys; launch them first
-    const int qb = a.mask.causal ? (nqb - 1 - (int)blockIdx.x) : (int)blockIdx.x;
-    const int h = blockIdx.y;
-    const int b = blockIdx.z;
+    const int logical = xcd_logical_id(blockIdx.x, nqb * a.Hq * a.B, gridDim.x);
+    if (logical < 0) return;
+    const int rank = logical % nqb;
+    const int h = (logical / nqb) % a.Hq;
+    const int b = logical / (nqb * a.Hq);
+    // causal: the last query blocks see the most keys; start them first
+    const int qb = a.mask.causal ? (nqb - 1 - rank) : rank;
     const int hk = h / (a.Hq / a.Hkv);
 
     int kv_end = S;
@@ -82,94 +72,114 @@ __global__ __launch_bounds__(256) void attn_fwd_kernel(FwdArgs a) {
     if (a.mask.causal) k_hi = min(k_hi, q0 + kFwdBM);
     const int nkb = (k_hi + kFwdBN - 1) / kFwdBN;
 
+    // the softmax FMA below needs a non-negative scale: fold the sign into Q
+    const bool neg = a.scale_log2 < 0.f;
+    const float c = neg ? -a.scale_log2 : a.scale_log2;
+
     // Q^T as the B operand: lane <-> query, in-lane d = 16c + 8g + e
     Frag<T> qf[NC];
     {
         const T* qrow = static_cast<const T*>(a.q) + a.mq.head_base(b, h) + (int64_t)qi * a.mq.ss;
 #pragma unroll
-        for (int c = 0; c < NC; ++c) {
+        for (int cc = 0; cc < NC; ++cc) {
+            float z[8] = {0, 0, 0, 0, 0, 0, 0, 0};
             if (qi < S) {
                 if constexpr (sizeof(T) == 2) {
-                    uint4 x = load16(qrow + 16 * c + 8 * g);
-                    qf[c].v = __builtin_bit_cast(bf16x8, x);
+                    uint4 x = load16(qrow + 16 * cc + 8 * g);
+                    if (neg) { x.x ^= 0x80008000u; x.y ^= 0x80008000u; x.z ^= 0x80008000u; x.w ^= 0x80008000u; }
+                    qf[cc].v = __builtin_bit_cast(bf16x8, x);
+                    continue;
                 } else {
-                    uint4 x0 = load16(qrow + 16 * c + 8 * g);
-                    uint4 x1 = load16(qrow + 16 * c + 8 * g + 4);
-                    f32x4 f0 = __builtin_bit_cast(f32x4, x0), f1 = __builtin_bit_cast(f32x4, x1);
+                    const f32x4 x0 = __builtin_bit_cast(f32x4, load16(qrow + 16 * cc + 8 * g));
+                    const f32x4 x1 = __builtin_bit_cast(f32x4, load16(qrow + 16 * cc + 8 * g + 4));
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) { qf[c].v[e] = f0[e]; qf[c].v[4 + e] = f1[e]; }
+                    for (int e = 0; e < 4; ++e) { z[e] = neg ? -x0[e] : x0[e]; z[4 + e] = neg ? -x1[e] : x1[e]; }
                 }
-            } else {
-                float z[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-                pack_frag(qf[c], z);
             }
+            pack_frag(qf[cc], z);
         }
     }
 
     f32x16 oacc[ND];
 #pragma unroll
     for (int t = 0; t < ND; ++t) oacc[t] = f32x16{};
-    float m = -INFINITY, l = 0.f;
+    float m = -INFINITY;  // running maximum (log2 units), equal in both lane halves
+    float l = 0.f;        // this lane half's share of the running sum
 
-    const T* kbase = static_cast<const T*>(a.k) + a.mk.head_base(b, hk);
-    const T* vbase = static_cast<const T*>(a.v) + a.mv.head_base(b, hk);
+    const uint32_t es = sizeof(T);
+    const Rsrc rk = make_rsrc(static_cast<const T*>(a.k) + a.mk.head_base(b, hk),
+                              (uint32_t)((int64_t)(S - 1) * a.mk.ss * es + D * es));
+    const Rsrc rv = make_rsrc(static_cast<const T*>(a.v) + a.mv.head_base(b, hk),
+                              (uint32_t)((int64_t)(S - 1) * a.mv.ss * es + D * es));
+    const uint32_t kbytes = (uint32_t)(a.mk.ss * es), vbytes = (uint32_t)(a.mv.ss * es);
+
+    if (nkb > 0) {
+        dma_tile<T, D, kFwdBN, kFwdWaves>(smem, rk, 0, kbytes, wave, lane);
+        dma_tile<T, D, kFwdBN, kFwdWaves>(smem + 2 * TILE, rv, 0, vbytes, wave, lane);
+    }
 
     for (int kb = 0; kb < nkb; ++kb) {
         const int k0 = kb * kFwdBN;
-        __syncthreads();
-        stage_rows<T, D>(sK, kbase, a.mk.ss, k0, min(kFwdBN, S - k0));
-        stage_rows<T, D>(sV, vbase, a.mv.ss, k0, min(kFwdBN, S - k0));
-        __syncthreads();
-
+        wait_vmcnt<0>();
+        __syncthreads();  // tile kb landed everywhere; tile kb-1's buffers are free
+        if (kb + 1 < nkb) {
+            const int nb = (kb + 1) & 1;
+            dma_tile<T, D, kFwdBN, kFwdWaves>(smem + nb * TILE, rk, k0 + kFwdBN, kbytes, wave, lane);
+            dma_tile<T, D, kFwdBN, kFwdWaves>(smem + (2 + nb) * TILE, rv, k0 + kFwdBN, vbytes, wave, lane);
+        }
         // a whole tile above this wave's diagonal contributes nothing
         if (a.mask.causal && k0 > qw0 + 31) continue;
+        const T* sK = smem + (kb & 1) * TILE;
+        const T* sV = smem + (2 + (kb & 1)) * TILE;
 
         f32x16 s[2];
 #pragma unroll
         for (int kt = 0; kt < 2; ++kt) {
             s[kt] = f32x16{};
 #pragma unroll
-            for (int c = 0; c < NC; ++c) {
+            for (int cc = 0; cc < NC; ++cc) {
                 Frag<T> kf;
-                lds_row_frag(kf, sK + (kt * 32 + c32) * PITCH + 16 * c + 8 * g);
-                mma(s[kt], kf, qf[c]);
+                tile_row_frag<D>(kf, sK, kt * 32 + c32, 16 * cc + 8 * g);
+                mma(s[kt], kf, qf[cc]);
             }
         }
 
-        const bool need_mask = (k0 + kFwdBN > kv_end) || (a.mask.causal && k0 + kFwdBN - 1 > qw0);
+        const bool boundary = (k0 + kFwdBN > kv_end) || (a.mask.causal && k0 + kFwdBN - 1 > qw0);
+        if (boundary) {
+#pragma unroll
+            for (int kt = 0; kt < 2; ++kt) {
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int key = k0 + kt * 32 + acc_row(r, g);
+                    if (key >= kv_end || (a.mask.causal && key > qi)) s[kt][r] = -INFINITY;
+                }
+            }
+        }
         float mx = -INFINITY;
 #pragma unroll
-        for (int kt = 0; kt < 2; ++kt) {
+        for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                float x = s[kt][r] * a.scale_log2;
-                if (need_mask) {
-                    const int key = k0 + kt * 32 + acc_row(r, g);
-                    if (key >= kv_end || (a.mask.causal && key > qi)) x = -INFINITY;
-                }
-                s[kt][r] = x;
-                mx = fmaxf(mx, x);
-            }
+            for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kt][r]);
+        mx = fmaxf(mx, other_half(mx)) * c;
+        if (__any(mx > m + kRescaleSlack)) {
+            const float m_new = fmaxf(m, mx);
+            const float alpha = (m_new == -INFINITY) ? 1.f : fast_exp2(m - m_new);  // 0 when m was -inf
+            l *= alpha;
+#pragma unroll
+            for (int t = 0; t < ND; ++t) oacc[t] *= alpha;
+            m = m_new;
         }
-        mx = fmaxf(mx, other_half(mx));
-        const float m_new = fmaxf(m, mx);
-        const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
-        const float alpha = fast_exp2(m - m_use);
-        float ls = 0.f;
+        const float m_use = (m == -INFINITY) ? 0.f : m;
 #pragma unroll
         for (int kt = 0; kt < 2; ++kt) {
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
-                const float p = fast_exp2(s[kt][r] - m_use);
+                float p = fast_exp2(__builtin_fmaf(s[kt][r], c, -m_use));
+                if (boundary && s[kt][r] == -INFINITY) p = 0.f;
                 s[kt][r] = p;
-                ls += p;
+                l += p;
             }
         }
-        ls += other_half(ls);
-        l = l * alpha + ls;
-        m = m_new;
-#pragma unroll
-        for (int t = 0; t < ND; ++t) oacc[t] *= alpha;
 
         // O^T += V^T P^T over the 64 keys: chunk (kt, cc) covers keys
         // kt*32 + 16cc + {4g..4g+3, 8+4g..8+4g+3} in accumulator order
@@ -186,13 +196,14 @@ __global__ __launch_bounds__(256) void attn_fwd_kernel(FwdArgs a) {
 #pragma unroll
                 for (int t = 0; t < ND; ++t) {
                     Frag<T> vf;
-                    lds_tr_frag(vf, sV, PITCH, row0, row0 + 8, 32 * t, lane);
+                    tile_tr_frag<D>(vf, sV, row0, row0 + 8, 32 * t, lane);
                     mma(oacc[t], vf, pf);
                 }
             }
         }
     }
 
+    l += other_half(l);
     if (qi < S) {
         const float inv = (l > 0.f) ? 1.f / l : 0.f;
         T* orow = static_cast<T*>(a.o) + a.mo.head_base(b, h) + (int64_t)qi * a.mo.ss;
@@ -211,13 +222,29 @@ __global__ __launch_bounds__(256) void attn_fwd_kernel(FwdArgs a) {
     }
 }
 
+template <typename T, int D>
+constexpr int fwd_lds_bytes() {
+    return 4 * kFwdBN * D * (int)sizeof(T);
+}
+
+template <typename T, int D>
+hipError_t set_fwd_lds() {
+    static hipError_t once = hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_fwd_kernel<T, D>),
+                                                 hipFuncAttributeMaxDynamicSharedMemorySize, fwd_lds_bytes<T, D>());
+    return once;
+}
+
 }  // namespace
 
 template <typename T, int D>
 hipError_t launch_attn_fwd(const FwdArgs& a, hipStream_t stream) {
+    const hipError_t e = set_fwd_lds<T, D>();
+    if (e != hipSuccess) return e;
     const int nqb = (a.S + kFwdBM - 1) / kFwdBM;
-    dim3 grid(nqb, a.Hq, a.B);
-    hipLaunchKernelGGL((attn_fwd_kernel<T, D>), grid, dim3(256), 0, stream, a);
+    const int total = nqb * a.Hq * a.B;
+    const int padded = (total + 7) / 8 * 8;
+    constexpr int lds = fwd_lds_bytes<T, D>();
+    hipLaunchKernelGGL((attn_fwd_kernel<T, D>), dim3(padded), dim3(256), lds, stream, a);
     return hipGetLastError();
 }
 

@@ -1,0 +1,138 @@
+// stage.hpp -- R-Tile staging of token-major rows into LDS on gfx950.
+//
+// A tile is ROWS token rows of one head (D contiguous elements each, read at
+// row_base + r*ss) placed in LDS without padding.  Each row is CPR 16-byte
+// chunks; chunk c of row r is stored in slot c ^ swz(r).  The XOR swizzle is
+// the intra-tile placement of the paper's R-Tile (section 4.2, intra-tile
+// mapping): it is chosen so that both ways the kernels read a tile hit every
+// LDS bank once per 256 bytes --
+//   row reads      16 consecutive rows at one chunk (MFMA operands whose
+//                  contraction runs along d), and
+//   transposed     4 consecutive rows x 4 consecutive chunks per 32 lanes
+//   reads          (ds_read_b64_tr_b16, operands contracted along tokens),
+// which is the tile invariance of section 4.2 carried to the LDS banks.
+//
+// Tiles are filled with buffer_load_dwordx4 ... lds: each lane moves 16 bytes
+// from global memory straight into LDS (no registers), so the next tile can be
+// in flight while the current one is consumed.  The buffer resource covers
+// exactly the rows of one (batch, head); rows beyond the sequence read as
+// zeros, so ragged tails need no branches.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "cdna4.hpp"
+
+namespace fbl {
+
+template <typename T, int D>
+struct TileGeom {
+    static constexpr int EPC = 16 / (int)sizeof(T);  // elements per 16-byte chunk
+    static constexpr int CPR = D / EPC;              // chunks per row
+
+    // Chunk XOR of row r (values < CPR).
+    static FBL_DEV int swz(int r) {
+        if constexpr (sizeof(T) == 2) {
+            if constexpr (CPR == 16) return ((r & 3) << 2) | ((r >> 2) & 3);
+            else if constexpr (CPR == 8) return (((r >> 1) & 1) << 2) | ((r >> 2) & 3);
+            else return (r >> 2) & 3;
+        } else {
+            if constexpr (CPR >= 16) return r & 15;
+            else return (r >> 1) & 7;
+        }
+    }
+    // Element offset of (row r, column col) inside a tile.
+    static FBL_DEV int off(int r, int col) { return r * D + (((col / EPC) ^ swz(r)) * EPC) + (col % EPC); }
+};
+
+typedef __amdgpu_buffer_rsrc_t Rsrc;
+
+// Buffer resource over `bytes` bytes from `base` (raw, unswizzled; reads past
+// the end return zeros).
+FBL_DEV Rsrc make_rsrc(const void* base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+
+// Issue the loads of ROWS rows starting at global row `row0` into `tile`.
+// Every wave issues INSTS/NWAVES loads (one 16-byte chunk per lane each).
+template <typename T, int D, int ROWS, int NWAVES>
+FBL_DEV void dma_tile(T* tile, Rsrc rs, int row0, uint32_t row_bytes, int wave, int lane) {
+    using G = TileGeom<T, D>;
+    constexpr int INSTS = ROWS * G::CPR / 64;
+    static_assert(INSTS % NWAVES == 0, "equal share of tile loads per wave");
+#pragma unroll
+    for (int j = 0; j < INSTS / NWAVES; ++j) {
+        const int i = j * NWAVES + wave;
+        const int q = i * 64 + lane;
+        const int r = q / G::CPR;
+        const int c = (q % G::CPR) ^ G::swz(r);
+        const uint32_t voff = (uint32_t)(row0 + r) * row_bytes + (uint32_t)c * 16u;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (FBL_LDS void*)(tile + i * 64 * G::EPC), 16, voff, 0, 0, 0);
+    }
+}
+
+template <typename T, int D, int ROWS, int NWAVES>
+constexpr int dma_loads_per_thread() {
+    return ROWS * TileGeom<T, D>::CPR / 64 / NWAVES;
+}
+
+// Wait until at most N vector-memory loads of this wave are outstanding.
+template <int N>
+FBL_DEV void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    // gfx9 s_waitcnt: vmcnt[3:0] | expcnt[6:4]=7 | lgkmcnt[11:8]=15 | vmcnt[5:4]<<14
+    __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
+// Row fragment (8 consecutive elements from column `col`, col % 8 == 0) of
+// row r of a staged tile.
+template <int D>
+FBL_DEV void tile_row_frag(Frag<bf16>& f, const bf16* tile, int r, int col) {
+    using G = TileGeom<bf16, D>;
+    f.v = *(const FBL_LDS bf16x8*)(tile + G::off(r, col));
+}
+template <int D>
+FBL_DEV void tile_row_frag(Frag<float>& f, const float* tile, int r, int col) {
+    using G = TileGeom<float, D>;
+    const f32x4 a = *(const FBL_LDS f32x4*)(tile + G::off(r, col));
+    const f32x4 b = *(const FBL_LDS f32x4*)(tile + G::off(r, col + 4));
+#pragma unroll
+    for (int e = 0; e < 4; ++e) { f.v[e] = a[e]; f.v[4 + e] = b[e]; }
+}
+
+// Transposed fragment: lane l gets column col0 + (l % 32) at rows
+// row0 + [0..3] (elements 0..3) and row1 + [0..3] (elements 4..7).
+// row0/row1 are multiples of 4 and uniform over each 16-lane group.
+template <int D>
+FBL_DEV void tile_tr_frag(Frag<bf16>& f, const bf16* tile, int row0, int row1, int col0, int lane) {
+    using G = TileGeom<bf16, D>;
+    const int t = lane & 15;
+    const int col = col0 + 16 * ((lane >> 4) & 1) + 4 * (t & 3);
+    const bf16* p0 = tile + G::off(row0 + (t >> 2), col);
+    const bf16* p1 = tile + G::off(row1 + (t >> 2), col);
+    const bf16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((FBL_LDS bf16x4*)p0);
+    const bf16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((FBL_LDS bf16x4*)p1);
+    f.v = bf16x8{a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+}
+template <int D>
+FBL_DEV void tile_tr_frag(Frag<float>& f, const float* tile, int row0, int row1, int col0, int lane) {
+    using G = TileGeom<float, D>;
+    const int col = col0 + (lane & 31);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        f.v[e] = tile[G::off(row0 + e, col)];
+        f.v[4 + e] = tile[G::off(row1 + e, col)];
+    }
+}
+
+// Map a linear workgroup id so that consecutive ids of the logical order land
+// on the same XCD (ids are dealt round-robin over the 8 XCDs, each with its own
+// L2): logical = (id % 8) * per_xcd + id / 8.  Returns -1 for padding ids.
+FBL_DEV int xcd_logical_id(int id, int total, int padded_total) {
+    const int per_xcd = padded_total / 8;
+    const int logical = (id % 8) * per_xcd + id / 8;
+    return logical < total ? logical : -1;
+}
+
+}  // namespace fbl

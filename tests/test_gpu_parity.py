@@ -219,3 +219,26 @@ def test_gradient_invariants_on_gpu_outputs():
             want = sum(inp["do"][b, :, h * d:(h + 1) * d].sum(axis=0) for h in range(g * G, (g + 1) * G))
             assert np.max(np.abs(dk.sum(axis=0))) <= 2e-2 * np.max(np.abs(dk)) * math.sqrt(w.S)
             assert np.max(np.abs(dv.sum(axis=0) - want)) <= 2e-2 * np.max(np.abs(want))
+
+
+@pytest.mark.parametrize("scale", [-0.3, 0.0, 2.5])
+def test_unusual_scales(scale):
+    """Negative, zero and large softmax scales (the API takes any finite scale)."""
+    import torch
+    fbl = _lib()
+    w = synth.Workload("scale", B=2, S=150, Hq=4, Hkv=2, d=64, dtype="bf16", mask=synth.MASK_CAUSAL, seed=12)
+    inp = synth.make_inputs(w)
+    note(f"scale={scale}")
+    q, k, v, do = (to_dev(inp[n], "bf16") for n in ("q", "k", "v", "do"))
+    o, lse = fbl.attn_fwd(q, k, v, w.Hq, w.Hkv, scale, True)
+    dq, dk, dv = fbl.attn_bwd(q, k, v, o, do, lse, w.Hq, w.Hkv, scale, True, None)
+    torch.cuda.synchronize()
+    ro, rl = oracle.attn_fwd(inp["q"], inp["k"], inp["v"], w.Hq, w.Hkv, scale, True)
+    rg = oracle.attn_bwd(inp["q"], inp["k"], inp["v"], inp["do"], w.Hq, w.Hkv, scale, True)
+    got = {"o": to_np(o), "lse": to_np(lse), "dq": to_np(dq), "dk": to_np(dk), "dv": to_np(dv)}
+    ref = {"o": ro, "lse": rl, "dq": rg[0], "dk": rg[1], "dv": rg[2]}
+    names = ("o", "lse", "dv") if scale == 0.0 else ("o", "lse", "dq", "dk", "dv")
+    errs, bad = compare(got, ref, "bf16", names)
+    assert not bad, bad
+    if scale == 0.0:
+        assert np.max(np.abs(got["dq"])) == 0.0 and np.max(np.abs(got["dk"])) == 0.0
