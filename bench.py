@@ -159,10 +159,10 @@ def main():
         bwd(fbl.FBL_BWD_PREP)
         if ev is not None:
             ev[2].record(stream)
-        bwd(fbl.FBL_BWD_MAIN)
+        bwd(fbl.FBL_BWD_KV)
         if ev is not None:
             ev[3].record(stream)
-        bwd(fbl.FBL_BWD_DQ)
+        bwd(fbl.FBL_BWD_Q)
         if ev is not None:
             ev[4].record(stream)
 

@@ -147,9 +147,9 @@ fbl_status fbl_attn_fwd(const fbl_layout* lq, const void* q, const fbl_layout* l
                         float scale, fbl_mask mask, void* stream);
 
 /*
- * Bytes of device workspace fbl_attn_bwd needs for these shapes: an fp32
- * dQ accumulator [B, S, Hq*D] and the fp32 row statistic
- * D_i = sum_k dO_ik O_ik, [B, Hq, S], 256-byte aligned sections.
+ * Bytes of device workspace fbl_attn_bwd needs for these shapes: one pair of
+ * fp32 per query row, [B, Hq, S] x (LSE * log2(e), D_i = sum_k dO_ik O_ik),
+ * rounded up to 256 bytes.
  */
 fbl_status fbl_attn_bwd_workspace(const fbl_layout* lq, const fbl_layout* lk, size_t* bytes);
 
@@ -157,12 +157,13 @@ fbl_status fbl_attn_bwd_workspace(const fbl_layout* lq, const fbl_layout* lk, si
  * Attention backward of L = sum(O * dO): writes dQ (Hq heads), dK and dV
  * (Hkv heads; each the sum over the query heads of its group).  The softmax
  * probabilities are recomputed from q, k and the saved lse; nothing of size
- * S x S is stored.  o and lse must be the forward's outputs for q, k, v.
+ * S x S is stored and no output is accumulated atomically, so the results
+ * are bitwise repeatable.  o and lse must be the forward's outputs for q, k, v.
  *   ws/ws_bytes  device workspace of at least fbl_attn_bwd_workspace bytes,
  *                256-byte aligned; its contents on entry do not matter.
  * Same checks as fbl_attn_fwd for the shared arguments, plus: ldo/ldq
  * extents equal lq's, ldk/ldv extents equal lk's, outputs do not overlap
- * inputs or the workspace.
+ * inputs, each other or the workspace.
  */
 fbl_status fbl_attn_bwd(const fbl_layout* lq, const void* q, const fbl_layout* lk, const void* k,
                         const fbl_layout* lv, const void* v, const fbl_layout* lo, const void* o,
@@ -174,16 +175,16 @@ fbl_status fbl_attn_bwd(const fbl_layout* lq, const void* q, const fbl_layout* l
  * The three launches of fbl_attn_bwd, selectable one by one (same arguments
  * and checks as fbl_attn_bwd; `phases` is an OR of the bits below, enqueued
  * in the order listed).  fbl_attn_bwd(...) equals
- * fbl_attn_bwd_phases(FBL_BWD_ALL, ...).  Running the phases as separate calls
- * on one stream gives the same result; a later phase reads what an earlier
- * one left in the workspace, so the same workspace must be passed to all.
- *   FBL_BWD_PREP  row statistic D_i = sum_k dO_ik O_ik and zeroed dQ accumulator
- *   FBL_BWD_MAIN  recompute P; dK, dV; dQ accumulated in fp32
- *   FBL_BWD_DQ    dQ = storage type of scale * accumulator
+ * fbl_attn_bwd_phases(FBL_BWD_ALL, ...).  FBL_BWD_KV and FBL_BWD_Q read what
+ * FBL_BWD_PREP left in the workspace, so the same workspace must be passed to
+ * all phases; KV and Q are independent of each other.
+ *   FBL_BWD_PREP  per query row: LSE * log2(e) and D_i = sum_k dO_ik O_ik
+ *   FBL_BWD_KV    key/value-major pass: recompute P, write dK and dV
+ *   FBL_BWD_Q     query-major pass: recompute P and dP, write dQ
  */
 #define FBL_BWD_PREP 1u
-#define FBL_BWD_MAIN 2u
-#define FBL_BWD_DQ 4u
+#define FBL_BWD_KV 2u
+#define FBL_BWD_Q 4u
 #define FBL_BWD_ALL 7u
 fbl_status fbl_attn_bwd_phases(uint32_t phases, const fbl_layout* lq, const void* q, const fbl_layout* lk,
                                const void* k, const fbl_layout* lv, const void* v, const fbl_layout* lo,

@@ -126,18 +126,9 @@ hipError_t dispatch_bwd(int D, const fbl::BwdArgs& a, unsigned phases, hipStream
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-struct WsLayout {
-    size_t dq_acc, drow, total;
-};
-
-WsLayout ws_layout(const fbl_layout* lq) {
-    WsLayout w;
-    w.dq_acc = 0;
-    const size_t n_dq = (size_t)lq->B * lq->S * lq->H * lq->D * sizeof(float);
-    w.drow = align256(n_dq);
-    const size_t n_dr = (size_t)lq->B * lq->H * lq->S * sizeof(float);
-    w.total = align256(w.drow + n_dr);
-    return w;
+// Workspace: the per-query-row statistics (LSE * log2(e), D) as float pairs.
+size_t ws_bytes_for(const fbl_layout* lq) {
+    return align256((size_t)lq->B * lq->H * lq->S * 2 * sizeof(float));
 }
 
 }  // namespace
@@ -246,7 +237,7 @@ fbl_status fbl_attn_bwd_workspace(const fbl_layout* lq, const fbl_layout* lk, si
     fbl_status st;
     if ((st = check_layout(lq)) != FBL_OK) return st;
     if ((st = check_layout(lk)) != FBL_OK) return st;
-    *bytes = ws_layout(lq).total;
+    *bytes = ws_bytes_for(lq);
     return FBL_OK;
 }
 
@@ -269,8 +260,7 @@ fbl_status fbl_attn_bwd_phases(uint32_t phases, const fbl_layout* lq, const void
     if (!aligned16(o) || !aligned16(dO) || !aligned16(lse) || !aligned16(dq) || !aligned16(dk) || !aligned16(dv))
         return FBL_ERR_ALIGN;
     if (!ws) return FBL_ERR_WORKSPACE;
-    const WsLayout w = ws_layout(lq);
-    if (ws_bytes < w.total) return FBL_ERR_WORKSPACE;
+    if (ws_bytes < ws_bytes_for(lq)) return FBL_ERR_WORKSPACE;
     if ((reinterpret_cast<uintptr_t>(ws) & 255u) != 0) return FBL_ERR_ALIGN;
 
     const int64_t lse_bytes = lq->B * lq->H * lq->S * 4;
@@ -297,8 +287,7 @@ fbl_status fbl_attn_bwd_phases(uint32_t phases, const fbl_layout* lq, const void
     a.dq = dq;
     a.dk = dk;
     a.dv = dv;
-    a.dq_acc = reinterpret_cast<float*>(static_cast<unsigned char*>(ws) + w.dq_acc);
-    a.drow = reinterpret_cast<float*>(static_cast<unsigned char*>(ws) + w.drow);
+    a.stats = static_cast<fbl::f32x2*>(ws);
     a.mq = tokmap(lq);
     a.mk = tokmap(lk);
     a.mv = tokmap(lv);

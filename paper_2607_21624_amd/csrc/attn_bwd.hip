@@ -1,92 +1,54 @@
 // attn_bwd.hip -- attention backward on token-major tensors, gfx950.
 //
-// Gradients of L = sum(O * dO) (chain rule through P = softmax(scale Q K^T)
-// and O = P V; the paper gives the matrix-product gradients in section 4.1
-// and softmax as forward-dependent, consistent-access in the same section):
-//   D_i  = sum_k dO_ik O_ik                         (bwd_pre)
-//   P    = exp(scale q_i.k_j - LSE_i)               (recomputed, bwd_main)
-//   dV  += P^T dO,  dP = dO V^T,  dS = P (dP - D)
-//   dK  += scale dS^T Q,  dQ += scale dS K          (bwd_main, dQ via fp32
-//                                                    atomics into a workspace)
-//   dQ   = storage type of the fp32 accumulator     (bwd_dq)
-//
-// Key/value-major main pass: one workgroup owns 128 keys of one (batch,
-// key/value head); each of its 4 wavefronts owns 32 keys and keeps them (K and
-// V rows) in registers, together with its dK and dV accumulators.  It walks
-// every query block of every query head of its GQA group, so the reductions
-// over queries that build dK/dV (the "reduce along M" direction of section
-// 4.2) and the group reduction over the G query heads both stay in registers.
-// Q and dO tiles are staged once per block in LDS and serve both reduction
-// directions (tile invariance, section 4.2): row reads for S = Q K^T and
-// dP = dO V^T (contraction over d), transposed reads (ds_read_b64_tr_b16) for
-// dV and dK (contraction over queries).  dS goes through LDS once so the dQ
-// product (contraction over keys) can be split over the 4 wavefronts by
-// output tile.
+// Gradients of L = sum(O * dO) by the chain rule through P = softmax(scale
+// Q K^T) and O = P V (the paper states the matrix-product gradients in
+// section 4.1, FTD-D, and classes softmax as forward-dependent with
+// consistent access, FTD-C):
+//   D_i  = sum_k dO_ik O_ik
+//   P    = exp(scale q_i.k_j - LSE_i)          (recomputed from the saved LSE)
+//   dP   = dO V^T,  dS = P (dP - D)
+//   dV   = P^T dO,  dK = scale dS^T Q,  dQ = scale dS K
+// Three launches, no atomics, every output written once:
+//   attn_bwd_stats  per query row: LSE*log2(e) (+inf for an empty row) and D.
+//   attn_bwd_kv     key/value-major.  A workgroup owns 128 keys of one
+//                   (batch, kv head); each wavefront keeps its 32 K and V rows
+//                   and its dK^T, dV^T accumulators in registers and walks the
+//                   query blocks of every query head of its GQA group.  The
+//                   reductions over queries that build dK/dV (the "reduce
+//                   along M" direction of section 4.2) and the group sum over
+//                   the G query heads never leave registers.
+//   attn_bwd_q      query-major.  A workgroup owns 128 queries of one
+//                   (batch, query head) and walks the key tiles, recomputing S
+//                   and dP, and accumulates dQ^T in registers (the "reduce
+//                   along N" direction).
+// Recomputing S and dP in the query-major pass costs two extra products per
+// (query, key) pair; it replaces fp32 atomics, which run at ~1.3 TB/s on this
+// part -- far slower than the 3 products they would save at these shapes.
+// Q/dO (kv pass) and K/V (q pass) tiles are staged once per block in LDS by
+// DMA and serve both reduction directions (tile invariance, section 4.2): row
+// reads where the contraction runs along d, transposed reads
+// (ds_read_b64_tr_b16) where it runs along tokens.
 #include "cdna4.hpp"
 #include "kernels.hpp"
+#include "stage.hpp"
 #include "tokmap.hpp"
 
 namespace fbl {
 
 namespace {
 
-constexpr int kBwdWaves = 4;
-constexpr int kBwdBN = 32 * kBwdWaves;  // keys per workgroup
+constexpr int kWaves = 4;
+constexpr int kKvBN = 32 * kWaves;  // keys per kv-pass workgroup
+constexpr int kKvBQ = 64;           // queries per kv-pass block
+constexpr int kQBM = 32 * kWaves;   // queries per q-pass workgroup
+constexpr int kQBN = 64;            // keys per q-pass tile
 
-template <typename T, int D>
-struct BwdTile {
-    static constexpr int BQ = 4096 / D;  // queries per block: 128, 64, 32 for D = 32, 64, 128
-    static constexpr int NQT = BQ / 32;
-    static constexpr int EPC = 16 / (int)sizeof(T);     // elements per 16-byte chunk
-    static constexpr int PITCH = D + EPC;               // Q, dO, K tile row pitch (elements)
-    static constexpr int SPITCH = BQ + EPC;             // dS^T tile row pitch (elements)
-    static constexpr int CPR = D / EPC;                 // 16-byte chunks per row
-    static constexpr int OFF_Q = 0;
-    static constexpr int OFF_DO = OFF_Q + BQ * PITCH * (int)sizeof(T);
-    static constexpr int OFF_K = OFF_DO + BQ * PITCH * (int)sizeof(T);
-    static constexpr int OFF_DS = OFF_K + kBwdBN * PITCH * (int)sizeof(T);
-    static constexpr int OFF_LSE = OFF_DS + kBwdBN * SPITCH * (int)sizeof(T);
-    static constexpr int OFF_DR = OFF_LSE + BQ * 4;
-    static constexpr int BYTES = OFF_DR + BQ * 4;
-    static_assert(NQT * (D / 32) == kBwdWaves, "one dQ output tile per wavefront");
-    static_assert(BYTES <= 160 * 1024, "LDS budget");
-};
-
-template <typename T, int D>
-__device__ __forceinline__ void stage_tile(T* dst, const T* src, int64_t ss, int row0, int nrows, int nvalid) {
-    using TL = BwdTile<T, D>;
-    for (int i = threadIdx.x; i < nrows * TL::CPR; i += kBwdWaves * 64) {
-        const int r = i / TL::CPR, cc = i % TL::CPR;
-        uint4 x = {0u, 0u, 0u, 0u};
-        if (r < nvalid) x = load16(src + (int64_t)(row0 + r) * ss + cc * TL::EPC);
-        *reinterpret_cast<uint4*>(dst + r * TL::PITCH + cc * TL::EPC) = x;
-    }
-}
-
-// Register fragment of one row (8 elements at column 16c + 8g).
-template <typename T>
-__device__ __forceinline__ void global_row_frag(Frag<T>& f, const T* p, bool valid) {
-    if (!valid) {
-        float z[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-        pack_frag(f, z);
-        return;
-    }
-    if constexpr (sizeof(T) == 2) {
-        f.v = __builtin_bit_cast(bf16x8, load16(p));
-    } else {
-        f32x4 a = __builtin_bit_cast(f32x4, load16(p));
-        f32x4 b = __builtin_bit_cast(f32x4, load16(p + 4));
-#pragma unroll
-        for (int e = 0; e < 4; ++e) { f.v[e] = a[e]; f.v[4 + e] = b[e]; }
-    }
-}
-
-// D_i = sum_k dO_ik O_ik per (b, h, i) and zeroing of the dQ accumulator.
+// ------------------------------------------------------------------ stats
 // Each (b, s, h) row of d elements is read by D*sizeof(T)/16 lanes (one
 // 16-byte chunk each); consecutive rows are consecutive heads of one token,
-// so a wavefront reads a contiguous run of the token-major tensor.
+// so a wavefront reads a contiguous run of the token-major tensors.
 template <typename T, int D>
-__global__ __launch_bounds__(256) void attn_bwd_pre(BwdArgs a) {
+__global__ __launch_bounds__(256) void attn_bwd_stats(BwdArgs a) {
     constexpr int EPC = 16 / (int)sizeof(T);
     constexpr int LPR = D / EPC;
     constexpr int RPB = 256 / LPR;
@@ -101,57 +63,66 @@ __global__ __launch_bounds__(256) void attn_bwd_pre(BwdArgs a) {
         b = (int)(row / ((int64_t)a.Hq * a.S));
         const T* o = static_cast<const T*>(a.o) + a.mo.offset(b, h, s, part * EPC);
         const T* g = static_cast<const T*>(a.dout) + a.mdo.offset(b, h, s, part * EPC);
-        uint4 xo = load16(o), xg = load16(g);
+        const uint4 xo = load16(o), xg = load16(g);
         if constexpr (sizeof(T) == 2) {
-            bf16x8 vo = __builtin_bit_cast(bf16x8, xo), vg = __builtin_bit_cast(bf16x8, xg);
+            const bf16x8 vo = __builtin_bit_cast(bf16x8, xo), vg = __builtin_bit_cast(bf16x8, xg);
 #pragma unroll
             for (int e = 0; e < 8; ++e) acc += (float)vo[e] * (float)vg[e];
         } else {
-            f32x4 vo = __builtin_bit_cast(f32x4, xo), vg = __builtin_bit_cast(f32x4, xg);
+            const f32x4 vo = __builtin_bit_cast(f32x4, xo), vg = __builtin_bit_cast(f32x4, xg);
 #pragma unroll
             for (int e = 0; e < 4; ++e) acc += vo[e] * vg[e];
         }
-        float* z = a.dq_acc + row * D + part * EPC;
-#pragma unroll
-        for (int e = 0; e < EPC; e += 4) *reinterpret_cast<f32x4*>(z + e) = f32x4{0.f, 0.f, 0.f, 0.f};
     }
 #pragma unroll
     for (int off = LPR / 2; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
-    if (row < nrows && part == 0) a.drow[((int64_t)b * a.Hq + h) * a.S + s] = acc;
+    if (row < nrows && part == 0) {
+        const int64_t i = ((int64_t)b * a.Hq + h) * a.S + s;
+        const float lse = a.lse[i];
+        a.stats[i] = f32x2{lse == -INFINITY ? INFINITY : lse * kLog2e, acc};
+    }
 }
 
+// ------------------------------------------------------------- kv pass
 template <typename T, int D>
-__global__ __launch_bounds__(256) void attn_bwd_main(BwdArgs a) {
-    using TL = BwdTile<T, D>;
+struct KvSmem {
+    static constexpr int TILE = kKvBQ * D;  // elements of one Q or dO tile
+    // [Q0 Q1 dO0 dO1] tiles, then two 1 KB stats buffers (64 (lse2, D) pairs
+    // plus room for the full 64-lane DMA of one instruction)
+    static constexpr int BYTES = 4 * TILE * (int)sizeof(T) + 2 * 1024;
+};
+
+template <typename T, int D>
+__global__ __launch_bounds__(256, 1) void attn_bwd_kv(BwdArgs a) {
+    using SM = KvSmem<T, D>;
     constexpr int NC = D / 16;
     constexpr int ND = D / 32;
-    constexpr int BQ = TL::BQ;
-    constexpr int NQT = TL::NQT;
-    constexpr int PITCH = TL::PITCH;
-    constexpr int SPITCH = TL::SPITCH;
-    extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
-    T* sQ = reinterpret_cast<T*>(smem + TL::OFF_Q);
-    T* sdO = reinterpret_cast<T*>(smem + TL::OFF_DO);
-    T* sK = reinterpret_cast<T*>(smem + TL::OFF_K);
-    T* sdS = reinterpret_cast<T*>(smem + TL::OFF_DS);
-    float* sLse = reinterpret_cast<float*>(smem + TL::OFF_LSE);
-    float* sDr = reinterpret_cast<float*>(smem + TL::OFF_DR);
+    constexpr int TILE = SM::TILE;
+    constexpr int NQT = kKvBQ / 32;
+    extern __shared__ __attribute__((aligned(1024))) unsigned char kv_smem[];
+    T* tiles = reinterpret_cast<T*>(kv_smem);
+    float* stat_buf = reinterpret_cast<float*>(kv_smem + 4 * TILE * sizeof(T));
 
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
     const int g = lane >> 5;
     const int c32 = lane & 31;
     const int S = a.S;
-    const int k0 = blockIdx.x * kBwdBN;
-    const int hk = blockIdx.y;
-    const int b = blockIdx.z;
-    const int G = a.Hq / a.Hkv;
+    const int nkb = (S + kKvBN - 1) / kKvBN;
+    const int logical = xcd_logical_id(blockIdx.x, nkb * a.Hkv * a.B, gridDim.x);
+    if (logical < 0) return;
+    const int kblk = logical % nkb;
+    const int hk = (logical / nkb) % a.Hkv;
+    const int b = logical / (nkb * a.Hkv);
+    const int G_ = a.Hq / a.Hkv;
     int kv_end = S;
     if (a.mask.kv_len) kv_end = min(max(a.mask.kv_len[b], 0), S);
+    const int k0 = kblk * kKvBN;
     const int kw0 = k0 + wave * 32;  // first key of this wave
     const int key = kw0 + c32;       // this lane's key (column of S)
     const bool key_ok = key < kv_end;
 
+    const uint32_t es = sizeof(T);
     const T* kbase = static_cast<const T*>(a.k) + a.mk.head_base(b, hk);
     const T* vbase = static_cast<const T*>(a.v) + a.mv.head_base(b, hk);
 
@@ -159,182 +130,327 @@ __global__ __launch_bounds__(256) void attn_bwd_main(BwdArgs a) {
     Frag<T> kf[NC], vf[NC];
 #pragma unroll
     for (int c = 0; c < NC; ++c) {
-        global_row_frag(kf[c], kbase + (int64_t)key * a.mk.ss + 16 * c + 8 * g, key < S);
-        global_row_frag(vf[c], vbase + (int64_t)key * a.mv.ss + 16 * c + 8 * g, key < S);
+        float z[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+        pack_frag(kf[c], z);
+        pack_frag(vf[c], z);
+        if (key < S) {
+            const T* kp = kbase + (int64_t)key * a.mk.ss + 16 * c + 8 * g;
+            const T* vp = vbase + (int64_t)key * a.mv.ss + 16 * c + 8 * g;
+            if constexpr (sizeof(T) == 2) {
+                kf[c].v = __builtin_bit_cast(bf16x8, load16(kp));
+                vf[c].v = __builtin_bit_cast(bf16x8, load16(vp));
+            } else {
+                const f32x4 k0v = __builtin_bit_cast(f32x4, load16(kp)), k1v = __builtin_bit_cast(f32x4, load16(kp + 4));
+                const f32x4 v0v = __builtin_bit_cast(f32x4, load16(vp)), v1v = __builtin_bit_cast(f32x4, load16(vp + 4));
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    kf[c].v[e] = k0v[e];
+                    kf[c].v[4 + e] = k1v[e];
+                    vf[c].v[e] = v0v[e];
+                    vf[c].v[4 + e] = v1v[e];
+                }
+            }
+        }
     }
-    stage_tile<T, D>(sK, kbase, a.mk.ss, k0, kBwdBN, min(kBwdBN, S - k0));
 
+    // dK^T and dV^T: accumulator rows = d (32t + acc_row), columns = keys (lane)
     f32x16 dk[ND], dv[ND];
 #pragma unroll
-    for (int t = 0; t < ND; ++t) { dk[t] = f32x16{}; dv[t] = f32x16{}; }
-
-    if (k0 < kv_end) {
-        const int qb_start = a.mask.causal ? k0 / BQ : 0;
-        const int nqb = (S + BQ - 1) / BQ;
-        for (int hh = 0; hh < G; ++hh) {
-            const int h = hk * G + hh;
-            const T* qbase = static_cast<const T*>(a.q) + a.mq.head_base(b, h);
-            const T* dobase = static_cast<const T*>(a.dout) + a.mdo.head_base(b, h);
-            const float* lse_row = a.lse + ((int64_t)b * a.Hq + h) * S;
-            const float* dr_row = a.drow + ((int64_t)b * a.Hq + h) * S;
-            for (int qb = qb_start; qb < nqb; ++qb) {
-                const int q0 = qb * BQ;
-                const int nvalid = min(BQ, S - q0);
-                __syncthreads();
-                stage_tile<T, D>(sQ, qbase, a.mq.ss, q0, BQ, nvalid);
-                stage_tile<T, D>(sdO, dobase, a.mdo.ss, q0, BQ, nvalid);
-                for (int i = threadIdx.x; i < BQ; i += kBwdWaves * 64) {
-                    float lse = -INFINITY, dr = 0.f;
-                    if (i < nvalid) { lse = lse_row[q0 + i]; dr = dr_row[q0 + i]; }
-                    sLse[i] = (lse == -INFINITY) ? INFINITY : lse * kLog2e;
-                    sDr[i] = dr;
-                }
-                __syncthreads();
-
-                // S = Q K_w^T and dP = dO V_w^T; accumulators: lane <-> key,
-                // in-lane query q0 + 32qt + acc_row(r, g)
-                f32x16 s[NQT], dp[NQT];
-#pragma unroll
-                for (int qt = 0; qt < NQT; ++qt) {
-                    s[qt] = f32x16{};
-                    dp[qt] = f32x16{};
-#pragma unroll
-                    for (int c = 0; c < NC; ++c) {
-                        Frag<T> fq, fo;
-                        lds_row_frag(fq, sQ + (qt * 32 + c32) * PITCH + 16 * c + 8 * g);
-                        lds_row_frag(fo, sdO + (qt * 32 + c32) * PITCH + 16 * c + 8 * g);
-                        mma(s[qt], fq, kf[c]);
-                        mma(dp[qt], fo, vf[c]);
-                    }
-                }
-                // P and dS in place (s <- P, dp <- dS)
-#pragma unroll
-                for (int qt = 0; qt < NQT; ++qt) {
-#pragma unroll
-                    for (int rr = 0; rr < 4; ++rr) {
-                        const int qloc = qt * 32 + 8 * rr + 4 * g;
-                        const f32x4 l4 = *reinterpret_cast<const f32x4*>(sLse + qloc);
-                        const f32x4 d4 = *reinterpret_cast<const f32x4*>(sDr + qloc);
-#pragma unroll
-                        for (int j = 0; j < 4; ++j) {
-                            const int r = 4 * rr + j;
-                            const int qi = q0 + qloc + j;
-                            const bool ok = key_ok && (!a.mask.causal || key <= qi);
-                            const float p = ok ? fast_exp2(s[qt][r] * a.scale_log2 - l4[j]) : 0.f;
-                            s[qt][r] = p;
-                            dp[qt][r] = p * (dp[qt][r] - d4[j]);
-                        }
-                    }
-                }
-                // dV_w += P^T dO and dK_w += dS^T Q, contracting over queries:
-                // chunk (qt, cc) covers queries 32qt + 16cc + {4g..4g+3, 8+4g..8+4g+3}
-#pragma unroll
-                for (int qt = 0; qt < NQT; ++qt) {
-#pragma unroll
-                    for (int cc = 0; cc < 2; ++cc) {
-                        Frag<T> pa, dsa;
-                        float pv[8], dsv[8];
-#pragma unroll
-                        for (int e = 0; e < 8; ++e) { pv[e] = s[qt][8 * cc + e]; dsv[e] = dp[qt][8 * cc + e]; }
-                        pack_frag(pa, pv);
-                        pack_frag(dsa, dsv);
-                        const int row0 = qt * 32 + 16 * cc + 4 * g;
-#pragma unroll
-                        for (int t = 0; t < ND; ++t) {
-                            Frag<T> fdo, fq;
-                            lds_tr_frag(fdo, sdO, PITCH, row0, row0 + 8, 32 * t, lane);
-                            lds_tr_frag(fq, sQ, PITCH, row0, row0 + 8, 32 * t, lane);
-                            mma(dv[t], pa, fdo);
-                            mma(dk[t], dsa, fq);
-                        }
-                    }
-                }
-                // dS^T (storage type) into LDS: row = key, columns = queries
-                T* dsrow = sdS + (wave * 32 + c32) * SPITCH;
-#pragma unroll
-                for (int qt = 0; qt < NQT; ++qt) {
-#pragma unroll
-                    for (int rr = 0; rr < 4; ++rr) {
-                        store4(dsrow + qt * 32 + 8 * rr + 4 * g, dp[qt][4 * rr], dp[qt][4 * rr + 1],
-                               dp[qt][4 * rr + 2], dp[qt][4 * rr + 3]);
-                    }
-                }
-                __syncthreads();
-                // dQ tile (qt, t) of this wavefront: dS[q, 0:128] K[0:128, 32t:32t+32]
-                {
-                    const int qt = wave / ND, t = wave % ND;
-                    f32x16 acc = f32x16{};
-#pragma unroll
-                    for (int ch = 0; ch < kBwdBN / 16; ++ch) {
-                        const int row0 = 16 * ch + 8 * g;
-                        Frag<T> fa, fb;
-                        lds_tr_frag(fa, sdS, SPITCH, row0, row0 + 4, 32 * qt, lane);
-                        lds_tr_frag(fb, sK, PITCH, row0, row0 + 4, 32 * t, lane);
-                        mma(acc, fa, fb);
-                    }
-                    float* dq_col = a.dq_acc + (int64_t)h * D + 32 * t + c32;
-#pragma unroll
-                    for (int r = 0; r < 16; ++r) {
-                        const int qi = q0 + qt * 32 + acc_row(r, g);
-                        if (qi < S) atomicAdd(dq_col + ((int64_t)b * S + qi) * ((int64_t)a.Hq * D), acc[r]);
-                    }
-                }
-            }
-        }
-    }
-
-    // dK (times scale) and dV rows of this wave's keys; lane <-> d column
-    T* dkbase = static_cast<T*>(a.dk) + a.mdk.head_base(b, hk);
-    T* dvbase = static_cast<T*>(a.dv) + a.mdv.head_base(b, hk);
-#pragma unroll
     for (int t = 0; t < ND; ++t) {
+        dk[t] = f32x16{};
+        dv[t] = f32x16{};
+    }
+
+    const int qb_start = a.mask.causal ? (k0 / kKvBQ) : 0;
+    const int nqb = (S + kKvBQ - 1) / kKvBQ;
+    const int per_head = nqb - qb_start;
+    const int n_iter = (k0 < kv_end) ? G_ * per_head : 0;
+
+    auto issue = [&](int it, int buf) {
+        const int h = hk * G_ + it / per_head;
+        const int q0 = (qb_start + it % per_head) * kKvBQ;
+        const Rsrc rq = make_rsrc(static_cast<const T*>(a.q) + a.mq.head_base(b, h),
+                                  (uint32_t)((int64_t)(S - 1) * a.mq.ss * es + D * es));
+        const Rsrc ro = make_rsrc(static_cast<const T*>(a.dout) + a.mdo.head_base(b, h),
+                                  (uint32_t)((int64_t)(S - 1) * a.mdo.ss * es + D * es));
+        dma_tile<T, D, kKvBQ, kWaves>(tiles + buf * TILE, rq, q0, (uint32_t)(a.mq.ss * es), wave, lane);
+        dma_tile<T, D, kKvBQ, kWaves>(tiles + (2 + buf) * TILE, ro, q0, (uint32_t)(a.mdo.ss * es), wave, lane);
+        if (wave == 0) {
+            // 64 (lse2, D) pairs = 512 bytes; lanes 32..63 fetch the following
+            // rows (zeros past the end) into the spare half of the buffer
+            const Rsrc rs = make_rsrc(a.stats + ((int64_t)b * a.Hq + h) * S, (uint32_t)(S * 8));
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (FBL_LDS void*)(stat_buf + buf * 256), 16,
+                                                     (uint32_t)(q0 * 8 + lane * 16), 0, 0, 0);
+        }
+    };
+
+    if (n_iter > 0) issue(0, 0);
+    for (int it = 0; it < n_iter; ++it) {
+        const int buf = it & 1;
+        wait_vmcnt<0>();
+        __syncthreads();  // block `it` landed; block it-1's buffers are free
+        if (it + 1 < n_iter) issue(it + 1, buf ^ 1);
+        const int q0 = (qb_start + it % per_head) * kKvBQ;
+        // nothing to do for a wave whose keys are all padding, or all after
+        // every query of the block
+        if (kw0 >= kv_end) continue;
+        if (a.mask.causal && q0 + kKvBQ - 1 < kw0) continue;
+        const T* sQ = tiles + buf * TILE;
+        const T* sdO = tiles + (2 + buf) * TILE;
+        const f32x2* st = reinterpret_cast<const f32x2*>(stat_buf + buf * 256);
+
+        // S = Q K_w^T and dP = dO V_w^T: lane <-> key, in-lane query 32qt + acc_row
+        f32x16 s[NQT], dp[NQT];
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            const int kk = kw0 + acc_row(r, g);
-            if (kk < S) {
-                store_out<T>(dkbase + (int64_t)kk * a.mdk.ss + 32 * t + c32, dk[t][r] * a.scale);
-                store_out<T>(dvbase + (int64_t)kk * a.mdv.ss + 32 * t + c32, dv[t][r]);
+        for (int qt = 0; qt < NQT; ++qt) {
+            s[qt] = f32x16{};
+            dp[qt] = f32x16{};
+#pragma unroll
+            for (int c = 0; c < NC; ++c) {
+                Frag<T> fq, fo;
+                tile_row_frag<D>(fq, sQ, qt * 32 + c32, 16 * c + 8 * g);
+                tile_row_frag<D>(fo, sdO, qt * 32 + c32, 16 * c + 8 * g);
+                mma(s[qt], fq, kf[c]);
+                mma(dp[qt], fo, vf[c]);
+            }
+        }
+        const bool diag = a.mask.causal && q0 < kw0 + 31;
+#pragma unroll
+        for (int qt = 0; qt < NQT; ++qt) {
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int ql = qt * 32 + acc_row(r, g);
+                const f32x2 sd = st[ql];
+                float p = fast_exp2(__builtin_fmaf(s[qt][r], a.scale_log2, -sd[0]));
+                if (!key_ok || (diag && key > q0 + ql)) p = 0.f;
+                s[qt][r] = p;
+                dp[qt][r] = p * (dp[qt][r] - sd[1]);
+            }
+        }
+        // dV^T += dO^T P and dK^T += Q^T dS, contracting over the 64 queries:
+        // chunk (qt, cc) covers queries 32qt + 16cc + {4g..4g+3, 8+4g..8+4g+3}
+#pragma unroll
+        for (int qt = 0; qt < NQT; ++qt) {
+#pragma unroll
+            for (int cc = 0; cc < 2; ++cc) {
+                Frag<T> pb, dsb;
+                float pv[8], dsv[8];
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    pv[e] = s[qt][8 * cc + e];
+                    dsv[e] = dp[qt][8 * cc + e];
+                }
+                pack_frag(pb, pv);
+                pack_frag(dsb, dsv);
+                const int row0 = qt * 32 + 16 * cc + 4 * g;
+#pragma unroll
+                for (int t = 0; t < ND; ++t) {
+                    Frag<T> fdo, fq;
+                    tile_tr_frag<D>(fdo, sdO, row0, row0 + 8, 32 * t, lane);
+                    tile_tr_frag<D>(fq, sQ, row0, row0 + 8, 32 * t, lane);
+                    mma(dv[t], fdo, pb);
+                    mma(dk[t], fq, dsb);
+                }
+            }
+        }
+    }
+
+    // dK (times scale) and dV rows of this wave's keys: lane <-> key, 4 consecutive d per store
+    if (key < S) {
+        T* dkrow = static_cast<T*>(a.dk) + a.mdk.head_base(b, hk) + (int64_t)key * a.mdk.ss;
+        T* dvrow = static_cast<T*>(a.dv) + a.mdv.head_base(b, hk) + (int64_t)key * a.mdv.ss;
+#pragma unroll
+        for (int t = 0; t < ND; ++t) {
+#pragma unroll
+            for (int rr = 0; rr < 4; ++rr) {
+                const int dcol = 32 * t + 8 * rr + 4 * g;
+                store4(dkrow + dcol, dk[t][4 * rr] * a.scale, dk[t][4 * rr + 1] * a.scale, dk[t][4 * rr + 2] * a.scale,
+                       dk[t][4 * rr + 3] * a.scale);
+                store4(dvrow + dcol, dv[t][4 * rr], dv[t][4 * rr + 1], dv[t][4 * rr + 2], dv[t][4 * rr + 3]);
             }
         }
     }
 }
 
-// dQ = scale * accumulator, converted to the storage type, written through
-// dQ's own index map.
+// --------------------------------------------------------------- q pass
 template <typename T, int D>
-__global__ __launch_bounds__(256) void attn_bwd_dq(BwdArgs a) {
-    constexpr int EPC = 16 / (int)sizeof(T);
-    constexpr int LPR = D / EPC;
-    constexpr int RPB = 256 / LPR;
-    const int64_t nrows = (int64_t)a.B * a.S * a.Hq;
-    const int64_t row = (int64_t)blockIdx.x * RPB + threadIdx.x / LPR;
-    const int part = threadIdx.x % LPR;
-    if (row >= nrows) return;
-    const int h = (int)(row % a.Hq);
-    const int s = (int)((row / a.Hq) % a.S);
-    const int b = (int)(row / ((int64_t)a.Hq * a.S));
-    const float* src = a.dq_acc + row * D + part * EPC;
-    T* dst = static_cast<T*>(a.dq) + a.mdq.offset(b, h, s, part * EPC);
-    if constexpr (sizeof(T) == 2) {
-        f32x4 x0 = *reinterpret_cast<const f32x4*>(src);
-        f32x4 x1 = *reinterpret_cast<const f32x4*>(src + 4);
-        bf16x8 y;
+struct QSmem {
+    static constexpr int TILE = kQBN * D;
+    static constexpr int BYTES = 4 * TILE * (int)sizeof(T);  // K0 K1 V0 V1
+};
+
+template <typename T, int D>
+__global__ __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) void attn_bwd_q(BwdArgs a) {
+    constexpr int NC = D / 16;
+    constexpr int ND = D / 32;
+    constexpr int TILE = QSmem<T, D>::TILE;
+    extern __shared__ __attribute__((aligned(1024))) unsigned char q_smem[];
+    T* smem = reinterpret_cast<T*>(q_smem);
+
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const int g = lane >> 5;
+    const int c32 = lane & 31;
+    const int S = a.S;
+    const int nqb = (S + kQBM - 1) / kQBM;
+    const int logical = xcd_logical_id(blockIdx.x, nqb * a.Hq * a.B, gridDim.x);
+    if (logical < 0) return;
+    const int rank = logical % nqb;
+    const int h = (logical / nqb) % a.Hq;
+    const int b = logical / (nqb * a.Hq);
+    const int qb = a.mask.causal ? (nqb - 1 - rank) : rank;
+    const int hk = h / (a.Hq / a.Hkv);
+    int kv_end = S;
+    if (a.mask.kv_len) kv_end = min(max(a.mask.kv_len[b], 0), S);
+    const int q0 = qb * kQBM;
+    const int qw0 = q0 + wave * 32;
+    const int qi = qw0 + c32;  // this lane's query (column of S^T)
+    int k_hi = kv_end;
+    if (a.mask.causal) k_hi = min(k_hi, q0 + kQBM);
+    const int nkb = (k_hi + kQBN - 1) / kQBN;
+
+    // Q^T and dO^T as B operands: lane <-> query, in-lane d = 16c + 8g + e
+    Frag<T> qf[NC], of[NC];
+    {
+        const T* qrow = static_cast<const T*>(a.q) + a.mq.head_base(b, h) + (int64_t)qi * a.mq.ss;
+        const T* orow = static_cast<const T*>(a.dout) + a.mdo.head_base(b, h) + (int64_t)qi * a.mdo.ss;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) { y[e] = (bf16)(x0[e] * a.scale); y[4 + e] = (bf16)(x1[e] * a.scale); }
-        *reinterpret_cast<bf16x8*>(dst) = y;
-    } else {
-        f32x4 x = *reinterpret_cast<const f32x4*>(src);
-        *reinterpret_cast<f32x4*>(dst) = x * a.scale;
+        for (int c = 0; c < NC; ++c) {
+            float z[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+            pack_frag(qf[c], z);
+            pack_frag(of[c], z);
+            if (qi < S) {
+                if constexpr (sizeof(T) == 2) {
+                    qf[c].v = __builtin_bit_cast(bf16x8, load16(qrow + 16 * c + 8 * g));
+                    of[c].v = __builtin_bit_cast(bf16x8, load16(orow + 16 * c + 8 * g));
+                } else {
+                    const f32x4 q0v = __builtin_bit_cast(f32x4, load16(qrow + 16 * c + 8 * g));
+                    const f32x4 q1v = __builtin_bit_cast(f32x4, load16(qrow + 16 * c + 8 * g + 4));
+                    const f32x4 o0v = __builtin_bit_cast(f32x4, load16(orow + 16 * c + 8 * g));
+                    const f32x4 o1v = __builtin_bit_cast(f32x4, load16(orow + 16 * c + 8 * g + 4));
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        qf[c].v[e] = q0v[e];
+                        qf[c].v[4 + e] = q1v[e];
+                        of[c].v[e] = o0v[e];
+                        of[c].v[4 + e] = o1v[e];
+                    }
+                }
+            }
+        }
+    }
+    f32x2 sd = f32x2{INFINITY, 0.f};  // (lse2, D) of this lane's query
+    if (qi < S) sd = a.stats[((int64_t)b * a.Hq + h) * S + qi];
+
+    f32x16 dq[ND];  // dQ^T: rows = d (32t + acc_row), columns = queries (lane)
+#pragma unroll
+    for (int t = 0; t < ND; ++t) dq[t] = f32x16{};
+
+    const uint32_t es = sizeof(T);
+    const Rsrc rk = make_rsrc(static_cast<const T*>(a.k) + a.mk.head_base(b, hk),
+                              (uint32_t)((int64_t)(S - 1) * a.mk.ss * es + D * es));
+    const Rsrc rv = make_rsrc(static_cast<const T*>(a.v) + a.mv.head_base(b, hk),
+                              (uint32_t)((int64_t)(S - 1) * a.mv.ss * es + D * es));
+    const uint32_t kbytes = (uint32_t)(a.mk.ss * es), vbytes = (uint32_t)(a.mv.ss * es);
+
+    if (nkb > 0) {
+        dma_tile<T, D, kQBN, kWaves>(smem, rk, 0, kbytes, wave, lane);
+        dma_tile<T, D, kQBN, kWaves>(smem + 2 * TILE, rv, 0, vbytes, wave, lane);
+    }
+    for (int kb = 0; kb < nkb; ++kb) {
+        const int k0 = kb * kQBN;
+        wait_vmcnt<0>();
+        __syncthreads();
+        if (kb + 1 < nkb) {
+            const int nb = (kb + 1) & 1;
+            dma_tile<T, D, kQBN, kWaves>(smem + nb * TILE, rk, k0 + kQBN, kbytes, wave, lane);
+            dma_tile<T, D, kQBN, kWaves>(smem + (2 + nb) * TILE, rv, k0 + kQBN, vbytes, wave, lane);
+        }
+        if (a.mask.causal && k0 > qw0 + 31) continue;
+        const T* sK = smem + (kb & 1) * TILE;
+        const T* sV = smem + (2 + (kb & 1)) * TILE;
+
+        // S^T = K Q^T and dP^T = V dO^T: lane <-> query, in-lane key kt*32 + acc_row
+        f32x16 s[2], dp[2];
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt) {
+            s[kt] = f32x16{};
+            dp[kt] = f32x16{};
+#pragma unroll
+            for (int c = 0; c < NC; ++c) {
+                Frag<T> fk, fv;
+                tile_row_frag<D>(fk, sK, kt * 32 + c32, 16 * c + 8 * g);
+                tile_row_frag<D>(fv, sV, kt * 32 + c32, 16 * c + 8 * g);
+                mma(s[kt], fk, qf[c]);
+                mma(dp[kt], fv, of[c]);
+            }
+        }
+        const bool boundary = (k0 + kQBN > kv_end) || (a.mask.causal && k0 + kQBN - 1 > qw0);
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt) {
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                float p = fast_exp2(__builtin_fmaf(s[kt][r], a.scale_log2, -sd[0]));
+                if (boundary) {
+                    const int kk = k0 + kt * 32 + acc_row(r, g);
+                    if (kk >= kv_end || (a.mask.causal && kk > qi)) p = 0.f;
+                }
+                dp[kt][r] = p * (dp[kt][r] - sd[1]);
+            }
+        }
+        // dQ^T += K^T dS^T over the 64 keys: chunk (kt, cc) covers keys
+        // kt*32 + 16cc + {4g..4g+3, 8+4g..8+4g+3} in accumulator order
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt) {
+#pragma unroll
+            for (int cc = 0; cc < 2; ++cc) {
+                Frag<T> dsb;
+                float dsv[8];
+#pragma unroll
+                for (int e = 0; e < 8; ++e) dsv[e] = dp[kt][8 * cc + e];
+                pack_frag(dsb, dsv);
+                const int row0 = kt * 32 + 16 * cc + 4 * g;
+#pragma unroll
+                for (int t = 0; t < ND; ++t) {
+                    Frag<T> fk;
+                    tile_tr_frag<D>(fk, sK, row0, row0 + 8, 32 * t, lane);
+                    mma(dq[t], fk, dsb);
+                }
+            }
+        }
+    }
+
+    if (qi < S) {
+        T* dqrow = static_cast<T*>(a.dq) + a.mdq.head_base(b, h) + (int64_t)qi * a.mdq.ss;
+#pragma unroll
+        for (int t = 0; t < ND; ++t) {
+#pragma unroll
+            for (int rr = 0; rr < 4; ++rr) {
+                const int dcol = 32 * t + 8 * rr + 4 * g;
+                store4(dqrow + dcol, dq[t][4 * rr] * a.scale, dq[t][4 * rr + 1] * a.scale, dq[t][4 * rr + 2] * a.scale,
+                       dq[t][4 * rr + 3] * a.scale);
+            }
+        }
     }
 }
 
+template <typename K>
+hipError_t set_lds(K kernel, int bytes) {
+    return hipFuncSetAttribute(reinterpret_cast<const void*>(kernel), hipFuncAttributeMaxDynamicSharedMemorySize,
+                               bytes);
+}
+
 template <typename T, int D>
-hipError_t set_main_lds() {
-    static hipError_t once = hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_bwd_main<T, D>),
-                                                 hipFuncAttributeMaxDynamicSharedMemorySize,
-                                                 BwdTile<T, D>::BYTES);
+hipError_t set_bwd_lds() {
+    static hipError_t once = [] {
+        const hipError_t e = set_lds(&attn_bwd_kv<T, D>, KvSmem<T, D>::BYTES);
+        if (e != hipSuccess) return e;
+        return set_lds(&attn_bwd_q<T, D>, QSmem<T, D>::BYTES);
+    }();
     return once;
 }
+
+int padded8(int n) { return (n + 7) / 8 * 8; }
 
 }  // namespace
 
@@ -342,17 +458,22 @@ template <typename T, int D>
 hipError_t launch_attn_bwd(const BwdArgs& a, unsigned phases, hipStream_t stream) {
     constexpr int LPR = D / (16 / (int)sizeof(T));
     constexpr int RPB = 256 / LPR;
-    const int64_t nrows = (int64_t)a.B * a.S * a.Hq;
-    const unsigned rblocks = (unsigned)((nrows + RPB - 1) / RPB);
-    hipError_t e = set_main_lds<T, D>();
+    const hipError_t e = set_bwd_lds<T, D>();
     if (e != hipSuccess) return e;
-    if (phases & 1u) hipLaunchKernelGGL((attn_bwd_pre<T, D>), dim3(rblocks), dim3(256), 0, stream, a);
-    if (phases & 2u) {
-        dim3 grid((a.S + kBwdBN - 1) / kBwdBN, a.Hkv, a.B);
-        constexpr int lds = BwdTile<T, D>::BYTES;
-        hipLaunchKernelGGL((attn_bwd_main<T, D>), grid, dim3(256), lds, stream, a);
+    if (phases & 1u) {
+        const int64_t nrows = (int64_t)a.B * a.S * a.Hq;
+        hipLaunchKernelGGL((attn_bwd_stats<T, D>), dim3((unsigned)((nrows + RPB - 1) / RPB)), dim3(256), 0, stream, a);
     }
-    if (phases & 4u) hipLaunchKernelGGL((attn_bwd_dq<T, D>), dim3(rblocks), dim3(256), 0, stream, a);
+    if (phases & 2u) {
+        const int n = (a.S + kKvBN - 1) / kKvBN * a.Hkv * a.B;
+        constexpr int lds = KvSmem<T, D>::BYTES;
+        hipLaunchKernelGGL((attn_bwd_kv<T, D>), dim3(padded8(n)), dim3(256), lds, stream, a);
+    }
+    if (phases & 4u) {
+        const int n = (a.S + kQBM - 1) / kQBM * a.Hq * a.B;
+        constexpr int lds = QSmem<T, D>::BYTES;
+        hipLaunchKernelGGL((attn_bwd_q<T, D>), dim3(padded8(n)), dim3(256), lds, stream, a);
+    }
     return hipGetLastError();
 }
 

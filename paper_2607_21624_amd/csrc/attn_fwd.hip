@@ -25,6 +25,8 @@
 // 2^8 (a stale maximum leaves every probability <= 256 and cancels in O/l),
 // which skips almost all rescales of the O accumulator.  The saved LSE is
 // converted to natural log at the store.
+#include <type_traits>
+
 #include "cdna4.hpp"
 #include "kernels.hpp"
 #include "stage.hpp"
@@ -41,15 +43,17 @@ constexpr float kRescaleSlack = 8.0f;   // log2 of the largest unnormalised prob
 
 template <typename T, int D>
 __global__ __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) void attn_fwd_kernel(FwdArgs a) {
-    using G = TileGeom<T, D>;
     constexpr int NC = D / 16;  // k-chunks over the head dim
     constexpr int ND = D / 32;  // 32-wide output column blocks
     constexpr int TILE = kFwdBN * D;
+    constexpr uint32_t TB = TILE * sizeof(T);  // tile bytes
+    constexpr bool kBf16 = sizeof(T) == 2;
     extern __shared__ __attribute__((aligned(1024))) unsigned char fwd_smem[];
     T* smem = reinterpret_cast<T*>(fwd_smem);  // K0 K1 V0 V1, TILE elements each
+    FBL_LDS char* lds = (FBL_LDS char*)fwd_smem;
 
     const int lane = threadIdx.x & 63;
-    const int wave = threadIdx.x >> 6;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int g = lane >> 5;
     const int c32 = lane & 31;
     const int S = a.S;
@@ -84,7 +88,7 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) void attn_fwd_kernel(F
         for (int cc = 0; cc < NC; ++cc) {
             float z[8] = {0, 0, 0, 0, 0, 0, 0, 0};
             if (qi < S) {
-                if constexpr (sizeof(T) == 2) {
+                if constexpr (kBf16) {
                     uint4 x = load16(qrow + 16 * cc + 8 * g);
                     if (neg) { x.x ^= 0x80008000u; x.y ^= 0x80008000u; x.z ^= 0x80008000u; x.w ^= 0x80008000u; }
                     qf[cc].v = __builtin_bit_cast(bf16x8, x);
@@ -112,26 +116,18 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) void attn_fwd_kernel(F
     const Rsrc rv = make_rsrc(static_cast<const T*>(a.v) + a.mv.head_base(b, hk),
                               (uint32_t)((int64_t)(S - 1) * a.mv.ss * es + D * es));
     const uint32_t kbytes = (uint32_t)(a.mk.ss * es), vbytes = (uint32_t)(a.mv.ss * es);
+    DmaPlan<T, D, kFwdBN, kFwdWaves> dk, dv;
+    dk.init(kbytes, wave, lane);
+    dv.init(vbytes, wave, lane);
+    LaneOffsets<D> lo;
+    if constexpr (kBf16) lo.init(lds_addr(fwd_smem), lane);
 
-    if (nkb > 0) {
-        dma_tile<T, D, kFwdBN, kFwdWaves>(smem, rk, 0, kbytes, wave, lane);
-        dma_tile<T, D, kFwdBN, kFwdWaves>(smem + 2 * TILE, rv, 0, vbytes, wave, lane);
-    }
-
-    for (int kb = 0; kb < nkb; ++kb) {
-        const int k0 = kb * kFwdBN;
-        wait_vmcnt<0>();
-        __syncthreads();  // tile kb landed everywhere; tile kb-1's buffers are free
-        if (kb + 1 < nkb) {
-            const int nb = (kb + 1) & 1;
-            dma_tile<T, D, kFwdBN, kFwdWaves>(smem + nb * TILE, rk, k0 + kFwdBN, kbytes, wave, lane);
-            dma_tile<T, D, kFwdBN, kFwdWaves>(smem + (2 + nb) * TILE, rv, k0 + kFwdBN, vbytes, wave, lane);
-        }
-        // a whole tile above this wave's diagonal contributes nothing
-        if (a.mask.causal && k0 > qw0 + 31) continue;
-        const T* sK = smem + (kb & 1) * TILE;
-        const T* sV = smem + (2 + (kb & 1)) * TILE;
-
+    // One key tile: scores, online softmax, and the P V update.  The lane
+    // offsets in `lo` point into the buffer pair holding the current tile;
+    // MASK selects causal/padding masking.
+    auto tile = [&](auto mask_c, int k0) {
+        constexpr bool MASK = decltype(mask_c)::value;
+        const int BUF = (k0 / kFwdBN) & 1;
         f32x16 s[2];
 #pragma unroll
         for (int kt = 0; kt < 2; ++kt) {
@@ -139,21 +135,19 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) void attn_fwd_kernel(F
 #pragma unroll
             for (int cc = 0; cc < NC; ++cc) {
                 Frag<T> kf;
-                tile_row_frag<D>(kf, sK, kt * 32 + c32, 16 * cc + 8 * g);
+                if constexpr (kBf16) kf.v = lds_b128(lo.row[cc], kt * 32 * D * 2);
+                else tile_row_frag<D>(kf, smem + BUF * TILE, kt * 32 + c32, 16 * cc + 8 * g);
                 mma(s[kt], kf, qf[cc]);
             }
         }
-
-        const bool boundary = (k0 + kFwdBN > kv_end) || (a.mask.causal && k0 + kFwdBN - 1 > qw0);
-        if (boundary) {
+        if constexpr (MASK) {
 #pragma unroll
-            for (int kt = 0; kt < 2; ++kt) {
+            for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
                 for (int r = 0; r < 16; ++r) {
                     const int key = k0 + kt * 32 + acc_row(r, g);
                     if (key >= kv_end || (a.mask.causal && key > qi)) s[kt][r] = -INFINITY;
                 }
-            }
         }
         float mx = -INFINITY;
 #pragma unroll
@@ -169,22 +163,22 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) void attn_fwd_kernel(F
             for (int t = 0; t < ND; ++t) oacc[t] *= alpha;
             m = m_new;
         }
-        const float m_use = (m == -INFINITY) ? 0.f : m;
+        const float nm = (m == -INFINITY) ? 0.f : -m;
 #pragma unroll
-        for (int kt = 0; kt < 2; ++kt) {
+        for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
-                float p = fast_exp2(__builtin_fmaf(s[kt][r], c, -m_use));
-                if (boundary && s[kt][r] == -INFINITY) p = 0.f;
+                float p = fast_exp2(__builtin_fmaf(s[kt][r], c, nm));
+                if constexpr (MASK) {
+                    if (s[kt][r] == -INFINITY) p = 0.f;
+                }
                 s[kt][r] = p;
                 l += p;
             }
-        }
-
         // O^T += V^T P^T over the 64 keys: chunk (kt, cc) covers keys
         // kt*32 + 16cc + {4g..4g+3, 8+4g..8+4g+3} in accumulator order
 #pragma unroll
-        for (int kt = 0; kt < 2; ++kt) {
+        for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
             for (int cc = 0; cc < 2; ++cc) {
                 Frag<T> pf;
@@ -192,16 +186,54 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) void attn_fwd_kernel(F
 #pragma unroll
                 for (int e = 0; e < 8; ++e) pv[e] = s[kt][8 * cc + e];
                 pack_frag(pf, pv);
-                const int row0 = kt * 32 + 16 * cc + 4 * g;
 #pragma unroll
                 for (int t = 0; t < ND; ++t) {
                     Frag<T> vf;
-                    tile_tr_frag<D>(vf, sV, row0, row0 + 8, 32 * t, lane);
+                    if constexpr (kBf16) {
+                        const uint32_t rb = 2 * TB + (kt * 32 + 16 * cc) * D * 2;
+                        const bf16x4 x0 = lds_tr(lo.tr[t][0], rb), x1 = lds_tr(lo.tr[t][1], rb);
+                        vf.v = bf16x8{x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
+                    } else {
+                        const int row0 = kt * 32 + 16 * cc + 4 * g;
+                        tile_tr_frag<D>(vf, smem + (2 + BUF) * TILE, row0, row0 + 8, 32 * t, lane);
+                    }
                     mma(oacc[t], vf, pf);
                 }
             }
+    };
+
+    // step kb: wait for its tile, start the next one's DMA into the other
+    // buffer pair, compute, then point the lane offsets at the other pair
+    auto step = [&](auto mask_c, int kb) {
+        const int k0 = kb * kFwdBN;
+        wait_vmcnt<0>();
+        __syncthreads();  // tile kb landed everywhere; the other buffer pair is free
+        if (kb + 1 < nkb) {
+            const uint32_t nb = (uint32_t)((kb + 1) & 1);
+            dk.issue(lds + nb * TB, rk, (uint32_t)(k0 + kFwdBN) * kbytes, wave);
+            dv.issue(lds + (2 + nb) * TB, rv, (uint32_t)(k0 + kFwdBN) * vbytes, wave);
         }
+        tile(mask_c, k0);
+        if constexpr (kBf16) {
+#pragma unroll
+            for (int cc = 0; cc < NC; ++cc) lo.row[cc] ^= TB;
+#pragma unroll
+            for (int t = 0; t < ND; ++t) {
+                lo.tr[t][0] ^= TB;
+                lo.tr[t][1] ^= TB;
+            }
+        }
+    };
+
+    if (nkb > 0) {
+        dk.issue(lds, rk, 0u, wave);
+        dv.issue(lds + 2 * TB, rv, 0u, wave);
     }
+    // Tiles that lie inside kv_end and (causal) at or below the block's first
+    // query need no mask for any wave; the rest of the block's tiles do.
+    const int n_full = min(nkb, min(kv_end, a.mask.causal ? q0 + 1 : S) / kFwdBN);
+    for (int kb = 0; kb < n_full; ++kb) step(std::false_type{}, kb);
+    for (int kb = n_full; kb < nkb; ++kb) step(std::true_type{}, kb);
 
     l += other_half(l);
     if (qi < S) {

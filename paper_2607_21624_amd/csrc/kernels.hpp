@@ -13,10 +13,9 @@ typedef __bf16 bf16;
 template <typename T, int D>
 hipError_t launch_attn_fwd(const FwdArgs& a, hipStream_t stream);
 
-// Backward: row statistic D = rowsum(dO * O) and zeroed dQ accumulator,
-// then the key/value-major main pass (dK, dV, dQ accumulation), then the
-// dQ conversion to the storage type.  Three launches on `stream`.
-// `phases`: bit 0 pre, bit 1 main, bit 2 dQ conversion.
+// Backward: per-row statistics (LSE * log2(e), D = rowsum(dO * O)), then the
+// key/value-major pass (dK, dV) and the query-major pass (dQ).
+// `phases`: bit 0 statistics, bit 1 kv pass, bit 2 q pass.
 template <typename T, int D>
 hipError_t launch_attn_bwd(const BwdArgs& a, unsigned phases, hipStream_t stream);
 

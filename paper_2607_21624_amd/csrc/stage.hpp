@@ -126,6 +126,74 @@ FBL_DEV void tile_tr_frag(Frag<float>& f, const float* tile, int row0, int row1,
     }
 }
 
+// Per-lane LDS byte addresses of the bf16 fragment reads of a staged tile,
+// computed once so every LDS read in the loops is "lane address +
+// compile-time constant" (the constant goes into the instruction's
+// immediate field).  Valid for any 16-row-aligned block of the tile because
+// swz() depends on r mod 16 only.
+//   row[c]     row fragment: row (lane % 32), columns 16c + 8g .. +7
+//   tr[t][h]   transposed fragment: column 32t + (lane % 32), rows 8h + 4g + [0..3]
+template <int D>
+struct LaneOffsets {
+    static constexpr int NC = D / 16;
+    static constexpr int ND = D / 32;
+    uint32_t row[NC];
+    uint32_t tr[ND][2];
+    FBL_DEV void init(uint32_t tile_base, int lane) {
+        using G = TileGeom<bf16, D>;
+        const int g = lane >> 5, c32 = lane & 31, t = lane & 15;
+#pragma unroll
+        for (int c = 0; c < NC; ++c) row[c] = tile_base + 2u * (uint32_t)G::off(c32, 16 * c + 8 * g);
+#pragma unroll
+        for (int tt = 0; tt < ND; ++tt)
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                const int r = 8 * h + 4 * g + (t >> 2);
+                const int col = 32 * tt + 16 * ((lane >> 4) & 1) + 4 * (t & 3);
+                tr[tt][h] = tile_base + 2u * (uint32_t)G::off(r, col);
+            }
+    }
+};
+
+// LDS byte address of a shared-memory object (its offset in the workgroup's LDS).
+FBL_DEV uint32_t lds_addr(const void* p) { return (uint32_t)(uintptr_t)(const FBL_LDS void*)p; }
+
+FBL_DEV bf16x8 lds_b128(uint32_t addr, uint32_t const_off) {
+    return *(const FBL_LDS bf16x8*)(uintptr_t)(addr + const_off);
+}
+FBL_DEV bf16x4 lds_tr(uint32_t addr, uint32_t const_off) {
+    return __builtin_amdgcn_ds_read_tr16_b64_v4bf16((FBL_LDS bf16x4*)(uintptr_t)(addr + const_off));
+}
+
+// DMA of a ROWS-row tile with per-lane global offsets computed once:
+// voff[j] is the byte offset (relative to the tile's first row) of the chunk
+// lane `lane` of wave `wave` moves in its j-th load.  The row origin goes in
+// the scalar offset of each load.
+template <typename T, int D, int ROWS, int NWAVES>
+struct DmaPlan {
+    using G = TileGeom<T, D>;
+    static constexpr int INSTS = ROWS * G::CPR / 64;
+    static constexpr int PER_WAVE = INSTS / NWAVES;
+    static_assert(INSTS % NWAVES == 0, "equal share of tile loads per wave");
+    uint32_t voff[PER_WAVE];
+    FBL_DEV void init(uint32_t row_bytes, int wave, int lane) {
+#pragma unroll
+        for (int j = 0; j < PER_WAVE; ++j) {
+            const int q = (j * NWAVES + wave) * 64 + lane;
+            const int r = q / G::CPR;
+            const int c = (q % G::CPR) ^ G::swz(r);
+            voff[j] = (uint32_t)r * row_bytes + (uint32_t)c * 16u;
+        }
+    }
+    // Loads rows row0.. of the tile at LDS byte address `tile`.
+    FBL_DEV void issue(FBL_LDS char* tile, Rsrc rs, uint32_t row0_bytes, int wave) const {
+#pragma unroll
+        for (int j = 0; j < PER_WAVE; ++j)
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (FBL_LDS void*)(tile + (j * NWAVES + wave) * 1024), 16, voff[j],
+                                                     row0_bytes, 0, 0);
+    }
+};
+
 // Map a linear workgroup id so that consecutive ids of the logical order land
 // on the same XCD (ids are dealt round-robin over the 8 XCDs, each with its own
 // L2): logical = (id % 8) * per_xcd + id / 8.  Returns -1 for padding ids.

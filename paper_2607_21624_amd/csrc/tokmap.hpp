@@ -11,6 +11,8 @@
 
 #include <stdint.h>
 
+#include "cdna4.hpp"
+
 namespace fbl {
 
 struct TokMap {
@@ -51,8 +53,7 @@ struct BwdArgs {
     void* dq;
     void* dk;
     void* dv;
-    float* dq_acc;   // fp32 [B, S, Hq*D] token-major workspace
-    float* drow;     // fp32 [B, Hq, S] workspace: sum_i dO * O per query row
+    f32x2* stats;      // workspace [B, Hq, S]: (LSE * log2(e), sum_k dO*O) per query row
     TokMap mq, mk, mv, mo, mdo, mdq, mdk, mdv;
     int B, S, Hq, Hkv;
     float scale;       // softmax scale

@@ -32,8 +32,8 @@ FBL_MASK_CAUSAL = 1
 FBL_MASK_KEY_PADDING = 2
 
 FBL_BWD_PREP = 1
-FBL_BWD_MAIN = 2
-FBL_BWD_DQ = 4
+FBL_BWD_KV = 2
+FBL_BWD_Q = 4
 FBL_BWD_ALL = 7
 
 EXPORTED = ("fbl_layout_desc", "fbl_layout_offset", "fbl_layout_map_device", "fbl_attn_fwd",

@@ -175,7 +175,7 @@ def test_strided_views_of_packed_projection():
 
 
 def test_repeatability_and_no_allocation():
-    """fwd and dK/dV are bitwise repeatable; dQ (fp32 atomics) within tolerance;
+    """fwd and bwd outputs are bitwise repeatable (no atomics anywhere);
     the calls allocate no device memory when outputs and workspace are given."""
     import torch
     fbl = _lib()
@@ -199,9 +199,8 @@ def test_repeatability_and_no_allocation():
         assert torch.cuda.memory_allocated() == before
         runs.append([t.clone() for t in (o, lse, dq, dk, dv)])
     for r in runs[1:]:
-        assert torch.equal(r[0], runs[0][0]) and torch.equal(r[1], runs[0][1])
-        assert torch.equal(r[3], runs[0][3]) and torch.equal(r[4], runs[0][4])
-        assert rel_err(to_np(r[2]), to_np(runs[0][2])) < 1e-2
+        for x, y in zip(r, runs[0]):
+            assert torch.equal(x, y)
 
 
 def test_gradient_invariants_on_gpu_outputs():
