@@ -126,7 +126,8 @@ hipError_t dispatch_bwd(int D, const fbl::BwdArgs& a, unsigned phases, hipStream
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-// Workspace: the per-query-row statistics (LSE * log2(e), D) as float pairs.
+// Workspace: the per-query-row statistics, [B, Hq, 2, S] floats (a row of
+// LSE * log2(e), then a row of D, for each (batch, query head)).
 size_t ws_bytes_for(const fbl_layout* lq) {
     return align256((size_t)lq->B * lq->H * lq->S * 2 * sizeof(float));
 }
@@ -287,7 +288,7 @@ fbl_status fbl_attn_bwd_phases(uint32_t phases, const fbl_layout* lq, const void
     a.dq = dq;
     a.dk = dk;
     a.dv = dv;
-    a.stats = static_cast<fbl::f32x2*>(ws);
+    a.stats = static_cast<float*>(ws);
     a.mq = tokmap(lq);
     a.mk = tokmap(lk);
     a.mv = tokmap(lv);

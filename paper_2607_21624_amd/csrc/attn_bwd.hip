@@ -28,6 +28,8 @@
 // DMA and serve both reduction directions (tile invariance, section 4.2): row
 // reads where the contraction runs along d, transposed reads
 // (ds_read_b64_tr_b16) where it runs along tokens.
+#include <type_traits>
+
 #include "cdna4.hpp"
 #include "kernels.hpp"
 #include "stage.hpp"
@@ -39,7 +41,6 @@ namespace {
 
 constexpr int kWaves = 4;
 constexpr int kKvBN = 32 * kWaves;  // keys per kv-pass workgroup
-constexpr int kKvBQ = 64;           // queries per kv-pass block
 constexpr int kQBM = 32 * kWaves;   // queries per q-pass workgroup
 constexpr int kQBN = 64;            // keys per q-pass tile
 
@@ -77,34 +78,40 @@ __global__ __launch_bounds__(256) void attn_bwd_stats(BwdArgs a) {
 #pragma unroll
     for (int off = LPR / 2; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
     if (row < nrows && part == 0) {
-        const int64_t i = ((int64_t)b * a.Hq + h) * a.S + s;
-        const float lse = a.lse[i];
-        a.stats[i] = f32x2{lse == -INFINITY ? INFINITY : lse * kLog2e, acc};
+        const int64_t bh = (int64_t)b * a.Hq + h;
+        const float lse = a.lse[bh * a.S + s];
+        a.stats[2 * bh * a.S + s] = lse == -INFINITY ? INFINITY : lse * kLog2e;
+        a.stats[(2 * bh + 1) * a.S + s] = acc;
     }
 }
 
 // ------------------------------------------------------------- kv pass
 template <typename T, int D>
-struct KvSmem {
-    static constexpr int TILE = kKvBQ * D;  // elements of one Q or dO tile
-    // [Q0 Q1 dO0 dO1] tiles, then two 1 KB stats buffers (64 (lse2, D) pairs
-    // plus room for the full 64-lane DMA of one instruction)
-    static constexpr int BYTES = 4 * TILE * (int)sizeof(T) + 2 * 1024;
+struct KvCfg {
+    static constexpr int BQ = D == 128 ? 32 : 64;  // queries per block (register budget)
+    static constexpr int NQT = BQ / 32;
+    static constexpr int TILE = BQ * D;             // elements of one Q or dO tile
+    static constexpr int TB = TILE * (int)sizeof(T);
+    // LDS: Q0 Q1 dO0 dO1 tiles, then lse2 0/1 and D 0/1 (256 bytes each: one
+    // 64-lane dword DMA; the first BQ floats are used)
+    static constexpr int OFF_STATS = 4 * TB;
+    static constexpr int BYTES = 4 * TB + 4 * 256;
 };
 
 template <typename T, int D>
 __global__ __launch_bounds__(256, 1) void attn_bwd_kv(BwdArgs a) {
-    using SM = KvSmem<T, D>;
+    using C = KvCfg<T, D>;
     constexpr int NC = D / 16;
     constexpr int ND = D / 32;
-    constexpr int TILE = SM::TILE;
-    constexpr int NQT = kKvBQ / 32;
+    constexpr int BQ = C::BQ;
+    constexpr int NQT = C::NQT;
+    constexpr int TB = C::TB;
+    constexpr bool kBf16 = sizeof(T) == 2;
     extern __shared__ __attribute__((aligned(1024))) unsigned char kv_smem[];
-    T* tiles = reinterpret_cast<T*>(kv_smem);
-    float* stat_buf = reinterpret_cast<float*>(kv_smem + 4 * TILE * sizeof(T));
+    FBL_LDS char* lds = (FBL_LDS char*)kv_smem;
 
     const int lane = threadIdx.x & 63;
-    const int wave = threadIdx.x >> 6;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int g = lane >> 5;
     const int c32 = lane & 31;
     const int S = a.S;
@@ -136,7 +143,7 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_kv(BwdArgs a) {
         if (key < S) {
             const T* kp = kbase + (int64_t)key * a.mk.ss + 16 * c + 8 * g;
             const T* vp = vbase + (int64_t)key * a.mv.ss + 16 * c + 8 * g;
-            if constexpr (sizeof(T) == 2) {
+            if constexpr (kBf16) {
                 kf[c].v = __builtin_bit_cast(bf16x8, load16(kp));
                 vf[c].v = __builtin_bit_cast(bf16x8, load16(vp));
             } else {
@@ -161,44 +168,49 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_kv(BwdArgs a) {
         dv[t] = f32x16{};
     }
 
-    const int qb_start = a.mask.causal ? (k0 / kKvBQ) : 0;
-    const int nqb = (S + kKvBQ - 1) / kKvBQ;
+    const int qb_start = a.mask.causal ? (k0 / BQ) : 0;
+    const int nqb = (S + BQ - 1) / BQ;
     const int per_head = nqb - qb_start;
     const int n_iter = (k0 < kv_end) ? G_ * per_head : 0;
+    // blocks needing a mask: all of them when this block's keys run past
+    // kv_end; else (causal) those holding a query before one of the keys
+    int n_mask = 0;
+    if (k0 + kKvBN > kv_end) n_mask = per_head;
+    else if (a.mask.causal) n_mask = min(per_head, (k0 + kKvBN - 2) / BQ - qb_start + 1);
 
-    auto issue = [&](int it, int buf) {
+    DmaPlan<T, D, BQ, kWaves> pq, po;
+    pq.init((uint32_t)(a.mq.ss * es), wave, lane);
+    po.init((uint32_t)(a.mdo.ss * es), wave, lane);
+    const uint32_t qbytes = (uint32_t)(a.mq.ss * es), obytes = (uint32_t)(a.mdo.ss * es);
+    const uint32_t qspan = (uint32_t)((int64_t)(S - 1) * a.mq.ss * es + D * es);
+    const uint32_t ospan = (uint32_t)((int64_t)(S - 1) * a.mdo.ss * es + D * es);
+
+    auto issue = [&](int it) {
+        const int buf = it & 1;
         const int h = hk * G_ + it / per_head;
-        const int q0 = (qb_start + it % per_head) * kKvBQ;
-        const Rsrc rq = make_rsrc(static_cast<const T*>(a.q) + a.mq.head_base(b, h),
-                                  (uint32_t)((int64_t)(S - 1) * a.mq.ss * es + D * es));
-        const Rsrc ro = make_rsrc(static_cast<const T*>(a.dout) + a.mdo.head_base(b, h),
-                                  (uint32_t)((int64_t)(S - 1) * a.mdo.ss * es + D * es));
-        dma_tile<T, D, kKvBQ, kWaves>(tiles + buf * TILE, rq, q0, (uint32_t)(a.mq.ss * es), wave, lane);
-        dma_tile<T, D, kKvBQ, kWaves>(tiles + (2 + buf) * TILE, ro, q0, (uint32_t)(a.mdo.ss * es), wave, lane);
-        if (wave == 0) {
-            // 64 (lse2, D) pairs = 512 bytes; lanes 32..63 fetch the following
-            // rows (zeros past the end) into the spare half of the buffer
-            const Rsrc rs = make_rsrc(a.stats + ((int64_t)b * a.Hq + h) * S, (uint32_t)(S * 8));
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (FBL_LDS void*)(stat_buf + buf * 256), 16,
-                                                     (uint32_t)(q0 * 8 + lane * 16), 0, 0, 0);
+        const int q0 = (qb_start + it % per_head) * BQ;
+        const Rsrc rq = make_rsrc(static_cast<const T*>(a.q) + a.mq.head_base(b, h), qspan);
+        const Rsrc ro = make_rsrc(static_cast<const T*>(a.dout) + a.mdo.head_base(b, h), ospan);
+        pq.issue(lds + buf * TB, rq, (uint32_t)q0 * qbytes, wave);
+        po.issue(lds + (2 + buf) * TB, ro, (uint32_t)q0 * obytes, wave);
+        if (wave < 2) {  // wave 0: lse2 of the block's queries, wave 1: D
+            const float* row = a.stats + (2 * ((int64_t)b * a.Hq + h) + wave) * S;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(make_rsrc(row, (uint32_t)(S * 4)),
+                                                     (FBL_LDS void*)(lds + C::OFF_STATS + (2 * wave + buf) * 256), 4,
+                                                     (uint32_t)(q0 + lane) * 4u, 0, 0, 0);
         }
     };
 
-    if (n_iter > 0) issue(0, 0);
-    for (int it = 0; it < n_iter; ++it) {
-        const int buf = it & 1;
-        wait_vmcnt<0>();
-        __syncthreads();  // block `it` landed; block it-1's buffers are free
-        if (it + 1 < n_iter) issue(it + 1, buf ^ 1);
-        const int q0 = (qb_start + it % per_head) * kKvBQ;
-        // nothing to do for a wave whose keys are all padding, or all after
-        // every query of the block
-        if (kw0 >= kv_end) continue;
-        if (a.mask.causal && q0 + kKvBQ - 1 < kw0) continue;
-        const T* sQ = tiles + buf * TILE;
-        const T* sdO = tiles + (2 + buf) * TILE;
-        const f32x2* st = reinterpret_cast<const f32x2*>(stat_buf + buf * 256);
+    // per-lane LDS addresses into buffer 0; `flip` moves them to the other buffer
+    LaneOffsets<D> lo;
+    if constexpr (kBf16) lo.init(lds_addr(kv_smem), lane);
+    uint32_t st_addr = lds_addr(kv_smem) + C::OFF_STATS + 16u * g;  // lse2 of queries 4g.. of buffer 0
+    int32_t flip = TB;
 
+    auto compute = [&](auto mask_c, int buf, int q0) {
+        constexpr bool MASK = decltype(mask_c)::value;
+        const T* sQ = reinterpret_cast<const T*>(kv_smem) + buf * C::TILE;
+        const T* sdO = reinterpret_cast<const T*>(kv_smem) + (2 + buf) * C::TILE;
         // S = Q K_w^T and dP = dO V_w^T: lane <-> key, in-lane query 32qt + acc_row
         f32x16 s[NQT], dp[NQT];
 #pragma unroll
@@ -208,26 +220,36 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_kv(BwdArgs a) {
 #pragma unroll
             for (int c = 0; c < NC; ++c) {
                 Frag<T> fq, fo;
-                tile_row_frag<D>(fq, sQ, qt * 32 + c32, 16 * c + 8 * g);
-                tile_row_frag<D>(fo, sdO, qt * 32 + c32, 16 * c + 8 * g);
+                if constexpr (kBf16) {
+                    fq.v = lds_b128(lo.row[c], qt * 32 * D * 2);
+                    fo.v = lds_b128(lo.row[c], 2 * TB + qt * 32 * D * 2);
+                } else {
+                    tile_row_frag<D>(fq, sQ, qt * 32 + c32, 16 * c + 8 * g);
+                    tile_row_frag<D>(fo, sdO, qt * 32 + c32, 16 * c + 8 * g);
+                }
                 mma(s[qt], fq, kf[c]);
                 mma(dp[qt], fo, vf[c]);
             }
         }
-        const bool diag = a.mask.causal && q0 < kw0 + 31;
 #pragma unroll
         for (int qt = 0; qt < NQT; ++qt) {
 #pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int ql = qt * 32 + acc_row(r, g);
-                const f32x2 sd = st[ql];
-                float p = fast_exp2(__builtin_fmaf(s[qt][r], a.scale_log2, -sd[0]));
-                if (!key_ok || (diag && key > q0 + ql)) p = 0.f;
-                s[qt][r] = p;
-                dp[qt][r] = p * (dp[qt][r] - sd[1]);
+            for (int rr = 0; rr < 4; ++rr) {
+                const f32x4 l4 = *(const FBL_LDS f32x4*)(uintptr_t)(st_addr + (qt * 32 + 8 * rr) * 4);
+                const f32x4 d4 = *(const FBL_LDS f32x4*)(uintptr_t)(st_addr + 512 + (qt * 32 + 8 * rr) * 4);
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const int r = 4 * rr + j;
+                    float p = fast_exp2(__builtin_fmaf(s[qt][r], a.scale_log2, -l4[j]));
+                    if constexpr (MASK) {
+                        if (!key_ok || (a.mask.causal && key > q0 + qt * 32 + acc_row(r, g))) p = 0.f;
+                    }
+                    s[qt][r] = p;
+                    dp[qt][r] = p * (dp[qt][r] - d4[j]);
+                }
             }
         }
-        // dV^T += dO^T P and dK^T += Q^T dS, contracting over the 64 queries:
+        // dV^T += dO^T P and dK^T += Q^T dS, contracting over the block's queries:
         // chunk (qt, cc) covers queries 32qt + 16cc + {4g..4g+3, 8+4g..8+4g+3}
 #pragma unroll
         for (int qt = 0; qt < NQT; ++qt) {
@@ -242,17 +264,53 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_kv(BwdArgs a) {
                 }
                 pack_frag(pb, pv);
                 pack_frag(dsb, dsv);
-                const int row0 = qt * 32 + 16 * cc + 4 * g;
 #pragma unroll
                 for (int t = 0; t < ND; ++t) {
                     Frag<T> fdo, fq;
-                    tile_tr_frag<D>(fdo, sdO, row0, row0 + 8, 32 * t, lane);
-                    tile_tr_frag<D>(fq, sQ, row0, row0 + 8, 32 * t, lane);
+                    if constexpr (kBf16) {
+                        const uint32_t rb = (qt * 32 + 16 * cc) * D * 2;
+                        const bf16x4 o0 = lds_tr(lo.tr[t][0], 2 * TB + rb), o1 = lds_tr(lo.tr[t][1], 2 * TB + rb);
+                        const bf16x4 x0 = lds_tr(lo.tr[t][0], rb), x1 = lds_tr(lo.tr[t][1], rb);
+                        fdo.v = bf16x8{o0[0], o0[1], o0[2], o0[3], o1[0], o1[1], o1[2], o1[3]};
+                        fq.v = bf16x8{x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
+                    } else {
+                        const int row0 = qt * 32 + 16 * cc + 4 * g;
+                        tile_tr_frag<D>(fdo, sdO, row0, row0 + 8, 32 * t, lane);
+                        tile_tr_frag<D>(fq, sQ, row0, row0 + 8, 32 * t, lane);
+                    }
                     mma(dv[t], fdo, pb);
                     mma(dk[t], fq, dsb);
                 }
             }
         }
+    };
+
+    auto step = [&](auto mask_c, int it) {
+        const int buf = it & 1;
+        wait_vmcnt<0>();
+        __syncthreads();  // block `it` landed; block it-1's buffers are free
+        if (it + 1 < n_iter) issue(it + 1);
+        const int q0 = (qb_start + it % per_head) * BQ;
+        // a wave whose keys all follow every query of the block has nothing to add
+        if (!(a.mask.causal && q0 + BQ - 1 < kw0) && kw0 < kv_end) compute(mask_c, buf, q0);
+        if constexpr (kBf16) {
+#pragma unroll
+            for (int c = 0; c < NC; ++c) lo.row[c] += flip;
+#pragma unroll
+            for (int t = 0; t < ND; ++t) {
+                lo.tr[t][0] += flip;
+                lo.tr[t][1] += flip;
+            }
+        }
+        st_addr += flip / TB * 256;
+        flip = -flip;
+    };
+
+    if (n_iter > 0) issue(0);
+    int it = 0;
+    for (int hh = 0; hh < G_ && n_iter > 0; ++hh) {
+        for (int j = 0; j < n_mask; ++j, ++it) step(std::true_type{}, it);
+        for (int j = n_mask; j < per_head; ++j, ++it) step(std::false_type{}, it);
     }
 
     // dK (times scale) and dV rows of this wave's keys: lane <-> key, 4 consecutive d per store
@@ -276,7 +334,8 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_kv(BwdArgs a) {
 template <typename T, int D>
 struct QSmem {
     static constexpr int TILE = kQBN * D;
-    static constexpr int BYTES = 4 * TILE * (int)sizeof(T);  // K0 K1 V0 V1
+    static constexpr int TB = TILE * (int)sizeof(T);
+    static constexpr int BYTES = 4 * TB;  // K0 K1 V0 V1
 };
 
 template <typename T, int D>
@@ -284,11 +343,14 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) void attn_bwd_q(BwdArg
     constexpr int NC = D / 16;
     constexpr int ND = D / 32;
     constexpr int TILE = QSmem<T, D>::TILE;
+    constexpr int TB = QSmem<T, D>::TB;
+    constexpr bool kBf16 = sizeof(T) == 2;
     extern __shared__ __attribute__((aligned(1024))) unsigned char q_smem[];
     T* smem = reinterpret_cast<T*>(q_smem);
+    FBL_LDS char* lds = (FBL_LDS char*)q_smem;
 
     const int lane = threadIdx.x & 63;
-    const int wave = threadIdx.x >> 6;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int g = lane >> 5;
     const int c32 = lane & 31;
     const int S = a.S;
@@ -320,7 +382,7 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) void attn_bwd_q(BwdArg
             pack_frag(qf[c], z);
             pack_frag(of[c], z);
             if (qi < S) {
-                if constexpr (sizeof(T) == 2) {
+                if constexpr (kBf16) {
                     qf[c].v = __builtin_bit_cast(bf16x8, load16(qrow + 16 * c + 8 * g));
                     of[c].v = __builtin_bit_cast(bf16x8, load16(orow + 16 * c + 8 * g));
                 } else {
@@ -339,8 +401,12 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) void attn_bwd_q(BwdArg
             }
         }
     }
-    f32x2 sd = f32x2{INFINITY, 0.f};  // (lse2, D) of this lane's query
-    if (qi < S) sd = a.stats[((int64_t)b * a.Hq + h) * S + qi];
+    float lse2 = INFINITY, drow = 0.f;  // this lane's query row statistics
+    if (qi < S) {
+        const int64_t bh = (int64_t)b * a.Hq + h;
+        lse2 = a.stats[2 * bh * S + qi];
+        drow = a.stats[(2 * bh + 1) * S + qi];
+    }
 
     f32x16 dq[ND];  // dQ^T: rows = d (32t + acc_row), columns = queries (lane)
 #pragma unroll
@@ -352,24 +418,16 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) void attn_bwd_q(BwdArg
     const Rsrc rv = make_rsrc(static_cast<const T*>(a.v) + a.mv.head_base(b, hk),
                               (uint32_t)((int64_t)(S - 1) * a.mv.ss * es + D * es));
     const uint32_t kbytes = (uint32_t)(a.mk.ss * es), vbytes = (uint32_t)(a.mv.ss * es);
+    DmaPlan<T, D, kQBN, kWaves> pk, pv;
+    pk.init(kbytes, wave, lane);
+    pv.init(vbytes, wave, lane);
+    LaneOffsets<D> lo;
+    if constexpr (kBf16) lo.init(lds_addr(q_smem), lane);
+    int32_t flip = TB;
 
-    if (nkb > 0) {
-        dma_tile<T, D, kQBN, kWaves>(smem, rk, 0, kbytes, wave, lane);
-        dma_tile<T, D, kQBN, kWaves>(smem + 2 * TILE, rv, 0, vbytes, wave, lane);
-    }
-    for (int kb = 0; kb < nkb; ++kb) {
-        const int k0 = kb * kQBN;
-        wait_vmcnt<0>();
-        __syncthreads();
-        if (kb + 1 < nkb) {
-            const int nb = (kb + 1) & 1;
-            dma_tile<T, D, kQBN, kWaves>(smem + nb * TILE, rk, k0 + kQBN, kbytes, wave, lane);
-            dma_tile<T, D, kQBN, kWaves>(smem + (2 + nb) * TILE, rv, k0 + kQBN, vbytes, wave, lane);
-        }
-        if (a.mask.causal && k0 > qw0 + 31) continue;
-        const T* sK = smem + (kb & 1) * TILE;
-        const T* sV = smem + (2 + (kb & 1)) * TILE;
-
+    auto tile = [&](auto mask_c, int k0) {
+        constexpr bool MASK = decltype(mask_c)::value;
+        const int BUF = (k0 / kQBN) & 1;
         // S^T = K Q^T and dP^T = V dO^T: lane <-> query, in-lane key kt*32 + acc_row
         f32x16 s[2], dp[2];
 #pragma unroll
@@ -379,23 +437,27 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) void attn_bwd_q(BwdArg
 #pragma unroll
             for (int c = 0; c < NC; ++c) {
                 Frag<T> fk, fv;
-                tile_row_frag<D>(fk, sK, kt * 32 + c32, 16 * c + 8 * g);
-                tile_row_frag<D>(fv, sV, kt * 32 + c32, 16 * c + 8 * g);
+                if constexpr (kBf16) {
+                    fk.v = lds_b128(lo.row[c], kt * 32 * D * 2);
+                    fv.v = lds_b128(lo.row[c], 2 * TB + kt * 32 * D * 2);
+                } else {
+                    tile_row_frag<D>(fk, smem + BUF * TILE, kt * 32 + c32, 16 * c + 8 * g);
+                    tile_row_frag<D>(fv, smem + (2 + BUF) * TILE, kt * 32 + c32, 16 * c + 8 * g);
+                }
                 mma(s[kt], fk, qf[c]);
                 mma(dp[kt], fv, of[c]);
             }
         }
-        const bool boundary = (k0 + kQBN > kv_end) || (a.mask.causal && k0 + kQBN - 1 > qw0);
 #pragma unroll
         for (int kt = 0; kt < 2; ++kt) {
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
-                float p = fast_exp2(__builtin_fmaf(s[kt][r], a.scale_log2, -sd[0]));
-                if (boundary) {
+                float p = fast_exp2(__builtin_fmaf(s[kt][r], a.scale_log2, -lse2));
+                if constexpr (MASK) {
                     const int kk = k0 + kt * 32 + acc_row(r, g);
                     if (kk >= kv_end || (a.mask.causal && kk > qi)) p = 0.f;
                 }
-                dp[kt][r] = p * (dp[kt][r] - sd[1]);
+                dp[kt][r] = p * (dp[kt][r] - drow);
             }
         }
         // dQ^T += K^T dS^T over the 64 keys: chunk (kt, cc) covers keys
@@ -409,16 +471,52 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) void attn_bwd_q(BwdArg
 #pragma unroll
                 for (int e = 0; e < 8; ++e) dsv[e] = dp[kt][8 * cc + e];
                 pack_frag(dsb, dsv);
-                const int row0 = kt * 32 + 16 * cc + 4 * g;
 #pragma unroll
                 for (int t = 0; t < ND; ++t) {
                     Frag<T> fk;
-                    tile_tr_frag<D>(fk, sK, row0, row0 + 8, 32 * t, lane);
+                    if constexpr (kBf16) {
+                        const uint32_t rb = (kt * 32 + 16 * cc) * D * 2;
+                        const bf16x4 x0 = lds_tr(lo.tr[t][0], rb), x1 = lds_tr(lo.tr[t][1], rb);
+                        fk.v = bf16x8{x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
+                    } else {
+                        const int row0 = kt * 32 + 16 * cc + 4 * g;
+                        tile_tr_frag<D>(fk, smem + BUF * TILE, row0, row0 + 8, 32 * t, lane);
+                    }
                     mma(dq[t], fk, dsb);
                 }
             }
         }
+    };
+
+    auto step = [&](auto mask_c, int kb) {
+        const int k0 = kb * kQBN;
+        wait_vmcnt<0>();
+        __syncthreads();
+        if (kb + 1 < nkb) {
+            const uint32_t nb = (uint32_t)((kb + 1) & 1);
+            pk.issue(lds + nb * TB, rk, (uint32_t)(k0 + kQBN) * kbytes, wave);
+            pv.issue(lds + (2 + nb) * TB, rv, (uint32_t)(k0 + kQBN) * vbytes, wave);
+        }
+        tile(mask_c, k0);
+        if constexpr (kBf16) {
+#pragma unroll
+            for (int c = 0; c < NC; ++c) lo.row[c] += flip;
+#pragma unroll
+            for (int t = 0; t < ND; ++t) {
+                lo.tr[t][0] += flip;
+                lo.tr[t][1] += flip;
+            }
+        }
+        flip = -flip;
+    };
+
+    if (nkb > 0) {
+        pk.issue(lds, rk, 0u, wave);
+        pv.issue(lds + 2 * TB, rv, 0u, wave);
     }
+    const int n_full = min(nkb, min(kv_end, a.mask.causal ? q0 + 1 : S) / kQBN);
+    for (int kb = 0; kb < n_full; ++kb) step(std::false_type{}, kb);
+    for (int kb = n_full; kb < nkb; ++kb) step(std::true_type{}, kb);
 
     if (qi < S) {
         T* dqrow = static_cast<T*>(a.dq) + a.mdq.head_base(b, h) + (int64_t)qi * a.mdq.ss;
@@ -434,6 +532,19 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) void attn_bwd_q(BwdArg
     }
 }
 
+// Explicit instantiations: the host-side launch stubs of every kernel used below.
+#define FBL_BWD_KERNELS(T, D)                                 \
+    template __global__ void attn_bwd_stats<T, D>(BwdArgs); \
+    template __global__ void attn_bwd_kv<T, D>(BwdArgs);    \
+    template __global__ void attn_bwd_q<T, D>(BwdArgs);
+FBL_BWD_KERNELS(float, 32)
+FBL_BWD_KERNELS(float, 64)
+FBL_BWD_KERNELS(float, 128)
+FBL_BWD_KERNELS(bf16, 32)
+FBL_BWD_KERNELS(bf16, 64)
+FBL_BWD_KERNELS(bf16, 128)
+#undef FBL_BWD_KERNELS
+
 template <typename K>
 hipError_t set_lds(K kernel, int bytes) {
     return hipFuncSetAttribute(reinterpret_cast<const void*>(kernel), hipFuncAttributeMaxDynamicSharedMemorySize,
@@ -443,7 +554,7 @@ hipError_t set_lds(K kernel, int bytes) {
 template <typename T, int D>
 hipError_t set_bwd_lds() {
     static hipError_t once = [] {
-        const hipError_t e = set_lds(&attn_bwd_kv<T, D>, KvSmem<T, D>::BYTES);
+        const hipError_t e = set_lds(&attn_bwd_kv<T, D>, KvCfg<T, D>::BYTES);
         if (e != hipSuccess) return e;
         return set_lds(&attn_bwd_q<T, D>, QSmem<T, D>::BYTES);
     }();
@@ -466,7 +577,7 @@ hipError_t launch_attn_bwd(const BwdArgs& a, unsigned phases, hipStream_t stream
     }
     if (phases & 2u) {
         const int n = (a.S + kKvBN - 1) / kKvBN * a.Hkv * a.B;
-        constexpr int lds = KvSmem<T, D>::BYTES;
+        constexpr int lds = KvCfg<T, D>::BYTES;
         hipLaunchKernelGGL((attn_bwd_kv<T, D>), dim3(padded8(n)), dim3(256), lds, stream, a);
     }
     if (phases & 4u) {

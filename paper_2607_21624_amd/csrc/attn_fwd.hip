@@ -121,6 +121,7 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) void attn_fwd_kernel(F
     dv.init(vbytes, wave, lane);
     LaneOffsets<D> lo;
     if constexpr (kBf16) lo.init(lds_addr(fwd_smem), lane);
+    int32_t flip = (int32_t)TB;  // moves the lane addresses to the other buffer pair
 
     // One key tile: scores, online softmax, and the P V update.  The lane
     // offsets in `lo` point into the buffer pair holding the current tile;
@@ -216,13 +217,14 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) void attn_fwd_kernel(F
         tile(mask_c, k0);
         if constexpr (kBf16) {
 #pragma unroll
-            for (int cc = 0; cc < NC; ++cc) lo.row[cc] ^= TB;
+            for (int cc = 0; cc < NC; ++cc) lo.row[cc] += flip;
 #pragma unroll
             for (int t = 0; t < ND; ++t) {
-                lo.tr[t][0] ^= TB;
-                lo.tr[t][1] ^= TB;
+                lo.tr[t][0] += flip;
+                lo.tr[t][1] += flip;
             }
         }
+        flip = -flip;
     };
 
     if (nkb > 0) {
@@ -253,6 +255,13 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) void attn_fwd_kernel(F
         }
     }
 }
+
+template __global__ void attn_fwd_kernel<float, 32>(FwdArgs);
+template __global__ void attn_fwd_kernel<float, 64>(FwdArgs);
+template __global__ void attn_fwd_kernel<float, 128>(FwdArgs);
+template __global__ void attn_fwd_kernel<bf16, 32>(FwdArgs);
+template __global__ void attn_fwd_kernel<bf16, 64>(FwdArgs);
+template __global__ void attn_fwd_kernel<bf16, 128>(FwdArgs);
 
 template <typename T, int D>
 constexpr int fwd_lds_bytes() {

@@ -60,21 +60,16 @@ template <typename T, int D, int ROWS, int NWAVES>
 FBL_DEV void dma_tile(T* tile, Rsrc rs, int row0, uint32_t row_bytes, int wave, int lane) {
     using G = TileGeom<T, D>;
     constexpr int INSTS = ROWS * G::CPR / 64;
-    static_assert(INSTS % NWAVES == 0, "equal share of tile loads per wave");
 #pragma unroll
-    for (int j = 0; j < INSTS / NWAVES; ++j) {
+    for (int j = 0; j < (INSTS + NWAVES - 1) / NWAVES; ++j) {
         const int i = j * NWAVES + wave;
+        if (INSTS % NWAVES != 0 && i >= INSTS) break;
         const int q = i * 64 + lane;
         const int r = q / G::CPR;
         const int c = (q % G::CPR) ^ G::swz(r);
         const uint32_t voff = (uint32_t)(row0 + r) * row_bytes + (uint32_t)c * 16u;
         __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (FBL_LDS void*)(tile + i * 64 * G::EPC), 16, voff, 0, 0, 0);
     }
-}
-
-template <typename T, int D, int ROWS, int NWAVES>
-constexpr int dma_loads_per_thread() {
-    return ROWS * TileGeom<T, D>::CPR / 64 / NWAVES;
 }
 
 // Wait until at most N vector-memory loads of this wave are outstanding.
@@ -173,13 +168,13 @@ template <typename T, int D, int ROWS, int NWAVES>
 struct DmaPlan {
     using G = TileGeom<T, D>;
     static constexpr int INSTS = ROWS * G::CPR / 64;
-    static constexpr int PER_WAVE = INSTS / NWAVES;
-    static_assert(INSTS % NWAVES == 0, "equal share of tile loads per wave");
+    static constexpr int PER_WAVE = (INSTS + NWAVES - 1) / NWAVES;
+    static_assert(INSTS >= 1, "a tile is at least one 1 KB load");
     uint32_t voff[PER_WAVE];
     FBL_DEV void init(uint32_t row_bytes, int wave, int lane) {
 #pragma unroll
         for (int j = 0; j < PER_WAVE; ++j) {
-            const int q = (j * NWAVES + wave) * 64 + lane;
+            const int q = ((j * NWAVES + wave) % INSTS) * 64 + lane;
             const int r = q / G::CPR;
             const int c = (q % G::CPR) ^ G::swz(r);
             voff[j] = (uint32_t)r * row_bytes + (uint32_t)c * 16u;
@@ -188,9 +183,12 @@ struct DmaPlan {
     // Loads rows row0.. of the tile at LDS byte address `tile`.
     FBL_DEV void issue(FBL_LDS char* tile, Rsrc rs, uint32_t row0_bytes, int wave) const {
 #pragma unroll
-        for (int j = 0; j < PER_WAVE; ++j)
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (FBL_LDS void*)(tile + (j * NWAVES + wave) * 1024), 16, voff[j],
-                                                     row0_bytes, 0, 0);
+        for (int j = 0; j < PER_WAVE; ++j) {
+            const int i = j * NWAVES + wave;
+            if (INSTS % NWAVES == 0 || i < INSTS)
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (FBL_LDS void*)(tile + i * 1024), 16, voff[j], row0_bytes,
+                                                         0, 0);
+        }
     }
 };
 

@@ -53,7 +53,7 @@ struct BwdArgs {
     void* dq;
     void* dk;
     void* dv;
-    f32x2* stats;      // workspace [B, Hq, S]: (LSE * log2(e), sum_k dO*O) per query row
+    float* stats;      // workspace [B, Hq, 2, S]: rows LSE * log2(e) and sum_k dO*O per query
     TokMap mq, mk, mv, mo, mdo, mdq, mdk, mdv;
     int B, S, Hq, Hkv;
     float scale;       // softmax scale
