@@ -182,25 +182,29 @@ def main():
     total_ms = start.elapsed_time(stop)
     ms_per_step = total_ms / args.steps
     k_fwd = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
-    k_pre = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
-    k_main = float(np.mean([e[2].elapsed_time(e[3]) for e in evs]))
-    k_dq = float(np.mean([e[3].elapsed_time(e[4]) for e in evs]))
+    k_stats = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
+    k_kv = float(np.mean([e[2].elapsed_time(e[3]) for e in evs]))
+    k_q = float(np.mean([e[3].elapsed_time(e[4]) for e in evs]))
     assert torch.cuda.memory_allocated() == mem_before, "the timed steps allocated device memory"
 
     pairs = allowed_pairs(w, inp["kv_len"])
     flops = 14 * w.d * pairs
     tflops = flops / (ms_per_step * 1e-3) / 1e12
     peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
-    fwd_tf = 4 * w.d * pairs / (k_fwd * 1e-3) / 1e12
-    main_tf = 10 * w.d * pairs / (k_main * 1e-3) / 1e12
-    if k_main >= k_fwd:
-        dom = {"kernel": "attn_bwd_main", "achieved": main_tf, "flops_per_launch": 10 * w.d * pairs,
-               "avg_ms": k_main}
-    else:
-        dom = {"kernel": "attn_fwd_kernel", "achieved": fwd_tf, "flops_per_launch": 4 * w.d * pairs, "avg_ms": k_fwd}
-    roofline = {"bound": "mfma", "achieved": round(dom["achieved"], 2), "peak": peak, "unit": "TFLOP/s",
-                "frac": round(dom["achieved"] / peak, 4), "traffic": None, "kernel": dom["kernel"],
-                "avg_launch_ms": round(dom["avg_ms"], 4), "flops_per_launch": dom["flops_per_launch"]}
+    # Algorithmic FLOPs per launch (2*d per allowed pair per matrix product):
+    #   attn_fwd     QK^T, PV                                    4*d
+    #   attn_bwd_kv  QK^T recompute, dO V^T, P^T dO, dS^T Q      8*d
+    #   attn_bwd_q   dS K (its QK^T and dO V^T recomputes are    2*d
+    #                not counted: they duplicate the kv pass's)
+    per_kernel = {"attn_fwd": (k_fwd, 4), "attn_bwd_kv": (k_kv, 8), "attn_bwd_q": (k_q, 2)}
+    ktf = {n: a * w.d * pairs / (t * 1e-3) / 1e12 for n, (t, a) in per_kernel.items()}
+    executed = {"attn_fwd": 4, "attn_bwd_kv": 8, "attn_bwd_q": 6}
+    ktf_exec = {n: executed[n] * w.d * pairs / (per_kernel[n][0] * 1e-3) / 1e12 for n in per_kernel}
+    dom = max(per_kernel, key=lambda n: per_kernel[n][0])
+    t_dom, a_dom = per_kernel[dom]
+    roofline = {"bound": "mfma", "achieved": round(ktf[dom], 2), "peak": peak, "unit": "TFLOP/s",
+                "frac": round(ktf[dom] / peak, 4), "traffic": None, "kernel": dom,
+                "avg_launch_ms": round(t_dom, 4), "flops_per_launch": a_dom * w.d * pairs}
 
     kernels = None if args.no_kernel_list else dispatched_kernels(step)
     foreign = None
@@ -231,9 +235,10 @@ def main():
         "pct_peak": round(100 * tflops / peak, 2),
         "layout_copy_bytes": 0 if foreign == [] else None,
         "dispatched_kernels": kernels,
-        "kernel_ms": {"attn_fwd": round(k_fwd, 4), "attn_bwd_pre": round(k_pre, 4), "attn_bwd_main": round(k_main, 4),
-                      "attn_bwd_dq": round(k_dq, 4)},
-        "kernel_tflops": {"attn_fwd": round(fwd_tf, 2), "attn_bwd_main": round(main_tf, 2)},
+        "kernel_ms": {"attn_fwd": round(k_fwd, 4), "attn_bwd_stats": round(k_stats, 4), "attn_bwd_kv": round(k_kv, 4),
+                      "attn_bwd_q": round(k_q, 4)},
+        "kernel_tflops_algorithmic": {n: round(v, 2) for n, v in ktf.items()},
+        "kernel_tflops_executed": {n: round(v, 2) for n, v in ktf_exec.items()},
         "algorithmic_gflop": round(flops / 1e9, 3),
         "algorithmic_bytes": algorithmic_bytes(w, es)["total"],
         "roofline": roofline,

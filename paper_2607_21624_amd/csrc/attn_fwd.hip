@@ -121,26 +121,37 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) void attn_fwd_kernel(F
     dv.init(vbytes, wave, lane);
     LaneOffsets<D> lo;
     if constexpr (kBf16) lo.init(lds_addr(fwd_smem), lane);
-    int32_t flip = (int32_t)TB;  // moves the lane addresses to the other buffer pair
 
-    // One key tile: scores, online softmax, and the P V update.  The lane
-    // offsets in `lo` point into the buffer pair holding the current tile;
-    // MASK selects causal/padding masking.
-    auto tile = [&](auto mask_c, int k0) {
-        constexpr bool MASK = decltype(mask_c)::value;
-        const int BUF = (k0 / kFwdBN) & 1;
-        f32x16 s[2];
+    // Software pipeline over key tiles j: while the softmax of tile j runs on
+    // the vector ALUs, the scores of tile j+1 are already in the matrix
+    // cores.  K tiles are fetched two ahead, V tiles one ahead:
+    //   iteration j: wait for K_{j+1}, V_j; barrier; DMA K_{j+2} -> Kbuf[j%2],
+    //                V_{j+1} -> Vbuf[(j+1)%2]; S_{j+1} = Q K_{j+1}^T;
+    //                P_j = softmax(S_j); O += P_j V_j.
+    // The loop runs in pairs so buffer and score-array parities are
+    // compile-time.
+    f32x16 sc[2][2];  // scores of two tiles: [parity][32-key half]
+
+    auto qk = [&](auto par_c, int kbuf) {
+        constexpr int P = decltype(par_c)::value;
 #pragma unroll
         for (int kt = 0; kt < 2; ++kt) {
-            s[kt] = f32x16{};
+            sc[P][kt] = f32x16{};
 #pragma unroll
             for (int cc = 0; cc < NC; ++cc) {
                 Frag<T> kf;
-                if constexpr (kBf16) kf.v = lds_b128(lo.row[cc], kt * 32 * D * 2);
-                else tile_row_frag<D>(kf, smem + BUF * TILE, kt * 32 + c32, 16 * cc + 8 * g);
-                mma(s[kt], kf, qf[cc]);
+                if constexpr (kBf16) kf.v = lds_b128(lo.row[cc], kbuf * TB + kt * 32 * D * 2);
+                else tile_row_frag<D>(kf, smem + kbuf * TILE, kt * 32 + c32, 16 * cc + 8 * g);
+                mma(sc[P][kt], kf, qf[cc]);
             }
         }
+    };
+
+    // softmax of the tile in sc[P] (keys k0..k0+63) and O += P V from V buffer P
+    auto softmax_pv = [&](auto par_c, auto mask_c, int k0) {
+        constexpr int P = decltype(par_c)::value;
+        constexpr bool MASK = decltype(mask_c)::value;
+        f32x16* s = sc[P];
         if constexpr (MASK) {
 #pragma unroll
             for (int kt = 0; kt < 2; ++kt)
@@ -191,51 +202,54 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) void attn_fwd_kernel(F
                 for (int t = 0; t < ND; ++t) {
                     Frag<T> vf;
                     if constexpr (kBf16) {
-                        const uint32_t rb = 2 * TB + (kt * 32 + 16 * cc) * D * 2;
+                        const uint32_t rb = (2 + P) * TB + (kt * 32 + 16 * cc) * D * 2;
                         const bf16x4 x0 = lds_tr(lo.tr[t][0], rb), x1 = lds_tr(lo.tr[t][1], rb);
                         vf.v = bf16x8{x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
                     } else {
                         const int row0 = kt * 32 + 16 * cc + 4 * g;
-                        tile_tr_frag<D>(vf, smem + (2 + BUF) * TILE, row0, row0 + 8, 32 * t, lane);
+                        tile_tr_frag<D>(vf, smem + (2 + P) * TILE, row0, row0 + 8, 32 * t, lane);
                     }
                     mma(oacc[t], vf, pf);
                 }
             }
     };
 
-    // step kb: wait for its tile, start the next one's DMA into the other
-    // buffer pair, compute, then point the lane offsets at the other pair
-    auto step = [&](auto mask_c, int kb) {
-        const int k0 = kb * kFwdBN;
+    // iteration j (parity P = j % 2)
+    auto step = [&](auto par_c, auto mask_c, int j) {
+        constexpr int P = decltype(par_c)::value;
+        constexpr int NP = 1 - P;
         wait_vmcnt<0>();
-        __syncthreads();  // tile kb landed everywhere; the other buffer pair is free
-        if (kb + 1 < nkb) {
-            const uint32_t nb = (uint32_t)((kb + 1) & 1);
-            dk.issue(lds + nb * TB, rk, (uint32_t)(k0 + kFwdBN) * kbytes, wave);
-            dv.issue(lds + (2 + nb) * TB, rv, (uint32_t)(k0 + kFwdBN) * vbytes, wave);
+        __syncthreads();  // K_{j+1} and V_j landed; iteration j-1 is done everywhere
+        if (j + 2 < nkb) dk.issue(lds + P * TB, rk, (uint32_t)((j + 2) * kFwdBN) * kbytes, wave);
+        if (j + 1 < nkb) {
+            dv.issue(lds + (2 + NP) * TB, rv, (uint32_t)((j + 1) * kFwdBN) * vbytes, wave);
+            qk(std::integral_constant<int, NP>{}, NP);
         }
-        tile(mask_c, k0);
-        if constexpr (kBf16) {
-#pragma unroll
-            for (int cc = 0; cc < NC; ++cc) lo.row[cc] += flip;
-#pragma unroll
-            for (int t = 0; t < ND; ++t) {
-                lo.tr[t][0] += flip;
-                lo.tr[t][1] += flip;
-            }
-        }
-        flip = -flip;
+        softmax_pv(par_c, mask_c, j * kFwdBN);
     };
 
     if (nkb > 0) {
         dk.issue(lds, rk, 0u, wave);
         dv.issue(lds + 2 * TB, rv, 0u, wave);
+        if (nkb > 1) dk.issue(lds + TB, rk, (uint32_t)kFwdBN * kbytes, wave);
+        wait_vmcnt<0>();
+        __syncthreads();
+        qk(std::integral_constant<int, 0>{}, 0);
     }
-    // Tiles that lie inside kv_end and (causal) at or below the block's first
-    // query need no mask for any wave; the rest of the block's tiles do.
-    const int n_full = min(nkb, min(kv_end, a.mask.causal ? q0 + 1 : S) / kFwdBN);
-    for (int kb = 0; kb < n_full; ++kb) step(std::false_type{}, kb);
-    for (int kb = n_full; kb < nkb; ++kb) step(std::true_type{}, kb);
+    // Tiles inside kv_end and (causal) at or below the block's first query need
+    // no mask for any wave; rounded down to an even count so the masked loop
+    // also starts on parity 0.
+    const int n_full = min(nkb, min(kv_end, a.mask.causal ? q0 + 1 : S) / kFwdBN) & ~1;
+    using P0 = std::integral_constant<int, 0>;
+    using P1 = std::integral_constant<int, 1>;
+    for (int j = 0; j < n_full; j += 2) {
+        step(P0{}, std::false_type{}, j);
+        step(P1{}, std::false_type{}, j + 1);
+    }
+    for (int j = n_full; j < nkb; j += 2) {
+        step(P0{}, std::true_type{}, j);
+        if (j + 1 < nkb) step(P1{}, std::true_type{}, j + 1);
+    }
 
     l += other_half(l);
     if (qi < S) {
