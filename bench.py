@@ -44,13 +44,43 @@ def allowed_pairs(w, kv_len) -> int:
 
 
 def algorithmic_bytes(w, es: int) -> dict:
-    """Minimum HBM traffic: fwd reads Q,K,V and writes O,LSE; bwd reads
-    Q,K,V,O,dO,LSE and writes dQ,dK,dV (workspace excluded)."""
+    """Minimum HBM traffic per kernel launch (each tensor read or written once)."""
     nq = w.B * w.S * w.Hq * w.d * es
     nk = w.B * w.S * w.Hkv * w.d * es
     lse = w.B * w.Hq * w.S * 4
-    return {"fwd": nq + 2 * nk + nq + lse, "bwd_main": nq + 2 * nk + nq + lse + 2 * nk,
-            "total": (nq + 2 * nk + nq + lse) + (nq + 2 * nk + 2 * nq + lse + nq + 2 * nk)}
+    stats = 2 * lse
+    return {"attn_fwd": 2 * nq + 2 * nk + lse,              # read Q K V, write O LSE
+            "attn_bwd_stats": 2 * nq + lse + stats,         # read O dO LSE, write stats
+            "attn_bwd_kv": 2 * nq + 2 * nk + stats + 2 * nk,  # read Q dO K V stats, write dK dV
+            "attn_bwd_q": 2 * nq + 2 * nk + stats + nq,     # read Q dO K V stats, write dQ
+            # the step as a whole: fwd reads Q K V, writes O LSE; bwd reads Q K V O dO LSE, writes dQ dK dV
+            "total": (2 * nq + 2 * nk + lse) + (3 * nq + 2 * nk + lse + nq + 2 * nk)}
+
+
+KERNEL_SOURCES = ("attn_fwd.hip", "attn_bwd.hip", "stage.hpp", "cdna4.hpp", "tokmap.hpp")
+
+
+def measured_traffic(workload: str):
+    """HBM bytes per launch from the committed rocprofv3 FETCH_SIZE/WRITE_SIZE summary,
+    only if it was taken on the kernel sources as they are now (else None)."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", f"attn_{workload}_hbm_traffic.txt")
+    if not os.path.exists(path):
+        return None
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, "paper_2607_21624_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    out, sha = {}, None
+    for line in open(path):
+        line = line.strip()
+        if line.startswith("sha="):
+            sha = line[4:]
+        elif line and not line.startswith("#"):
+            name, *kv = line.split()
+            d = dict(x.split("=") for x in kv)
+            out[name] = int(d["fetch_bytes"]) + int(d["write_bytes"])
+    return out if sha == h.hexdigest()[:16] else None
 
 
 def cpu_baseline(w, inp, budget_s: float):
@@ -118,6 +148,9 @@ def main():
     ap.add_argument("--no-kernel-list", action="store_true",
                     help="skip the torch-profiler dispatch listing (use under rocprofv3)")
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle work for cpu_baseline")
+    ap.add_argument("--copy-mib", type=int, default=0,
+                    help="instead of attention, run 5 plain device copies of this many MiB (calibrates the HBM "
+                         "byte counters FETCH_SIZE / WRITE_SIZE against a kernel of known traffic)")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -127,6 +160,16 @@ def main():
 
     import numpy as np
     import torch
+
+    if args.copy_mib:
+        n = args.copy_mib * (1 << 20) // 2
+        src = torch.ones(n, dtype=torch.bfloat16, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_mib": args.copy_mib, "bytes_read_per_copy": 2 * n, "bytes_written_per_copy": 2 * n}))
+        return
 
     import paper_2607_21624_amd as fbl
     import synth
@@ -202,9 +245,17 @@ def main():
     ktf_exec = {n: executed[n] * w.d * pairs / (per_kernel[n][0] * 1e-3) / 1e12 for n in per_kernel}
     dom = max(per_kernel, key=lambda n: per_kernel[n][0])
     t_dom, a_dom = per_kernel[dom]
+    es = 2 if w.dtype == "bf16" else 4
+    alg_bytes = algorithmic_bytes(w, es)
+    traffic = measured_traffic(w.name)
+    dom_traffic = None
+    if traffic is not None:
+        key = "attn_fwd_kernel" if dom == "attn_fwd" else dom
+        dom_traffic = traffic.get(key)
     roofline = {"bound": "mfma", "achieved": round(ktf[dom], 2), "peak": peak, "unit": "TFLOP/s",
-                "frac": round(ktf[dom] / peak, 4), "traffic": None, "kernel": dom,
-                "avg_launch_ms": round(t_dom, 4), "flops_per_launch": a_dom * w.d * pairs}
+                "frac": round(ktf[dom] / peak, 4), "traffic": dom_traffic, "kernel": dom,
+                "avg_launch_ms": round(t_dom, 4), "flops_per_launch": a_dom * w.d * pairs,
+                "algorithmic_bytes_per_launch": alg_bytes[dom]}
 
     kernels = None if args.no_kernel_list else dispatched_kernels(step)
     foreign = None
@@ -215,7 +266,6 @@ def main():
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(w, inp, args.cpu_budget)
 
-    es = 2 if w.dtype == "bf16" else 4
     line = {
         "metric": "attn fwd+bwd TFLOP/s & % bf16 MFMA peak at 1 GPU; layout-copy bytes (=0)",
         "value": round(tflops, 2),
@@ -240,7 +290,7 @@ def main():
         "kernel_tflops_algorithmic": {n: round(v, 2) for n, v in ktf.items()},
         "kernel_tflops_executed": {n: round(v, 2) for n, v in ktf_exec.items()},
         "algorithmic_gflop": round(flops / 1e9, 3),
-        "algorithmic_bytes": algorithmic_bytes(w, es)["total"],
+        "algorithmic_bytes": alg_bytes["total"],
         "roofline": roofline,
         "cpu_baseline": cpu,
     }
