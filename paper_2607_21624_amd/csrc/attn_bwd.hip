@@ -108,7 +108,7 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_kv(BwdArgs a) {
     constexpr int TB = C::TB;
     constexpr bool kBf16 = sizeof(T) == 2;
     extern __shared__ __attribute__((aligned(1024))) unsigned char kv_smem[];
-    FBL_LDS char* lds = (FBL_LDS char*)kv_smem;
+    const uint32_t lds = lds_addr(kv_smem);  // LDS byte address of the tiles
 
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -195,9 +195,7 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_kv(BwdArgs a) {
         po.issue(lds + (2 + buf) * TB, ro, (uint32_t)q0 * obytes, wave);
         if (wave < 2) {  // wave 0: lse2 of the block's queries, wave 1: D
             const float* row = a.stats + (2 * ((int64_t)b * a.Hq + h) + wave) * S;
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(make_rsrc(row, (uint32_t)(S * 4)),
-                                                     (FBL_LDS void*)(lds + C::OFF_STATS + (2 * wave + buf) * 256), 4,
-                                                     (uint32_t)(q0 + lane) * 4u, 0, 0, 0);
+            dma4(make_rsrc(row, (uint32_t)(S * 4)), lds + C::OFF_STATS + (2 * wave + buf) * 256, (uint32_t)lane * 4u, (uint32_t)q0 * 4u);
         }
     };
 
@@ -347,7 +345,7 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) void attn_bwd_q(BwdArg
     constexpr bool kBf16 = sizeof(T) == 2;
     extern __shared__ __attribute__((aligned(1024))) unsigned char q_smem[];
     T* smem = reinterpret_cast<T*>(q_smem);
-    FBL_LDS char* lds = (FBL_LDS char*)q_smem;
+    const uint32_t lds = lds_addr(q_smem);  // LDS byte address of the tiles
 
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -576,9 +574,14 @@ hipError_t launch_attn_bwd(const BwdArgs& a, unsigned phases, hipStream_t stream
         hipLaunchKernelGGL((attn_bwd_stats<T, D>), dim3((unsigned)((nrows + RPB - 1) / RPB)), dim3(256), 0, stream, a);
     }
     if (phases & 2u) {
+        if constexpr (sizeof(T) == 2) {
+            const hipError_t ek = launch_attn_bwd_kv_bf16<D>(a, stream);
+            if (ek != hipSuccess) return ek;
+        } else {
         const int n = (a.S + kKvBN - 1) / kKvBN * a.Hkv * a.B;
         constexpr int lds = KvCfg<T, D>::BYTES;
         hipLaunchKernelGGL((attn_bwd_kv<T, D>), dim3(padded8(n)), dim3(256), lds, stream, a);
+        }
     }
     if (phases & 4u) {
         const int n = (a.S + kQBM - 1) / kQBM * a.Hq * a.B;

@@ -1,0 +1,414 @@
+// attn_bwd_kv.hip -- key/value-major backward pass for bf16 storage, gfx950.
+//
+// Computes dV = P^T dO and dK = scale dS^T Q (section 4.1, the reductions
+// over queries: "reduce along M" of section 4.2) for one workgroup of 128
+// keys of one (batch, kv head), over the query blocks of every query head of
+// the GQA group.  Each wavefront keeps its 32 K and V rows as MFMA operands
+// and its dK^T, dV^T accumulators in registers for the whole pass.
+//
+// Per query block i the wavefront runs four products and an elementwise step:
+//   S_i  = Q_i K_w^T,  dP_i = dO_i V_w^T        (row reads of the Q/dO tiles)
+//   P_i  = exp2(S_i scale log2e - LSE_i log2e), dS_i = P_i (dP_i - D_i)
+//   dV^T += dO_i^T P_i,  dK^T += Q_i^T dS_i      (transposed reads)
+// With one wavefront per SIMD (the accumulators take half the register file)
+// nothing else hides latency, and every instruction the wavefront issues
+// besides the products costs time, so the loop is software-pipelined by hand:
+//   phase X(i): S/dP products of block i+1  |  elementwise step of block i
+//   barrier; DMA of block i+3
+//   phase Y(i): dV/dK products of block i   |  LDS reads of block i's
+//               transposed operands and block i+2's row operands
+// Operands are read a few product slots ahead of their use (kLead).  Four
+// LDS buffers: while blocks i..i+2 are resident, block i+3 streams in by DMA
+// (global -> LDS, no registers) a full iteration before it is first read.  The
+// loop is unrolled over the four buffers so that every LDS address is a
+// per-lane base plus an immediate.
+#include <type_traits>
+
+#include "cdna4.hpp"
+#include "kernels.hpp"
+#include "stage.hpp"
+#include "tokmap.hpp"
+
+namespace fbl {
+
+namespace {
+
+constexpr int kPWaves = 4;
+constexpr int kPKeys = 32 * kPWaves;  // keys per workgroup
+constexpr int kLead = 4;              // product slots between an operand read and its use
+
+template <int D>
+struct KvPipe {
+    static constexpr int BQ = D == 128 ? 32 : 64;  // queries per block (register budget)
+    static constexpr int NQT = BQ / 32;
+    static constexpr int TB = BQ * D * 2;  // bytes of one bf16 Q or dO tile
+    static constexpr int NBUF = 4;
+    static constexpr int BUFB = 2 * TB;            // buffer: Q tile, dO tile
+    // per buffer, the block's LSE*log2e and D rows (64 floats each: one dword
+    // per lane of a 64-lane DMA; the first BQ are used)
+    static constexpr int OFF_ST = NBUF * BUFB;
+    static constexpr int STB = 512;
+    static constexpr int SPARE = OFF_ST + NBUF * STB;  // sink of the statistics loads of waves 2, 3
+    static constexpr int BYTES = SPARE + 256;
+    static_assert(BUFB % 256 == 0, "tiles start on a 256-byte (all-bank) boundary");
+    static_assert((NBUF - 1) * BUFB + TB + 2 * 16 * D + (NQT - 1) * 32 * D * 2 < 65536,
+                  "buffer offsets fit the 16-bit LDS immediate");
+    static_assert(BYTES <= 160 * 1024, "LDS of one workgroup");
+};
+
+template <int D>
+__global__ __launch_bounds__(256, 1) void attn_bwd_kv_bf16(BwdArgs a) {
+    using P = KvPipe<D>;
+    constexpr int NC = D / 16;
+    constexpr int ND = D / 32;
+    constexpr int BQ = P::BQ;
+    constexpr int NQT = P::NQT;
+    constexpr int TB = P::TB;
+    constexpr int BUFB = P::BUFB;
+    extern __shared__ __attribute__((aligned(1024))) unsigned char kvp_smem[];
+    const uint32_t lds = lds_addr(kvp_smem);
+
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int g = lane >> 5;
+    const int c32 = lane & 31;
+    const int S = a.S;
+    const int nkb = (S + kPKeys - 1) / kPKeys;
+    const int logical = xcd_logical_id(blockIdx.x, nkb * a.Hkv * a.B, gridDim.x);
+    if (logical < 0) return;
+    const int kblk = logical % nkb;
+    const int hk = (logical / nkb) % a.Hkv;
+    const int b = logical / (nkb * a.Hkv);
+    const int G_ = a.Hq / a.Hkv;
+    int kv_end = S;
+    if (a.mask.kv_len) kv_end = min(max(a.mask.kv_len[b], 0), S);
+    const int k0 = kblk * kPKeys;
+    const int kw0 = k0 + wave * 32;  // first key of this wave
+    const int key = kw0 + c32;       // this lane's key (column of S)
+
+    // K and V rows of this wave's keys as B operands: lane <-> key, in-lane d = 16c + 8g + e
+    Frag<bf16> kf[NC], vf[NC];
+    {
+        const bf16* kp = static_cast<const bf16*>(a.k) + a.mk.head_base(b, hk) + (int64_t)key * a.mk.ss + 8 * g;
+        const bf16* vp = static_cast<const bf16*>(a.v) + a.mv.head_base(b, hk) + (int64_t)key * a.mv.ss + 8 * g;
+#pragma unroll
+        for (int c = 0; c < NC; ++c) {
+            kf[c].v = bf16x8{};
+            vf[c].v = bf16x8{};
+            if (key < S) {
+                kf[c].v = __builtin_bit_cast(bf16x8, load16(kp + 16 * c));
+                vf[c].v = __builtin_bit_cast(bf16x8, load16(vp + 16 * c));
+            }
+        }
+    }
+    // dK^T and dV^T: accumulator rows = d (32t + acc_row), columns = keys (lane)
+    f32x16 dk[ND], dv[ND];
+#pragma unroll
+    for (int t = 0; t < ND; ++t) {
+        dk[t] = f32x16{};
+        dv[t] = f32x16{};
+    }
+
+    const int qb_start = a.mask.causal ? (k0 / BQ) : 0;
+    const int nqb = (S + BQ - 1) / BQ;
+    const int per_head = nqb - qb_start;
+    const int n_iter = (k0 < kv_end) ? G_ * per_head : 0;
+    // Blocks of each head whose scores need the causal mask: those holding a
+    // query before one of the workgroup's keys.  Keys at or past kv_end need no
+    // mask: a key's P and dS only reach that key's own dK and dV rows, which are
+    // stored as zeros.
+    const int n_mask = a.mask.causal ? min(per_head, (k0 + kPKeys - 2) / BQ - qb_start + 1) : 0;
+
+    // ---- DMA of the Q, dO tiles and the row statistics of one block
+    const uint32_t qbytes = (uint32_t)(a.mq.ss * 2), obytes = (uint32_t)(a.mdo.ss * 2);
+    const uint32_t qspan = (uint32_t)((int64_t)(S - 1) * a.mq.ss * 2 + D * 2);
+    const uint32_t ospan = (uint32_t)((int64_t)(S - 1) * a.mdo.ss * 2 + D * 2);
+    DmaPlan<bf16, D, BQ, kPWaves> pq, po;
+    pq.init(qbytes, wave, lane);
+    po.init(obytes, wave, lane);
+    const bf16* q_head = static_cast<const bf16*>(a.q) + a.mq.head_base(b, hk * G_);
+    const bf16* o_head = static_cast<const bf16*>(a.dout) + a.mdo.head_base(b, hk * G_);
+    // wave 0 loads the LSE*log2e row, wave 1 the D row, waves 2 and 3 nothing
+    // (no records) into a spare slot
+    const float* st_head = a.stats + (2 * ((int64_t)b * a.Hq + hk * G_) + (wave & 1)) * S;
+    const uint32_t st_bytes = wave < 2 ? (uint32_t)S * 4u : 0u;
+    const uint32_t st_lds0 = wave < 2 ? lds + P::OFF_ST + wave * 256 : lds + P::SPARE;
+    const uint32_t st_step = wave < 2 ? P::STB : 0;
+    Rsrc rq = make_rsrc(q_head, qspan), ro = make_rsrc(o_head, ospan), rst = make_rsrc(st_head, st_bytes);
+    uint32_t dma_q0 = (uint32_t)(qb_start * BQ);  // first query of the next block to stage
+    int dma_j = 0;                                // its index within its head
+    // A block is staged in NPART loads per wave (Q tile, dO tile, statistics
+    // row).
+    constexpr int NPQ = DmaPlan<bf16, D, BQ, kPWaves>::PER_WAVE;
+    static_assert(DmaPlan<bf16, D, BQ, kPWaves>::INSTS % kPWaves == 0, "whole loads per wave");
+    constexpr int NPART = 2 * NPQ + 1;
+    auto issue_part = [&](auto buf_c, int part) {
+        constexpr int BB = decltype(buf_c)::value;
+        if (part < NPQ)
+            dma16(rq, lds + BB * BUFB + (part * kPWaves + wave) * 1024, pq.voff[part], dma_q0 * qbytes);
+        else if (part < 2 * NPQ)
+            dma16(ro, lds + BB * BUFB + TB + ((part - NPQ) * kPWaves + wave) * 1024, po.voff[part - NPQ],
+                  dma_q0 * obytes);
+        else
+            dma4(rst, st_lds0 + BB * st_step, (uint32_t)lane * 4u, dma_q0 * 4u);
+    };
+    auto advance_dma = [&]() {
+        dma_q0 += BQ;
+        if (++dma_j == per_head) {  // next query head of the group
+            dma_j = 0;
+            dma_q0 = (uint32_t)(qb_start * BQ);
+            q_head += a.mq.sh;
+            o_head += a.mdo.sh;
+            st_head += 2 * S;
+            rq = make_rsrc(q_head, qspan);
+            ro = make_rsrc(o_head, ospan);
+            rst = make_rsrc(st_head, st_bytes);
+        }
+    };
+    auto issue = [&](auto buf_c) {
+#pragma unroll
+        for (int part = 0; part < NPART; ++part) issue_part(buf_c, part);
+        advance_dma();
+    };
+    // (measured: spreading the loads over the products of phase Y, or moving
+    // the accumulator reads there, is slower -- with one wavefront per SIMD
+    // every non-product instruction costs issue time wherever it sits)
+
+    // ---- per-lane LDS addresses of buffer 0; buffers are reached by immediates
+    LaneOffsets<D> lo;
+    lo.init(lds, lane);
+    const uint32_t st_a = lds + P::OFF_ST + 16u * g;  // LSE of queries 4g.. (D at +256)
+
+    // S/dP products of a block: product k is S (k even) or dP (k odd) of query
+    // tile qt = k / (2 NC) over d-chunk c = (k / 2) % NC; its A operand is one
+    // row fragment of the Q or dO tile.
+    constexpr int NSDP = 2 * NQT * NC;
+    Frag<bf16> fa[NSDP];
+    auto read_row = [&](auto buf_c, int k) {
+        constexpr int BB = decltype(buf_c)::value;
+        const int qt = k / (2 * NC), c = (k / 2) % NC;
+        fa[k].v = lds_b128(lo.row[c], BB * BUFB + (k % 2 ? TB : 0) + qt * 32 * D * 2);
+    };
+    // S and dP accumulators of the block whose products are in flight: lane <->
+    // key, in-lane query 32qt + acc_row.  At the start of each phase X their
+    // values move to vector registers (the elementwise step reads them there)
+    // and the accumulators start the next block.
+    f32x16 s_acc[NQT], dp_acc[NQT];
+    auto sdp_one = [&](int k) {
+        const int qt = k / (2 * NC), c = (k / 2) % NC;
+        if (k % 2 == 0) {
+            if (c == 0) s_acc[qt] = f32x16{};
+            mma(s_acc[qt], fa[k], kf[c]);
+        } else {
+            if (c == 0) dp_acc[qt] = f32x16{};
+            mma(dp_acc[qt], fa[k], vf[c]);
+        }
+    };
+    // dV/dK products of a block: product m is dV^T += dO^T P (m even) or
+    // dK^T += Q^T dS (m odd) for d-tile t = (m / 2) % ND over the 16 queries of
+    // chunk cc = (m / (2 ND)) % 2 of query tile qt = m / (4 ND); its A operand is
+    // two transposed reads.
+    constexpr int NCM = NQT * 2 * ND * 2;
+    static_assert(NCM == NSDP, "one row read per dV/dK product slot");
+    bf16x4 trv[2 * NCM];
+    auto read_tr = [&](auto buf_c, int m) {
+        constexpr int BB = decltype(buf_c)::value;
+        const int qt = m / (4 * ND), cc = (m / (2 * ND)) % 2, t = (m / 2) % ND;
+        const uint32_t off = BB * BUFB + (qt * 32 + 16 * cc) * D * 2 + (m % 2 ? 0 : TB);
+        trv[2 * m] = lds_tr(lo.tr[t][0], off);
+        trv[2 * m + 1] = lds_tr(lo.tr[t][1], off);
+    };
+    // row statistics (LSE*log2e, D) of a block: per lane, its 16 query rows per tile
+    constexpr int NST = 2 * NQT * 4;
+    f32x4 st[NST];  // index (qt * 4 + rr) * 2 + {0: LSE, 1: D}
+    auto read_st = [&](auto buf_c, int i) {
+        constexpr int BB = decltype(buf_c)::value;
+        const int qt = i / 8, rr = (i / 2) % 4;
+        st[i] = *(const FBL_LDS f32x4*)(uintptr_t)(st_a + BB * P::STB + (i % 2) * 256 + (qt * 32 + 8 * rr) * 4);
+    };
+
+    // Elementwise work of phase X spread over its product slots: slot k takes
+    // elements [el0(k), el0(k+1)); the first two slots take none (the
+    // statistics reads are landing).
+    constexpr int NEL = 16 * NQT;
+    auto el0 = [](int k) { return k < 2 ? 0 : (k - 2) * NEL / (NSDP - 2); };
+
+    // One iteration on block `it`, held in buffer B; j is its index within its
+    // head's blocks.
+    auto step = [&](auto buf_c, int it, int j) {
+        constexpr int B = decltype(buf_c)::value;
+        using B2 = std::integral_constant<int, (B + 2) % 4>;
+        using B3 = std::integral_constant<int, (B + 3) % 4>;
+        // ---------------- phase X
+        __builtin_amdgcn_sched_barrier(0);
+        float sv[NEL], dpv[NEL];  // S and dP of block it, out of the accumulators
+#pragma unroll
+        for (int e = 0; e < NEL; ++e) {
+            sv[e] = s_acc[e / 16][e % 16];
+            dpv[e] = dp_acc[e / 16][e % 16];
+            asm volatile("" : "+v"(sv[e]), "+v"(dpv[e]));
+        }
+        // row statistics of block it (the first element needs them two slots later)
+#pragma unroll
+        for (int i = 0; i < NST; ++i) read_st(buf_c, i);
+        float pv[NEL], dsv[NEL];
+        Frag<bf16> pb[NQT][2], dsb[NQT][2];
+#pragma unroll
+        for (int k = 0; k < NSDP; ++k) {
+            // product k of block it+1 (stale operands past the last block: unused)
+            sdp_one(k);
+            // the first transposed operands of phase Y
+            if (k >= NSDP - kLead) read_tr(buf_c, k - (NSDP - kLead));
+#pragma unroll
+            for (int e = el0(k); e < el0(k + 1); ++e) {
+                const int qt = e / 16, r = e % 16, i = (qt * 4 + r / 4) * 2;
+                float p = fast_exp2(__builtin_fmaf(sv[e], a.scale_log2, -st[i][r % 4]));
+                float ds = p * (dpv[e] - st[i + 1][r % 4]);
+                // pin: keeps this element's arithmetic in its slot (pure
+                // arithmetic is otherwise free to drift towards its uses)
+                asm volatile("" : "+v"(p), "+v"(ds));
+                pv[e] = p;
+                dsv[e] = ds;
+                if (e % 8 == 7) {
+                    pack_frag(pb[qt][r / 8], pv + e - 7);
+                    pack_frag(dsb[qt][r / 8], dsv + e - 7);
+                }
+            }
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        // causal mask on the diagonal blocks, applied to the packed P and dS:
+        // query row acc_row(r, 0) + 4g of tile qt (first query q0 + 32 qt) is
+        // kept iff it does not precede the lane's key.  Bitwise, so that a
+        // masked element's value (which may be inf) does not matter.
+        if (j < n_mask) {
+            const int q0 = (qb_start + j) * BQ;
+#pragma unroll
+            for (int qt = 0; qt < NQT; ++qt) {
+                const int thr = key - 4 * g - (q0 + 32 * qt);  // keep iff acc_row(r, 0) >= thr
+#pragma unroll
+                for (int cc = 0; cc < 2; ++cc) {
+                    uint32_t w[4];
+#pragma unroll
+                    for (int u = 0; u < 4; ++u) {
+                        const int r = 8 * cc + 2 * u;
+                        w[u] = (acc_row(r, 0) >= thr ? 0x0000ffffu : 0u) | (acc_row(r + 1, 0) >= thr ? 0xffff0000u : 0u);
+                    }
+                    using u32x4 = uint32_t __attribute__((ext_vector_type(4)));
+                    const u32x4 wm = u32x4{w[0], w[1], w[2], w[3]};
+                    pb[qt][cc].v = __builtin_bit_cast(bf16x8, __builtin_bit_cast(u32x4, pb[qt][cc].v) & wm);
+                    dsb[qt][cc].v = __builtin_bit_cast(bf16x8, __builtin_bit_cast(u32x4, dsb[qt][cc].v) & wm);
+                }
+            }
+        }
+        // ---------------- block it+2 landed in every wave; block it-1's buffer is free
+        wait_vmcnt<0>();
+        __syncthreads();
+        const bool stage = it + 3 < n_iter;  // block it+3 exists
+        if (stage) {
+#pragma unroll
+            for (int part = 0; part < NPART; ++part) issue_part(B3{}, part);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        // ---------------- phase Y
+#pragma unroll
+        for (int m = 0; m < NCM; ++m) {
+            Frag<bf16> f;
+            f.v = bf16x8{trv[2 * m][0], trv[2 * m][1], trv[2 * m][2], trv[2 * m][3],
+                         trv[2 * m + 1][0], trv[2 * m + 1][1], trv[2 * m + 1][2], trv[2 * m + 1][3]};
+            const int qt = m / (4 * ND), cc = (m / (2 * ND)) % 2, t = (m / 2) % ND;
+            if (m % 2 == 0) mma(dv[t], f, pb[qt][cc]);
+            else mma(dk[t], f, dsb[qt][cc]);
+            if (m + kLead < NCM) read_tr(buf_c, m + kLead);
+            // row operands of block it+2, for phase X(it+1) (stale past the last block: unused)
+            read_row(B2{}, m);
+            // DMA of block it+3 into the buffer of block it-1
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        if (stage) advance_dma();
+    };
+
+    using C0 = std::integral_constant<int, 0>;
+    using C1 = std::integral_constant<int, 1>;
+    using C2 = std::integral_constant<int, 2>;
+    using C3 = std::integral_constant<int, 3>;
+    if (n_iter > 0) {
+        issue(C0{});
+        if (n_iter > 1) issue(C1{});
+        if (n_iter > 2) issue(C2{});
+        wait_vmcnt<0>();
+        __syncthreads();
+#pragma unroll
+        for (int k = 0; k < NSDP; ++k) read_row(C0{}, k);
+#pragma unroll
+        for (int k = 0; k < NSDP; ++k) sdp_one(k);
+#pragma unroll
+        for (int k = 0; k < NSDP; ++k) read_row(C1{}, k);  // stale when there is no block 1
+    }
+    // Blocks in order, four per trip (one per LDS buffer).
+    int j = 0;  // index of block `it` within its head's blocks
+    auto next_j = [&]() { j = j + 1 == per_head ? 0 : j + 1; };
+    for (int it = 0; it < n_iter; it += 4) {
+        step(C0{}, it, j);
+        next_j();
+        if (it + 1 < n_iter) {
+            step(C1{}, it + 1, j);
+            next_j();
+        }
+        if (it + 2 < n_iter) {
+            step(C2{}, it + 2, j);
+            next_j();
+        }
+        if (it + 3 < n_iter) {
+            step(C3{}, it + 3, j);
+            next_j();
+        }
+    }
+
+    // dK (times scale) and dV rows of this wave's keys: lane <-> key, 4
+    // consecutive d per store.  Keys at or past kv_end take no part: their
+    // accumulators hold unmasked (possibly non-finite) sums and are replaced
+    // by zeros.
+    if (key < S) {
+        const bool live = key < kv_end;
+        bf16* dkrow = static_cast<bf16*>(a.dk) + a.mdk.head_base(b, hk) + (int64_t)key * a.mdk.ss;
+        bf16* dvrow = static_cast<bf16*>(a.dv) + a.mdv.head_base(b, hk) + (int64_t)key * a.mdv.ss;
+#pragma unroll
+        for (int t = 0; t < ND; ++t) {
+#pragma unroll
+            for (int rr = 0; rr < 4; ++rr) {
+                const int dcol = 32 * t + 8 * rr + 4 * g;
+                float k4[4], v4[4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    k4[e] = live ? dk[t][4 * rr + e] * a.scale : 0.f;
+                    v4[e] = live ? dv[t][4 * rr + e] : 0.f;
+                }
+                store4(dkrow + dcol, k4[0], k4[1], k4[2], k4[3]);
+                store4(dvrow + dcol, v4[0], v4[1], v4[2], v4[3]);
+            }
+        }
+    }
+}
+
+template __global__ void attn_bwd_kv_bf16<32>(BwdArgs);
+template __global__ void attn_bwd_kv_bf16<64>(BwdArgs);
+template __global__ void attn_bwd_kv_bf16<128>(BwdArgs);
+
+}  // namespace
+
+template <int D>
+hipError_t launch_attn_bwd_kv_bf16(const BwdArgs& a, hipStream_t stream) {
+    static const hipError_t once = hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_bwd_kv_bf16<D>),
+                                                       hipFuncAttributeMaxDynamicSharedMemorySize, KvPipe<D>::BYTES);
+    if (once != hipSuccess) return once;
+    const int n = (a.S + kPKeys - 1) / kPKeys * a.Hkv * a.B;
+    constexpr int lds = KvPipe<D>::BYTES;
+    hipLaunchKernelGGL((attn_bwd_kv_bf16<D>), dim3((n + 7) / 8 * 8), dim3(256), lds, stream, a);
+    return hipGetLastError();
+}
+
+template hipError_t launch_attn_bwd_kv_bf16<32>(const BwdArgs&, hipStream_t);
+template hipError_t launch_attn_bwd_kv_bf16<64>(const BwdArgs&, hipStream_t);
+template hipError_t launch_attn_bwd_kv_bf16<128>(const BwdArgs&, hipStream_t);
+
+}  // namespace fbl

@@ -50,7 +50,7 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) void attn_fwd_kernel(F
     constexpr bool kBf16 = sizeof(T) == 2;
     extern __shared__ __attribute__((aligned(1024))) unsigned char fwd_smem[];
     T* smem = reinterpret_cast<T*>(fwd_smem);  // K0 K1 V0 V1, TILE elements each
-    FBL_LDS char* lds = (FBL_LDS char*)fwd_smem;
+    const uint32_t lds = lds_addr(fwd_smem);  // LDS byte address of the tiles
 
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);

@@ -19,6 +19,10 @@ hipError_t launch_attn_fwd(const FwdArgs& a, hipStream_t stream);
 template <typename T, int D>
 hipError_t launch_attn_bwd(const BwdArgs& a, unsigned phases, hipStream_t stream);
 
+// Key/value-major backward pass for bf16 storage (software-pipelined kernel).
+template <int D>
+hipError_t launch_attn_bwd_kv_bf16(const BwdArgs& a, hipStream_t stream);
+
 // Diagnostic: offsets of a token-major tensor computed by the device index map.
 hipError_t launch_layout_map(const TokMap& m, int B, int H, int S, int D, int64_t* out, hipStream_t stream);
 

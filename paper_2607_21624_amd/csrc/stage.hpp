@@ -46,30 +46,48 @@ struct TileGeom {
     static FBL_DEV int off(int r, int col) { return r * D + (((col / EPC) ^ swz(r)) * EPC) + (col % EPC); }
 };
 
-typedef __amdgpu_buffer_rsrc_t Rsrc;
-
-// Buffer resource over `bytes` bytes from `base` (raw, unswizzled; reads past
-// the end return zeros).
+// Buffer resource (four SGPRs) over `bytes` bytes from `base`: raw, no
+// swizzle, stride 0; loads past the end return zeros and touch no memory.
+typedef int Rsrc __attribute__((ext_vector_type(4)));
 FBL_DEV Rsrc make_rsrc(const void* base, uint32_t bytes) {
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+    const uint64_t p = reinterpret_cast<uint64_t>(base);
+    return Rsrc{(int)(uint32_t)p, (int)((p >> 32) & 0xffffu), (int)bytes, 0x00020000};
 }
 
-// Issue the loads of ROWS rows starting at global row `row0` into `tile`.
-// Every wave issues INSTS/NWAVES loads (one 16-byte chunk per lane each).
-template <typename T, int D, int ROWS, int NWAVES>
-FBL_DEV void dma_tile(T* tile, Rsrc rs, int row0, uint32_t row_bytes, int wave, int lane) {
-    using G = TileGeom<T, D>;
-    constexpr int INSTS = ROWS * G::CPR / 64;
-#pragma unroll
-    for (int j = 0; j < (INSTS + NWAVES - 1) / NWAVES; ++j) {
-        const int i = j * NWAVES + wave;
-        if (INSTS % NWAVES != 0 && i >= INSTS) break;
-        const int q = i * 64 + lane;
-        const int r = q / G::CPR;
-        const int c = (q % G::CPR) ^ G::swz(r);
-        const uint32_t voff = (uint32_t)(row0 + r) * row_bytes + (uint32_t)c * 16u;
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (FBL_LDS void*)(tile + i * 64 * G::EPC), 16, voff, 0, 0, 0);
-    }
+// LDS DMA: every lane moves 16 (dma16) or 4 (dma4) bytes from buffer offset
+// voff + soff straight into LDS at byte address lds + lane * size (the LDS
+// address goes in M0).
+//
+// Issued as inline assembly on purpose.  The compiler cannot tell which LDS
+// bytes a DMA writes, so after one of its own it makes the next LDS read of
+// any address wait for every outstanding global load -- which would expose
+// the full latency of the prefetch of the next tile in every loop iteration.
+// The kernels order these writes against their reads themselves: they wait
+// for their own loads (s_waitcnt vmcnt) and then meet at a workgroup barrier
+// before any wave reads the tile.  Extra loads the compiler does not know of
+// only make its own vmcnt waits stricter (loads retire in order).
+// Wait states: s_nop 0 after the M0 write (1 before an LDS DMA); the first
+// load of a batch also gets s_nop 4, for an SGPR operand written by a vector
+// instruction just before it (5 wait states).  Later loads of the batch reuse
+// operands the first one has already read.
+template <bool FIRST = true>
+FBL_DEV void dma16(Rsrc rs, uint32_t lds, uint32_t voff, uint32_t soff) {
+    if constexpr (FIRST)
+        asm volatile("s_nop 4\n\ts_nop 0\n\tbuffer_load_dwordx4 %0, %1, %2 offen lds"
+                     :
+                     : "v"(voff), "s"(rs), "s"(soff), "{m0}"(lds)
+                     : "memory");
+    else
+        asm volatile("s_nop 0\n\tbuffer_load_dwordx4 %0, %1, %2 offen lds"
+                     :
+                     : "v"(voff), "s"(rs), "s"(soff), "{m0}"(lds)
+                     : "memory");
+}
+FBL_DEV void dma4(Rsrc rs, uint32_t lds, uint32_t voff, uint32_t soff) {
+    asm volatile("s_nop 4\n\ts_nop 0\n\tbuffer_load_dword %0, %1, %2 offen lds"
+                 :
+                 : "v"(voff), "s"(rs), "s"(soff), "{m0}"(lds)
+                 : "memory");
 }
 
 // Wait until at most N vector-memory loads of this wave are outstanding.
@@ -181,13 +199,14 @@ struct DmaPlan {
         }
     }
     // Loads rows row0.. of the tile at LDS byte address `tile`.
-    FBL_DEV void issue(FBL_LDS char* tile, Rsrc rs, uint32_t row0_bytes, int wave) const {
+    FBL_DEV void issue(uint32_t tile, Rsrc rs, uint32_t row0_bytes, int wave) const {
 #pragma unroll
         for (int j = 0; j < PER_WAVE; ++j) {
             const int i = j * NWAVES + wave;
-            if (INSTS % NWAVES == 0 || i < INSTS)
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (FBL_LDS void*)(tile + i * 1024), 16, voff[j], row0_bytes,
-                                                         0, 0);
+            if (INSTS % NWAVES == 0 || i < INSTS) {
+                if (j == 0) dma16<true>(rs, tile + (uint32_t)i * 1024u, voff[j], row0_bytes);
+                else dma16<false>(rs, tile + (uint32_t)i * 1024u, voff[j], row0_bytes);
+            }
         }
     }
 };

@@ -125,6 +125,28 @@ def test_zero_and_overlong_key_lengths():
     assert not bad, bad
 
 
+@pytest.mark.parametrize("mask", [synth.MASK_KEY_PADDING, synth.MASK_KEY_PADDING | synth.MASK_CAUSAL])
+@pytest.mark.parametrize("d", [64, 128])
+def test_padding_keys_with_overflowing_scores(mask, d):
+    """Keys past kv_len carry huge values (their unmasked scores overflow exp):
+    the outputs must not see them, and their dK, dV rows must be exact zeros."""
+    w = synth.Workload("padinf", B=2, S=200, Hq=4, Hkv=2, d=d, dtype="bf16", mask=mask, len_lo=1, len_hi=1,
+                       seed=11 + d + mask)
+    inp = synth.make_inputs(w)
+    inp["kv_len"] = np.array([100, 37], dtype=np.int32)
+    for b, n in enumerate(inp["kv_len"]):
+        inp["k"][b, n:] = 300.0
+        inp["v"][b, n:] = -300.0
+    note(f"padding keys overflow d={d} mask={mask}")
+    got = gpu_fwd_bwd(inp)
+    for b, n in enumerate(inp["kv_len"]):
+        assert np.all(got["dk"][b, n:] == 0) and np.all(got["dv"][b, n:] == 0)
+    for name in ("o", "lse", "dq", "dk", "dv"):
+        assert np.all(np.isfinite(got[name]) | np.isneginf(got[name])), name
+    errs, bad = compare(got, oracle_fwd_bwd(inp), "bf16")
+    assert not bad, bad
+
+
 def test_backward_alone_from_oracle_forward():
     """Feed the oracle's O and LSE (cast to storage) to the GPU backward."""
     import torch
