@@ -214,8 +214,111 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) void attn_fwd_kernel(F
             }
     };
 
+    // bf16 iteration j (parity P): the products of S_{j+1} interleaved with the
+    // softmax of tile j, operands read from LDS kLead product slots ahead of
+    // their use, then O += P_j V_j.
+    constexpr int kLead = 4;
+    constexpr int NQK = 2 * NC;      // S^T products per tile: key half kt = k / NC, d-chunk k % NC
+    constexpr int NPV = 2 * 2 * ND;  // O^T products: d-block n % ND, chunk (n / ND) % 2, half n / (2 ND)
+    Frag<T> fk[NQK];
+    auto read_k = [&](int kbuf, int k) __attribute__((always_inline)) {
+        if constexpr (kBf16) fk[k].v = lds_b128(lo.row[k % NC], kbuf * TB + (k / NC) * 32 * D * 2);
+    };
+    bf16x4 vv[2 * NPV];
+    auto read_v = [&](int vbuf, int n) __attribute__((always_inline)) {
+        if constexpr (kBf16) {
+            const int t = n % ND, cc = (n / ND) % 2, kt = n / (2 * ND);
+            const uint32_t off = (2 + vbuf) * TB + (kt * 32 + 16 * cc) * D * 2;
+            vv[2 * n] = lds_tr(lo.tr[t][0], off);
+            vv[2 * n + 1] = lds_tr(lo.tr[t][1], off);
+        }
+    };
+    auto step_bf16 = [&](auto par_c, auto mask_c, int j) __attribute__((always_inline)) {
+        constexpr int P = decltype(par_c)::value;
+        constexpr int NP = 1 - P;
+        constexpr bool MASK = decltype(mask_c)::value;
+        wait_vmcnt<0>();
+        __syncthreads();  // K_{j+1} and V_j landed; iteration j-1 is done everywhere
+        if (j + 2 < nkb) dk.issue(lds + P * TB, rk, (uint32_t)((j + 2) * kFwdBN) * kbytes, wave);
+        const bool more = j + 1 < nkb;
+        if (more) dv.issue(lds + (2 + NP) * TB, rv, (uint32_t)((j + 1) * kFwdBN) * vbytes, wave);
+        f32x16* s = sc[P];
+        const int k0 = j * kFwdBN;
+        if constexpr (MASK) {
+#pragma unroll
+            for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int key = k0 + kt * 32 + acc_row(r, g);
+                    if (key >= kv_end || (a.mask.causal && key > qi)) s[kt][r] = -INFINITY;
+                }
+        }
+#pragma unroll
+        for (int k = 0; k < kLead; ++k) read_k(NP, k);
+        __builtin_amdgcn_sched_barrier(0);
+        // slots 0..3: products of S_{j+1} with the row maximum of tile j
+        float mx = -INFINITY;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            if (k % NC == 0) sc[NP][k / NC] = f32x16{};
+            mma(sc[NP][k / NC], fk[k], qf[k % NC]);
+            read_k(NP, k + kLead);
+#pragma unroll
+            for (int e = 8 * k; e < 8 * k + 8; ++e) mx = fmaxf(mx, s[e / 16][e % 16]);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        mx = fmaxf(mx, other_half(mx)) * c;
+        if (__any(mx > m + kRescaleSlack)) {
+            const float m_new = fmaxf(m, mx);
+            const float alpha = (m_new == -INFINITY) ? 1.f : fast_exp2(m - m_new);  // 0 when m was -inf
+            l *= alpha;
+#pragma unroll
+            for (int t = 0; t < ND; ++t) oacc[t] *= alpha;
+            m = m_new;
+        }
+        const float nm = (m == -INFINITY) ? 0.f : -m;
+        __builtin_amdgcn_sched_barrier(0);
+        // slots 4..NQK-1: the remaining products with exp2, row sum and packing
+        constexpr int NSL = NQK - 4;
+        float pv[32];
+        Frag<T> pf[2][2];
+#pragma unroll
+        for (int k = 4; k < NQK; ++k) {
+            if (k % NC == 0) sc[NP][k / NC] = f32x16{};
+            mma(sc[NP][k / NC], fk[k], qf[k % NC]);
+            if (k + kLead < NQK) read_k(NP, k + kLead);
+#pragma unroll
+            for (int e = (k - 4) * 32 / NSL; e < (k - 3) * 32 / NSL; ++e) {
+                const float x = s[e / 16][e % 16];
+                float p = fast_exp2(__builtin_fmaf(x, c, nm));
+                if constexpr (MASK) p = x == -INFINITY ? 0.f : p;
+                asm volatile("" : "+v"(p));
+                pv[e] = p;
+                l += p;
+                if (e % 8 == 7) pack_frag(pf[e / 16][(e % 16) / 8], pv + e - 7);
+            }
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        // O^T += V^T P^T over the 64 keys
+#pragma unroll
+        for (int n = 0; n < kLead; ++n) read_v(P, n);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int n = 0; n < NPV; ++n) {
+            const int t = n % ND, cc = (n / ND) % 2, kt = n / (2 * ND);
+            Frag<T> vf;
+            if constexpr (kBf16)
+                vf.v = bf16x8{vv[2 * n][0], vv[2 * n][1], vv[2 * n][2], vv[2 * n][3],
+                              vv[2 * n + 1][0], vv[2 * n + 1][1], vv[2 * n + 1][2], vv[2 * n + 1][3]};
+            mma(oacc[t], vf, pf[kt][cc]);
+            if (n + kLead < NPV) read_v(P, n + kLead);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        (void)more;
+    };
+
     // iteration j (parity P = j % 2)
-    auto step = [&](auto par_c, auto mask_c, int j) {
+    auto step_generic = [&](auto par_c, auto mask_c, int j) {
         constexpr int P = decltype(par_c)::value;
         constexpr int NP = 1 - P;
         wait_vmcnt<0>();
@@ -226,6 +329,10 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) void attn_fwd_kernel(F
             qk(std::integral_constant<int, NP>{}, NP);
         }
         softmax_pv(par_c, mask_c, j * kFwdBN);
+    };
+    auto step = [&](auto par_c, auto mask_c, int j) __attribute__((always_inline)) {
+        if constexpr (kBf16 && D >= 64) step_bf16(par_c, mask_c, j);  // NQK >= 8: four max slots + exp slots
+        else step_generic(par_c, mask_c, j);
     };
 
     if (nkb > 0) {
