@@ -57,7 +57,7 @@ def algorithmic_bytes(w, es: int) -> dict:
             "total": (2 * nq + 2 * nk + lse) + (3 * nq + 2 * nk + lse + nq + 2 * nk)}
 
 
-KERNEL_SOURCES = ("attn_fwd.hip", "attn_bwd.hip", "attn_bwd_kv.hip", "stage.hpp", "cdna4.hpp", "tokmap.hpp")
+KERNEL_SOURCES = ("attn_fwd.hip", "attn_bwd.hip", "attn_bwd_kv.hip", "attn_bwd_q.hip", "stage.hpp", "cdna4.hpp", "tokmap.hpp")
 
 
 def measured_traffic(workload: str):

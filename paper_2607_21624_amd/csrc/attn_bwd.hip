@@ -584,9 +584,14 @@ hipError_t launch_attn_bwd(const BwdArgs& a, unsigned phases, hipStream_t stream
         }
     }
     if (phases & 4u) {
-        const int n = (a.S + kQBM - 1) / kQBM * a.Hq * a.B;
-        constexpr int lds = QSmem<T, D>::BYTES;
-        hipLaunchKernelGGL((attn_bwd_q<T, D>), dim3(padded8(n)), dim3(256), lds, stream, a);
+        if constexpr (sizeof(T) == 2) {
+            const hipError_t eq = launch_attn_bwd_q_bf16<D>(a, stream);
+            if (eq != hipSuccess) return eq;
+        } else {
+            const int n = (a.S + kQBM - 1) / kQBM * a.Hq * a.B;
+            constexpr int lds = QSmem<T, D>::BYTES;
+            hipLaunchKernelGGL((attn_bwd_q<T, D>), dim3(padded8(n)), dim3(256), lds, stream, a);
+        }
     }
     return hipGetLastError();
 }
