@@ -43,21 +43,37 @@ def allowed_pairs(w, kv_len) -> int:
     return total * w.Hq
 
 
-def algorithmic_bytes(w, es: int) -> dict:
-    """Minimum HBM traffic per kernel launch (each tensor read or written once)."""
+def ds_blocks(w, kv_len) -> int:
+    """32x32 dS blocks the key/value pass stores and the dQ pass reads: per
+    (batch, query head), blocks (qb, kb) with kb < ceil(len/32) and, causal,
+    kb <= qb (qb < ceil(S/32))."""
+    nb = (w.S + 31) // 32
+    total = 0
+    for b in range(w.B):
+        L = w.S if kv_len is None else int(min(max(int(kv_len[b]), 0), w.S))
+        nk = (L + 31) // 32
+        total += sum(min(nk, qb + 1) for qb in range(nb)) if w.mask & 1 else nb * nk
+    return total * w.Hq
+
+
+def algorithmic_bytes(w, es: int, kv_len=None) -> dict:
+    """Minimum HBM traffic per kernel launch (each tensor read or written once;
+    the dS blocks written once by the kv pass and read once by the dQ pass)."""
     nq = w.B * w.S * w.Hq * w.d * es
     nk = w.B * w.S * w.Hkv * w.d * es
     lse = w.B * w.Hq * w.S * 4
     stats = 2 * lse
+    ds = ds_blocks(w, kv_len) * 2048 if es == 2 else 0
     return {"attn_fwd": 2 * nq + 2 * nk + lse,              # read Q K V, write O LSE
             "attn_bwd_stats": 2 * nq + lse + stats,         # read O dO LSE, write stats
-            "attn_bwd_kv": 2 * nq + 2 * nk + stats + 2 * nk,  # read Q dO K V stats, write dK dV
-            "attn_bwd_q": 2 * nq + 2 * nk + stats + nq,     # read Q dO K V stats, write dQ
+            "attn_bwd_kv": 2 * nq + 2 * nk + stats + 2 * nk + ds,  # read Q dO K V stats, write dK dV dS
+            "attn_bwd_dq": ds + nk + nq,                    # read dS K, write dQ
             # the step as a whole: fwd reads Q K V, writes O LSE; bwd reads Q K V O dO LSE, writes dQ dK dV
             "total": (2 * nq + 2 * nk + lse) + (3 * nq + 2 * nk + lse + nq + 2 * nk)}
 
 
-KERNEL_SOURCES = ("attn_fwd.hip", "attn_bwd.hip", "attn_bwd_kv.hip", "attn_bwd_q.hip", "stage.hpp", "cdna4.hpp", "tokmap.hpp")
+KERNEL_SOURCES = ("attn_fwd.hip", "attn_bwd.hip", "attn_bwd_kv.hip", "attn_bwd_q.hip", "attn_bwd_dq.hip", "stage.hpp",
+                  "cdna4.hpp", "tokmap.hpp")
 
 
 def measured_traffic(workload: str):
@@ -237,16 +253,17 @@ def main():
     # Algorithmic FLOPs per launch (2*d per allowed pair per matrix product):
     #   attn_fwd     QK^T, PV                                    4*d
     #   attn_bwd_kv  QK^T recompute, dO V^T, P^T dO, dS^T Q      8*d
-    #   attn_bwd_q   dS K (its QK^T and dO V^T recomputes are    2*d
-    #                not counted: they duplicate the kv pass's)
-    per_kernel = {"attn_fwd": (k_fwd, 4), "attn_bwd_kv": (k_kv, 8), "attn_bwd_q": (k_q, 2)}
+    #   attn_bwd_dq  dS K from the dS the kv pass stored         2*d
+    #   (fp32 storage has no stored-dS path: attn_bwd_q recomputes QK^T and dO V^T, 6*d executed)
+    qname = "attn_bwd_dq" if w.dtype == "bf16" else "attn_bwd_q"
+    per_kernel = {"attn_fwd": (k_fwd, 4), "attn_bwd_kv": (k_kv, 8), qname: (k_q, 2)}
     ktf = {n: a * w.d * pairs / (t * 1e-3) / 1e12 for n, (t, a) in per_kernel.items()}
-    executed = {"attn_fwd": 4, "attn_bwd_kv": 8, "attn_bwd_q": 6}
+    executed = {"attn_fwd": 4, "attn_bwd_kv": 8, qname: 2 if qname == "attn_bwd_dq" else 6}
     ktf_exec = {n: executed[n] * w.d * pairs / (per_kernel[n][0] * 1e-3) / 1e12 for n in per_kernel}
     dom = max(per_kernel, key=lambda n: per_kernel[n][0])
     t_dom, a_dom = per_kernel[dom]
     es = 2 if w.dtype == "bf16" else 4
-    alg_bytes = algorithmic_bytes(w, es)
+    alg_bytes = algorithmic_bytes(w, es, inp["kv_len"])
     traffic = measured_traffic(w.name)
     dom_traffic = None
     if traffic is not None:
@@ -286,7 +303,10 @@ def main():
         "layout_copy_bytes": 0 if foreign == [] else None,
         "dispatched_kernels": kernels,
         "kernel_ms": {"attn_fwd": round(k_fwd, 4), "attn_bwd_stats": round(k_stats, 4), "attn_bwd_kv": round(k_kv, 4),
-                      "attn_bwd_q": round(k_q, 4)},
+                      qname: round(k_q, 4)},
+        # the HBM-bound launches: algorithmic bytes over their time
+        "kernel_gbs_algorithmic": {"attn_bwd_stats": round(alg_bytes["attn_bwd_stats"] / (k_stats * 1e-3) / 1e9, 1),
+                                   qname: round(alg_bytes["attn_bwd_dq"] / (k_q * 1e-3) / 1e9, 1)},
         "kernel_tflops_algorithmic": {n: round(v, 2) for n, v in ktf.items()},
         "kernel_tflops_executed": {n: round(v, 2) for n, v in ktf_exec.items()},
         "algorithmic_gflop": round(flops / 1e9, 3),

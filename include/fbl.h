@@ -55,7 +55,7 @@ typedef enum {
     FBL_ERR_LAYOUT = 4,      /* a tile-legality check failed (strides, tile shape)  */
     FBL_ERR_ALIGN = 5,       /* base pointer or row stride not 16-byte aligned      */
     FBL_ERR_UNSUPPORTED = 6, /* head dim / mask combination not implemented         */
-    FBL_ERR_WORKSPACE = 7,   /* workspace NULL or smaller than fbl_attn_bwd_workspace */
+    FBL_ERR_WORKSPACE = 7,   /* workspace NULL or below fbl_attn_bwd_workspace_min  */
     FBL_ERR_HIP = 8,         /* the HIP runtime reported an error at launch         */
     FBL_ERR_ARG = 9          /* other invalid argument (non-finite scale, aliasing) */
 } fbl_status;
@@ -147,20 +147,36 @@ fbl_status fbl_attn_fwd(const fbl_layout* lq, const void* q, const fbl_layout* l
                         float scale, fbl_mask mask, void* stream);
 
 /*
- * Bytes of device workspace fbl_attn_bwd needs for these shapes: one pair of
- * fp32 per query row, [B, Hq, S] x (LSE * log2(e), D_i = sum_k dO_ik O_ik),
- * rounded up to 256 bytes.
+ * Bytes of device workspace for the fastest backward at these shapes.
+ * Part 1, always: one pair of fp32 per query row, [B, Hq, S] x
+ * (LSE * log2(e), D_i = sum_k dO_ik O_ik), rounded up to 256 bytes.
+ * Part 2, bf16 storage only: the gradient of the scores dS = P o (dP - D)
+ * (section 4.1's softmax backward, FTD-C) in bf16, B*Hq*ceil(S/32)^2 blocks
+ * of 32x32 elements (2 KB each), written by the key/value pass and contracted
+ * with K by the dQ pass -- the dQ pass then does not recompute S and dP.
+ * Part 2 is omitted (the size equals fbl_attn_bwd_workspace_min) for fp32
+ * storage and when one head's blocks would reach 2 GiB (S above 32736).
  */
 fbl_status fbl_attn_bwd_workspace(const fbl_layout* lq, const fbl_layout* lk, size_t* bytes);
 
 /*
+ * Smallest workspace fbl_attn_bwd accepts: part 1 above only.  With any
+ * workspace smaller than fbl_attn_bwd_workspace the dQ pass recomputes S and
+ * dP from Q, K, V, dO and the row statistics instead of reading stored dS
+ * (same results up to rounding order).
+ */
+fbl_status fbl_attn_bwd_workspace_min(const fbl_layout* lq, const fbl_layout* lk, size_t* bytes);
+
+/*
  * Attention backward of L = sum(O * dO): writes dQ (Hq heads), dK and dV
  * (Hkv heads; each the sum over the query heads of its group).  The softmax
- * probabilities are recomputed from q, k and the saved lse; nothing of size
- * S x S is stored and no output is accumulated atomically, so the results
- * are bitwise repeatable.  o and lse must be the forward's outputs for q, k, v.
- *   ws/ws_bytes  device workspace of at least fbl_attn_bwd_workspace bytes,
- *                256-byte aligned; its contents on entry do not matter.
+ * probabilities are recomputed from q, k and the saved lse.  No output is
+ * accumulated atomically, so the results are bitwise repeatable.  o and lse
+ * must be the forward's outputs for q, k, v.
+ *   ws/ws_bytes  device workspace of at least fbl_attn_bwd_workspace_min
+ *                bytes, 256-byte aligned; its contents on entry do not matter.
+ *                With at least fbl_attn_bwd_workspace bytes the key/value pass
+ *                stores dS there for the dQ pass (see fbl_attn_bwd_workspace).
  * Same checks as fbl_attn_fwd for the shared arguments, plus: ldo/ldq
  * extents equal lq's, ldk/ldv extents equal lk's, outputs do not overlap
  * inputs, each other or the workspace.
@@ -177,10 +193,14 @@ fbl_status fbl_attn_bwd(const fbl_layout* lq, const void* q, const fbl_layout* l
  * in the order listed).  fbl_attn_bwd(...) equals
  * fbl_attn_bwd_phases(FBL_BWD_ALL, ...).  FBL_BWD_KV and FBL_BWD_Q read what
  * FBL_BWD_PREP left in the workspace, so the same workspace must be passed to
- * all phases; KV and Q are independent of each other.
+ * all phases.  With the full workspace (fbl_attn_bwd_workspace bytes, bf16)
+ * FBL_BWD_Q reads the dS that FBL_BWD_KV stored, so KV must run before Q;
+ * with a smaller one KV and Q are independent of each other.
  *   FBL_BWD_PREP  per query row: LSE * log2(e) and D_i = sum_k dO_ik O_ik
- *   FBL_BWD_KV    key/value-major pass: recompute P, write dK and dV
- *   FBL_BWD_Q     query-major pass: recompute P and dP, write dQ
+ *   FBL_BWD_KV    key/value-major pass: recompute P, write dK and dV (and,
+ *                 with the full workspace, dS)
+ *   FBL_BWD_Q     dQ: from the stored dS, or query-major with P and dP
+ *                 recomputed
  */
 #define FBL_BWD_PREP 1u
 #define FBL_BWD_KV 2u

@@ -126,11 +126,28 @@ hipError_t dispatch_bwd(int D, const fbl::BwdArgs& a, unsigned phases, hipStream
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-// Workspace: the per-query-row statistics, [B, Hq, 2, S] floats (a row of
-// LSE * log2(e), then a row of D, for each (batch, query head)).
-size_t ws_bytes_for(const fbl_layout* lq) {
+// Workspace, part 1: the per-query-row statistics, [B, Hq, 2, S] floats (a
+// row of LSE * log2(e), then a row of D, for each (batch, query head)).
+size_t ws_stats_bytes(const fbl_layout* lq) {
     return align256((size_t)lq->B * lq->H * lq->S * 2 * sizeof(float));
 }
+
+// Workspace, part 2 (bf16 only): dS in 32x32-element blocks, [B, Hq, nb32,
+// nb32] x 2 KB with nb32 = ceil(S / 32), so that the dQ pass contracts the
+// stored dS with K instead of recomputing S and dP.  0 when the storage type
+// is fp32 or one head's blocks would reach 2 GiB (the dQ pass addresses a head
+// with a 32-bit buffer offset); the backward then recomputes.
+size_t ws_ds_bytes(const fbl_layout* lq) {
+    if (lq->dtype != FBL_BF16) return 0;
+    const uint64_t nb32 = (uint64_t)(lq->S + 31) / 32;
+    const uint64_t per_head = nb32 * nb32 * 2048u;
+    if (per_head >= (uint64_t(1) << 31)) return 0;
+    const uint64_t heads = (uint64_t)lq->B * (uint64_t)lq->H;
+    if (heads > (uint64_t(1) << 46) / per_head) return 0;  // keep the total far from overflow
+    return (size_t)(heads * per_head);
+}
+
+size_t ws_bytes_for(const fbl_layout* lq) { return ws_stats_bytes(lq) + ws_ds_bytes(lq); }
 
 }  // namespace
 
@@ -242,6 +259,15 @@ fbl_status fbl_attn_bwd_workspace(const fbl_layout* lq, const fbl_layout* lk, si
     return FBL_OK;
 }
 
+fbl_status fbl_attn_bwd_workspace_min(const fbl_layout* lq, const fbl_layout* lk, size_t* bytes) {
+    if (!lq || !lk || !bytes) return FBL_ERR_NULL;
+    fbl_status st;
+    if ((st = check_layout(lq)) != FBL_OK) return st;
+    if ((st = check_layout(lk)) != FBL_OK) return st;
+    *bytes = ws_stats_bytes(lq);
+    return FBL_OK;
+}
+
 fbl_status fbl_attn_bwd_phases(uint32_t phases, const fbl_layout* lq, const void* q, const fbl_layout* lk,
                                const void* k, const fbl_layout* lv, const void* v, const fbl_layout* lo,
                                const void* o, const fbl_layout* ldo, const void* dO, const float* lse, float scale,
@@ -261,7 +287,7 @@ fbl_status fbl_attn_bwd_phases(uint32_t phases, const fbl_layout* lq, const void
     if (!aligned16(o) || !aligned16(dO) || !aligned16(lse) || !aligned16(dq) || !aligned16(dk) || !aligned16(dv))
         return FBL_ERR_ALIGN;
     if (!ws) return FBL_ERR_WORKSPACE;
-    if (ws_bytes < ws_bytes_for(lq)) return FBL_ERR_WORKSPACE;
+    if (ws_bytes < ws_stats_bytes(lq)) return FBL_ERR_WORKSPACE;
     if ((reinterpret_cast<uintptr_t>(ws) & 255u) != 0) return FBL_ERR_ALIGN;
 
     const int64_t lse_bytes = lq->B * lq->H * lq->S * 4;
@@ -289,6 +315,11 @@ fbl_status fbl_attn_bwd_phases(uint32_t phases, const fbl_layout* lq, const void
     a.dk = dk;
     a.dv = dv;
     a.stats = static_cast<float*>(ws);
+    // stored-dS path when the workspace holds the dS blocks, else recompute
+    const size_t ds_bytes = ws_ds_bytes(lq);
+    a.ds = ds_bytes && ws_bytes >= ws_stats_bytes(lq) + ds_bytes ? static_cast<char*>(ws) + ws_stats_bytes(lq)
+                                                                 : nullptr;
+    a.nb32 = (int)((lq->S + 31) / 32);
     a.mq = tokmap(lq);
     a.mk = tokmap(lk);
     a.mv = tokmap(lv);

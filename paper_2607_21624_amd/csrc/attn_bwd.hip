@@ -585,7 +585,7 @@ hipError_t launch_attn_bwd(const BwdArgs& a, unsigned phases, hipStream_t stream
     }
     if (phases & 4u) {
         if constexpr (sizeof(T) == 2) {
-            const hipError_t eq = launch_attn_bwd_q_bf16<D>(a, stream);
+            const hipError_t eq = a.ds ? launch_attn_bwd_dq_bf16<D>(a, stream) : launch_attn_bwd_q_bf16<D>(a, stream);
             if (eq != hipSuccess) return eq;
         } else {
             const int n = (a.S + kQBM - 1) / kQBM * a.Hq * a.B;

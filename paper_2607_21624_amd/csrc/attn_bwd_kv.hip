@@ -22,6 +22,19 @@
 // (global -> LDS, no registers) a full iteration before it is first read.  The
 // loop is unrolled over the four buffers so that every LDS address is a
 // per-lane base plus an immediate.
+//
+// With DS set the pass also stores dS (bf16, the values its dK product
+// consumes) block by block into the workspace, for the dQ pass to contract
+// with K instead of recomputing S and dP.  A 32-query x 32-key block is 2 KB
+// (blocks of one query head key-block major: block (qb32, kb32) at
+// (kb32*nb32 + qb32)*1024, so one wavefront's stores stream through
+// consecutive blocks) in the accumulator order the fragments already have:
+// element
+// cc*512 + lane*8 + e holds dS[query acc_row(8cc + e, lane / 32)][key lane % 32],
+// so each store is one coalesced 1 KB row of the wavefront.  Entries of keys
+// at or past kv_end are stored unmasked (the dQ pass masks them); blocks
+// wholly above the causal diagonal, or whose keys all lie past kv_end, are not
+// stored (the dQ pass never reads them).
 #include <type_traits>
 
 #include "cdna4.hpp"
@@ -56,7 +69,7 @@ struct KvPipe {
     static_assert(BYTES <= 160 * 1024, "LDS of one workgroup");
 };
 
-template <int D>
+template <int D, bool DS>
 __global__ __launch_bounds__(256, 1) void attn_bwd_kv_bf16(BwdArgs a) {
     using P = KvPipe<D>;
     constexpr int NC = D / 16;
@@ -118,6 +131,18 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_kv_bf16(BwdArgs a) {
     // mask: a key's P and dS only reach that key's own dK and dV rows, which are
     // stored as zeros.
     const int n_mask = a.mask.causal ? min(per_head, (k0 + kPKeys - 2) / BQ - qb_start + 1) : 0;
+
+    // dS blocks of this wave's 32 keys (DS only): block (qb32, kb32) of query
+    // head h starts at element ((b*Hq + h)*nb32 + kb32)*nb32*1024 + qb32*1024;
+    // one buffer resource per query head, the block offset in the scalar
+    // offset of the stores, which are non-temporal (read once, by the dQ
+    // pass; they should not displace the Q/dO tiles other workgroups reuse).
+    const int kb32 = kw0 / 32;
+    const bool ds_live = DS && kw0 < kv_end;  // keys past kv_end: never read
+    const uint32_t ds_head_elems = (uint32_t)a.nb32 * (uint32_t)a.nb32 * 1024u;
+    const bf16* ds_head = DS ? static_cast<const bf16*>(a.ds) + ((int64_t)b * a.Hq + hk * G_) * ds_head_elems : nullptr;
+    __amdgpu_buffer_rsrc_t ds_rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16*>(ds_head), 0,
+                                                                     (int)(ds_head_elems * 2u), 0x00020000);
 
     // ---- DMA of the Q, dO tiles and the row statistics of one block
     const uint32_t qbytes = (uint32_t)(a.mq.ss * 2), obytes = (uint32_t)(a.mdo.ss * 2);
@@ -308,6 +333,25 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_kv_bf16(BwdArgs a) {
 #pragma unroll
             for (int part = 0; part < NPART; ++part) issue_part(B3{}, part);
         }
+        // dS of block it to the workspace; the stores retire during phase Y
+        // and X(it+1), before the next vmcnt wait
+        if constexpr (DS) {
+            if (ds_live) {
+#pragma unroll
+                for (int qt = 0; qt < NQT; ++qt) {
+                    const int qb32 = (qb_start + j) * NQT + qt;
+                    if (qb32 < a.nb32 && (!a.mask.causal || qb32 >= kb32)) {
+                        const int soff = (kb32 * a.nb32 + qb32) * 2048;
+#pragma unroll
+                        for (int cc = 0; cc < 2; ++cc) {
+                            using i32x4 = int __attribute__((ext_vector_type(4)));
+                            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(i32x4, dsb[qt][cc].v), ds_rs,
+                                                                   lane * 16 + cc * 1024, soff, 2 /* nt */);
+                        }
+                    }
+                }
+            }
+        }
         __builtin_amdgcn_sched_barrier(0);
         // ---------------- phase Y
 #pragma unroll
@@ -346,7 +390,16 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_kv_bf16(BwdArgs a) {
     }
     // Blocks in order, four per trip (one per LDS buffer).
     int j = 0;  // index of block `it` within its head's blocks
-    auto next_j = [&]() { j = j + 1 == per_head ? 0 : j + 1; };
+    auto next_j = [&]() {
+        if (++j == per_head) {
+            j = 0;
+            if constexpr (DS) {  // the next query head's dS blocks
+                ds_head += ds_head_elems;
+                ds_rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16*>(ds_head), 0, (int)(ds_head_elems * 2u),
+                                                          0x00020000);
+            }
+        }
+    };
     for (int it = 0; it < n_iter; it += 4) {
         step(C0{}, it, j);
         next_j();
@@ -390,21 +443,29 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_kv_bf16(BwdArgs a) {
     }
 }
 
-template __global__ void attn_bwd_kv_bf16<32>(BwdArgs);
-template __global__ void attn_bwd_kv_bf16<64>(BwdArgs);
-template __global__ void attn_bwd_kv_bf16<128>(BwdArgs);
+template __global__ void attn_bwd_kv_bf16<32, false>(BwdArgs);
+template __global__ void attn_bwd_kv_bf16<64, false>(BwdArgs);
+template __global__ void attn_bwd_kv_bf16<128, false>(BwdArgs);
+template __global__ void attn_bwd_kv_bf16<32, true>(BwdArgs);
+template __global__ void attn_bwd_kv_bf16<64, true>(BwdArgs);
+template __global__ void attn_bwd_kv_bf16<128, true>(BwdArgs);
+
+template <int D, bool DS>
+hipError_t launch_kv(const BwdArgs& a, hipStream_t stream) {
+    static const hipError_t once = hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_bwd_kv_bf16<D, DS>),
+                                                       hipFuncAttributeMaxDynamicSharedMemorySize, KvPipe<D>::BYTES);
+    if (once != hipSuccess) return once;
+    const int n = (a.S + kPKeys - 1) / kPKeys * a.Hkv * a.B;
+    constexpr int lds = KvPipe<D>::BYTES;
+    hipLaunchKernelGGL((attn_bwd_kv_bf16<D, DS>), dim3((n + 7) / 8 * 8), dim3(256), lds, stream, a);
+    return hipGetLastError();
+}
 
 }  // namespace
 
 template <int D>
 hipError_t launch_attn_bwd_kv_bf16(const BwdArgs& a, hipStream_t stream) {
-    static const hipError_t once = hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_bwd_kv_bf16<D>),
-                                                       hipFuncAttributeMaxDynamicSharedMemorySize, KvPipe<D>::BYTES);
-    if (once != hipSuccess) return once;
-    const int n = (a.S + kPKeys - 1) / kPKeys * a.Hkv * a.B;
-    constexpr int lds = KvPipe<D>::BYTES;
-    hipLaunchKernelGGL((attn_bwd_kv_bf16<D>), dim3((n + 7) / 8 * 8), dim3(256), lds, stream, a);
-    return hipGetLastError();
+    return a.ds ? launch_kv<D, true>(a, stream) : launch_kv<D, false>(a, stream);
 }
 
 template hipError_t launch_attn_bwd_kv_bf16<32>(const BwdArgs&, hipStream_t);

@@ -23,9 +23,15 @@ hipError_t launch_attn_bwd(const BwdArgs& a, unsigned phases, hipStream_t stream
 template <int D>
 hipError_t launch_attn_bwd_kv_bf16(const BwdArgs& a, hipStream_t stream);
 
-// Query-major backward pass (dQ) for bf16 storage (software-pipelined kernel).
+// Query-major backward pass (dQ) for bf16 storage (software-pipelined kernel),
+// recomputing S and dP.
 template <int D>
 hipError_t launch_attn_bwd_q_bf16(const BwdArgs& a, hipStream_t stream);
+
+// dQ for bf16 storage from the dS blocks the key/value-major pass stored in
+// the workspace (a.ds != nullptr).
+template <int D>
+hipError_t launch_attn_bwd_dq_bf16(const BwdArgs& a, hipStream_t stream);
 
 // Diagnostic: offsets of a token-major tensor computed by the device index map.
 hipError_t launch_layout_map(const TokMap& m, int B, int H, int S, int D, int64_t* out, hipStream_t stream);

@@ -83,6 +83,14 @@ FBL_DEV void dma16(Rsrc rs, uint32_t lds, uint32_t voff, uint32_t soff) {
                      : "v"(voff), "s"(rs), "s"(soff), "{m0}"(lds)
                      : "memory");
 }
+// dma16 for data read exactly once: the non-temporal hint keeps it from
+// displacing reused tiles in L2.
+FBL_DEV void dma16_stream(Rsrc rs, uint32_t lds, uint32_t voff, uint32_t soff) {
+    asm volatile("s_nop 4\n\ts_nop 0\n\tbuffer_load_dwordx4 %0, %1, %2 offen nt lds"
+                 :
+                 : "v"(voff), "s"(rs), "s"(soff), "{m0}"(lds)
+                 : "memory");
+}
 FBL_DEV void dma4(Rsrc rs, uint32_t lds, uint32_t voff, uint32_t soff) {
     asm volatile("s_nop 4\n\ts_nop 0\n\tbuffer_load_dword %0, %1, %2 offen lds"
                  :

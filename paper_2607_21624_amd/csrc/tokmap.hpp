@@ -54,6 +54,8 @@ struct BwdArgs {
     void* dk;
     void* dv;
     float* stats;      // workspace [B, Hq, 2, S]: rows LSE * log2(e) and sum_k dO*O per query
+    void* ds;          // nullptr, or workspace [B, Hq, nb32 (key), nb32 (query)] blocks of 32x32 bf16 dS
+    int nb32;          // ceil(S / 32)
     TokMap mq, mk, mv, mo, mdo, mdq, mdk, mdv;
     int B, S, Hq, Hkv;
     float scale;       // softmax scale

@@ -37,7 +37,7 @@ FBL_BWD_Q = 4
 FBL_BWD_ALL = 7
 
 EXPORTED = ("fbl_layout_desc", "fbl_layout_offset", "fbl_layout_map_device", "fbl_attn_fwd",
-            "fbl_attn_bwd_workspace", "fbl_attn_bwd", "fbl_attn_bwd_phases", "fbl_status_str")
+            "fbl_attn_bwd_workspace", "fbl_attn_bwd_workspace_min", "fbl_attn_bwd", "fbl_attn_bwd_phases", "fbl_status_str")
 
 
 class Layout(ctypes.Structure):
@@ -86,6 +86,8 @@ def _load() -> ctypes.CDLL:
     lib.fbl_attn_fwd.restype = ctypes.c_int
     lib.fbl_attn_bwd_workspace.argtypes = [P(Layout), P(Layout), P(ctypes.c_size_t)]
     lib.fbl_attn_bwd_workspace.restype = ctypes.c_int
+    lib.fbl_attn_bwd_workspace_min.argtypes = [P(Layout), P(Layout), P(ctypes.c_size_t)]
+    lib.fbl_attn_bwd_workspace_min.restype = ctypes.c_int
     lib.fbl_attn_bwd.argtypes = [P(Layout), vp, P(Layout), vp, P(Layout), vp, P(Layout), vp, P(Layout), vp,
                                  vp, ctypes.c_float, Mask, P(Layout), vp, P(Layout), vp, P(Layout), vp,
                                  vp, ctypes.c_size_t, vp]
@@ -171,6 +173,13 @@ def fbl_attn_bwd_workspace(lq: Layout, lk: Layout) -> int:
     return int(n.value)
 
 
+def fbl_attn_bwd_workspace_min(lq: Layout, lk: Layout) -> int:
+    n = ctypes.c_size_t(0)
+    _check(LIB.fbl_attn_bwd_workspace_min(ctypes.byref(lq), ctypes.byref(lk), ctypes.byref(n)),
+           "fbl_attn_bwd_workspace_min")
+    return int(n.value)
+
+
 def fbl_attn_bwd_raw(lq, q, lk, k, lv, v, lo, o, ldo, do, lse, scale, mask: Mask, ldq, dq, ldk, dk, ldv, dv,
                      ws, ws_bytes, stream=None, phases: int = FBL_BWD_ALL) -> int:
     """Direct call of fbl_attn_bwd (phases == FBL_BWD_ALL) or fbl_attn_bwd_phases; returns the status."""
@@ -240,8 +249,8 @@ def attn_bwd(q, k, v, o, do, lse, Hq: int, Hkv: int, scale: Optional[float] = No
         dk = torch.empty(k.shape, dtype=k.dtype, device=k.device)
     if dv is None:
         dv = torch.empty(v.shape, dtype=v.dtype, device=v.device)
-    need = fbl_attn_bwd_workspace(lq, lk)
     if workspace is None:
+        need = fbl_attn_bwd_workspace(lq, lk)
         workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
     ldq, ldk, ldv = layout_of(dq, Hq), layout_of(dk, Hkv), layout_of(dv, Hkv)
     _check(fbl_attn_bwd_raw(lq, q, lk, k, lv, v, lo, o, ldo, do, lse, scale, _mask(causal, kv_len), ldq, dq, ldk,

@@ -46,8 +46,10 @@ def rel_err(got: np.ndarray, ref: np.ndarray) -> float:
     return diff / denom if denom > 0 else diff
 
 
-def gpu_fwd_bwd(inp: dict, stream=None, dO=None):
+def gpu_fwd_bwd(inp: dict, stream=None, dO=None, workspace: str = "full"):
     """Run fbl_attn_fwd then fbl_attn_bwd on the inputs of one workload.
+    workspace "full" (fbl_attn_bwd_workspace bytes: dQ from the stored dS for
+    bf16) or "min" (fbl_attn_bwd_workspace_min bytes: dQ recomputes S and dP).
     Returns a dict of numpy float64 arrays (o, lse, dq, dk, dv)."""
     import torch
     import paper_2607_21624_amd as fbl
@@ -61,7 +63,10 @@ def gpu_fwd_bwd(inp: dict, stream=None, dO=None):
     causal = bool(w.mask & synth.MASK_CAUSAL)
     scale = 1.0 / math.sqrt(w.d)
     o, lse = fbl.attn_fwd(q, k, v, w.Hq, w.Hkv, scale, causal, kv_len)
-    dq, dk, dv = fbl.attn_bwd(q, k, v, o, do, lse, w.Hq, w.Hkv, scale, causal, kv_len)
+    lq, lk = fbl.layout_of(q, w.Hq), fbl.layout_of(k, w.Hkv)
+    size = fbl.fbl_attn_bwd_workspace(lq, lk) if workspace == "full" else fbl.fbl_attn_bwd_workspace_min(lq, lk)
+    ws = torch.empty(size, dtype=torch.uint8, device="cuda")
+    dq, dk, dv = fbl.attn_bwd(q, k, v, o, do, lse, w.Hq, w.Hkv, scale, causal, kv_len, workspace=ws)
     torch.cuda.synchronize()
     return {"o": to_np(o), "lse": to_np(lse), "dq": to_np(dq), "dk": to_np(dk), "dv": to_np(dv)}
 

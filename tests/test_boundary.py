@@ -204,11 +204,19 @@ def _bwd(lq, lk, lv, lo, p, ws_bytes, ldo=None, ldq=None, ldk=None, ldv=None, ki
 
 
 def test_bwd_workspace_size():
-    lq = fbl.fbl_layout_desc(BF16, 2, 16, 4, 64)
-    lk = fbl.fbl_layout_desc(BF16, 2, 16, 2, 64)
-    n = fbl.fbl_attn_bwd_workspace(lq, lk)
-    assert n >= 2 * 4 * 16 * 8
-    assert n % 256 == 0
+    """Minimum: the row statistics, [B, Hq, 2, S] fp32 rounded up to 256 bytes.
+    Full (bf16): plus B*Hq*ceil(S/32)^2 dS blocks of 2 KB; fp32: statistics only."""
+    for dt, with_ds in ((BF16, True), (F32, False)):
+        for S in (16, 100, 1024):
+            lq = fbl.fbl_layout_desc(dt, 2, S, 6, 64)
+            lk = fbl.fbl_layout_desc(dt, 2, S, 3, 64)
+            stats = (2 * 6 * S * 2 * 4 + 255) // 256 * 256
+            assert fbl.fbl_attn_bwd_workspace_min(lq, lk) == stats
+            nb = (S + 31) // 32
+            assert fbl.fbl_attn_bwd_workspace(lq, lk) == stats + (2 * 6 * nb * nb * 2048 if with_ds else 0)
+    # one head's dS blocks would reach 2 GiB: no stored-dS part
+    lq = fbl.fbl_layout_desc(BF16, 1, 32768, 1, 64)
+    assert fbl.fbl_attn_bwd_workspace(lq, lq) == fbl.fbl_attn_bwd_workspace_min(lq, lq)
 
 
 def test_bwd_rejections():
@@ -217,7 +225,8 @@ def test_bwd_rejections():
     assert _bwd(lq, lk, lv, lo, dict(p, do=None), ws) == E.FBL_ERR_NULL
     assert _bwd(lq, lk, lv, lo, dict(p, dk=None), ws) == E.FBL_ERR_NULL
     assert _bwd(lq, lk, lv, lo, dict(p, ws=None), ws) == E.FBL_ERR_WORKSPACE
-    assert _bwd(lq, lk, lv, lo, p, ws - 256) == E.FBL_ERR_WORKSPACE
+    ws_min = fbl.fbl_attn_bwd_workspace_min(lq, lk)
+    assert _bwd(lq, lk, lv, lo, p, ws_min - 256) == E.FBL_ERR_WORKSPACE
     assert _bwd(lq, lk, lv, lo, dict(p, ws=p["ws"] + 16), ws) == E.FBL_ERR_ALIGN
     assert _bwd(lq, lk, lv, lo, p, ws, ldq=_copy(lq, dtype=F32)) == E.FBL_ERR_DTYPE
     assert _bwd(lq, lk, lv, lo, p, ws, ldk=_copy(lq)) == E.FBL_ERR_SHAPE

@@ -107,6 +107,22 @@ def test_ragged_lengths_causal_gqa(S, d):
     assert not bad, f"S={S} d={d}: {bad}"
 
 
+# ------------------------------------------- recompute dQ path (min workspace)
+@pytest.mark.parametrize("d,mask,S", [(128, synth.MASK_CAUSAL, 300), (64, synth.MASK_CAUSAL, 129),
+                                      (32, synth.MASK_KEY_PADDING, 200), (64, synth.MASK_NONE, 97),
+                                      (128, synth.MASK_CAUSAL | synth.MASK_KEY_PADDING, 257)])
+def test_recompute_dq_path(d, mask, S):
+    """With the smallest workspace the dQ pass recomputes S and dP instead of
+    reading stored dS; both ways must meet the oracle."""
+    w = synth.Workload(f"recompute{S}", B=2, S=S, Hq=4, Hkv=2, d=d, dtype="bf16", mask=mask, seed=S + d + mask)
+    inp = synth.make_inputs(w)
+    note(f"recompute dQ S={S} d={d} mask={mask}")
+    ref = oracle_fwd_bwd(inp)
+    for ws in ("min", "full"):
+        errs, bad = compare(gpu_fwd_bwd(inp, workspace=ws), ref, "bf16")
+        assert not bad, f"workspace {ws}: {bad}"
+
+
 # ------------------------------------------------------------- edge cases
 def test_zero_and_overlong_key_lengths():
     import torch
