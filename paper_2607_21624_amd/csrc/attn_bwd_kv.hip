@@ -87,11 +87,10 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_kv_bf16(BwdArgs a) {
     const int c32 = lane & 31;
     const int S = a.S;
     const int nkb = (S + kPKeys - 1) / kPKeys;
-    const int logical = xcd_logical_id(blockIdx.x, nkb * a.Hkv * a.B, gridDim.x);
-    if (logical < 0) return;
-    const int kblk = logical % nkb;
-    const int hk = (logical / nkb) % a.Hkv;
-    const int b = logical / (nkb * a.Hkv);
+    int kblk, bh;  // causal: key block 0 meets the most queries; start it first
+    if (!rank_major_item(blockIdx.x, nkb, a.Hkv * a.B, kblk, bh)) return;
+    const int hk = bh % a.Hkv;
+    const int b = bh / a.Hkv;
     const int G_ = a.Hq / a.Hkv;
     int kv_end = S;
     if (a.mask.kv_len) kv_end = min(max(a.mask.kv_len[b], 0), S);
@@ -455,9 +454,9 @@ hipError_t launch_kv(const BwdArgs& a, hipStream_t stream) {
     static const hipError_t once = hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_bwd_kv_bf16<D, DS>),
                                                        hipFuncAttributeMaxDynamicSharedMemorySize, KvPipe<D>::BYTES);
     if (once != hipSuccess) return once;
-    const int n = (a.S + kPKeys - 1) / kPKeys * a.Hkv * a.B;
     constexpr int lds = KvPipe<D>::BYTES;
-    hipLaunchKernelGGL((attn_bwd_kv_bf16<D, DS>), dim3((n + 7) / 8 * 8), dim3(256), lds, stream, a);
+    hipLaunchKernelGGL((attn_bwd_kv_bf16<D, DS>), dim3(rank_major_grid((a.S + kPKeys - 1) / kPKeys, a.Hkv * a.B)),
+                       dim3(256), lds, stream, a);
     return hipGetLastError();
 }
 

@@ -63,11 +63,10 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_q_bf16(BwdArgs a) {
     const int c32 = lane & 31;
     const int S = a.S;
     const int nqb = (S + kQRows - 1) / kQRows;
-    const int logical = xcd_logical_id(blockIdx.x, nqb * a.Hq * a.B, gridDim.x);
-    if (logical < 0) return;
-    const int rank = logical % nqb;
-    const int h = (logical / nqb) % a.Hq;
-    const int b = logical / (nqb * a.Hq);
+    int rank, bh;
+    if (!rank_major_item(blockIdx.x, nqb, a.Hq * a.B, rank, bh)) return;
+    const int h = bh % a.Hq;
+    const int b = bh / a.Hq;
     // causal: the last query blocks see the most keys; start them first
     const int qb = a.mask.causal ? (nqb - 1 - rank) : rank;
     const int hk = h / (a.Hq / a.Hkv);
@@ -298,9 +297,9 @@ hipError_t launch_attn_bwd_q_bf16(const BwdArgs& a, hipStream_t stream) {
     static const hipError_t once = hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_bwd_q_bf16<D>),
                                                        hipFuncAttributeMaxDynamicSharedMemorySize, QPipe<D>::BYTES);
     if (once != hipSuccess) return once;
-    const int n = (a.S + kQRows - 1) / kQRows * a.Hq * a.B;
     constexpr int lds = QPipe<D>::BYTES;
-    hipLaunchKernelGGL((attn_bwd_q_bf16<D>), dim3((n + 7) / 8 * 8), dim3(256), lds, stream, a);
+    hipLaunchKernelGGL((attn_bwd_q_bf16<D>), dim3(rank_major_grid((a.S + kQRows - 1) / kQRows, a.Hq * a.B)), dim3(256),
+                       lds, stream, a);
     return hipGetLastError();
 }
 

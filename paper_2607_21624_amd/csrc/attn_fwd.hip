@@ -58,11 +58,10 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) void attn_fwd_kernel(F
     const int c32 = lane & 31;
     const int S = a.S;
     const int nqb = (S + kFwdBM - 1) / kFwdBM;
-    const int logical = xcd_logical_id(blockIdx.x, nqb * a.Hq * a.B, gridDim.x);
-    if (logical < 0) return;
-    const int rank = logical % nqb;
-    const int h = (logical / nqb) % a.Hq;
-    const int b = logical / (nqb * a.Hq);
+    int rank, bh;
+    if (!rank_major_item(blockIdx.x, nqb, a.Hq * a.B, rank, bh)) return;
+    const int h = bh % a.Hq;
+    const int b = bh / a.Hq;
     // causal: the last query blocks see the most keys; start them first
     const int qb = a.mask.causal ? (nqb - 1 - rank) : rank;
     const int hk = h / (a.Hq / a.Hkv);
@@ -403,10 +402,8 @@ hipError_t launch_attn_fwd(const FwdArgs& a, hipStream_t stream) {
     const hipError_t e = set_fwd_lds<T, D>();
     if (e != hipSuccess) return e;
     const int nqb = (a.S + kFwdBM - 1) / kFwdBM;
-    const int total = nqb * a.Hq * a.B;
-    const int padded = (total + 7) / 8 * 8;
     constexpr int lds = fwd_lds_bytes<T, D>();
-    hipLaunchKernelGGL((attn_fwd_kernel<T, D>), dim3(padded), dim3(256), lds, stream, a);
+    hipLaunchKernelGGL((attn_fwd_kernel<T, D>), dim3(rank_major_grid(nqb, a.Hq * a.B)), dim3(256), lds, stream, a);
     return hipGetLastError();
 }
 

@@ -219,6 +219,30 @@ struct DmaPlan {
     }
 };
 
+// Workgroup order for (rank, head) work items whose cost falls with rank (the
+// causal schedule: rank 0 = heaviest block).  With at least 8 heads, XCD x
+// (ids are dealt round-robin over the 8 XCDs, each with its own L2) serves
+// heads x, x+8, x+16, ... and walks them rank-major -- rank 0 of all its
+// heads, then rank 1, ... -- so the heaviest blocks of every head start first
+// (longest-first list scheduling) while each head's tiles stay in one L2.
+// With fewer heads, plain rank-major order over all XCDs.  Grid size:
+// rank_major_grid(); returns false for padding ids.
+FBL_DEV bool rank_major_item(int id, int nrank, int nhead, int& rank, int& head) {
+    if (nhead < 8) {
+        rank = id / nhead;
+        head = id % nhead;
+        return rank < nrank;
+    }
+    const int x = id % 8, i = id / 8;
+    const int nh = (nhead - x + 7) / 8;  // heads served by XCD x
+    rank = i / nh;
+    head = x + 8 * (i % nh);
+    return rank < nrank;
+}
+inline int rank_major_grid(int nrank, int nhead) {
+    return nhead < 8 ? nrank * nhead : 8 * ((nhead + 7) / 8) * nrank;
+}
+
 // Map a linear workgroup id so that consecutive ids of the logical order land
 // on the same XCD (ids are dealt round-robin over the 8 XCDs, each with its own
 // L2): logical = (id % 8) * per_xcd + id / 8.  Returns -1 for padding ids.
