@@ -7,11 +7,12 @@
 //   dQ^T(32 queries) += K_kb^T dS_kb^T       for the key blocks kb of the row
 // It is bound by HBM (2 bytes of dS per allowed pair against 2*d MFMA flops),
 // so the design goal is a full memory pipe, not MFMA issue: a workgroup
-// covers 256-query blocks of one (batch, query head), four wavefronts of two
-// 32-query tiles; per 32-key step it brings the K tile (shared) and each
-// wavefront's dS blocks into LDS by DMA, with three steps in flight.  Under a
-// causal mask block q reads q+1 key blocks of 256, so a workgroup takes the
-// pair (nqb-1-r, r): every workgroup streams the same number of steps.
+// covers 128-query blocks of one (batch, query head), four wavefronts of one
+// 32-query tile; per 32-key step it brings the K tile (shared) and each
+// wavefront's dS block into LDS by DMA, with three steps in flight, and two
+// workgroups share a CU so that one computes while the other waits.  Under a
+// causal mask block q reads 4(q+1) key blocks, so a workgroup takes the pair
+// (nqb-1-r, r): every workgroup streams the same number of steps.
 //
 // dS block layout (written by the key/value-major pass): block (qb32, kb32)
 // of query head h is 1024 bf16 at ((b*Hq + h)*nb32 + kb32)*nb32*1024 +
@@ -38,7 +39,7 @@ namespace fbl {
 namespace {
 
 constexpr int kDqWaves = 4;
-constexpr int kDqTiles = 2;                        // 32-query tiles per wavefront
+constexpr int kDqTiles = 1;                        // 32-query tiles per wavefront
 constexpr int kDqRows = 32 * kDqTiles * kDqWaves;  // queries per block
 constexpr int kDqTilesPerBlock = kDqRows / 32;
 
@@ -57,11 +58,11 @@ struct DqPipe {
     static_assert(KINST % kDqWaves == 0 || KINST < kDqWaves, "K tile loads spread evenly");
     static_assert((NBUF - 1) * DSBUF + (kDqTiles - 1) * 2048 + 384 < 65536 && (NBUF - 1) * KT + KT < 65536,
                   "buffer offsets fit the 16-bit LDS immediate");
-    static_assert(BYTES <= 160 * 1024, "LDS of one workgroup");
+    static_assert(2 * BYTES <= 160 * 1024, "two workgroups per CU");
 };
 
 template <int D>
-__global__ __launch_bounds__(256, 1) void attn_bwd_dq_bf16(BwdArgs a) {
+__global__ __launch_bounds__(256, 2) void attn_bwd_dq_bf16(BwdArgs a) {
     using P = DqPipe<D>;
     using u32x4 = uint32_t __attribute__((ext_vector_type(4)));
     constexpr int ND = D / 32;
