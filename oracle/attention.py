@@ -25,9 +25,13 @@ notes of the repository):
   (no key padding or j < kv_len[b]); a disallowed score is -inf (hard mask).
   Padded query rows are computed like any other row.
 * a row with no allowed key has O = 0, LSE = -inf and no gradient.
-* LSE is the natural-log log-sum-exp of the scaled, masked scores, [B, Hq, S].
+* LSE is the natural-log log-sum-exp of the scaled, masked scores, [B, Hq, S_q].
+* Cross-attention: queries (S_q tokens) and keys/values (S_k tokens) may
+  differ in length (encoder-decoder attention, the layout-incompatible
+  attention variant the paper lists among its workloads); the causal rule
+  j <= i is then aligned at the first token of both.
 
-Everything runs one (batch, head) at a time with full S x S matrices.
+Everything runs one (batch, head) at a time with full S_q x S_k matrices.
 Inputs are upcast exactly to float64.
 
 Pins (tests/test_oracle.py): scalar brute force (oracle/brute.py), float64
@@ -92,18 +96,19 @@ def softmax_rows(s: np.ndarray):
     return p, lse
 
 
-def _mask_for(b: int, S: int, causal: bool, kv_len) -> np.ndarray:
-    return allowed_mask(S, S, causal, None if kv_len is None else int(kv_len[b]))
+def _mask_for(b: int, S_q: int, S_k: int, causal: bool, kv_len) -> np.ndarray:
+    return allowed_mask(S_q, S_k, causal, None if kv_len is None else int(kv_len[b]))
 
 
 def head_probs(q, k, Hq: int, Hkv: int, scale: float, causal: bool = False, kv_len=None):
-    """Full probability tensor P, float64 (B, Hq, S, S).  For tests of small shapes."""
+    """Full probability tensor P, float64 (B, Hq, S_q, S_k).  For tests of small shapes."""
     Q = split_heads(q, Hq)
     K = split_heads(k, Hkv)
     B, _, S, _ = Q.shape
-    P = np.zeros((B, Hq, S, S))
+    Sk = K.shape[2]
+    P = np.zeros((B, Hq, S, Sk))
     for b in range(B):
-        allowed = _mask_for(b, S, causal, kv_len)
+        allowed = _mask_for(b, S, Sk, causal, kv_len)
         for h in range(Hq):
             g = kv_head_of(h, Hq, Hkv)
             P[b, h], _ = softmax_rows(masked_scores(Q[b, h], K[b, g], scale, allowed))
@@ -113,17 +118,18 @@ def head_probs(q, k, Hq: int, Hkv: int, scale: float, causal: bool = False, kv_l
 def attn_fwd(q, k, v, Hq: int, Hkv: int, scale: float, causal: bool = False, kv_len=None):
     """Forward pass.
 
-    q: (B, S, Hq*d), k, v: (B, S, Hkv*d) token-major (any float dtype; upcast).
-    Returns (O (B, S, Hq*d) float64, LSE (B, Hq, S) float64).
+    q: (B, S_q, Hq*d), k, v: (B, S_k, Hkv*d) token-major (any float dtype; upcast).
+    Returns (O (B, S_q, Hq*d) float64, LSE (B, Hq, S_q) float64).
     """
     Q = split_heads(q, Hq)
     K = split_heads(k, Hkv)
     V = split_heads(v, Hkv)
     B, _, S, d = Q.shape
+    Sk = K.shape[2]
     O = np.zeros((B, Hq, S, d))
     LSE = np.zeros((B, Hq, S))
     for b in range(B):
-        allowed = _mask_for(b, S, causal, kv_len)
+        allowed = _mask_for(b, S, Sk, causal, kv_len)
         for h in range(Hq):
             g = kv_head_of(h, Hq, Hkv)
             p, lse = softmax_rows(masked_scores(Q[b, h], K[b, g], scale, allowed))
@@ -136,18 +142,19 @@ def attn_bwd(q, k, v, do, Hq: int, Hkv: int, scale: float, causal: bool = False,
     """Backward pass of L = sum(O * dO) with O = attn_fwd(q, k, v).
 
     P is recomputed from q and k (the oracle saves nothing between passes).
-    Returns (dQ (B, S, Hq*d), dK (B, S, Hkv*d), dV (B, S, Hkv*d)), float64.
+    Returns (dQ (B, S_q, Hq*d), dK (B, S_k, Hkv*d), dV (B, S_k, Hkv*d)), float64.
     """
     Q = split_heads(q, Hq)
     K = split_heads(k, Hkv)
     V = split_heads(v, Hkv)
     dO = split_heads(do, Hq)
     B, _, S, d = Q.shape
+    Sk = K.shape[2]
     dQ = np.zeros((B, Hq, S, d))
-    dK = np.zeros((B, Hkv, S, d))
-    dV = np.zeros((B, Hkv, S, d))
+    dK = np.zeros((B, Hkv, Sk, d))
+    dV = np.zeros((B, Hkv, Sk, d))
     for b in range(B):
-        allowed = _mask_for(b, S, causal, kv_len)
+        allowed = _mask_for(b, S, Sk, causal, kv_len)
         for h in range(Hq):
             g = kv_head_of(h, Hq, Hkv)
             p, _ = softmax_rows(masked_scores(Q[b, h], K[b, g], scale, allowed))
@@ -159,7 +166,7 @@ def attn_bwd(q, k, v, do, Hq: int, Hkv: int, scale: float, causal: bool = False,
 
 
 def head_bwd(p, qh, kh, vh, doh, scale):
-    """Gradients of one (batch, query head) given its probabilities p (S, S).
+    """Gradients of one (batch, query head) given its probabilities p (S_q, S_k).
 
     Returns (dq, dk, dv), the latter two being this head's contribution to its
     key/value head.
@@ -172,5 +179,5 @@ def head_bwd(p, qh, kh, vh, doh, scale):
 
 
 def bwd_row_dot(o, do, Hq: int) -> np.ndarray:
-    """D[b, h, i] = sum_k dO[b, i, h, k] * O[b, i, h, k], float64 (B, Hq, S)."""
+    """D[b, h, i] = sum_k dO[b, i, h, k] * O[b, i, h, k], float64 (B, Hq, S_q)."""
     return np.sum(split_heads(o, Hq) * split_heads(do, Hq), axis=3)
