@@ -34,7 +34,7 @@ def allowed_pairs(w, kv_len) -> int:
     S = w.S
     total = 0
     for b in range(w.B):
-        L = S if kv_len is None else int(min(max(int(kv_len[b]), 0), S))
+        L = w.Skv if kv_len is None else int(min(max(int(kv_len[b]), 0), w.Skv))
         if w.mask & 1:
             # query i sees keys j <= i, j < L
             total += sum(min(i + 1, L) for i in range(S)) if L < S else S * (S + 1) // 2
@@ -50,7 +50,7 @@ def ds_blocks(w, kv_len) -> int:
     nb = (w.S + 31) // 32
     total = 0
     for b in range(w.B):
-        L = w.S if kv_len is None else int(min(max(int(kv_len[b]), 0), w.S))
+        L = w.Skv if kv_len is None else int(min(max(int(kv_len[b]), 0), w.Skv))
         nk = (L + 31) // 32
         total += sum(min(nk, qb + 1) for qb in range(nb)) if w.mask & 1 else nb * nk
     return total * w.Hq
@@ -60,7 +60,7 @@ def algorithmic_bytes(w, es: int, kv_len=None) -> dict:
     """Minimum HBM traffic per kernel launch (each tensor read or written once;
     the dS blocks written once by the kv pass and read once by the dQ pass)."""
     nq = w.B * w.S * w.Hq * w.d * es
-    nk = w.B * w.S * w.Hkv * w.d * es
+    nk = w.B * w.Skv * w.Hkv * w.d * es
     lse = w.B * w.Hq * w.S * 4
     stats = 2 * lse
     ds = ds_blocks(w, kv_len) * 2048 if es == 2 else 0
@@ -128,7 +128,7 @@ def cpu_baseline(w, inp, budget_s: float):
         oracle.attn_fwd(q, k, v, G, 1, scale, bool(w.mask & 1), kl)
         oracle.attn_bwd(q, k, v, do, G, 1, scale, bool(w.mask & 1), kl)
         heads += G
-        sub = type(w)(w.name, B=1, S=w.S, Hq=G, Hkv=1, d=d, dtype=w.dtype, mask=w.mask)
+        sub = type(w)(w.name, B=1, S=w.S, Hq=G, Hkv=1, d=d, dtype=w.dtype, mask=w.mask, S_kv=w.S_kv)
         done_pairs += allowed_pairs(sub, kl)
         if time.perf_counter() - t0 >= budget_s:
             break
@@ -190,7 +190,7 @@ def main():
     import paper_2607_21624_amd as fbl
     import synth
 
-    w = synth.WORKLOADS[args.workload]
+    w = {**synth.WORKLOADS, **synth.CROSS_WORKLOADS}[args.workload]
     inp = synth.make_inputs(w)
     dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
     dev = lambda x: torch.from_numpy(x).to("cuda").to(dt)
@@ -296,7 +296,7 @@ def main():
         "vs_baseline": None,
         "dtype": w.dtype,
         "data": "synthetic (seeded N(0,1) token-major Q,K,V,dO)",
-        "config": {"workload": w.name, "B": w.B, "S": w.S, "Hq": w.Hq, "Hkv": w.Hkv, "d": w.d,
+        "config": {"workload": w.name, "B": w.B, "S": w.S, "S_kv": w.Skv, "Hq": w.Hq, "Hkv": w.Hkv, "d": w.d,
                    "mask": {0: "none", 1: "causal", 2: "key_padding", 3: "causal+key_padding"}[w.mask],
                    "layout": "token-major [B,S,H*d]", "parallelism": "single GPU"},
         "pct_peak": round(100 * tflops / peak, 2),

@@ -16,14 +16,17 @@
  * Conventions shared by every entry point.
  *  - Element (b, h, s, i) of a tensor described by an fbl_layout L is at
  *    element offset  b*L.sb + s*L.ss + h*L.sh + i*L.sd  from its base pointer.
- *  - Q, O, dO, dQ have Hq heads; K, V, dK, dV have Hkv heads; query head h
- *    reads key/value head h / (Hq/Hkv) (grouped-query attention with
- *    contiguous groups).  Self-attention: all tensors share B and S.
+ *  - Q, O, dO, dQ have Hq heads and S_q tokens; K, V, dK, dV have Hkv heads
+ *    and S_kv tokens; query head h reads key/value head h / (Hq/Hkv)
+ *    (grouped-query attention with contiguous groups).  All tensors share B.
+ *    S_q == S_kv is self-attention; S_q != S_kv is cross-attention (the
+ *    encoder-decoder attention section 2.2 lists among the attention variants
+ *    whose layouts conflict), which takes no causal mask.
  *  - Scores are  scale * q_i . k_j ; key j is allowed for query i iff
  *    (!causal || j <= i) && (!key_padding || j < kv_len[b]).  Disallowed
  *    scores are -inf.  A query row with no allowed key gets O = 0,
  *    LSE = -inf and contributes no gradient.
- *  - LSE is float32 [B, Hq, S], contiguous, natural-log log-sum-exp of the
+ *  - LSE is float32 [B, Hq, S_q], contiguous, natural-log log-sum-exp of the
  *    scaled masked scores.
  *  - Storage type of Q, K, V, O, dO, dQ, dK, dV is one fbl_dtype for the whole
  *    call (fp32 or bf16); accumulation is fp32.
@@ -64,7 +67,7 @@ typedef enum { FBL_F32 = 0, FBL_BF16 = 1 } fbl_dtype;
 
 /*
  * Layout descriptor of one tensor with logical dims (B, H, S, D) -- the
- * "logical dimensions S(t) and physical layout L(t)" of the paper's problem
+ * logical shape S(t) and physical layout L(t) of a tensor in the paper's problem
  * statement (section 3.1) -- plus the R-Tile the kernels stage it in.
  *
  * Strides are in elements.  Token-major defaults: sd = 1, sh = D,
@@ -90,7 +93,7 @@ typedef struct {
     uint32_t kind;          /* OR of FBL_MASK_* bits                             */
     uint32_t reserved;      /* zero                                              */
     const int32_t* kv_len;  /* device pointer, int32 [B]; required with KEY_PADDING;
-                               values are clamped to [0, S]                     */
+                               values are clamped to [0, S_kv]                  */
 } fbl_mask;
 
 /*
@@ -132,12 +135,13 @@ fbl_status fbl_layout_map_device(const fbl_layout* l, int64_t* out, void* stream
  * Attention forward.
  *   lq/q     queries, Hq heads.       lk/k, lv/v  keys and values, Hkv heads.
  *   lo/o     output, same extents as q.
- *   lse      float32 [B, Hq, S] contiguous, written (saved for the backward).
+ *   lse      float32 [B, Hq, S_q] contiguous, written (saved for the backward).
  *   scale    softmax scale (finite), e.g. 1/sqrt(D).
  *   mask     see fbl_mask.
- * Supported: D in {32, 64, 128}; Hq % Hkv == 0; S up to 2^30.
+ * Supported: D in {32, 64, 128}; Hq % Hkv == 0; S_q, S_kv up to 2^30; a
+ * causal mask needs S_q == S_kv (else FBL_ERR_UNSUPPORTED).
  * Checks: non-NULL pointers; one dtype; lq.B == lk.B == lv.B == lo.B;
- * lq.S == lk.S == lv.S == lo.S; lk and lv extents equal; lq.D == lk.D;
+ * lk and lv extents equal (S_kv = lk.S); lq.D == lk.D;
  * lo extents equal lq's; sd == 1; tile_d divides D; base pointers and
  * row strides 16-byte aligned; kv_len given with KEY_PADDING; o and lse do
  * not overlap any input.
@@ -151,11 +155,12 @@ fbl_status fbl_attn_fwd(const fbl_layout* lq, const void* q, const fbl_layout* l
  * Part 1, always: one pair of fp32 per query row, [B, Hq, S] x
  * (LSE * log2(e), D_i = sum_k dO_ik O_ik), rounded up to 256 bytes.
  * Part 2, bf16 storage only: the gradient of the scores dS = P o (dP - D)
- * (section 4.1's softmax backward, FTD-C) in bf16, B*Hq*ceil(S/32)^2 blocks
- * of 32x32 elements (2 KB each), written by the key/value pass and contracted
- * with K by the dQ pass -- the dQ pass then does not recompute S and dP.
- * Part 2 is omitted (the size equals fbl_attn_bwd_workspace_min) for fp32
- * storage and when one head's blocks would reach 2 GiB (S above 32736).
+ * (section 4.1's softmax backward, FTD-C) in bf16,
+ * B*Hq*ceil(S_q/32)*ceil(S_kv/32) blocks of 32x32 elements (2 KB each),
+ * written by the key/value pass and contracted with K by the dQ pass -- the
+ * dQ pass then does not recompute S and dP.  Part 2 is omitted (the size
+ * equals fbl_attn_bwd_workspace_min) for fp32 storage and when one head's
+ * blocks would reach 2 GiB (S_q = S_kv above 32736).
  */
 fbl_status fbl_attn_bwd_workspace(const fbl_layout* lq, const fbl_layout* lk, size_t* bytes);
 

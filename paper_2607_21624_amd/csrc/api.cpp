@@ -91,8 +91,8 @@ fbl_status check_qkv(const fbl_layout* lq, const void* q, const fbl_layout* lk, 
     if ((st = check_layout(lk)) != FBL_OK) return st;
     if ((st = check_layout(lv)) != FBL_OK) return st;
     if (lq->dtype != lk->dtype || lq->dtype != lv->dtype) return FBL_ERR_DTYPE;
-    if (lq->B != lk->B || lq->B != lv->B || lq->S != lk->S || lq->S != lv->S) return FBL_ERR_SHAPE;
-    if (!same_extents(lk, lv)) return FBL_ERR_SHAPE;
+    if (lq->B != lk->B || lq->B != lv->B) return FBL_ERR_SHAPE;
+    if (!same_extents(lk, lv)) return FBL_ERR_SHAPE;  // K and V: the same S_kv tokens
     if (lq->D != lk->D) return FBL_ERR_SHAPE;
     if (lq->H % lk->H != 0) return FBL_ERR_SHAPE;
     if (lq->D != 32 && lq->D != 64 && lq->D != 128) return FBL_ERR_UNSUPPORTED;
@@ -102,6 +102,8 @@ fbl_status check_qkv(const fbl_layout* lq, const void* q, const fbl_layout* lk, 
     if (!aligned16(q) || !aligned16(k) || !aligned16(v)) return FBL_ERR_ALIGN;
     if (mask.kind & ~(FBL_MASK_CAUSAL | FBL_MASK_KEY_PADDING)) return FBL_ERR_ARG;
     if ((mask.kind & FBL_MASK_KEY_PADDING) && !mask.kv_len) return FBL_ERR_NULL;
+    // cross-attention (S_q != S_kv) takes no causal mask: its alignment is not defined here
+    if ((mask.kind & FBL_MASK_CAUSAL) && lq->S != lk->S) return FBL_ERR_UNSUPPORTED;
     if (!std::isfinite(scale)) return FBL_ERR_ARG;
     return FBL_OK;
 }
@@ -132,22 +134,22 @@ size_t ws_stats_bytes(const fbl_layout* lq) {
     return align256((size_t)lq->B * lq->H * lq->S * 2 * sizeof(float));
 }
 
-// Workspace, part 2 (bf16 only): dS in 32x32-element blocks, [B, Hq, nb32,
-// nb32] x 2 KB with nb32 = ceil(S / 32), so that the dQ pass contracts the
-// stored dS with K instead of recomputing S and dP.  0 when the storage type
-// is fp32 or one head's blocks would reach 2 GiB (the dQ pass addresses a head
-// with a 32-bit buffer offset); the backward then recomputes.
-size_t ws_ds_bytes(const fbl_layout* lq) {
+// Workspace, part 2 (bf16 only): dS in 32x32-element blocks, [B, Hq, nk32,
+// nq32] x 2 KB with nq32 = ceil(S_q / 32), nk32 = ceil(S_kv / 32), so that the
+// dQ pass contracts the stored dS with K instead of recomputing S and dP.  0
+// when the storage type is fp32 or one head's blocks would reach 2 GiB (the dQ
+// pass addresses a head with a 32-bit buffer offset); the backward then
+// recomputes.
+size_t ws_ds_bytes(const fbl_layout* lq, const fbl_layout* lk) {
     if (lq->dtype != FBL_BF16) return 0;
-    const uint64_t nb32 = (uint64_t)(lq->S + 31) / 32;
-    const uint64_t per_head = nb32 * nb32 * 2048u;
+    const uint64_t per_head = (uint64_t)((lq->S + 31) / 32) * (uint64_t)((lk->S + 31) / 32) * 2048u;
     if (per_head >= (uint64_t(1) << 31)) return 0;
     const uint64_t heads = (uint64_t)lq->B * (uint64_t)lq->H;
     if (heads > (uint64_t(1) << 46) / per_head) return 0;  // keep the total far from overflow
     return (size_t)(heads * per_head);
 }
 
-size_t ws_bytes_for(const fbl_layout* lq) { return ws_stats_bytes(lq) + ws_ds_bytes(lq); }
+size_t ws_bytes_for(const fbl_layout* lq, const fbl_layout* lk) { return ws_stats_bytes(lq) + ws_ds_bytes(lq, lk); }
 
 }  // namespace
 
@@ -240,6 +242,7 @@ fbl_status fbl_attn_fwd(const fbl_layout* lq, const void* q, const fbl_layout* l
     a.mo = tokmap(lo);
     a.B = (int)lq->B;
     a.S = (int)lq->S;
+    a.Skv = (int)lk->S;
     a.Hq = (int)lq->H;
     a.Hkv = (int)lk->H;
     a.scale_log2 = scale * 1.4426950408889634f;
@@ -255,7 +258,7 @@ fbl_status fbl_attn_bwd_workspace(const fbl_layout* lq, const fbl_layout* lk, si
     fbl_status st;
     if ((st = check_layout(lq)) != FBL_OK) return st;
     if ((st = check_layout(lk)) != FBL_OK) return st;
-    *bytes = ws_bytes_for(lq);
+    *bytes = ws_bytes_for(lq, lk);
     return FBL_OK;
 }
 
@@ -316,10 +319,11 @@ fbl_status fbl_attn_bwd_phases(uint32_t phases, const fbl_layout* lq, const void
     a.dv = dv;
     a.stats = static_cast<float*>(ws);
     // stored-dS path when the workspace holds the dS blocks, else recompute
-    const size_t ds_bytes = ws_ds_bytes(lq);
+    const size_t ds_bytes = ws_ds_bytes(lq, lk);
     a.ds = ds_bytes && ws_bytes >= ws_stats_bytes(lq) + ds_bytes ? static_cast<char*>(ws) + ws_stats_bytes(lq)
                                                                  : nullptr;
-    a.nb32 = (int)((lq->S + 31) / 32);
+    a.nq32 = (int)((lq->S + 31) / 32);
+    a.nk32 = (int)((lk->S + 31) / 32);
     a.mq = tokmap(lq);
     a.mk = tokmap(lk);
     a.mv = tokmap(lv);
@@ -330,6 +334,7 @@ fbl_status fbl_attn_bwd_phases(uint32_t phases, const fbl_layout* lq, const void
     a.mdv = tokmap(ldv);
     a.B = (int)lq->B;
     a.S = (int)lq->S;
+    a.Skv = (int)lk->S;
     a.Hq = (int)lq->H;
     a.Hkv = (int)lk->H;
     a.scale = scale;

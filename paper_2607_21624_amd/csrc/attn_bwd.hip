@@ -114,16 +114,16 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_kv(BwdArgs a) {
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int g = lane >> 5;
     const int c32 = lane & 31;
-    const int S = a.S;
-    const int nkb = (S + kKvBN - 1) / kKvBN;
+    const int S = a.S, Skv = a.Skv;  // query tokens, key tokens
+    const int nkb = (Skv + kKvBN - 1) / kKvBN;
     const int logical = xcd_logical_id(blockIdx.x, nkb * a.Hkv * a.B, gridDim.x);
     if (logical < 0) return;
     const int kblk = logical % nkb;
     const int hk = (logical / nkb) % a.Hkv;
     const int b = logical / (nkb * a.Hkv);
     const int G_ = a.Hq / a.Hkv;
-    int kv_end = S;
-    if (a.mask.kv_len) kv_end = min(max(a.mask.kv_len[b], 0), S);
+    int kv_end = Skv;
+    if (a.mask.kv_len) kv_end = min(max(a.mask.kv_len[b], 0), Skv);
     const int k0 = kblk * kKvBN;
     const int kw0 = k0 + wave * 32;  // first key of this wave
     const int key = kw0 + c32;       // this lane's key (column of S)
@@ -140,7 +140,7 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_kv(BwdArgs a) {
         float z[8] = {0, 0, 0, 0, 0, 0, 0, 0};
         pack_frag(kf[c], z);
         pack_frag(vf[c], z);
-        if (key < S) {
+        if (key < Skv) {
             const T* kp = kbase + (int64_t)key * a.mk.ss + 16 * c + 8 * g;
             const T* vp = vbase + (int64_t)key * a.mv.ss + 16 * c + 8 * g;
             if constexpr (kBf16) {
@@ -312,7 +312,7 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_kv(BwdArgs a) {
     }
 
     // dK (times scale) and dV rows of this wave's keys: lane <-> key, 4 consecutive d per store
-    if (key < S) {
+    if (key < Skv) {
         T* dkrow = static_cast<T*>(a.dk) + a.mdk.head_base(b, hk) + (int64_t)key * a.mdk.ss;
         T* dvrow = static_cast<T*>(a.dv) + a.mdv.head_base(b, hk) + (int64_t)key * a.mdv.ss;
 #pragma unroll
@@ -360,8 +360,9 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) void attn_bwd_q(BwdArg
     const int b = logical / (nqb * a.Hq);
     const int qb = a.mask.causal ? (nqb - 1 - rank) : rank;
     const int hk = h / (a.Hq / a.Hkv);
-    int kv_end = S;
-    if (a.mask.kv_len) kv_end = min(max(a.mask.kv_len[b], 0), S);
+    const int Skv = a.Skv;  // key tokens
+    int kv_end = Skv;
+    if (a.mask.kv_len) kv_end = min(max(a.mask.kv_len[b], 0), Skv);
     const int q0 = qb * kQBM;
     const int qw0 = q0 + wave * 32;
     const int qi = qw0 + c32;  // this lane's query (column of S^T)
@@ -412,9 +413,9 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) void attn_bwd_q(BwdArg
 
     const uint32_t es = sizeof(T);
     const Rsrc rk = make_rsrc(static_cast<const T*>(a.k) + a.mk.head_base(b, hk),
-                              (uint32_t)((int64_t)(S - 1) * a.mk.ss * es + D * es));
+                              (uint32_t)((int64_t)(Skv - 1) * a.mk.ss * es + D * es));
     const Rsrc rv = make_rsrc(static_cast<const T*>(a.v) + a.mv.head_base(b, hk),
-                              (uint32_t)((int64_t)(S - 1) * a.mv.ss * es + D * es));
+                              (uint32_t)((int64_t)(Skv - 1) * a.mv.ss * es + D * es));
     const uint32_t kbytes = (uint32_t)(a.mk.ss * es), vbytes = (uint32_t)(a.mv.ss * es);
     DmaPlan<T, D, kQBN, kWaves> pk, pv;
     pk.init(kbytes, wave, lane);
@@ -512,7 +513,7 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) void attn_bwd_q(BwdArg
         pk.issue(lds, rk, 0u, wave);
         pv.issue(lds + 2 * TB, rv, 0u, wave);
     }
-    const int n_full = min(nkb, min(kv_end, a.mask.causal ? q0 + 1 : S) / kQBN);
+    const int n_full = min(nkb, min(kv_end, a.mask.causal ? q0 + 1 : Skv) / kQBN);
     for (int kb = 0; kb < n_full; ++kb) step(std::false_type{}, kb);
     for (int kb = n_full; kb < nkb; ++kb) step(std::true_type{}, kb);
 
@@ -578,7 +579,7 @@ hipError_t launch_attn_bwd(const BwdArgs& a, unsigned phases, hipStream_t stream
             const hipError_t ek = launch_attn_bwd_kv_bf16<D>(a, stream);
             if (ek != hipSuccess) return ek;
         } else {
-        const int n = (a.S + kKvBN - 1) / kKvBN * a.Hkv * a.B;
+        const int n = (a.Skv + kKvBN - 1) / kKvBN * a.Hkv * a.B;
         constexpr int lds = KvCfg<T, D>::BYTES;
         hipLaunchKernelGGL((attn_bwd_kv<T, D>), dim3(padded8(n)), dim3(256), lds, stream, a);
         }

@@ -15,7 +15,7 @@
 // (nqb-1-r, r): every workgroup streams the same number of steps.
 //
 // dS block layout (written by the key/value-major pass): block (qb32, kb32)
-// of query head h is 1024 bf16 at ((b*Hq + h)*nb32 + kb32)*nb32*1024 +
+// of query head h is 1024 bf16 at ((b*Hq + h)*nk32 + kb32)*nq32*1024 +
 // qb32*1024 -- key-block major, so the blocks one step reads (consecutive
 // query tiles at one key block) are contiguous; element cc*512 + l*8 + e
 // holds dS[query acc_row(8cc + e, l/32)]
@@ -74,8 +74,8 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_bf16(BwdArgs a) {
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int g = lane >> 5;
     const int c32 = lane & 31;
-    const int S = a.S;
-    const int nb32 = a.nb32;
+    const int S = a.S, Skv = a.Skv;  // query tokens, key tokens
+    const int nq32 = a.nq32;
     const bool causal = a.mask.causal != 0;
     const int nqb = (S + kDqRows - 1) / kDqRows;
     const int per_bh = causal ? (nqb + 1) / 2 : nqb;  // workgroups per (batch, query head)
@@ -85,8 +85,8 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_bf16(BwdArgs a) {
     const int h = (logical / per_bh) % a.Hq;
     const int b = logical / (per_bh * a.Hq);
     const int hk = h / (a.Hq / a.Hkv);
-    int kv_end = S;
-    if (a.mask.kv_len) kv_end = min(max(a.mask.kv_len[b], 0), S);
+    int kv_end = Skv;
+    if (a.mask.kv_len) kv_end = min(max(a.mask.kv_len[b], 0), Skv);
     const int nkv = (kv_end + 31) / 32;  // key blocks holding an allowed key
     // Query blocks of this workgroup and the key blocks each reads.
     const int qa = causal ? nqb - 1 - r : r;
@@ -97,7 +97,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_bf16(BwdArgs a) {
     // step s -> (first 32-query tile of this wavefront, key block)
     auto tile0_of = [&](int s) __attribute__((always_inline)) { return (s < n_a ? qa : qz) * kDqTilesPerBlock + wave * NT; };
     auto kb_of = [&](int s) __attribute__((always_inline)) { return s < n_a ? s : s - n_a; };
-    auto tile_ok = [&](int tile, int kb) __attribute__((always_inline)) { return tile < nb32 && (!causal || kb <= tile); };
+    auto tile_ok = [&](int tile, int kb) __attribute__((always_inline)) { return tile < nq32 && (!causal || kb <= tile); };
 
     // ---- DMA.  K rows past S and dS blocks outside the head's range read as
     // zeros; blocks above the causal diagonal are not fetched (their loads
@@ -105,10 +105,10 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_bf16(BwdArgs a) {
     const uint32_t kbytes = (uint32_t)(a.mk.ss * 2);
     const bool k_loader = wave < P::KINST;
     const Rsrc rk = make_rsrc(static_cast<const bf16*>(a.k) + a.mk.head_base(b, hk),
-                              k_loader ? (uint32_t)((int64_t)(S - 1) * a.mk.ss * 2 + D * 2) : 0u);
+                              k_loader ? (uint32_t)((int64_t)(Skv - 1) * a.mk.ss * 2 + D * 2) : 0u);
     DmaPlan<bf16, D, 32, kDqWaves> pk;
     pk.init(kbytes, wave, lane);
-    const uint32_t ds_head_elems = (uint32_t)nb32 * (uint32_t)nb32 * 1024u;
+    const uint32_t ds_head_elems = (uint32_t)nq32 * (uint32_t)a.nk32 * 1024u;
     const Rsrc rds = make_rsrc(static_cast<const bf16*>(a.ds) + ((int64_t)b * a.Hq + h) * ds_head_elems,
                                ds_head_elems * 2u);
     constexpr uint32_t kNoRecord = 0x80000000u;  // past every head's dS range (< 2 GiB)
@@ -129,7 +129,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_bf16(BwdArgs a) {
 #pragma unroll
         for (int qt = 0; qt < NT; ++qt) {
             const uint32_t soff =
-                tile_ok(tile0 + qt, kb) ? ((uint32_t)kb * (uint32_t)nb32 + (uint32_t)(tile0 + qt)) * 2048u : kNoRecord;
+                tile_ok(tile0 + qt, kb) ? ((uint32_t)kb * (uint32_t)nq32 + (uint32_t)(tile0 + qt)) * 2048u : kNoRecord;
             const uint32_t dl = lds + buf * P::DSBUF + wave * P::DSW + qt * 2048;
             dma16_stream(rds_s, dl, (uint32_t)lane * 16u, __builtin_amdgcn_readfirstlane(soff));
             dma16_stream(rds_s, dl + 1024, (uint32_t)lane * 16u + 1024u, __builtin_amdgcn_readfirstlane(soff));

@@ -27,7 +27,7 @@
 // consumes) block by block into the workspace, for the dQ pass to contract
 // with K instead of recomputing S and dP.  A 32-query x 32-key block is 2 KB
 // (blocks of one query head key-block major: block (qb32, kb32) at
-// (kb32*nb32 + qb32)*1024, so one wavefront's stores stream through
+// (kb32*nq32 + qb32)*1024, so one wavefront's stores stream through
 // consecutive blocks) in the accumulator order the fragments already have:
 // element
 // cc*512 + lane*8 + e holds dS[query acc_row(8cc + e, lane / 32)][key lane % 32],
@@ -85,15 +85,15 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_kv_bf16(BwdArgs a) {
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int g = lane >> 5;
     const int c32 = lane & 31;
-    const int S = a.S;
-    const int nkb = (S + kPKeys - 1) / kPKeys;
+    const int S = a.S, Skv = a.Skv;  // query tokens, key tokens
+    const int nkb = (Skv + kPKeys - 1) / kPKeys;
     int kblk, bh;  // causal: key block 0 meets the most queries; start it first
     if (!rank_major_item(blockIdx.x, nkb, a.Hkv * a.B, kblk, bh)) return;
     const int hk = bh % a.Hkv;
     const int b = bh / a.Hkv;
     const int G_ = a.Hq / a.Hkv;
-    int kv_end = S;
-    if (a.mask.kv_len) kv_end = min(max(a.mask.kv_len[b], 0), S);
+    int kv_end = Skv;
+    if (a.mask.kv_len) kv_end = min(max(a.mask.kv_len[b], 0), Skv);
     const int k0 = kblk * kPKeys;
     const int kw0 = k0 + wave * 32;  // first key of this wave
     const int key = kw0 + c32;       // this lane's key (column of S)
@@ -107,7 +107,7 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_kv_bf16(BwdArgs a) {
         for (int c = 0; c < NC; ++c) {
             kf[c].v = bf16x8{};
             vf[c].v = bf16x8{};
-            if (key < S) {
+            if (key < Skv) {
                 kf[c].v = __builtin_bit_cast(bf16x8, load16(kp + 16 * c));
                 vf[c].v = __builtin_bit_cast(bf16x8, load16(vp + 16 * c));
             }
@@ -132,13 +132,13 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_kv_bf16(BwdArgs a) {
     const int n_mask = a.mask.causal ? min(per_head, (k0 + kPKeys - 2) / BQ - qb_start + 1) : 0;
 
     // dS blocks of this wave's 32 keys (DS only): block (qb32, kb32) of query
-    // head h starts at element ((b*Hq + h)*nb32 + kb32)*nb32*1024 + qb32*1024;
+    // head h starts at element ((b*Hq + h)*nk32 + kb32)*nq32*1024 + qb32*1024;
     // one buffer resource per query head, the block offset in the scalar
     // offset of the stores, which are non-temporal (read once, by the dQ
     // pass; they should not displace the Q/dO tiles other workgroups reuse).
     const int kb32 = kw0 / 32;
     const bool ds_live = DS && kw0 < kv_end;  // keys past kv_end: never read
-    const uint32_t ds_head_elems = (uint32_t)a.nb32 * (uint32_t)a.nb32 * 1024u;
+    const uint32_t ds_head_elems = (uint32_t)a.nq32 * (uint32_t)a.nk32 * 1024u;
     const bf16* ds_head = DS ? static_cast<const bf16*>(a.ds) + ((int64_t)b * a.Hq + hk * G_) * ds_head_elems : nullptr;
     __amdgpu_buffer_rsrc_t ds_rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16*>(ds_head), 0,
                                                                      (int)(ds_head_elems * 2u), 0x00020000);
@@ -339,8 +339,8 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_kv_bf16(BwdArgs a) {
 #pragma unroll
                 for (int qt = 0; qt < NQT; ++qt) {
                     const int qb32 = (qb_start + j) * NQT + qt;
-                    if (qb32 < a.nb32 && (!a.mask.causal || qb32 >= kb32)) {
-                        const int soff = (kb32 * a.nb32 + qb32) * 2048;
+                    if (qb32 < a.nq32 && (!a.mask.causal || qb32 >= kb32)) {
+                        const int soff = (kb32 * a.nq32 + qb32) * 2048;
 #pragma unroll
                         for (int cc = 0; cc < 2; ++cc) {
                             using i32x4 = int __attribute__((ext_vector_type(4)));
@@ -420,7 +420,7 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_kv_bf16(BwdArgs a) {
     // consecutive d per store.  Keys at or past kv_end take no part: their
     // accumulators hold unmasked (possibly non-finite) sums and are replaced
     // by zeros.
-    if (key < S) {
+    if (key < Skv) {
         const bool live = key < kv_end;
         bf16* dkrow = static_cast<bf16*>(a.dk) + a.mdk.head_base(b, hk) + (int64_t)key * a.mdk.ss;
         bf16* dvrow = static_cast<bf16*>(a.dv) + a.mdv.head_base(b, hk) + (int64_t)key * a.mdv.ss;
@@ -455,7 +455,7 @@ hipError_t launch_kv(const BwdArgs& a, hipStream_t stream) {
                                                        hipFuncAttributeMaxDynamicSharedMemorySize, KvPipe<D>::BYTES);
     if (once != hipSuccess) return once;
     constexpr int lds = KvPipe<D>::BYTES;
-    hipLaunchKernelGGL((attn_bwd_kv_bf16<D, DS>), dim3(rank_major_grid((a.S + kPKeys - 1) / kPKeys, a.Hkv * a.B)),
+    hipLaunchKernelGGL((attn_bwd_kv_bf16<D, DS>), dim3(rank_major_grid((a.Skv + kPKeys - 1) / kPKeys, a.Hkv * a.B)),
                        dim3(256), lds, stream, a);
     return hipGetLastError();
 }

@@ -70,8 +70,9 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_q_bf16(BwdArgs a) {
     // causal: the last query blocks see the most keys; start them first
     const int qb = a.mask.causal ? (nqb - 1 - rank) : rank;
     const int hk = h / (a.Hq / a.Hkv);
-    int kv_end = S;
-    if (a.mask.kv_len) kv_end = min(max(a.mask.kv_len[b], 0), S);
+    const int Skv = a.Skv;  // key tokens
+    int kv_end = Skv;
+    if (a.mask.kv_len) kv_end = min(max(a.mask.kv_len[b], 0), Skv);
     const int q0 = qb * kQRows;
     const int qi = q0 + wave * 32 + c32;  // this lane's query (column of S^T)
     int k_hi = kv_end;
@@ -79,7 +80,7 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_q_bf16(BwdArgs a) {
     const int n_iter = (k_hi + BK - 1) / BK;
     // blocks every query of the workgroup sees whole: inside kv_end and (causal)
     // at or below the workgroup's first query
-    const int n_full = min(n_iter, min(kv_end, a.mask.causal ? q0 + 1 : S) / BK);
+    const int n_full = min(n_iter, min(kv_end, a.mask.causal ? q0 + 1 : Skv) / BK);
 
     // Q^T and dO^T rows of this wave's queries as B operands: lane <-> query,
     // in-lane d = 16c + 8g + e
@@ -111,9 +112,9 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_q_bf16(BwdArgs a) {
     // ---- DMA of the K and V tiles of one block
     const uint32_t kbytes = (uint32_t)(a.mk.ss * 2), vbytes = (uint32_t)(a.mv.ss * 2);
     const Rsrc rk = make_rsrc(static_cast<const bf16*>(a.k) + a.mk.head_base(b, hk),
-                              (uint32_t)((int64_t)(S - 1) * a.mk.ss * 2 + D * 2));
+                              (uint32_t)((int64_t)(Skv - 1) * a.mk.ss * 2 + D * 2));
     const Rsrc rv = make_rsrc(static_cast<const bf16*>(a.v) + a.mv.head_base(b, hk),
-                              (uint32_t)((int64_t)(S - 1) * a.mv.ss * 2 + D * 2));
+                              (uint32_t)((int64_t)(Skv - 1) * a.mv.ss * 2 + D * 2));
     DmaPlan<bf16, D, BK, kQWaves> pk, pv;
     pk.init(kbytes, wave, lane);
     pv.init(vbytes, wave, lane);

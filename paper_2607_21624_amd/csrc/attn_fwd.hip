@@ -66,8 +66,9 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) void attn_fwd_kernel(F
     const int qb = a.mask.causal ? (nqb - 1 - rank) : rank;
     const int hk = h / (a.Hq / a.Hkv);
 
-    int kv_end = S;
-    if (a.mask.kv_len) kv_end = min(max(a.mask.kv_len[b], 0), S);
+    const int Skv = a.Skv;
+    int kv_end = Skv;
+    if (a.mask.kv_len) kv_end = min(max(a.mask.kv_len[b], 0), Skv);
     const int q0 = qb * kFwdBM;
     const int qw0 = q0 + wave * 32;  // first query of this wave
     const int qi = qw0 + c32;        // this lane's query (column of S^T)
@@ -111,9 +112,9 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) void attn_fwd_kernel(F
 
     const uint32_t es = sizeof(T);
     const Rsrc rk = make_rsrc(static_cast<const T*>(a.k) + a.mk.head_base(b, hk),
-                              (uint32_t)((int64_t)(S - 1) * a.mk.ss * es + D * es));
+                              (uint32_t)((int64_t)(Skv - 1) * a.mk.ss * es + D * es));
     const Rsrc rv = make_rsrc(static_cast<const T*>(a.v) + a.mv.head_base(b, hk),
-                              (uint32_t)((int64_t)(S - 1) * a.mv.ss * es + D * es));
+                              (uint32_t)((int64_t)(Skv - 1) * a.mv.ss * es + D * es));
     const uint32_t kbytes = (uint32_t)(a.mk.ss * es), vbytes = (uint32_t)(a.mv.ss * es);
     DmaPlan<T, D, kFwdBN, kFwdWaves> dk, dv;
     dk.init(kbytes, wave, lane);
@@ -345,7 +346,7 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) void attn_fwd_kernel(F
     // Tiles inside kv_end and (causal) at or below the block's first query need
     // no mask for any wave; rounded down to an even count so the masked loop
     // also starts on parity 0.
-    const int n_full = min(nkb, min(kv_end, a.mask.causal ? q0 + 1 : S) / kFwdBN) & ~1;
+    const int n_full = min(nkb, min(kv_end, a.mask.causal ? q0 + 1 : Skv) / kFwdBN) & ~1;
     using P0 = std::integral_constant<int, 0>;
     using P1 = std::integral_constant<int, 1>;
     for (int j = 0; j < n_full; j += 2) {

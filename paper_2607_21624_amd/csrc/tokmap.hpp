@@ -38,7 +38,8 @@ struct FwdArgs {
     void* o;
     float* lse;
     TokMap mq, mk, mv, mo;
-    int B, S, Hq, Hkv;
+    int B, S, Hq, Hkv;  // S: query tokens
+    int Skv;            // key/value tokens (S for self-attention)
     float scale_log2;  // softmax scale times log2(e)
     MaskArgs mask;
 };
@@ -54,10 +55,11 @@ struct BwdArgs {
     void* dk;
     void* dv;
     float* stats;      // workspace [B, Hq, 2, S]: rows LSE * log2(e) and sum_k dO*O per query
-    void* ds;          // nullptr, or workspace [B, Hq, nb32 (key), nb32 (query)] blocks of 32x32 bf16 dS
-    int nb32;          // ceil(S / 32)
+    void* ds;          // nullptr, or workspace [B, Hq, nk32, nq32] blocks of 32x32 bf16 dS
+    int nq32, nk32;    // ceil(S / 32), ceil(Skv / 32)
     TokMap mq, mk, mv, mo, mdo, mdq, mdk, mdv;
-    int B, S, Hq, Hkv;
+    int B, S, Hq, Hkv;  // S: query tokens
+    int Skv;            // key/value tokens (S for self-attention)
     float scale;       // softmax scale
     float scale_log2;  // scale * log2(e)
     MaskArgs mask;

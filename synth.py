@@ -4,11 +4,13 @@ This module is shared by the oracle-side tests and the HIP-side tests and bench.
 It holds workload shapes and random draws only, none of the attention
 arithmetic: every tensor it returns is an input (Q, K, V, dO, key lengths).
 
-Draw recipe (one ``numpy.random.default_rng(seed)`` PCG64 stream per workload):
-  Q  (B, S, Hq*d)   standard normal, fp64
-  K  (B, S, Hkv*d)  standard normal, fp64
-  V  (B, S, Hkv*d)  standard normal, fp64
-  dO (B, S, Hq*d)   standard normal, fp64
+Draw recipe (one ``numpy.random.default_rng(seed)`` PCG64 stream per workload;
+S is the query length, S_kv the key/value length, equal to S for
+self-attention):
+  Q  (B, S, Hq*d)      standard normal, fp64
+  K  (B, S_kv, Hkv*d)  standard normal, fp64
+  V  (B, S_kv, Hkv*d)  standard normal, fp64
+  dO (B, S, Hq*d)      standard normal, fp64
   kv_len (B,)       integers uniform on [len_lo, len_hi] inclusive, only for
                     key-padding workloads, drawn after dO
 Values are then rounded to the storage type: fp32 by IEEE round-to-nearest-even,
@@ -47,6 +49,11 @@ class Workload:
     len_lo: int = 0       # key-padding length range (inclusive), used when mask & 2
     len_hi: int = 0
     note: str = field(default="", compare=False)
+    S_kv: int = 0         # key/value tokens; 0 means S (self-attention)
+
+    @property
+    def Skv(self) -> int:
+        return self.S_kv or self.S
 
 
 # The five workload shapes the build is measured and checked on.  Names say what
@@ -75,6 +82,20 @@ PAPER_MHA_SHAPES = {
     "paper_mha_c1": Workload("paper_mha_c1", B=1, S=512, Hq=32, Hkv=32, d=64, dtype="bf16", mask=MASK_CAUSAL),
     "paper_mha_c2": Workload("paper_mha_c2", B=1, S=512, Hq=16, Hkv=16, d=64, dtype="bf16", mask=MASK_NONE),
     "paper_mha_c3": Workload("paper_mha_c3", B=1, S=512, Hq=8, Hkv=8, d=128, dtype="bf16", mask=MASK_CAUSAL),
+}
+
+
+# Cross-attention (S_kv != S): the decoder-side attention of the encoder-decoder
+# models in the paper's evaluation, here Whisper-large-like (20 heads of 64;
+# decoder tokens attend to the encoder's audio frames, 300 as in the paper's
+# model table).  Not one of the five measured shapes above.
+CROSS_WORKLOADS = {
+    "whisper_large_cross": Workload("whisper_large_cross", B=2, S=448, S_kv=300, Hq=20, Hkv=20, d=64,
+                                    dtype="bf16", mask=MASK_NONE,
+                                    note="Whisper-large-like decoder cross-attention, 448 tokens x 300 frames"),
+    "whisper_large_cross_keypad": Workload("whisper_large_cross_keypad", B=4, S=448, S_kv=300, Hq=20, Hkv=20,
+                                           d=64, dtype="bf16", mask=MASK_KEY_PADDING, len_lo=100, len_hi=300,
+                                           note="as above with padded encoder frames, lengths U[100,300]"),
 }
 
 
@@ -116,8 +137,8 @@ def make_inputs(w: Workload, seed: Optional[int] = None, zero_q: bool = False) -
     s = w.seed if seed is None else seed
     rng = np.random.default_rng(s)
     q = rng.standard_normal((w.B, w.S, w.Hq * w.d))
-    k = rng.standard_normal((w.B, w.S, w.Hkv * w.d))
-    v = rng.standard_normal((w.B, w.S, w.Hkv * w.d))
+    k = rng.standard_normal((w.B, w.Skv, w.Hkv * w.d))
+    v = rng.standard_normal((w.B, w.Skv, w.Hkv * w.d))
     do = rng.standard_normal((w.B, w.S, w.Hq * w.d))
     kv_len = None
     if w.mask & MASK_KEY_PADDING:

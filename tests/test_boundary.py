@@ -174,6 +174,11 @@ def test_fwd_rejections():
     # scale
     assert _fwd(lq, lk, lv, lo, p, scale=float("nan")) == E.FBL_ERR_ARG
     assert _fwd(lq, lk, lv, lo, p, scale=float("inf")) == E.FBL_ERR_ARG
+    # cross-attention (S_kv != S_q) takes no causal mask
+    lk8, lv8 = _copy(lk, S=8, sb=8 * 128), _copy(lv, S=8, sb=8 * 128)
+    assert _fwd(lq, lk8, lv8, lo, p, kind=F.FBL_MASK_CAUSAL) == E.FBL_ERR_UNSUPPORTED
+    assert _fwd(lq, lk8, lv8, lo, p, kind=F.FBL_MASK_CAUSAL | F.FBL_MASK_KEY_PADDING, kv_len=64) \
+        == E.FBL_ERR_UNSUPPORTED
     # output aliasing an input
     assert _fwd(lq, lk, lv, lo, dict(p, o=p["q"])) == E.FBL_ERR_ARG
     assert _fwd(lq, lk, lv, lo, dict(p, lse=p["v"] + 64)) == E.FBL_ERR_ARG
@@ -214,6 +219,12 @@ def test_bwd_workspace_size():
             assert fbl.fbl_attn_bwd_workspace_min(lq, lk) == stats
             nb = (S + 31) // 32
             assert fbl.fbl_attn_bwd_workspace(lq, lk) == stats + (2 * 6 * nb * nb * 2048 if with_ds else 0)
+    # cross-attention: statistics per query row, dS blocks ceil(S_q/32) x ceil(S_kv/32)
+    lq = fbl.fbl_layout_desc(BF16, 2, 100, 6, 64)
+    lk = fbl.fbl_layout_desc(BF16, 2, 70, 3, 64)
+    stats = (2 * 6 * 100 * 2 * 4 + 255) // 256 * 256
+    assert fbl.fbl_attn_bwd_workspace_min(lq, lk) == stats
+    assert fbl.fbl_attn_bwd_workspace(lq, lk) == stats + 2 * 6 * 4 * 3 * 2048
     # one head's dS blocks would reach 2 GiB: no stored-dS part
     lq = fbl.fbl_layout_desc(BF16, 1, 32768, 1, 64)
     assert fbl.fbl_attn_bwd_workspace(lq, lq) == fbl.fbl_attn_bwd_workspace_min(lq, lq)

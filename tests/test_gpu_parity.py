@@ -123,6 +123,49 @@ def test_recompute_dq_path(d, mask, S):
         assert not bad, f"workspace {ws}: {bad}"
 
 
+# ---------------------------------------------------------- cross-attention
+@pytest.mark.parametrize("name", list(synth.CROSS_WORKLOADS))
+def test_cross_attention_workloads(name):
+    """Whisper-large-like decoder cross-attention (448 tokens x 300 frames), all
+    heads against the oracle, dQ from stored dS and from the recompute pass."""
+    w = synth.CROSS_WORKLOADS[name]
+    inp = synth.make_inputs(w)
+    note(f"{name} B={w.B} S_q={w.S} S_kv={w.Skv} H={w.Hq} d={w.d} mask={w.mask} kv_len={inp['kv_len']}")
+    ref = oracle_fwd_bwd(inp)
+    for ws in ("full", "min"):
+        errs, bad = compare(gpu_fwd_bwd(inp, workspace=ws), ref, w.dtype)
+        note(f"{name} workspace={ws} rel errs {errs}")
+        assert not bad, f"{name} workspace {ws}: {bad}"
+
+
+CROSS_CASES = [
+    # (d, dtype, S_q, S_kv, mask, Hq, Hkv)
+    (128, "bf16", 300, 77, synth.MASK_NONE, 4, 2),
+    (128, "bf16", 65, 257, synth.MASK_KEY_PADDING, 2, 2),
+    (64, "bf16", 1, 200, synth.MASK_NONE, 4, 1),
+    (64, "bf16", 190, 1, synth.MASK_NONE, 2, 2),
+    (64, "bf16", 129, 33, synth.MASK_KEY_PADDING, 8, 2),
+    (32, "bf16", 97, 160, synth.MASK_NONE, 3, 3),
+    (128, "f32", 70, 130, synth.MASK_KEY_PADDING, 2, 1),
+    (64, "f32", 150, 40, synth.MASK_NONE, 4, 2),
+    (32, "f32", 33, 95, synth.MASK_NONE, 2, 2),
+]
+
+
+@pytest.mark.parametrize("d,dt,Sq,Skv,mask,Hq,Hkv", CROSS_CASES)
+def test_cross_attention_shapes(d, dt, Sq, Skv, mask, Hq, Hkv):
+    """Rectangular score matrices: S_q < S_kv and S_q > S_kv, ragged tails on
+    both sides, a single query and a single key, MHA and GQA, fp32 and bf16."""
+    w = synth.Workload(f"cross{Sq}x{Skv}", B=2, S=Sq, S_kv=Skv, Hq=Hq, Hkv=Hkv, d=d, dtype=dt, mask=mask,
+                       len_lo=1, len_hi=Skv, seed=Sq * 1000 + Skv + d)
+    inp = synth.make_inputs(w)
+    note(f"cross S_q={Sq} S_kv={Skv} d={d} {dt} mask={mask} Hq={Hq} Hkv={Hkv} kv_len={inp['kv_len']}")
+    ref = oracle_fwd_bwd(inp)
+    for ws in ("full", "min"):
+        errs, bad = compare(gpu_fwd_bwd(inp, workspace=ws), ref, dt)
+        assert not bad, f"workspace {ws}: {bad}"
+
+
 # ------------------------------------------------------------- edge cases
 def test_zero_and_overlong_key_lengths():
     import torch
