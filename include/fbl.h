@@ -118,6 +118,27 @@ fbl_status fbl_layout_desc(fbl_layout* out, int32_t dtype, int64_t B, int64_t S,
                            int64_t row_stride, int64_t batch_stride, int64_t tile_d);
 
 /*
+ * Descriptors of Q, K and V as views into one packed projection output of
+ * logical shape [B, S, (Hq + 2*Hkv) * D] -- the fused QKV projection writes
+ * each token row as Hq query heads, then Hkv key heads, then Hkv value heads.
+ * The reshape/transpose chain of section 4.3.1 then splits the row into three
+ * head-split tensors; here each is an index map with row stride
+ * (Hq + 2*Hkv) * D and a start offset, so none of them is copied out.
+ *   lq, lk, lv      filled with the three descriptors (as fbl_layout_desc
+ *                   would for a tensor of Hq, Hkv, Hkv heads with that row
+ *                   stride, and the same tile-legality checks).
+ *   k_off, v_off    element offsets of K and V from the packed base (Q is at
+ *                   offset 0): Hq*D and (Hq + Hkv)*D.
+ *   batch_stride    elements between batches; 0 means S * (Hq + 2*Hkv) * D.
+ * The same descriptors and offsets describe a packed gradient buffer
+ * [B, S, (Hq + 2*Hkv) * D] receiving dQ, dK, dV.  Returns the status of
+ * fbl_layout_desc; on failure all outputs are left zeroed.  Pure host function.
+ */
+fbl_status fbl_layout_packed_qkv(fbl_layout* lq, fbl_layout* lk, fbl_layout* lv, int64_t* k_off, int64_t* v_off,
+                                 int32_t dtype, int64_t B, int64_t S, int64_t Hq, int64_t Hkv, int64_t D,
+                                 int64_t batch_stride, int64_t tile_d);
+
+/*
  * Host evaluation of the index map: element offset of logical (b, h, s, i),
  * or -1 when the descriptor is NULL or an index is out of range.
  */

@@ -13,7 +13,8 @@ Modules
   brute      scalar triple loops of the same definition, for tiny inputs; used
              to cross-check ``attention``.
   layout     the logical (b, h, s, i) -> physical offset map of a token-major
-             tensor, built by the reshape-then-transpose chain itself.
+             tensor, built by the reshape-then-transpose chain itself, also
+             for Q, K, V split out of one packed projection output.
 
 Pins (tests/test_oracle.py, tests/test_layout.py) tie each function to
 something other than itself: brute force, float64 torch SDPA with autograd,
@@ -21,4 +22,4 @@ central finite differences, closed forms, invariants and the paper's own
 layout examples.  Each function's docstring names the pin(s).
 """
 from .attention import attn_fwd, attn_bwd, bwd_row_dot, head_probs, kv_head_of, allowed_mask  # noqa: F401
-from .layout import token_major_offsets, head_split_offsets  # noqa: F401
+from .layout import token_major_offsets, head_split_offsets, packed_qkv_offsets  # noqa: F401

@@ -37,3 +37,17 @@ def head_split_offsets(B: int, S: int, H: int, d: int, row_stride: int, batch_st
     c = np.arange(H * d, dtype=np.int64)[None, None, :]
     grid = b + s + c                       # logical (B, S, H*d) -> physical offset
     return grid.reshape(B, S, H, d).transpose(0, 2, 1, 3)
+
+
+def packed_qkv_offsets(B: int, S: int, Hq: int, Hkv: int, d: int):
+    """Offsets of Q, K and V inside one packed projection output
+    [B, S, (Hq + 2 Hkv) d] whose rows hold Hq query heads, then Hkv key heads,
+    then Hkv value heads.  Built by splitting an array of flat indices of the
+    packed tensor with numpy slicing, then the reshape/transpose chain.
+    Returns three int64 arrays shaped (B, H, S, d)."""
+    H = Hq + 2 * Hkv
+    flat = np.arange(B * S * H * d, dtype=np.int64).reshape(B, S, H, d)
+    q = flat[:, :, :Hq]
+    k = flat[:, :, Hq:Hq + Hkv]
+    v = flat[:, :, Hq + Hkv:]
+    return tuple(x.transpose(0, 2, 1, 3) for x in (q, k, v))

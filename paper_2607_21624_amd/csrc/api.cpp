@@ -197,6 +197,30 @@ fbl_status fbl_layout_desc(fbl_layout* out, int32_t dtype, int64_t B, int64_t S,
     return FBL_OK;
 }
 
+fbl_status fbl_layout_packed_qkv(fbl_layout* lq, fbl_layout* lk, fbl_layout* lv, int64_t* k_off, int64_t* v_off,
+                                 int32_t dtype, int64_t B, int64_t S, int64_t Hq, int64_t Hkv, int64_t D,
+                                 int64_t batch_stride, int64_t tile_d) {
+    if (!lq || !lk || !lv || !k_off || !v_off) return FBL_ERR_NULL;
+    std::memset(lq, 0, sizeof(*lq));
+    std::memset(lk, 0, sizeof(*lk));
+    std::memset(lv, 0, sizeof(*lv));
+    *k_off = 0;
+    *v_off = 0;
+    if (Hq <= 0 || Hkv <= 0 || D <= 0 || Hq > INT32_MAX || Hkv > INT32_MAX) return FBL_ERR_SHAPE;
+    const int64_t row = (Hq + 2 * Hkv) * D;  // one token of the packed projection output
+    fbl_layout q, k, v;
+    fbl_status st;
+    if ((st = fbl_layout_desc(&q, dtype, B, S, Hq, D, row, batch_stride, tile_d)) != FBL_OK) return st;
+    if ((st = fbl_layout_desc(&k, dtype, B, S, Hkv, D, row, batch_stride, tile_d)) != FBL_OK) return st;
+    if ((st = fbl_layout_desc(&v, dtype, B, S, Hkv, D, row, batch_stride, tile_d)) != FBL_OK) return st;
+    *lq = q;
+    *lk = k;
+    *lv = v;
+    *k_off = Hq * D;
+    *v_off = (Hq + Hkv) * D;
+    return FBL_OK;
+}
+
 int64_t fbl_layout_offset(const fbl_layout* l, int64_t b, int64_t h, int64_t s, int64_t i) {
     if (!l) return -1;
     if (b < 0 || b >= l->B || h < 0 || h >= l->H || s < 0 || s >= l->S || i < 0 || i >= l->D) return -1;

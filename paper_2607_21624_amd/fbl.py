@@ -36,7 +36,7 @@ FBL_BWD_KV = 2
 FBL_BWD_Q = 4
 FBL_BWD_ALL = 7
 
-EXPORTED = ("fbl_layout_desc", "fbl_layout_offset", "fbl_layout_map_device", "fbl_attn_fwd",
+EXPORTED = ("fbl_layout_desc", "fbl_layout_packed_qkv", "fbl_layout_offset", "fbl_layout_map_device", "fbl_attn_fwd",
             "fbl_attn_bwd_workspace", "fbl_attn_bwd_workspace_min", "fbl_attn_bwd", "fbl_attn_bwd_phases", "fbl_status_str")
 
 
@@ -77,6 +77,9 @@ def _load() -> ctypes.CDLL:
     vp = ctypes.c_void_p
     lib.fbl_layout_desc.argtypes = [P(Layout), ctypes.c_int32] + [ctypes.c_int64] * 7
     lib.fbl_layout_desc.restype = ctypes.c_int
+    lib.fbl_layout_packed_qkv.argtypes = [P(Layout), P(Layout), P(Layout), P(ctypes.c_int64), P(ctypes.c_int64),
+                                          ctypes.c_int32] + [ctypes.c_int64] * 7
+    lib.fbl_layout_packed_qkv.restype = ctypes.c_int
     lib.fbl_layout_offset.argtypes = [P(Layout)] + [ctypes.c_int64] * 4
     lib.fbl_layout_offset.restype = ctypes.c_int64
     lib.fbl_layout_map_device.argtypes = [P(Layout), vp, vp]
@@ -126,6 +129,18 @@ def fbl_layout_desc_status(dtype: int, B: int, S: int, H: int, D: int, row_strid
     out = Layout()
     st = LIB.fbl_layout_desc(ctypes.byref(out), dtype, B, S, H, D, row_stride, batch_stride, tile_d)
     return st, out
+
+
+def fbl_layout_packed_qkv(dtype: int, B: int, S: int, Hq: int, Hkv: int, D: int, batch_stride: int = 0,
+                          tile_d: int = 0):
+    """Descriptors of Q, K, V inside one packed [B, S, (Hq + 2 Hkv) D] projection
+    output: returns (lq, lk, lv, k_off, v_off), offsets in elements."""
+    lq, lk, lv = Layout(), Layout(), Layout()
+    ko, vo = ctypes.c_int64(0), ctypes.c_int64(0)
+    _check(LIB.fbl_layout_packed_qkv(ctypes.byref(lq), ctypes.byref(lk), ctypes.byref(lv), ctypes.byref(ko),
+                                     ctypes.byref(vo), dtype, B, S, Hq, Hkv, D, batch_stride, tile_d),
+           "fbl_layout_packed_qkv")
+    return lq, lk, lv, int(ko.value), int(vo.value)
 
 
 def fbl_layout_offset(l: Layout, b: int, h: int, s: int, i: int) -> int:
@@ -257,3 +272,61 @@ def attn_bwd(q, k, v, o, do, lse, Hq: int, Hkv: int, scale: Optional[float] = No
                             dk, ldv, dv, workspace, workspace.numel() * workspace.element_size(), stream,
                             phases), "fbl_attn_bwd")
     return dq, dk, dv
+
+
+# ------------------------------------------------- packed QKV projection output
+def _packed(qkv, Hq: int, Hkv: int):
+    import torch
+    if qkv.dim() != 3 or qkv.stride(2) != 1 or qkv.stride(1) != qkv.shape[2]:
+        raise FblError(FBL_ERR_LAYOUT, "expected a [B, S, (Hq + 2 Hkv) D] tensor with contiguous rows")
+    B, S, W = qkv.shape
+    if W % (Hq + 2 * Hkv):
+        raise FblError(FBL_ERR_SHAPE, f"row width {W} not divisible by Hq + 2 Hkv = {Hq + 2 * Hkv}")
+    D = W // (Hq + 2 * Hkv)
+    lq, lk, lv, ko, vo = fbl_layout_packed_qkv(_dtype_code(qkv), B, S, Hq, Hkv, D,
+                                               batch_stride=qkv.stride(0) if B > 1 else 0)
+    es = qkv.element_size()
+    base = qkv.data_ptr()
+    return lq, lk, lv, base, base + ko * es, base + vo * es
+
+
+def attn_fwd_packed(qkv, Hq: int, Hkv: int, scale: Optional[float] = None, causal: bool = False, kv_len=None,
+                    out=None, lse=None, stream=None):
+    """Forward on a packed QKV projection output [B, S, (Hq + 2 Hkv) D]: Q, K and
+    V are read in place through fbl_layout_packed_qkv descriptors.  Returns
+    (O [B, S, Hq D], LSE [B, Hq, S])."""
+    import torch
+    lq, lk, lv, pq, pk, pv = _packed(qkv, Hq, Hkv)
+    if scale is None:
+        scale = 1.0 / math.sqrt(lq.D)
+    B, S = qkv.shape[0], qkv.shape[1]
+    if out is None:
+        out = torch.empty((B, S, Hq * lq.D), dtype=qkv.dtype, device=qkv.device)
+    if lse is None:
+        lse = torch.empty((B, Hq, S), dtype=torch.float32, device=qkv.device)
+    lo = layout_of(out, Hq)
+    _check(fbl_attn_fwd_raw(lq, pq, lk, pk, lv, pv, lo, out, lse, scale, _mask(causal, kv_len), stream),
+           "fbl_attn_fwd")
+    return out, lse
+
+
+def attn_bwd_packed(qkv, o, do, lse, Hq: int, Hkv: int, scale: Optional[float] = None, causal: bool = False,
+                    kv_len=None, dqkv=None, workspace=None, stream=None):
+    """Backward on a packed QKV projection output: dQ, dK, dV are written into
+    one packed gradient tensor shaped like ``qkv`` (allocated unless given)."""
+    import torch
+    lq, lk, lv, pq, pk, pv = _packed(qkv, Hq, Hkv)
+    if scale is None:
+        scale = 1.0 / math.sqrt(lq.D)
+    if dqkv is None:
+        dqkv = torch.empty(qkv.shape, dtype=qkv.dtype, device=qkv.device)
+    if dqkv.shape != qkv.shape or dqkv.stride() != qkv.stride() or dqkv.dtype != qkv.dtype:
+        raise FblError(FBL_ERR_SHAPE, "dqkv must have qkv's shape, strides and dtype")
+    _, _, _, gq, gk, gv = _packed(dqkv, Hq, Hkv)
+    lo, ldo = layout_of(o, Hq), layout_of(do, Hq)
+    if workspace is None:
+        workspace = torch.empty(fbl_attn_bwd_workspace(lq, lk), dtype=torch.uint8, device=qkv.device)
+    _check(fbl_attn_bwd_raw(lq, pq, lk, pk, lv, pv, lo, o, ldo, do, lse, scale, _mask(causal, kv_len), lq, gq, lk,
+                            gk, lv, gv, workspace, workspace.numel() * workspace.element_size(), stream),
+           "fbl_attn_bwd")
+    return dqkv

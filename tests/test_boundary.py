@@ -272,3 +272,39 @@ def test_bwd_rejects_overlapping_packed_views():
     # dv starts inside dk's columns
     bad = dict(p, dq=base, dk=base + Hq * D * 2, dv=base + (Hq + 1) * D * 2)
     assert _bwd(lq, lk, lv, lo, bad, ws, ldq=ldq, ldk=ldk, ldv=ldv) == F.FBL_ERR_ARG
+
+
+@pytest.mark.parametrize("B,S,Hq,Hkv,D,bstride", [(2, 5, 4, 2, 64, 0), (3, 7, 6, 3, 32, 0), (2, 4, 8, 8, 128, 0),
+                                                   (2, 6, 4, 1, 64, 6 * 6 * 64 + 128)])
+def test_packed_qkv_descriptors_bit_exact(B, S, Hq, Hkv, D, bstride):
+    """fbl_layout_packed_qkv + fbl_layout_offset against the oracle's split of
+    a packed projection output (numpy slicing of flat indices)."""
+    import numpy as np
+    import oracle
+    lq, lk, lv, ko, vo = fbl.fbl_layout_packed_qkv(BF16, B, S, Hq, Hkv, D, batch_stride=bstride)
+    W = (Hq + 2 * Hkv) * D
+    assert (lq.ss, lk.ss, lv.ss) == (W, W, W) and (ko, vo) == (Hq * D, (Hq + Hkv) * D)
+    assert lq.sb == (bstride or S * W)
+    want = oracle.packed_qkv_offsets(B, S, Hq, Hkv, D)
+    if bstride:  # batches further apart than S rows: shift the oracle's batch index
+        want = tuple(x - (np.arange(B)[:, None, None, None] * S * W) + np.arange(B)[:, None, None, None] * bstride
+                     for x in want)
+    for l, off, base in ((lq, want[0], 0), (lk, want[1], ko), (lv, want[2], vo)):
+        got = np.zeros_like(off)
+        for b, h, s, i in np.ndindex(*off.shape):
+            got[b, h, s, i] = base + fbl.fbl_layout_offset(l, b, h, s, i)
+        assert np.array_equal(got, off)
+
+
+def test_packed_qkv_rejections():
+    st = F.LIB.fbl_layout_packed_qkv(None, None, None, None, None, BF16, 1, 1, 1, 1, 64, 0, 0)
+    assert st == F.FBL_ERR_NULL
+    with pytest.raises(F.FblError) as e:
+        fbl.fbl_layout_packed_qkv(BF16, 2, 4, 0, 1, 64)
+    assert e.value.status == F.FBL_ERR_SHAPE
+    with pytest.raises(F.FblError) as e:
+        fbl.fbl_layout_packed_qkv(BF16, 2, 4, 4, 2, 64, tile_d=48)
+    assert e.value.status == F.FBL_ERR_LAYOUT
+    with pytest.raises(F.FblError) as e:
+        fbl.fbl_layout_packed_qkv(BF16, 2, 4, 4, 2, 64, batch_stride=100)  # batches overlap
+    assert e.value.status == F.FBL_ERR_LAYOUT

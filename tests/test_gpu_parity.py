@@ -255,6 +255,39 @@ def test_strided_views_of_packed_projection():
     assert not bad, bad
 
 
+@pytest.mark.parametrize("causal,Hq,Hkv,d,S", [(True, 8, 2, 64, 200), (False, 4, 4, 128, 131), (True, 6, 3, 32, 97)])
+def test_packed_qkv_entry_points(causal, Hq, Hkv, d, S):
+    """attn_fwd_packed / attn_bwd_packed: Q, K, V read in place from one packed
+    [B, S, (Hq + 2 Hkv) d] projection output through fbl_layout_packed_qkv
+    descriptors, gradients written into one packed dQKV tensor; the device
+    index map of each descriptor (plus its offset) equals the oracle's split."""
+    import torch
+    fbl = _lib()
+    B = 2
+    w = synth.Workload("packedqkv", B=B, S=S, Hq=Hq, Hkv=Hkv, d=d, dtype="bf16",
+                       mask=synth.MASK_CAUSAL if causal else synth.MASK_NONE, seed=S + d)
+    inp = synth.make_inputs(w)
+    note(f"packed qkv causal={causal} Hq={Hq} Hkv={Hkv} d={d} S={S}")
+    qkv = to_dev(np.concatenate([inp["q"], inp["k"], inp["v"]], axis=2), "bf16")
+    do = to_dev(inp["do"], "bf16")
+    o, lse = fbl.attn_fwd_packed(qkv, Hq, Hkv, causal=causal)
+    dqkv = fbl.attn_bwd_packed(qkv, o, do, lse, Hq, Hkv, causal=causal)
+    torch.cuda.synchronize()
+    ref = oracle_fwd_bwd(inp)
+    g = to_np(dqkv)
+    got = {"o": to_np(o), "lse": to_np(lse), "dq": g[:, :, :Hq * d], "dk": g[:, :, Hq * d:(Hq + Hkv) * d],
+           "dv": g[:, :, (Hq + Hkv) * d:]}
+    errs, bad = compare(got, ref, "bf16")
+    assert not bad, bad
+    lq, lk, lv, ko, vo = fbl.fbl_layout_packed_qkv(fbl.FBL_BF16, B, S, Hq, Hkv, d)
+    want = oracle.packed_qkv_offsets(B, S, Hq, Hkv, d)
+    for l, off, base in ((lq, want[0], 0), (lk, want[1], ko), (lv, want[2], vo)):
+        out = torch.full((off.size,), -7, dtype=torch.int64, device="cuda")
+        fbl.fbl_layout_map_device(l, out)
+        torch.cuda.synchronize()
+        assert np.array_equal(out.cpu().numpy().reshape(off.shape) + base, off)
+
+
 def test_repeatability_and_no_allocation():
     """fwd and bwd outputs are bitwise repeatable (no atomics anywhere);
     the calls allocate no device memory when outputs and workspace are given."""

@@ -53,3 +53,17 @@ def test_strength_reduction_identity_from_paper():
         i = np.arange(0, 4 * c["Ca"] * c["Cb"] + 17, dtype=np.int64)
         assert c["Ca"] % c["Cb"] == 0
         assert np.array_equal((i % c["Ca"]) % c["Cb"], i % c["Cb"])
+
+
+@pytest.mark.parametrize("B,S,Hq,Hkv,d", [(1, 1, 1, 1, 1), (2, 5, 4, 2, 8), (3, 7, 6, 3, 4), (2, 4, 12, 12, 64)])
+def test_packed_qkv_offsets_closed_form(B, S, Hq, Hkv, d):
+    """Packed [B, S, (Hq + 2 Hkv) d] rows: Q heads, then K heads, then V heads."""
+    W = Hq + 2 * Hkv
+    q, k, v = oracle.packed_qkv_offsets(B, S, Hq, Hkv, d)
+    for off, H, first in ((q, Hq, 0), (k, Hkv, Hq), (v, Hkv, Hq + Hkv)):
+        assert off.shape == (B, H, S, d)
+        b, h, s, i = np.meshgrid(np.arange(B), np.arange(H), np.arange(S), np.arange(d), indexing="ij")
+        assert np.array_equal(off, ((b * S + s) * W + first + h) * d + i)
+    # together they cover every element of the packed tensor exactly once
+    allo = np.concatenate([x.ravel() for x in (q, k, v)])
+    assert np.array_equal(np.sort(allo), np.arange(B * S * W * d))
