@@ -12,6 +12,8 @@ Modules
              matrices (the textbook definition, written out).
   brute      scalar triple loops of the same definition, for tiny inputs; used
              to cross-check ``attention``.
+  proj       the projection matrix products around attention: Y = X W and its
+             data and weight gradients.
   layout     the logical (b, h, s, i) -> physical offset map of a token-major
              tensor, built by the reshape-then-transpose chain itself, also
              for Q, K, V split out of one packed projection output.
@@ -23,3 +25,4 @@ layout examples.  Each function's docstring names the pin(s).
 """
 from .attention import attn_fwd, attn_bwd, bwd_row_dot, head_probs, kv_head_of, allowed_mask  # noqa: F401
 from .layout import token_major_offsets, head_split_offsets, packed_qkv_offsets  # noqa: F401
+from .proj import proj_fwd, proj_bwd_data, proj_bwd_weight  # noqa: F401
