@@ -140,6 +140,58 @@ def cpu_baseline(w, inp, budget_s: float):
             "seconds": dt, "host_cpus": os.cpu_count()}
 
 
+def bench_proj(args, fbl, torch, np):
+    """Projection products at one shape: per product and output tile, the
+    average of `steps` launches timed with HIP events on the current stream
+    (inputs resident, outputs preallocated).  `value` is the three products
+    back to back with the automatic tile choice: 3 * 2 M K N flops per step."""
+    M, K, N = (int(x) for x in args.proj_shape.split(","))
+    g = torch.Generator(device="cpu").manual_seed(0)
+    mk = lambda r, c: torch.randn(r, c, generator=g).to(device="cuda", dtype=torch.bfloat16)
+    X, W, dY = mk(M, K), mk(K, N), mk(M, N)
+    Y, dX, dW = (torch.empty(s, dtype=torch.bfloat16, device="cuda") for s in ((M, N), (M, K), (K, N)))
+    ops = {"fwd": (fbl.FBL_PROJ_FWD, X, W, Y), "bwd_data": (fbl.FBL_PROJ_BWD_DATA, dY, W, dX),
+           "bwd_weight": (fbl.FBL_PROJ_BWD_WEIGHT, X, dY, dW)}
+    tiles = {"auto": fbl.FBL_GEMM_TILE_AUTO, "128x128": fbl.FBL_GEMM_TILE_128x128, "128x64": fbl.FBL_GEMM_TILE_128x64,
+             "64x128": fbl.FBL_GEMM_TILE_64x128, "64x64": fbl.FBL_GEMM_TILE_64x64}
+    stream = torch.cuda.current_stream()
+    flops = 2.0 * M * K * N
+    res = {}
+    for name, (op, a, b, c) in ops.items():
+        res[name] = {}
+        for tn, t in tiles.items():
+            try:
+                call = lambda: fbl.proj(op, a, b, out=c, tile=t)
+                call()
+            except fbl.FblError:
+                continue
+            for _ in range(args.warmup):
+                call()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            e0.record(stream)
+            for _ in range(args.steps):
+                call()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            ms = e0.elapsed_time(e1) / args.steps
+            res[name][tn] = {"ms": round(ms, 4), "tflops": round(flops / (ms * 1e-3) / 1e12, 1)}
+    step_ms = sum(res[n]["auto"]["ms"] for n in ops)
+    tf = 3 * flops / (step_ms * 1e-3) / 1e12
+    best = max(res[n][t]["tflops"] for n in ops for t in res[n])
+    print(json.dumps({
+        "metric": "projection products Y = X W, dX = dY W^T, dW = X^T dY: TFLOP/s at 1 GPU",
+        "value": round(tf, 2), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(step_ms, 4), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic (seeded N(0,1))",
+        "config": {"workload": "proj", "M": M, "K": K, "N": N, "layout": "token-major rows, no transposed copies"},
+        "pct_peak": round(100 * tf / PEAK_BF16_TFLOPS, 2),
+        "roofline": {"bound": "mfma", "achieved": best, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(best / PEAK_BF16_TFLOPS, 4), "traffic": None},
+        "per_op": res,
+    }), flush=True)
+
+
 def dispatched_kernels(step):
     """Kernel names dispatched by one step (torch profiler; None if unavailable)."""
     try:
@@ -164,6 +216,10 @@ def main():
     ap.add_argument("--no-kernel-list", action="store_true",
                     help="skip the torch-profiler dispatch listing (use under rocprofv3)")
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle work for cpu_baseline")
+    ap.add_argument("--op", default="attention", choices=["attention", "proj"],
+                    help="attention: the fwd+bwd step (default); proj: the projection products Y = X W, dX = dY W^T, "
+                         "dW = X^T dY on token-major activations, every tile shape")
+    ap.add_argument("--proj-shape", default="512,2048,8192", help="M,K,N for --op proj")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="instead of attention, run 5 plain device copies of this many MiB (calibrates the HBM "
                          "byte counters FETCH_SIZE / WRITE_SIZE against a kernel of known traffic)")
@@ -189,6 +245,10 @@ def main():
 
     import paper_2607_21624_amd as fbl
     import synth
+
+    if args.op == "proj":
+        bench_proj(args, fbl, torch, np)
+        return
 
     w = {**synth.WORKLOADS, **synth.CROSS_WORKLOADS}[args.workload]
     inp = synth.make_inputs(w)

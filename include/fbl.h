@@ -57,7 +57,7 @@ typedef enum {
     FBL_ERR_DTYPE = 3,       /* unknown dtype, or dtypes differ between tensors     */
     FBL_ERR_LAYOUT = 4,      /* a tile-legality check failed (strides, tile shape)  */
     FBL_ERR_ALIGN = 5,       /* base pointer or row stride not 16-byte aligned      */
-    FBL_ERR_UNSUPPORTED = 6, /* head dim / mask combination not implemented         */
+    FBL_ERR_UNSUPPORTED = 6, /* shape, head dim or mask combination not implemented  */
     FBL_ERR_WORKSPACE = 7,   /* workspace NULL or below fbl_attn_bwd_workspace_min  */
     FBL_ERR_HIP = 8,         /* the HIP runtime reported an error at launch         */
     FBL_ERR_ARG = 9          /* other invalid argument (non-finite scale, aliasing) */
@@ -237,6 +237,40 @@ fbl_status fbl_attn_bwd_phases(uint32_t phases, const fbl_layout* lq, const void
                                const void* o, const fbl_layout* ldo, const void* dO, const float* lse, float scale,
                                fbl_mask mask, const fbl_layout* ldq, void* dq, const fbl_layout* ldk, void* dk,
                                const fbl_layout* ldv, void* dv, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Projection matrix products of the linear layers around attention, on the
+ * same token-major activations (bf16 operands and result, fp32 accumulation).
+ * Section 4.1 classes matrix products as forward-tensor-dependent: the
+ * gradients read the stored X, W and dY along other axes than the forward
+ * (section 4.2).  No operand is transposed in memory; each product reads the
+ * stored tiles row-wise or transposed as its contraction requires.
+ *   FBL_PROJ_FWD         c = Y  [M, N] = X [M, K] . W [K, N]     a = X,  b = W
+ *   FBL_PROJ_BWD_DATA    c = dX [M, K] = dY [M, N] . W^T         a = dY, b = W
+ *   FBL_PROJ_BWD_WEIGHT  c = dW [K, N] = X^T . dY [M, N]         a = X,  b = dY
+ * All matrices are row-major with leading dimensions (elements between rows)
+ * lda, ldb, ldc, each at least its row width, so column views of wider
+ * buffers (e.g. a packed QKV projection output) are accepted without copies.
+ *   tile     output tile of one workgroup: FBL_GEMM_TILE_AUTO, or one of
+ *            FBL_GEMM_TILE_128x128, _128x64, _64x128, _64x64 (rows x cols of
+ *            the op's output).
+ * Supported: the output's row and column counts multiples of 64 (of the
+ * chosen tile's sides when one is given) and the contraction length a
+ * multiple of 32, else FBL_ERR_UNSUPPORTED.  Checks: non-NULL pointers,
+ * positive extents, leading dimensions >= widths, 16-byte aligned pointers and
+ * rows, each operand's span below 2 GiB, c not overlapping a or b.  The
+ * caller owns all memory; enqueued on `stream`; c is fully overwritten.
+ */
+#define FBL_PROJ_FWD 0u
+#define FBL_PROJ_BWD_DATA 1u
+#define FBL_PROJ_BWD_WEIGHT 2u
+#define FBL_GEMM_TILE_AUTO (-1)
+#define FBL_GEMM_TILE_128x128 0
+#define FBL_GEMM_TILE_128x64 1
+#define FBL_GEMM_TILE_64x128 2
+#define FBL_GEMM_TILE_64x64 3
+fbl_status fbl_proj(uint32_t op, int64_t M, int64_t K, int64_t N, const void* a, int64_t lda, const void* b,
+                    int64_t ldb, void* c, int64_t ldc, int32_t tile, void* stream);
 
 /* Static, human-readable name of a status code. */
 const char* fbl_status_str(fbl_status s);

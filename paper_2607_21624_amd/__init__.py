@@ -8,6 +8,7 @@ argument marshalling only, torch for device memory and streams.
 from .fbl import (  # noqa: F401
     EXPORTED, FBL_BF16, FBL_BWD_ALL, FBL_BWD_KV, FBL_BWD_PREP, FBL_BWD_Q, FBL_F32, FBL_MASK_CAUSAL, FBL_MASK_KEY_PADDING, FblError, LIB, LIB_PATH, Layout, Mask,
     attn_bwd, attn_bwd_packed, attn_fwd, attn_fwd_packed, fbl_attn_bwd_raw, fbl_attn_bwd_workspace, fbl_attn_bwd_workspace_min, fbl_attn_fwd_raw,
-    fbl_layout_desc, fbl_layout_packed_qkv,
+    fbl_layout_desc, fbl_layout_packed_qkv, fbl_proj_raw, proj, FBL_PROJ_FWD, FBL_PROJ_BWD_DATA, FBL_PROJ_BWD_WEIGHT,
+    FBL_GEMM_TILE_AUTO, FBL_GEMM_TILE_128x128, FBL_GEMM_TILE_128x64, FBL_GEMM_TILE_64x128, FBL_GEMM_TILE_64x64,
     fbl_layout_desc_status, fbl_layout_map_device, fbl_layout_offset, layout_of, status_str,
 )

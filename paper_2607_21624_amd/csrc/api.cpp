@@ -163,7 +163,7 @@ const char* fbl_status_str(fbl_status s) {
         case FBL_ERR_DTYPE: return "FBL_ERR_DTYPE: unknown or mismatched dtype";
         case FBL_ERR_LAYOUT: return "FBL_ERR_LAYOUT: tile-legality check failed";
         case FBL_ERR_ALIGN: return "FBL_ERR_ALIGN: pointer or stride not 16-byte aligned";
-        case FBL_ERR_UNSUPPORTED: return "FBL_ERR_UNSUPPORTED: head dim or mask not implemented";
+        case FBL_ERR_UNSUPPORTED: return "FBL_ERR_UNSUPPORTED: shape, head dim or mask not implemented";
         case FBL_ERR_WORKSPACE: return "FBL_ERR_WORKSPACE: workspace missing or too small";
         case FBL_ERR_HIP: return "FBL_ERR_HIP: HIP runtime error at launch";
         case FBL_ERR_ARG: return "FBL_ERR_ARG: invalid argument";
@@ -377,6 +377,62 @@ fbl_status fbl_attn_bwd(const fbl_layout* lq, const void* q, const fbl_layout* l
                         void* dv, void* ws, size_t ws_bytes, void* stream) {
     return fbl_attn_bwd_phases(FBL_BWD_ALL, lq, q, lk, k, lv, v, lo, o, ldo, dO, lse, scale, mask, ldq, dq, ldk, dk,
                                ldv, dv, ws, ws_bytes, stream);
+}
+
+fbl_status fbl_proj(uint32_t op, int64_t M, int64_t K, int64_t N, const void* a, int64_t lda, const void* b,
+                    int64_t ldb, void* c, int64_t ldc, int32_t tile, void* stream) {
+    if (op > FBL_PROJ_BWD_WEIGHT) return FBL_ERR_ARG;
+    if (!a || !b || !c) return FBL_ERR_NULL;
+    if (M <= 0 || K <= 0 || N <= 0 || M > INT32_MAX || K > INT32_MAX || N > INT32_MAX) return FBL_ERR_SHAPE;
+    // stored shapes: a [ra, wa], b [rb, wb], c [rc, wc]; the product's output
+    // rows/cols and contraction length
+    int64_t ra, wa, rb, wb, rc, wc, orows, ocols, kc;
+    int a_kmajor = 0, b_nmajor = 0;
+    if (op == FBL_PROJ_FWD) {  // Y = X W
+        ra = M, wa = K, rb = K, wb = N, rc = M, wc = N, orows = M, ocols = N, kc = K;
+    } else if (op == FBL_PROJ_BWD_DATA) {  // dX = dY W^T
+        ra = M, wa = N, rb = K, wb = N, rc = M, wc = K, orows = M, ocols = K, kc = N;
+        b_nmajor = 1;
+    } else {  // dW = X^T dY
+        ra = M, wa = K, rb = M, wb = N, rc = K, wc = N, orows = K, ocols = N, kc = M;
+        a_kmajor = 1;
+    }
+    if (lda < wa || ldb < wb || ldc < wc) return FBL_ERR_LAYOUT;
+    if (!aligned16(a) || !aligned16(b) || !aligned16(c) || (lda * 2) % 16 || (ldb * 2) % 16 || (ldc * 2) % 16)
+        return FBL_ERR_ALIGN;
+    if (tile < FBL_GEMM_TILE_AUTO || tile > FBL_GEMM_TILE_64x64) return FBL_ERR_ARG;
+    if (orows % 64 || ocols % 64 || kc % 32) return FBL_ERR_UNSUPPORTED;
+    if (tile == FBL_GEMM_TILE_AUTO) {
+        // largest tile that still gives every CU a workgroup (256 CUs), else the smallest
+        const int order[4] = {FBL_GEMM_TILE_128x128, FBL_GEMM_TILE_128x64, FBL_GEMM_TILE_64x128,
+                              FBL_GEMM_TILE_64x64};
+        tile = FBL_GEMM_TILE_64x64;
+        for (int t : order) {
+            const int64_t br = fbl::gemm_tile_rows(t), bc = fbl::gemm_tile_cols(t);
+            if (orows % br == 0 && ocols % bc == 0 && (orows / br) * (ocols / bc) >= 256) {
+                tile = t;
+                break;
+            }
+        }
+    }
+    if (orows % fbl::gemm_tile_rows(tile) || ocols % fbl::gemm_tile_cols(tile)) return FBL_ERR_UNSUPPORTED;
+    const int64_t sa = ((ra - 1) * lda + wa) * 2, sb = ((rb - 1) * ldb + wb) * 2, sc = ((rc - 1) * ldc + wc) * 2;
+    if (sa >= ((int64_t)1 << 31) || sb >= ((int64_t)1 << 31) || sc >= ((int64_t)1 << 31)) return FBL_ERR_UNSUPPORTED;
+    if (overlaps(c, sc, a, sa) || overlaps(c, sc, b, sb)) return FBL_ERR_ARG;
+    fbl::GemmArgs p;
+    p.a = a;
+    p.b = b;
+    p.c = c;
+    p.lda = lda;
+    p.ldb = ldb;
+    p.ldc = ldc;
+    p.M = (int)orows;
+    p.N = (int)ocols;
+    p.K = (int)kc;
+    p.a_bytes = (uint32_t)sa;
+    p.b_bytes = (uint32_t)sb;
+    const hipError_t e = fbl::launch_proj_gemm(a_kmajor, b_nmajor, tile, p, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? FBL_OK : FBL_ERR_HIP;
 }
 
 }  // extern "C"

@@ -33,6 +33,13 @@ hipError_t launch_attn_bwd_q_bf16(const BwdArgs& a, hipStream_t stream);
 template <int D>
 hipError_t launch_attn_bwd_dq_bf16(const BwdArgs& a, hipStream_t stream);
 
+// Projection matrix products (proj_gemm.hip).  Output tile shapes:
+constexpr int kGemmTile128x128 = 0, kGemmTile128x64 = 1, kGemmTile64x128 = 2, kGemmTile64x64 = 3;
+int gemm_tile_rows(int tile);
+int gemm_tile_cols(int tile);
+// a_kmajor: A stored [K, M]; b_nmajor: B stored [N, K].
+hipError_t launch_proj_gemm(int a_kmajor, int b_nmajor, int tile, const GemmArgs& p, hipStream_t stream);
+
 // Diagnostic: offsets of a token-major tensor computed by the device index map.
 hipError_t launch_layout_map(const TokMap& m, int B, int H, int S, int D, int64_t* out, hipStream_t stream);
 

@@ -65,4 +65,17 @@ struct BwdArgs {
     MaskArgs mask;
 };
 
+// Matrix product C[M, N] = sum_k A(m, k) B(k, n), bf16 operands, row-major
+// storage with leading dimensions in elements.  A is stored [M, K] (or [K, M]
+// when read k-major), B [K, N] (or [N, K] when read n-major); a_bytes/b_bytes
+// bound the bytes the buffer resources may touch.
+struct GemmArgs {
+    const void* a;
+    const void* b;
+    void* c;
+    int64_t lda, ldb, ldc;
+    int M, N, K;
+    uint32_t a_bytes, b_bytes;
+};
+
 }  // namespace fbl

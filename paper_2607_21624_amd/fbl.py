@@ -36,8 +36,17 @@ FBL_BWD_KV = 2
 FBL_BWD_Q = 4
 FBL_BWD_ALL = 7
 
+FBL_PROJ_FWD = 0
+FBL_PROJ_BWD_DATA = 1
+FBL_PROJ_BWD_WEIGHT = 2
+FBL_GEMM_TILE_AUTO = -1
+FBL_GEMM_TILE_128x128 = 0
+FBL_GEMM_TILE_128x64 = 1
+FBL_GEMM_TILE_64x128 = 2
+FBL_GEMM_TILE_64x64 = 3
+
 EXPORTED = ("fbl_layout_desc", "fbl_layout_packed_qkv", "fbl_layout_offset", "fbl_layout_map_device", "fbl_attn_fwd",
-            "fbl_attn_bwd_workspace", "fbl_attn_bwd_workspace_min", "fbl_attn_bwd", "fbl_attn_bwd_phases", "fbl_status_str")
+            "fbl_attn_bwd_workspace", "fbl_attn_bwd_workspace_min", "fbl_attn_bwd", "fbl_attn_bwd_phases", "fbl_proj", "fbl_status_str")
 
 
 class Layout(ctypes.Structure):
@@ -97,6 +106,9 @@ def _load() -> ctypes.CDLL:
     lib.fbl_attn_bwd.restype = ctypes.c_int
     lib.fbl_attn_bwd_phases.argtypes = [ctypes.c_uint32] + lib.fbl_attn_bwd.argtypes
     lib.fbl_attn_bwd_phases.restype = ctypes.c_int
+    lib.fbl_proj.argtypes = [ctypes.c_uint32] + [ctypes.c_int64] * 3 + [vp, ctypes.c_int64, vp, ctypes.c_int64, vp,
+                                                                        ctypes.c_int64, ctypes.c_int32, vp]
+    lib.fbl_proj.restype = ctypes.c_int
     lib.fbl_status_str.argtypes = [ctypes.c_int]
     lib.fbl_status_str.restype = ctypes.c_char_p
     return lib
@@ -330,3 +342,37 @@ def attn_bwd_packed(qkv, o, do, lse, Hq: int, Hkv: int, scale: Optional[float] =
                             gk, lv, gv, workspace, workspace.numel() * workspace.element_size(), stream),
            "fbl_attn_bwd")
     return dqkv
+
+
+# ------------------------------------------------------- projection products
+def fbl_proj_raw(op, M, K, N, a, lda, b, ldb, c, ldc, tile=FBL_GEMM_TILE_AUTO, stream=None) -> int:
+    """Direct call of fbl_proj; returns the status code."""
+    return LIB.fbl_proj(op, M, K, N, _ptr(a), lda, _ptr(b), ldb, _ptr(c), ldc, tile,
+                        _stream(stream) if stream != 0 else None)
+
+
+def _rows(t, name):
+    if t.dim() != 2 or t.stride(1) != 1:
+        raise FblError(FBL_ERR_LAYOUT, f"{name}: expected a 2-D row-major tensor (inner stride 1)")
+    return t.shape[0], t.shape[1], t.stride(0)
+
+
+def proj(op: int, a, b, out=None, tile: int = FBL_GEMM_TILE_AUTO, stream=None):
+    """One projection product on 2-D bf16 tensors (row-major, any row stride):
+    FBL_PROJ_FWD (a = X [M, K], b = W [K, N]) -> Y [M, N];
+    FBL_PROJ_BWD_DATA (a = dY [M, N], b = W [K, N]) -> dX [M, K];
+    FBL_PROJ_BWD_WEIGHT (a = X [M, K], b = dY [M, N]) -> dW [K, N]."""
+    import torch
+    ra, wa, lda = _rows(a, "a")
+    rb, wb, ldb = _rows(b, "b")
+    if op == FBL_PROJ_FWD:
+        M, K, N, shape = ra, wa, wb, (ra, wb)
+    elif op == FBL_PROJ_BWD_DATA:
+        M, N, K, shape = ra, wa, rb, (ra, rb)
+    else:
+        M, K, N, shape = ra, wa, wb, (wa, wb)
+    if out is None:
+        out = torch.empty(shape, dtype=a.dtype, device=a.device)
+    _, _, ldc = _rows(out, "out")
+    _check(fbl_proj_raw(op, M, K, N, a, lda, b, ldb, out, ldc, tile, stream), "fbl_proj")
+    return out

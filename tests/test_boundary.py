@@ -308,3 +308,23 @@ def test_packed_qkv_rejections():
     with pytest.raises(F.FblError) as e:
         fbl.fbl_layout_packed_qkv(BF16, 2, 4, 4, 2, 64, batch_stride=100)  # batches overlap
     assert e.value.status == F.FBL_ERR_LAYOUT
+
+
+# ------------------------------------------------------ projection products
+def test_proj_rejections():
+    P = lambda op, M, K, N, a=FAKE, lda=None, b=FAKE + (1 << 24), ldb=None, c=FAKE + (1 << 26), ldc=None, tile=-1: \
+        fbl.fbl_proj_raw(op, M, K, N, a, lda if lda is not None else 4096, b, ldb if ldb is not None else 4096, c,
+                         ldc if ldc is not None else 4096, tile, stream=0)
+    E = F
+    assert P(3, 64, 64, 64) == E.FBL_ERR_ARG                       # unknown op
+    assert P(E.FBL_PROJ_FWD, 64, 64, 64, a=None) == E.FBL_ERR_NULL
+    assert P(E.FBL_PROJ_FWD, 0, 64, 64) == E.FBL_ERR_SHAPE
+    assert P(E.FBL_PROJ_FWD, 64, 64, 64, lda=32) == E.FBL_ERR_LAYOUT  # lda < K
+    assert P(E.FBL_PROJ_BWD_DATA, 64, 64, 128, lda=64) == E.FBL_ERR_LAYOUT  # dY rows hold N
+    assert P(E.FBL_PROJ_FWD, 64, 64, 64, a=FAKE + 2) == E.FBL_ERR_ALIGN
+    assert P(E.FBL_PROJ_FWD, 64, 64, 64, lda=4100) == E.FBL_ERR_ALIGN  # row not 16-byte aligned
+    assert P(E.FBL_PROJ_FWD, 64, 48, 64) == E.FBL_ERR_UNSUPPORTED     # contraction not a multiple of 32
+    assert P(E.FBL_PROJ_FWD, 96, 64, 64) == E.FBL_ERR_UNSUPPORTED     # output rows not a multiple of 64
+    assert P(E.FBL_PROJ_FWD, 64, 64, 64, tile=E.FBL_GEMM_TILE_128x128) == E.FBL_ERR_UNSUPPORTED
+    assert P(E.FBL_PROJ_FWD, 64, 64, 64, tile=7) == E.FBL_ERR_ARG
+    assert P(E.FBL_PROJ_FWD, 64, 64, 64, c=FAKE + 64) == E.FBL_ERR_ARG  # output overlaps an input
