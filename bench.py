@@ -152,8 +152,10 @@ def bench_proj(args, fbl, torch, np):
     Y, dX, dW = (torch.empty(s, dtype=torch.bfloat16, device="cuda") for s in ((M, N), (M, K), (K, N)))
     ops = {"fwd": (fbl.FBL_PROJ_FWD, X, W, Y), "bwd_data": (fbl.FBL_PROJ_BWD_DATA, dY, W, dX),
            "bwd_weight": (fbl.FBL_PROJ_BWD_WEIGHT, X, dY, dW)}
-    tiles = {"auto": fbl.FBL_GEMM_TILE_AUTO, "128x128": fbl.FBL_GEMM_TILE_128x128, "128x64": fbl.FBL_GEMM_TILE_128x64,
-             "64x128": fbl.FBL_GEMM_TILE_64x128, "64x64": fbl.FBL_GEMM_TILE_64x64}
+    info = fbl.gemm_tiles()
+    name = lambda g: f"{g['bm']}x{g['bn']}x{g['bk']}/w{g['wm']}{g['wn']}{g['wk']}"
+    tiles = {"auto": fbl.FBL_GEMM_TILE_AUTO}
+    tiles.update({f"t{t}:{name(g)}": t for t, g in info.items()})
     stream = torch.cuda.current_stream()
     flops = 2.0 * M * K * N
     res = {}

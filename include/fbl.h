@@ -251,15 +251,22 @@ fbl_status fbl_attn_bwd_phases(uint32_t phases, const fbl_layout* lq, const void
  * All matrices are row-major with leading dimensions (elements between rows)
  * lda, ldb, ldc, each at least its row width, so column views of wider
  * buffers (e.g. a packed QKV projection output) are accepted without copies.
- *   tile     output tile of one workgroup: FBL_GEMM_TILE_AUTO, or one of
- *            FBL_GEMM_TILE_128x128, _128x64, _64x128, _64x64 (rows x cols of
- *            the op's output).
- * Supported: the output's row and column counts multiples of 64 (of the
- * chosen tile's sides when one is given) and the contraction length a
- * multiple of 32, else FBL_ERR_UNSUPPORTED.  Checks: non-NULL pointers,
- * positive extents, leading dimensions >= widths, 16-byte aligned pointers and
- * rows, each operand's span below 2 GiB, c not overlapping a or b.  The
- * caller owns all memory; enqueued on `stream`; c is fully overwritten.
+ *   tile     the workgroup tile configuration: FBL_GEMM_TILE_AUTO, or an
+ *            id in [0, fbl_gemm_tile_count()) (see fbl_gemm_tile_info;
+ *            ids 0-3 have the names below, rows x cols of the op's output).
+ *            AUTO takes the tile fbl_proj_tune measured best for this
+ *            (op, M, K, N) in this process, else the first candidate (see
+ *            fbl_proj_candidates) that gives at least 256 workgroups in a
+ *            preference order set by the number of 128 x 128 output tiles
+ *            (>= 1024: 4-wavefront tiles with small LDS; >= 256: the
+ *            8-wavefront 128 x 128 tile; fewer: 64 x 64 tiles whose
+ *            wavefronts split the contraction).
+ * Supported: the output's row and column counts multiples of 64 and the
+ * contraction length a multiple of 32; an explicit tile must divide them
+ * exactly (else FBL_ERR_UNSUPPORTED).  Checks: non-NULL pointers, positive
+ * extents, leading dimensions >= widths, 16-byte aligned pointers and rows,
+ * each operand's span below 2 GiB, c not overlapping a or b.  The caller owns
+ * all memory; enqueued on `stream`; c is fully overwritten.
  */
 #define FBL_PROJ_FWD 0u
 #define FBL_PROJ_BWD_DATA 1u
@@ -271,6 +278,64 @@ fbl_status fbl_attn_bwd_phases(uint32_t phases, const fbl_layout* lq, const void
 #define FBL_GEMM_TILE_64x64 3
 fbl_status fbl_proj(uint32_t op, int64_t M, int64_t K, int64_t N, const void* a, int64_t lda, const void* b,
                     int64_t ldb, void* c, int64_t ldc, int32_t tile, void* stream);
+
+/*
+ * Tile configurations of the projection products.  fbl_gemm_tile_count gives
+ * the number of ids; fbl_gemm_tile_info writes 8 values for one id:
+ *   info[0..1]  bm, bn   output tile rows x cols of one workgroup
+ *   info[2]     bk       contraction elements staged per step
+ *   info[3]     stages   LDS stages (stages - 1 steps in flight)
+ *   info[4..6]  wm, wn, wk  wavefront grid: wm x wn wavefront tiles, each
+ *               computed by wk wavefronts that split every step's contraction
+ *   info[7]     LDS bytes of one workgroup
+ * FBL_ERR_NULL / FBL_ERR_ARG for a NULL info or an id out of range.
+ */
+int32_t fbl_gemm_tile_count(void);
+fbl_status fbl_gemm_tile_info(int32_t tile, int32_t* info);
+
+/*
+ * Candidate tiles of one product shape: the three progressive filters of the
+ * R-Tile shape candidate generation (section 4.2, step 1, and the
+ * supplementary algorithm), read for gfx950 --
+ *   C1 compute alignment: wavefront tiles of whole 32x32 MFMA blocks, whole
+ *      16-deep MFMA chunks per wavefront and step;
+ *   C2 memory alignment: the workgroup's LDS fits the 160 KB of a CU and
+ *      every staged row is a whole number of 128-byte cache lines;
+ *   C3 shape: the tile divides the output and the contraction exactly.
+ * Writes up to `cap` ids in increasing order to `tiles` and the number of
+ * candidates to *count (which may exceed cap).  Host only, no GPU work.
+ */
+fbl_status fbl_proj_candidates(uint32_t op, int64_t M, int64_t K, int64_t N, int32_t* tiles, int32_t cap,
+                               int32_t* count);
+
+/*
+ * Measured tile selection for one product: every candidate of
+ * fbl_proj_candidates runs once untimed and `reps` (1..1000) times timed with
+ * HIP events on `stream`, on the caller's operands.  The choice maximises
+ *   FBL_TUNE_TIME              1 / average time, or
+ *   FBL_TUNE_GFLOPS_X_MEMEFF   GFLOP/s x MemEfficiency (section 4.2, the
+ *                              unified R-Tile objective, per product): minimal
+ *                              bytes (each operand and the result once) over
+ *                              the bytes the tile schedule stages (each row
+ *                              block of A once per output column block, each
+ *                              column block of B once per output row block,
+ *                              plus the result).
+ * The choice is kept in a per-process table keyed by (op, M, K, N) that
+ * FBL_GEMM_TILE_AUTO consults (thread-safe; fbl_proj_tune_reset clears it,
+ * fbl_proj_tuned_tile reads it, -1 if absent).  ms (optional,
+ * fbl_gemm_tile_count() floats) receives each id's average milliseconds, -1
+ * for ids that are not candidates; *best (optional) the chosen id.  Blocks
+ * until the timed launches finish.  On return c holds the product computed
+ * with the chosen tile.  Same checks as fbl_proj; FBL_ERR_ARG for an unknown
+ * objective or reps out of range, FBL_ERR_UNSUPPORTED with no candidate.
+ */
+#define FBL_TUNE_TIME 0u
+#define FBL_TUNE_GFLOPS_X_MEMEFF 1u
+fbl_status fbl_proj_tune(uint32_t op, int64_t M, int64_t K, int64_t N, const void* a, int64_t lda, const void* b,
+                         int64_t ldb, void* c, int64_t ldc, uint32_t objective, int32_t reps, float* ms,
+                         int32_t* best, void* stream);
+int32_t fbl_proj_tuned_tile(uint32_t op, int64_t M, int64_t K, int64_t N);
+void fbl_proj_tune_reset(void);
 
 /* Static, human-readable name of a status code. */
 const char* fbl_status_str(fbl_status s);

@@ -9,6 +9,9 @@
 #include <cmath>
 #include <cstdint>
 #include <cstring>
+#include <map>
+#include <mutex>
+#include <tuple>
 
 #include "../../include/fbl.h"
 #include "kernels.hpp"
@@ -379,60 +382,232 @@ fbl_status fbl_attn_bwd(const fbl_layout* lq, const void* q, const fbl_layout* l
                                ldv, dv, ws, ws_bytes, stream);
 }
 
-fbl_status fbl_proj(uint32_t op, int64_t M, int64_t K, int64_t N, const void* a, int64_t lda, const void* b,
-                    int64_t ldb, void* c, int64_t ldc, int32_t tile, void* stream) {
+}  // extern "C"
+
+namespace {
+
+// A projection product, validated: kernel arguments, operand orientation and
+// the output/contraction extents the tile must divide.
+struct ProjPlan {
+    fbl::GemmArgs p;
+    int a_kmajor = 0, b_nmajor = 0;
+    int64_t orows = 0, ocols = 0, kc = 0;
+};
+
+fbl_status proj_plan(uint32_t op, int64_t M, int64_t K, int64_t N, const void* a, int64_t lda, const void* b,
+                     int64_t ldb, void* c, int64_t ldc, ProjPlan& pl) {
     if (op > FBL_PROJ_BWD_WEIGHT) return FBL_ERR_ARG;
     if (!a || !b || !c) return FBL_ERR_NULL;
     if (M <= 0 || K <= 0 || N <= 0 || M > INT32_MAX || K > INT32_MAX || N > INT32_MAX) return FBL_ERR_SHAPE;
     // stored shapes: a [ra, wa], b [rb, wb], c [rc, wc]; the product's output
     // rows/cols and contraction length
-    int64_t ra, wa, rb, wb, rc, wc, orows, ocols, kc;
-    int a_kmajor = 0, b_nmajor = 0;
+    int64_t ra, wa, rb, wb, rc, wc;
     if (op == FBL_PROJ_FWD) {  // Y = X W
-        ra = M, wa = K, rb = K, wb = N, rc = M, wc = N, orows = M, ocols = N, kc = K;
+        ra = M, wa = K, rb = K, wb = N, rc = M, wc = N, pl.orows = M, pl.ocols = N, pl.kc = K;
     } else if (op == FBL_PROJ_BWD_DATA) {  // dX = dY W^T
-        ra = M, wa = N, rb = K, wb = N, rc = M, wc = K, orows = M, ocols = K, kc = N;
-        b_nmajor = 1;
+        ra = M, wa = N, rb = K, wb = N, rc = M, wc = K, pl.orows = M, pl.ocols = K, pl.kc = N;
+        pl.b_nmajor = 1;
     } else {  // dW = X^T dY
-        ra = M, wa = K, rb = M, wb = N, rc = K, wc = N, orows = K, ocols = N, kc = M;
-        a_kmajor = 1;
+        ra = M, wa = K, rb = M, wb = N, rc = K, wc = N, pl.orows = K, pl.ocols = N, pl.kc = M;
+        pl.a_kmajor = 1;
     }
     if (lda < wa || ldb < wb || ldc < wc) return FBL_ERR_LAYOUT;
     if (!aligned16(a) || !aligned16(b) || !aligned16(c) || (lda * 2) % 16 || (ldb * 2) % 16 || (ldc * 2) % 16)
         return FBL_ERR_ALIGN;
-    if (tile < FBL_GEMM_TILE_AUTO || tile > FBL_GEMM_TILE_64x64) return FBL_ERR_ARG;
-    if (orows % 64 || ocols % 64 || kc % 32) return FBL_ERR_UNSUPPORTED;
-    if (tile == FBL_GEMM_TILE_AUTO) {
-        // largest tile that still gives every CU a workgroup (256 CUs), else the smallest
-        const int order[4] = {FBL_GEMM_TILE_128x128, FBL_GEMM_TILE_128x64, FBL_GEMM_TILE_64x128,
-                              FBL_GEMM_TILE_64x64};
-        tile = FBL_GEMM_TILE_64x64;
-        for (int t : order) {
-            const int64_t br = fbl::gemm_tile_rows(t), bc = fbl::gemm_tile_cols(t);
-            if (orows % br == 0 && ocols % bc == 0 && (orows / br) * (ocols / bc) >= 256) {
-                tile = t;
-                break;
-            }
-        }
-    }
-    if (orows % fbl::gemm_tile_rows(tile) || ocols % fbl::gemm_tile_cols(tile)) return FBL_ERR_UNSUPPORTED;
+    if (pl.orows % 64 || pl.ocols % 64 || pl.kc % 32) return FBL_ERR_UNSUPPORTED;
     const int64_t sa = ((ra - 1) * lda + wa) * 2, sb = ((rb - 1) * ldb + wb) * 2, sc = ((rc - 1) * ldc + wc) * 2;
     if (sa >= ((int64_t)1 << 31) || sb >= ((int64_t)1 << 31) || sc >= ((int64_t)1 << 31)) return FBL_ERR_UNSUPPORTED;
     if (overlaps(c, sc, a, sa) || overlaps(c, sc, b, sb)) return FBL_ERR_ARG;
-    fbl::GemmArgs p;
+    fbl::GemmArgs& p = pl.p;
     p.a = a;
     p.b = b;
     p.c = c;
     p.lda = lda;
     p.ldb = ldb;
     p.ldc = ldc;
-    p.M = (int)orows;
-    p.N = (int)ocols;
-    p.K = (int)kc;
+    p.M = (int)pl.orows;
+    p.N = (int)pl.ocols;
+    p.K = (int)pl.kc;
     p.a_bytes = (uint32_t)sa;
     p.b_bytes = (uint32_t)sb;
-    const hipError_t e = fbl::launch_proj_gemm(a_kmajor, b_nmajor, tile, p, static_cast<hipStream_t>(stream));
+    return FBL_OK;
+}
+
+bool tile_runs(int tile, const ProjPlan& pl) {
+    return fbl::gemm_c3(fbl::kGemmTiles[tile], pl.orows, pl.ocols, pl.kc);
+}
+bool tile_candidate(int tile, const ProjPlan& pl) {
+    const fbl::GemmTile& t = fbl::kGemmTiles[tile];
+    return fbl::gemm_c1(t) && fbl::gemm_c2(t, pl.a_kmajor, pl.b_nmajor) && tile_runs(tile, pl);
+}
+
+// Per-shape table of measured choices (fbl_proj_tune), the run-time analogue
+// of a lookup table keyed by input shape.
+struct TunedKey {
+    uint32_t op;
+    int64_t M, K, N;
+    bool operator<(const TunedKey& o) const {
+        return std::tie(op, M, K, N) < std::tie(o.op, o.M, o.K, o.N);
+    }
+};
+std::mutex g_tuned_mu;
+std::map<TunedKey, int32_t> g_tuned;
+
+int32_t tuned_tile(uint32_t op, int64_t M, int64_t K, int64_t N) {
+    std::lock_guard<std::mutex> lock(g_tuned_mu);
+    const auto it = g_tuned.find(TunedKey{op, M, K, N});
+    return it == g_tuned.end() ? -1 : it->second;
+}
+
+// Untuned choice among the candidates, by how many 128 x 128 output tiles the
+// product has (measured on the 512 x 2048 x 8192 products and their
+// transposes): with at least four per CU (1024), 4-wavefront tiles with small
+// LDS, several workgroups per CU; with at least one per CU, the 8-wavefront
+// 128 x 128 tile; below that, 64 x 64 tiles whose four wavefronts split the
+// contraction.  The first candidate of the order that gives at least one
+// workgroup per CU (256) wins, else the first candidate.
+int32_t default_tile(const ProjPlan& pl) {
+    static const int many[] = {0, 4, 8, 1, 2, 5, 6, 11, 12, 10, 9, 7, 3};
+    static const int some[] = {8, 4, 6, 5, 11, 12, 0, 2, 1, 10, 9, 7, 3};
+    static const int few[] = {9, 10, 7, 6, 5, 8, 4, 3, 2, 1, 0, 11, 12};
+    static_assert(sizeof(many) == sizeof(int) * fbl::kGemmTileCount && sizeof(some) == sizeof(many) &&
+                      sizeof(few) == sizeof(many),
+                  "every tile ranked once");
+    const int64_t n128 = (pl.orows / 128) * (pl.ocols / 128);
+    const int* order = n128 >= 1024 ? many : (n128 >= 256 ? some : few);
+    int32_t first = -1;
+    for (int i = 0; i < fbl::kGemmTileCount; ++i) {
+        const int t = order[i];
+        if (!tile_candidate(t, pl)) continue;
+        const fbl::GemmTile& g = fbl::kGemmTiles[t];
+        if ((pl.orows / g.bm) * (pl.ocols / g.bn) >= 256) return t;
+        if (first < 0) first = t;
+    }
+    if (first >= 0) return first;
+    for (int t = 0; t < fbl::kGemmTileCount; ++t)
+        if (tile_runs(t, pl)) return t;
+    return -1;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t fbl_gemm_tile_count(void) { return fbl::kGemmTileCount; }
+
+fbl_status fbl_gemm_tile_info(int32_t tile, int32_t* info) {
+    if (!info) return FBL_ERR_NULL;
+    if (tile < 0 || tile >= fbl::kGemmTileCount) return FBL_ERR_ARG;
+    const fbl::GemmTile& t = fbl::kGemmTiles[tile];
+    const int32_t v[8] = {t.bm, t.bn, t.bk, t.ns, t.wm, t.wn, t.wk, fbl::gemm_lds_bytes(t)};
+    std::memcpy(info, v, sizeof(v));
+    return FBL_OK;
+}
+
+fbl_status fbl_proj_candidates(uint32_t op, int64_t M, int64_t K, int64_t N, int32_t* tiles, int32_t cap,
+                               int32_t* count) {
+    if (!count || (cap > 0 && !tiles)) return FBL_ERR_NULL;
+    if (op > FBL_PROJ_BWD_WEIGHT) return FBL_ERR_ARG;
+    if (M <= 0 || K <= 0 || N <= 0 || M > INT32_MAX || K > INT32_MAX || N > INT32_MAX) return FBL_ERR_SHAPE;
+    ProjPlan pl;
+    pl.a_kmajor = op == FBL_PROJ_BWD_WEIGHT;
+    pl.b_nmajor = op == FBL_PROJ_BWD_DATA;
+    pl.orows = op == FBL_PROJ_BWD_WEIGHT ? K : M;
+    pl.ocols = op == FBL_PROJ_BWD_DATA ? K : N;
+    pl.kc = op == FBL_PROJ_FWD ? K : (op == FBL_PROJ_BWD_DATA ? N : M);
+    int32_t n = 0;
+    for (int t = 0; t < fbl::kGemmTileCount; ++t)
+        if (tile_candidate(t, pl)) {
+            if (n < cap) tiles[n] = t;
+            ++n;
+        }
+    *count = n;
+    return FBL_OK;
+}
+
+fbl_status fbl_proj(uint32_t op, int64_t M, int64_t K, int64_t N, const void* a, int64_t lda, const void* b,
+                    int64_t ldb, void* c, int64_t ldc, int32_t tile, void* stream) {
+    ProjPlan pl;
+    const fbl_status st = proj_plan(op, M, K, N, a, lda, b, ldb, c, ldc, pl);
+    if (st != FBL_OK) return st;
+    if (tile < FBL_GEMM_TILE_AUTO || tile >= fbl::kGemmTileCount) return FBL_ERR_ARG;
+    if (tile == FBL_GEMM_TILE_AUTO) {
+        tile = tuned_tile(op, M, K, N);
+        if (tile < 0) tile = default_tile(pl);
+        if (tile < 0) return FBL_ERR_UNSUPPORTED;
+    }
+    if (!tile_runs(tile, pl)) return FBL_ERR_UNSUPPORTED;
+    const hipError_t e = fbl::launch_proj_gemm(pl.a_kmajor, pl.b_nmajor, tile, pl.p, static_cast<hipStream_t>(stream));
     return e == hipSuccess ? FBL_OK : FBL_ERR_HIP;
+}
+
+fbl_status fbl_proj_tune(uint32_t op, int64_t M, int64_t K, int64_t N, const void* a, int64_t lda, const void* b,
+                         int64_t ldb, void* c, int64_t ldc, uint32_t objective, int32_t reps, float* ms,
+                         int32_t* best, void* stream) {
+    ProjPlan pl;
+    const fbl_status st = proj_plan(op, M, K, N, a, lda, b, ldb, c, ldc, pl);
+    if (st != FBL_OK) return st;
+    if (objective > FBL_TUNE_GFLOPS_X_MEMEFF || reps < 1 || reps > 1000) return FBL_ERR_ARG;
+    const hipStream_t s = static_cast<hipStream_t>(stream);
+    if (ms)
+        for (int t = 0; t < fbl::kGemmTileCount; ++t) ms[t] = -1.0f;
+    hipEvent_t e0 = nullptr, e1 = nullptr;
+    if (hipEventCreate(&e0) != hipSuccess || hipEventCreate(&e1) != hipSuccess) {
+        if (e0) hipEventDestroy(e0);
+        return FBL_ERR_HIP;
+    }
+    // minimal bytes: every operand read once, the result written once
+    const double flops = 2.0 * (double)pl.orows * (double)pl.ocols * (double)pl.kc;
+    const double min_bytes = 2.0 * ((double)pl.orows * pl.kc + (double)pl.kc * pl.ocols + (double)pl.orows * pl.ocols);
+    int32_t pick = -1;
+    double pick_score = 0;
+    fbl_status out = FBL_OK;
+    for (int t = 0; t < fbl::kGemmTileCount && out == FBL_OK; ++t) {
+        if (!tile_candidate(t, pl)) continue;
+        hipError_t e = fbl::launch_proj_gemm(pl.a_kmajor, pl.b_nmajor, t, pl.p, s);  // warm-up
+        if (e == hipSuccess) e = hipEventRecord(e0, s);
+        for (int r = 0; r < reps && e == hipSuccess; ++r) e = fbl::launch_proj_gemm(pl.a_kmajor, pl.b_nmajor, t, pl.p, s);
+        if (e == hipSuccess) e = hipEventRecord(e1, s);
+        if (e == hipSuccess) e = hipEventSynchronize(e1);
+        float total = 0;
+        if (e == hipSuccess) e = hipEventElapsedTime(&total, e0, e1);
+        if (e != hipSuccess) {
+            out = FBL_ERR_HIP;
+            break;
+        }
+        const float avg = total / (float)reps;
+        if (ms) ms[t] = avg;
+        double score = 1.0 / (double)avg;
+        if (objective == FBL_TUNE_GFLOPS_X_MEMEFF) {
+            // staged bytes: each row block of A is read once per column block
+            // of the output and each column block of B once per row block
+            const fbl::GemmTile& g = fbl::kGemmTiles[t];
+            const double staged = 2.0 * ((double)pl.orows * pl.kc * (double)(pl.ocols / g.bn) +
+                                         (double)pl.kc * pl.ocols * (double)(pl.orows / g.bm) +
+                                         (double)pl.orows * pl.ocols);
+            score = flops / (avg * 1e-3) * (min_bytes / staged);
+        }
+        if (pick < 0 || score > pick_score) pick = t, pick_score = score;
+    }
+    hipEventDestroy(e0);
+    hipEventDestroy(e1);
+    if (out != FBL_OK) return out;
+    if (pick < 0) return FBL_ERR_UNSUPPORTED;
+    {
+        std::lock_guard<std::mutex> lock(g_tuned_mu);
+        g_tuned[TunedKey{op, M, K, N}] = pick;
+    }
+    if (best) *best = pick;
+    // leave c holding the product computed with the chosen tile
+    const hipError_t e = fbl::launch_proj_gemm(pl.a_kmajor, pl.b_nmajor, pick, pl.p, s);
+    return e == hipSuccess ? FBL_OK : FBL_ERR_HIP;
+}
+
+int32_t fbl_proj_tuned_tile(uint32_t op, int64_t M, int64_t K, int64_t N) { return tuned_tile(op, M, K, N); }
+
+void fbl_proj_tune_reset(void) {
+    std::lock_guard<std::mutex> lock(g_tuned_mu);
+    g_tuned.clear();
 }
 
 }  // extern "C"

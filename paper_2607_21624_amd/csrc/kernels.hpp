@@ -3,6 +3,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include "gemm_tiles.hpp"
 #include "tokmap.hpp"
 
 namespace fbl {
@@ -34,9 +35,7 @@ template <int D>
 hipError_t launch_attn_bwd_dq_bf16(const BwdArgs& a, hipStream_t stream);
 
 // Projection matrix products (proj_gemm.hip).  Output tile shapes:
-constexpr int kGemmTile128x128 = 0, kGemmTile128x64 = 1, kGemmTile64x128 = 2, kGemmTile64x64 = 3;
-int gemm_tile_rows(int tile);
-int gemm_tile_cols(int tile);
+// `tile` indexes kGemmTiles (gemm_tiles.hpp).
 // a_kmajor: A stored [K, M]; b_nmajor: B stored [N, K].
 hipError_t launch_proj_gemm(int a_kmajor, int b_nmajor, int tile, const GemmArgs& p, hipStream_t stream);
 

@@ -20,13 +20,17 @@
 // 8g .. 8g+7 of a 16-element chunk, in order, so any pair of them forms a
 // consistent MFMA operand pair.
 //
-// Workgroup: 4 wavefronts in a 2 x 2 grid over a BM x BN output tile, 32-deep
-// contraction steps, three LDS stages (two in flight), two workgroups per CU.
-// The products accumulate C^T tiles (lane <-> m, in-lane n), so each lane
-// stores four consecutive outputs of a row.
-#include <type_traits>
+// Workgroup (gemm_tiles.hpp): a WM x WN grid of wavefront tiles over a
+// BM x BN output tile, each computed by WK wavefronts that split every step's
+// contraction; BK-deep steps through NS LDS stages (NS - 1 in flight).  The
+// WK partial sums of a wavefront tile are added through LDS at the end, in a
+// fixed order.  The products accumulate C^T tiles (lane <-> m, in-lane n), so
+// each lane stores four consecutive outputs of a row.
+#include <array>
+#include <utility>
 
 #include "cdna4.hpp"
+#include "gemm_tiles.hpp"
 #include "kernels.hpp"
 #include "stage.hpp"
 
@@ -34,16 +38,15 @@ namespace fbl {
 
 namespace {
 
-constexpr int kGemmBK = 32;  // contraction elements per step
-constexpr int kGemmStages = 3;
-
-// LDS tile of ROWS stored rows of COLS bf16 elements (swizzled as in stage.hpp).
-template <int ROWS, int COLS>
+// LDS tile of ROWS stored rows of COLS bf16 elements (swizzled as in stage.hpp),
+// loaded by NW wavefronts.
+template <int ROWS, int COLS, int NW>
 struct GTile {
     using G = TileGeom<bf16, COLS>;
-    using Dma = DmaPlan<bf16, COLS, ROWS, 4>;
+    using Dma = DmaPlan<bf16, COLS, ROWS, NW>;
     static constexpr int BYTES = ROWS * COLS * 2;
-    static_assert(Dma::INSTS % 4 == 0, "whole 1 KB loads per wavefront");
+    // every wavefront issues the same number of loads, so one vmcnt count fits all
+    static_assert(Dma::INSTS % NW == 0, "whole 1 KB loads per wavefront");
     // row read: stored row r (lane % 32 + 32 * tile), columns 16c + 8g .. +7
     static FBL_DEV uint32_t row_addr(int lane, int c) {
         return 2u * (uint32_t)G::off(lane & 31, 16 * c + 8 * (lane >> 5));
@@ -59,94 +62,108 @@ struct GTile {
 };
 
 // AT: A stored k-major ([K, M] rows); BT: B stored n-major ([N, K] rows).
-template <int BM, int BN, bool AT, bool BT>
+template <int BM, int BN, int BK, int NS, int WM, int WN, int WK, bool AT, bool BT>
 struct GemmCfg {
-    using TA = GTile<AT ? kGemmBK : BM, AT ? BM : kGemmBK>;
-    using TB = GTile<BT ? BN : kGemmBK, BT ? kGemmBK : BN>;
-    static constexpr int TM = BM / 64, TN = BN / 64;  // 32x32 tiles per wavefront
+    static constexpr int NW = WM * WN * WK;
+    using TA = GTile<AT ? BK : BM, AT ? BM : BK, NW>;
+    using TB = GTile<BT ? BN : BK, BT ? BK : BN, NW>;
+    static constexpr int TM = BM / (32 * WM), TN = BN / (32 * WN);  // 32x32 tiles per wavefront
+    static constexpr int NKC = BK / 16;                              // 16-deep MFMA chunks per step
+    static constexpr int KCW = NKC / WK;                             // chunks per wavefront per step
     static constexpr int SA = TA::BYTES, SB = TB::BYTES;
     static constexpr int STAGE = SA + SB;
-    static constexpr int BYTES = kGemmStages * STAGE;
+    static constexpr int BYTES = gemm_lds_bytes(GemmTile{BM, BN, BK, NS, WM, WN, WK});
     static constexpr int LOADS = TA::Dma::PER_WAVE + TB::Dma::PER_WAVE;
-    static_assert(BM % 64 == 0 && BN % 64 == 0, "2 x 2 wavefronts of 32-multiples");
-    static_assert(kGemmStages * STAGE < 65536, "stage offsets fit the 16-bit LDS immediate");
+    static constexpr int PART = TM * TN * 4096;  // bytes of one wavefront's partial sums
+    static_assert(BM % (32 * WM) == 0 && BN % (32 * WN) == 0, "wavefront tiles of whole 32x32 blocks");
+    static_assert(BK % 32 == 0 && NKC % WK == 0 && NS >= 2, "whole chunks per wavefront, at least double buffered");
+    static_assert(NW == 4 || NW == 8, "4 or 8 wavefronts");
+    static_assert(STAGE < 65536, "in-stage offsets fit the 16-bit LDS immediate");
+    static_assert(BYTES <= 160 * 1024 && NS * STAGE <= BYTES && (WK - 1) * WM * WN * PART <= BYTES, "LDS");
+    static_assert((NS - 1) * LOADS < 64, "vmcnt range");
+    static constexpr int OCC = (NW == 4 && BYTES <= 80 * 1024) ? 2 : 1;
 };
 
-template <int BM, int BN, bool AT, bool BT>
-__global__ __launch_bounds__(256, 2) void proj_gemm_bf16(GemmArgs p) {
-    using C = GemmCfg<BM, BN, AT, BT>;
+template <int BM, int BN, int BK, int NS, int WM, int WN, int WK, bool AT, bool BT>
+__global__ __launch_bounds__(64 * WM * WN * WK, (GemmCfg<BM, BN, BK, NS, WM, WN, WK, AT, BT>::OCC)) void
+proj_gemm_bf16(GemmArgs p) {
+    using C = GemmCfg<BM, BN, BK, NS, WM, WN, WK, AT, BT>;
     using TA = typename C::TA;
     using TB = typename C::TB;
-    constexpr int TM = C::TM, TN = C::TN;
+    constexpr int TM = C::TM, TN = C::TN, KCW = C::KCW;
     extern __shared__ __attribute__((aligned(1024))) unsigned char gemm_smem[];
     const uint32_t lds = lds_addr(gemm_smem);
 
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int g = lane >> 5;
-    const int wm = wave & 1, wn = wave >> 1;  // wavefront position in the 2 x 2 grid
+    // wavefront position: (wm, wn) in the tile grid, wk = its share of each step
+    const int wm = wave % WM, wn = (wave / WM) % WN, wk = wave / (WM * WN);
     const int mt = p.M / BM, nt = p.N / BN;
     // consecutive ids share a column block of B (the weight) and land on one XCD
     const int logical = xcd_logical_id(blockIdx.x, mt * nt, gridDim.x);
     if (logical < 0) return;
     const int m0 = (logical % mt) * BM, n0 = (logical / mt) * BN;
-    const int nk = p.K / kGemmBK;
+    const int nk = p.K / BK;
 
-    // ---- DMA: each stage holds the A and B tiles of one 32-deep step
+    // ---- DMA: each stage holds the A and B tiles of one BK-deep step
     const Rsrc ra = make_rsrc(p.a, p.a_bytes), rb = make_rsrc(p.b, p.b_bytes);
     typename TA::Dma da;
     typename TB::Dma db;
     da.init((uint32_t)(p.lda * 2), wave, lane);
     db.init((uint32_t)(p.ldb * 2), wave, lane);
     auto issue = [&](int s, int buf) __attribute__((always_inline)) {
-        const int k0 = s * kGemmBK;
+        const int k0 = s * BK;
         const uint32_t sa = (uint32_t)((AT ? (int64_t)k0 * p.lda + m0 : (int64_t)m0 * p.lda + k0) * 2);
         const uint32_t sb = (uint32_t)((BT ? (int64_t)n0 * p.ldb + k0 : (int64_t)k0 * p.ldb + n0) * 2);
         da.issue(lds + buf * C::STAGE, ra, sa, wave);
         db.issue(lds + buf * C::STAGE + C::SA, rb, sb, wave);
     };
 
-    // ---- per-lane LDS read addresses (stage 0, contraction chunk 0)
-    uint32_t aaddr[AT ? TM : 2][2], baddr[BT ? 2 : TN][2];
+    // ---- per-lane LDS read addresses (stage 0, the wavefront's first chunk)
+    const int kc0 = wk * KCW;
+    uint32_t aaddr[AT ? TM : KCW][2], baddr[BT ? KCW : TN][2];
     if constexpr (AT) {
 #pragma unroll
         for (int tm = 0; tm < TM; ++tm)
 #pragma unroll
-            for (int h = 0; h < 2; ++h) aaddr[tm][h] = lds + TA::tr_addr(lane, wm * TM + tm, h);
+            for (int h = 0; h < 2; ++h)
+                aaddr[tm][h] = lds + TA::tr_addr(lane, wm * TM + tm, h) + (uint32_t)(kc0 * 16 * BM * 2);
     } else {
 #pragma unroll
-        for (int c = 0; c < 2; ++c) aaddr[c][0] = lds + TA::row_addr(lane, c);
+        for (int j = 0; j < KCW; ++j) aaddr[j][0] = lds + TA::row_addr(lane, kc0 + j);
     }
     if constexpr (BT) {
 #pragma unroll
-        for (int c = 0; c < 2; ++c) baddr[c][0] = lds + C::SA + TB::row_addr(lane, c);
+        for (int j = 0; j < KCW; ++j) baddr[j][0] = lds + C::SA + TB::row_addr(lane, kc0 + j);
     } else {
 #pragma unroll
         for (int tn = 0; tn < TN; ++tn)
 #pragma unroll
-            for (int h = 0; h < 2; ++h) baddr[tn][h] = lds + C::SA + TB::tr_addr(lane, wn * TN + tn, h);
+            for (int h = 0; h < 2; ++h)
+                baddr[tn][h] = lds + C::SA + TB::tr_addr(lane, wn * TN + tn, h) + (uint32_t)(kc0 * 16 * BN * 2);
     }
-    // fragment of A for m-tile tm, contraction chunk kc, from stage buffer B
-    auto frag_a = [&](auto buf_c, int tm, int kc) __attribute__((always_inline)) {
-        constexpr int B = decltype(buf_c)::value;
+    const uint32_t arow = (uint32_t)(wm * TM * 32 * BK * 2), brow = (uint32_t)(wn * TN * 32 * BK * 2);
+    // fragment of A for m-tile tm, the wavefront's chunk j, from the stage at
+    // byte offset `stage` (a run-time, wave-uniform value added to the address)
+    auto frag_a = [&](uint32_t stage, int tm, int j) __attribute__((always_inline)) {
         Frag<bf16> f;
         if constexpr (AT) {
-            const uint32_t off = B * C::STAGE + kc * 16 * BM * 2;
-            const bf16x4 x = lds_tr(aaddr[tm][0], off), y = lds_tr(aaddr[tm][1], off);
+            const uint32_t off = j * 16 * BM * 2;
+            const bf16x4 x = lds_tr(aaddr[tm][0] + stage, off), y = lds_tr(aaddr[tm][1] + stage, off);
             f.v = bf16x8{x[0], x[1], x[2], x[3], y[0], y[1], y[2], y[3]};
         } else {
-            f.v = lds_b128(aaddr[kc][0], B * C::STAGE + (wm * TM + tm) * 32 * kGemmBK * 2);
+            f.v = lds_b128(aaddr[j][0] + stage + arow, tm * 32 * BK * 2);
         }
         return f;
     };
-    auto frag_b = [&](auto buf_c, int tn, int kc) __attribute__((always_inline)) {
-        constexpr int B = decltype(buf_c)::value;
+    auto frag_b = [&](uint32_t stage, int tn, int j) __attribute__((always_inline)) {
         Frag<bf16> f;
         if constexpr (BT) {
-            f.v = lds_b128(baddr[kc][0], B * C::STAGE + (wn * TN + tn) * 32 * kGemmBK * 2);
+            f.v = lds_b128(baddr[j][0] + stage + brow, tn * 32 * BK * 2);
         } else {
-            const uint32_t off = B * C::STAGE + kc * 16 * BN * 2;
-            const bf16x4 x = lds_tr(baddr[tn][0], off), y = lds_tr(baddr[tn][1], off);
+            const uint32_t off = j * 16 * BN * 2;
+            const bf16x4 x = lds_tr(baddr[tn][0] + stage, off), y = lds_tr(baddr[tn][1] + stage, off);
             f.v = bf16x8{x[0], x[1], x[2], x[3], y[0], y[1], y[2], y[3]};
         }
         return f;
@@ -159,35 +176,84 @@ __global__ __launch_bounds__(256, 2) void proj_gemm_bf16(GemmArgs p) {
 #pragma unroll
         for (int tm = 0; tm < TM; ++tm) acc[tn][tm] = f32x16{};
 
-    auto step = [&](auto buf_c, int s) __attribute__((always_inline)) {
-        constexpr int B = decltype(buf_c)::value;
-        if (s + 1 < nk) wait_vmcnt<C::LOADS>();  // step s landed; step s+1 may be in flight
-        else wait_vmcnt<0>();
+    // Step s: wait until step s has landed (the NS - 2 later steps may still
+    // be in flight), meet, refill the stage step s-1 used with step s+NS-1,
+    // then contract the wavefront's chunks of step s.
+    auto wait_step = [&](int s) __attribute__((always_inline)) {
+        const int later = min(NS - 2, nk - 1 - s);  // steps issued after step s
+        if constexpr (NS >= 5) {
+            if (later >= 3) { wait_vmcnt<(NS >= 5 ? 3 : 0) * C::LOADS>(); return; }
+        }
+        if constexpr (NS >= 4) {
+            if (later == 2) { wait_vmcnt<(NS >= 4 ? 2 : 0) * C::LOADS>(); return; }
+        }
+        if constexpr (NS >= 3) {
+            if (later == 1) { wait_vmcnt<C::LOADS>(); return; }
+        }
+        wait_vmcnt<0>();
+    };
+    static_assert(NS <= 5, "wait_step covers at most three steps in flight behind the awaited one");
+    for (int s = 0; s < NS - 1 && s < nk; ++s) issue(s, s);
+    int buf = 0;
+    for (int s = 0; s < nk; ++s) {
+        wait_step(s);
         __syncthreads();
-        if (s + 2 < nk) issue(s + 2, (B + 2) % kGemmStages);
+        if (s + NS - 1 < nk) issue(s + NS - 1, buf == 0 ? NS - 1 : buf - 1);
+        const uint32_t stage = (uint32_t)buf * C::STAGE;
 #pragma unroll
-        for (int kc = 0; kc < 2; ++kc) {
+        for (int j = 0; j < KCW; ++j) {
             Frag<bf16> fa[TM], fb[TN];
 #pragma unroll
-            for (int tm = 0; tm < TM; ++tm) fa[tm] = frag_a(buf_c, tm, kc);
+            for (int tm = 0; tm < TM; ++tm) fa[tm] = frag_a(stage, tm, j);
 #pragma unroll
-            for (int tn = 0; tn < TN; ++tn) fb[tn] = frag_b(buf_c, tn, kc);
+            for (int tn = 0; tn < TN; ++tn) fb[tn] = frag_b(stage, tn, j);
 #pragma unroll
             for (int tn = 0; tn < TN; ++tn)
 #pragma unroll
                 for (int tm = 0; tm < TM; ++tm) mma(acc[tn][tm], fb[tn], fa[tm]);
         }
-    };
+        buf = buf + 1 == NS ? 0 : buf + 1;
+    }
 
-    using S0 = std::integral_constant<int, 0>;
-    using S1 = std::integral_constant<int, 1>;
-    using S2 = std::integral_constant<int, 2>;
-    issue(0, 0);
-    if (nk > 1) issue(1, 1);
-    for (int s = 0; s < nk; s += 3) {
-        step(S0{}, s);
-        if (s + 1 < nk) step(S1{}, s + 1);
-        if (s + 2 < nk) step(S2{}, s + 2);
+    if constexpr (WK > 1) {
+        // Partial sums: wavefront (wm, wn, wk > 0) parks its accumulators in LDS
+        // (the stages are free once every wavefront has passed the barrier
+        // after its last step, whose loads it waited for in full); the wk = 0
+        // wavefront of the tile adds them in the order wk = 1, 2, ... and stores.
+        // Layout per wavefront: [tn][tm][quad][lane] x 16 bytes.
+        __syncthreads();
+        const uint32_t part0 = lds + (uint32_t)((wn * WM + wm) * C::PART);
+        constexpr uint32_t kSlot = (uint32_t)(WM * WN * C::PART);
+        if (wk > 0) {
+            const uint32_t mine = part0 + (uint32_t)(wk - 1) * kSlot;
+#pragma unroll
+            for (int tn = 0; tn < TN; ++tn)
+#pragma unroll
+                for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+                    for (int qd = 0; qd < 4; ++qd) {
+                        const uint32_t a = mine + (uint32_t)((((tn * TM + tm) * 4 + qd) * 64 + lane) * 16);
+                        *(FBL_LDS f32x4*)(uintptr_t)a = f32x4{acc[tn][tm][4 * qd], acc[tn][tm][4 * qd + 1],
+                                                              acc[tn][tm][4 * qd + 2], acc[tn][tm][4 * qd + 3]};
+                    }
+        }
+        __syncthreads();
+        if (wk > 0) return;
+#pragma unroll
+        for (int w = 1; w < WK; ++w) {
+            const uint32_t theirs = part0 + (uint32_t)(w - 1) * kSlot;
+#pragma unroll
+            for (int tn = 0; tn < TN; ++tn)
+#pragma unroll
+                for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+                    for (int qd = 0; qd < 4; ++qd) {
+                        const uint32_t a = theirs + (uint32_t)((((tn * TM + tm) * 4 + qd) * 64 + lane) * 16);
+                        const f32x4 v = *(const FBL_LDS f32x4*)(uintptr_t)a;
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) acc[tn][tm][4 * qd + e] += v[e];
+                    }
+        }
     }
 
     // C[m][n .. n+3]: lane <-> m, four consecutive n per store
@@ -206,30 +272,36 @@ __global__ __launch_bounds__(256, 2) void proj_gemm_bf16(GemmArgs p) {
     }
 }
 
-template <int BM, int BN, bool AT, bool BT>
-hipError_t launch_cfg(const GemmArgs& p, hipStream_t stream) {
-    using C = GemmCfg<BM, BN, AT, BT>;
-    const int tiles = (p.M / BM) * (p.N / BN);
-    hipLaunchKernelGGL((proj_gemm_bf16<BM, BN, AT, BT>), dim3((tiles + 7) / 8 * 8), dim3(256), C::BYTES, stream, p);
+template <int I, bool AT, bool BT>
+hipError_t launch_id(const GemmArgs& p, hipStream_t stream) {
+    constexpr GemmTile t = kGemmTiles[I];
+    using C = GemmCfg<t.bm, t.bn, t.bk, t.ns, t.wm, t.wn, t.wk, AT, BT>;
+    auto kernel = &proj_gemm_bf16<t.bm, t.bn, t.bk, t.ns, t.wm, t.wn, t.wk, AT, BT>;
+    static const hipError_t once = hipFuncSetAttribute(reinterpret_cast<const void*>(kernel),
+                                                       hipFuncAttributeMaxDynamicSharedMemorySize, C::BYTES);
+    if (once != hipSuccess) return once;
+    const int tiles = (p.M / t.bm) * (p.N / t.bn);
+    hipLaunchKernelGGL(kernel, dim3((tiles + 7) / 8 * 8), dim3(64 * C::NW), C::BYTES, stream, p);
     return hipGetLastError();
+}
+
+using Launcher = hipError_t (*)(const GemmArgs&, hipStream_t);
+
+template <bool AT, bool BT, int... I>
+constexpr std::array<Launcher, sizeof...(I)> launchers(std::integer_sequence<int, I...>) {
+    return {&launch_id<I, AT, BT>...};
 }
 
 template <bool AT, bool BT>
 hipError_t launch_tile(int tile, const GemmArgs& p, hipStream_t stream) {
-    switch (tile) {
-        case kGemmTile128x128: return launch_cfg<128, 128, AT, BT>(p, stream);
-        case kGemmTile128x64: return launch_cfg<128, 64, AT, BT>(p, stream);
-        case kGemmTile64x128: return launch_cfg<64, 128, AT, BT>(p, stream);
-        default: return launch_cfg<64, 64, AT, BT>(p, stream);
-    }
+    static constexpr auto table = launchers<AT, BT>(std::make_integer_sequence<int, kGemmTileCount>{});
+    return table[tile](p, stream);
 }
 
 }  // namespace
 
-int gemm_tile_rows(int tile) { return tile == kGemmTile128x128 || tile == kGemmTile128x64 ? 128 : 64; }
-int gemm_tile_cols(int tile) { return tile == kGemmTile128x128 || tile == kGemmTile64x128 ? 128 : 64; }
-
 hipError_t launch_proj_gemm(int a_kmajor, int b_nmajor, int tile, const GemmArgs& p, hipStream_t stream) {
+    if (tile < 0 || tile >= kGemmTileCount) return hipErrorInvalidValue;
     if (a_kmajor) return b_nmajor ? launch_tile<true, true>(tile, p, stream) : launch_tile<true, false>(tile, p, stream);
     return b_nmajor ? launch_tile<false, true>(tile, p, stream) : launch_tile<false, false>(tile, p, stream);
 }

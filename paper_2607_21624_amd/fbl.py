@@ -44,9 +44,13 @@ FBL_GEMM_TILE_128x128 = 0
 FBL_GEMM_TILE_128x64 = 1
 FBL_GEMM_TILE_64x128 = 2
 FBL_GEMM_TILE_64x64 = 3
+FBL_TUNE_TIME = 0
+FBL_TUNE_GFLOPS_X_MEMEFF = 1
 
 EXPORTED = ("fbl_layout_desc", "fbl_layout_packed_qkv", "fbl_layout_offset", "fbl_layout_map_device", "fbl_attn_fwd",
-            "fbl_attn_bwd_workspace", "fbl_attn_bwd_workspace_min", "fbl_attn_bwd", "fbl_attn_bwd_phases", "fbl_proj", "fbl_status_str")
+            "fbl_attn_bwd_workspace", "fbl_attn_bwd_workspace_min", "fbl_attn_bwd", "fbl_attn_bwd_phases", "fbl_proj",
+            "fbl_gemm_tile_count", "fbl_gemm_tile_info", "fbl_proj_candidates", "fbl_proj_tune", "fbl_proj_tuned_tile",
+            "fbl_proj_tune_reset", "fbl_status_str")
 
 
 class Layout(ctypes.Structure):
@@ -109,6 +113,20 @@ def _load() -> ctypes.CDLL:
     lib.fbl_proj.argtypes = [ctypes.c_uint32] + [ctypes.c_int64] * 3 + [vp, ctypes.c_int64, vp, ctypes.c_int64, vp,
                                                                         ctypes.c_int64, ctypes.c_int32, vp]
     lib.fbl_proj.restype = ctypes.c_int
+    lib.fbl_gemm_tile_count.argtypes = []
+    lib.fbl_gemm_tile_count.restype = ctypes.c_int32
+    lib.fbl_gemm_tile_info.argtypes = [ctypes.c_int32, P(ctypes.c_int32)]
+    lib.fbl_gemm_tile_info.restype = ctypes.c_int
+    lib.fbl_proj_candidates.argtypes = [ctypes.c_uint32] + [ctypes.c_int64] * 3 + [P(ctypes.c_int32), ctypes.c_int32,
+                                                                                 P(ctypes.c_int32)]
+    lib.fbl_proj_candidates.restype = ctypes.c_int
+    lib.fbl_proj_tune.argtypes = lib.fbl_proj.argtypes[:10] + [ctypes.c_uint32, ctypes.c_int32, P(ctypes.c_float),
+                                                              P(ctypes.c_int32), vp]
+    lib.fbl_proj_tune.restype = ctypes.c_int
+    lib.fbl_proj_tuned_tile.argtypes = [ctypes.c_uint32] + [ctypes.c_int64] * 3
+    lib.fbl_proj_tuned_tile.restype = ctypes.c_int32
+    lib.fbl_proj_tune_reset.argtypes = []
+    lib.fbl_proj_tune_reset.restype = None
     lib.fbl_status_str.argtypes = [ctypes.c_int]
     lib.fbl_status_str.restype = ctypes.c_char_p
     return lib
@@ -357,12 +375,7 @@ def _rows(t, name):
     return t.shape[0], t.shape[1], t.stride(0)
 
 
-def proj(op: int, a, b, out=None, tile: int = FBL_GEMM_TILE_AUTO, stream=None):
-    """One projection product on 2-D bf16 tensors (row-major, any row stride):
-    FBL_PROJ_FWD (a = X [M, K], b = W [K, N]) -> Y [M, N];
-    FBL_PROJ_BWD_DATA (a = dY [M, N], b = W [K, N]) -> dX [M, K];
-    FBL_PROJ_BWD_WEIGHT (a = X [M, K], b = dY [M, N]) -> dW [K, N]."""
-    import torch
+def _proj_shape(op, a, b):
     ra, wa, lda = _rows(a, "a")
     rb, wb, ldb = _rows(b, "b")
     if op == FBL_PROJ_FWD:
@@ -371,8 +384,61 @@ def proj(op: int, a, b, out=None, tile: int = FBL_GEMM_TILE_AUTO, stream=None):
         M, N, K, shape = ra, wa, rb, (ra, rb)
     else:
         M, K, N, shape = ra, wa, wb, (wa, wb)
+    return M, K, N, shape, lda, ldb
+
+
+def proj(op: int, a, b, out=None, tile: int = FBL_GEMM_TILE_AUTO, stream=None):
+    """One projection product on 2-D bf16 tensors (row-major, any row stride):
+    FBL_PROJ_FWD (a = X [M, K], b = W [K, N]) -> Y [M, N];
+    FBL_PROJ_BWD_DATA (a = dY [M, N], b = W [K, N]) -> dX [M, K];
+    FBL_PROJ_BWD_WEIGHT (a = X [M, K], b = dY [M, N]) -> dW [K, N]."""
+    import torch
+    M, K, N, shape, lda, ldb = _proj_shape(op, a, b)
     if out is None:
         out = torch.empty(shape, dtype=a.dtype, device=a.device)
     _, _, ldc = _rows(out, "out")
     _check(fbl_proj_raw(op, M, K, N, a, lda, b, ldb, out, ldc, tile, stream), "fbl_proj")
     return out
+
+
+def gemm_tiles():
+    """Every tile configuration: {id: dict(bm, bn, bk, stages, wm, wn, wk, lds_bytes)}."""
+    keys = ("bm", "bn", "bk", "stages", "wm", "wn", "wk", "lds_bytes")
+    out = {}
+    for t in range(LIB.fbl_gemm_tile_count()):
+        info = (ctypes.c_int32 * 8)()
+        _check(LIB.fbl_gemm_tile_info(t, info), "fbl_gemm_tile_info")
+        out[t] = dict(zip(keys, list(info)))
+    return out
+
+
+def proj_candidates(op: int, M: int, K: int, N: int):
+    """Candidate tile ids of one product shape (the C1/C2/C3 filters)."""
+    n = ctypes.c_int32()
+    cap = LIB.fbl_gemm_tile_count()
+    ids = (ctypes.c_int32 * cap)()
+    _check(LIB.fbl_proj_candidates(op, M, K, N, ids, cap, ctypes.byref(n)), "fbl_proj_candidates")
+    return list(ids[:n.value])
+
+
+def proj_tune(op: int, a, b, out, objective: int = FBL_TUNE_TIME, reps: int = 10, stream=None):
+    """Measured tile selection for one product (fbl_proj_tune).  Returns
+    (chosen id, {id: average ms} over the candidates); `out` then holds the
+    product computed with the chosen tile."""
+    M, K, N, _, lda, ldb = _proj_shape(op, a, b)
+    _, _, ldc = _rows(out, "out")
+    cap = LIB.fbl_gemm_tile_count()
+    ms = (ctypes.c_float * cap)()
+    best = ctypes.c_int32(-1)
+    _check(LIB.fbl_proj_tune(op, M, K, N, _ptr(a), lda, _ptr(b), ldb, _ptr(out), ldc, objective, reps, ms,
+                             ctypes.byref(best), _stream(stream) if stream != 0 else None), "fbl_proj_tune")
+    return best.value, {t: ms[t] for t in range(cap) if ms[t] >= 0}
+
+
+def proj_tuned_tile(op: int, M: int, K: int, N: int) -> int:
+    """The tile fbl_proj_tune chose for this shape in this process, or -1."""
+    return LIB.fbl_proj_tuned_tile(op, M, K, N)
+
+
+def proj_tune_reset() -> None:
+    LIB.fbl_proj_tune_reset()

@@ -326,5 +326,69 @@ def test_proj_rejections():
     assert P(E.FBL_PROJ_FWD, 64, 48, 64) == E.FBL_ERR_UNSUPPORTED     # contraction not a multiple of 32
     assert P(E.FBL_PROJ_FWD, 96, 64, 64) == E.FBL_ERR_UNSUPPORTED     # output rows not a multiple of 64
     assert P(E.FBL_PROJ_FWD, 64, 64, 64, tile=E.FBL_GEMM_TILE_128x128) == E.FBL_ERR_UNSUPPORTED
-    assert P(E.FBL_PROJ_FWD, 64, 64, 64, tile=7) == E.FBL_ERR_ARG
+    assert P(E.FBL_PROJ_FWD, 64, 32, 64, tile=7) == E.FBL_ERR_UNSUPPORTED  # 64-deep steps, contraction 32
+    assert P(E.FBL_PROJ_FWD, 64, 64, 64, tile=13) == E.FBL_ERR_ARG    # no such tile id
+    assert P(E.FBL_PROJ_FWD, 64, 64, 64, tile=-2) == E.FBL_ERR_ARG
     assert P(E.FBL_PROJ_FWD, 64, 64, 64, c=FAKE + 64) == E.FBL_ERR_ARG  # output overlaps an input
+
+
+def test_gemm_tile_table():
+    """The tile table the GPU tests enumerate: 13 configurations, ids 0-3 the
+    named output shapes, LDS within the 160 KB of a CU, and the contraction
+    split and wavefront grid consistent with the output tile."""
+    tiles = fbl.gemm_tiles()
+    assert len(tiles) == 13 and fbl.LIB.fbl_gemm_tile_count() == 13
+    named = {F.FBL_GEMM_TILE_128x128: (128, 128), F.FBL_GEMM_TILE_128x64: (128, 64),
+             F.FBL_GEMM_TILE_64x128: (64, 128), F.FBL_GEMM_TILE_64x64: (64, 64)}
+    for t, (bm, bn) in named.items():
+        assert (tiles[t]["bm"], tiles[t]["bn"]) == (bm, bn)
+    for t, g in tiles.items():
+        assert g["wm"] * g["wn"] * g["wk"] in (4, 8)
+        assert g["bm"] % (32 * g["wm"]) == 0 and g["bn"] % (32 * g["wn"]) == 0
+        assert (g["bk"] // 16) % g["wk"] == 0
+        stages = g["stages"] * (g["bm"] + g["bn"]) * g["bk"] * 2
+        partial = (g["wk"] - 1) * g["bm"] * g["bn"] * 4
+        assert g["lds_bytes"] == max(stages, partial) <= 160 * 1024
+    info = (ctypes.c_int32 * 8)()
+    assert fbl.LIB.fbl_gemm_tile_info(13, info) == F.FBL_ERR_ARG
+    assert fbl.LIB.fbl_gemm_tile_info(0, None) == F.FBL_ERR_NULL
+
+
+def test_proj_candidates_filters():
+    """C3 keeps only tiles that divide the product exactly; C2 drops staged
+    rows that are not whole 128-byte lines: a 32-deep step stages 64-byte rows
+    of a row-read operand, so the forward and data-gradient products (row-read
+    A) lose the 32-deep tiles while the weight gradient (both operands read
+    transposed, rows of bm or bn elements) keeps them."""
+    tiles = fbl.gemm_tiles()
+    M, K, N = 512, 2048, 8192
+    fwd = fbl.proj_candidates(F.FBL_PROJ_FWD, M, K, N)
+    bwd_w = fbl.proj_candidates(F.FBL_PROJ_BWD_WEIGHT, M, K, N)
+    assert fwd == fbl.proj_candidates(F.FBL_PROJ_BWD_DATA, M, K, N)
+    assert fwd == [t for t in sorted(tiles) if tiles[t]["bk"] >= 64]
+    assert bwd_w == sorted(tiles)
+    # only the 64 x 64 output tile divides a 64 x 64 product; only 64-deep steps a contraction of 64
+    assert fbl.proj_candidates(F.FBL_PROJ_FWD, 64, 64, 64) == [7]
+    assert fbl.proj_candidates(F.FBL_PROJ_BWD_WEIGHT, 64, 64, 64) == [3, 7]
+    # 192 output rows: no 128-row tile; contraction 96: no 64- or 128-deep step, and 32-deep ones fail C2
+    assert all(tiles[t]["bm"] == 64 for t in fbl.proj_candidates(F.FBL_PROJ_FWD, 192, 128, 256))
+    assert fbl.proj_candidates(F.FBL_PROJ_FWD, 64, 96, 64) == []
+    n = ctypes.c_int32()
+    assert fbl.LIB.fbl_proj_candidates(F.FBL_PROJ_FWD, M, K, N, None, 0, ctypes.byref(n)) == F.FBL_OK
+    assert n.value == len(fwd)
+    assert fbl.LIB.fbl_proj_candidates(3, M, K, N, None, 0, ctypes.byref(n)) == F.FBL_ERR_ARG
+    assert fbl.LIB.fbl_proj_candidates(F.FBL_PROJ_FWD, 0, K, N, None, 0, ctypes.byref(n)) == F.FBL_ERR_SHAPE
+    assert fbl.LIB.fbl_proj_candidates(F.FBL_PROJ_FWD, M, K, N, None, 4, ctypes.byref(n)) == F.FBL_ERR_NULL
+
+
+def test_proj_tune_rejections():
+    """Argument checks that return before any GPU work."""
+    T = lambda op=0, obj=0, reps=5, a=FAKE: fbl.LIB.fbl_proj_tune(
+        op, 64, 64, 64, ctypes.c_void_p(a) if a else None, 4096, ctypes.c_void_p(FAKE + (1 << 24)), 4096,
+        ctypes.c_void_p(FAKE + (1 << 26)), 4096, obj, reps, None, None, None)
+    assert T(op=3) == F.FBL_ERR_ARG
+    assert T(a=0) == F.FBL_ERR_NULL
+    assert T(obj=2) == F.FBL_ERR_ARG
+    assert T(reps=0) == F.FBL_ERR_ARG
+    assert T(reps=1001) == F.FBL_ERR_ARG
+    assert fbl.proj_tuned_tile(F.FBL_PROJ_FWD, 64, 64, 64) == -1

@@ -1,6 +1,6 @@
 """GPU parity of the projection products (fbl_proj, through the C ABI) against
 the fp64 oracle: Y = X W, dX = dY W^T, dW = X^T dY on bf16 token-major
-operands, every tile shape, strided (column-view) operands and outputs, and the
+operands, every tile configuration, strided (column-view) operands and outputs, and the
 paper-scale shape on sampled output rows.
 
 Tolerance: max|gpu - ref| / max|ref| <= 2e-2 (bf16 storage, fp32 accumulation).
@@ -27,41 +27,43 @@ def _inputs(M, K, N, seed):
             synth.round_to_bf16(rng.standard_normal((M, N))))
 
 
-TILES = ["auto", "128x128", "128x64", "64x128", "64x64"]
-SHAPES = [(64, 64, 64), (128, 192, 64), (192, 256, 128), (256, 128, 320)]  # M, K, N multiples of 64: every output fits
+SHAPES = [(64, 64, 64), (128, 192, 64), (192, 256, 128), (256, 128, 320), (256, 256, 256), (512, 128, 384)]
 
 
-def _tile(fbl, name):
-    return {"auto": fbl.FBL_GEMM_TILE_AUTO, "128x128": fbl.FBL_GEMM_TILE_128x128, "128x64": fbl.FBL_GEMM_TILE_128x64,
-            "64x128": fbl.FBL_GEMM_TILE_64x128, "64x64": fbl.FBL_GEMM_TILE_64x64}[name]
+NTILES = 13  # fbl_gemm_tile_count(); tests/test_boundary.py pins it
 
 
-def _fits(tile, rows, cols):
-    if tile == "auto":
-        return True
-    r, c = (int(x) for x in tile.split("x"))
-    return rows % r == 0 and cols % c == 0
+def _runs(info, rows, cols, kc):
+    return rows % info["bm"] == 0 and cols % info["bn"] == 0 and kc % info["bk"] == 0
 
 
-@pytest.mark.parametrize("tile", TILES)
+@pytest.mark.parametrize("tile", ["auto"] + list(range(NTILES)))
 @pytest.mark.parametrize("M,K,N", SHAPES)
 def test_proj_products_match_oracle(M, K, N, tile):
+    """Every tile configuration (output tile, staged depth, wavefront grid and
+    contraction split) on every product; a tile that does not divide the
+    product is refused with FBL_ERR_UNSUPPORTED."""
     import torch
     fbl = _lib()
+    tiles = fbl.gemm_tiles()
     x, w, dy = _inputs(M, K, N, M + 3 * K + 7 * N)
     X, W, dY = to_dev(x, "bf16"), to_dev(w, "bf16"), to_dev(dy, "bf16")
     note(f"proj M={M} K={K} N={N} tile={tile}")
-    cases = [(fbl.FBL_PROJ_FWD, X, W, oracle.proj_fwd(x, w)),
-             (fbl.FBL_PROJ_BWD_DATA, dY, W, oracle.proj_bwd_data(dy, w)),
-             (fbl.FBL_PROJ_BWD_WEIGHT, X, dY, oracle.proj_bwd_weight(x, dy))]
-    for op, a, b, ref in cases:
-        if not _fits(tile, *ref.shape):
+    cases = [(fbl.FBL_PROJ_FWD, X, W, oracle.proj_fwd(x, w), K),
+             (fbl.FBL_PROJ_BWD_DATA, dY, W, oracle.proj_bwd_data(dy, w), N),
+             (fbl.FBL_PROJ_BWD_WEIGHT, X, dY, oracle.proj_bwd_weight(x, dy), M)]
+    t = fbl.FBL_GEMM_TILE_AUTO if tile == "auto" else tile
+    for op, a, b, ref, kc in cases:
+        if tile != "auto" and not _runs(tiles[tile], *ref.shape, kc):
+            with pytest.raises(fbl.FblError) as err:
+                fbl.proj(op, a, b, tile=t)
+            assert err.value.status == fbl.fbl.FBL_ERR_UNSUPPORTED
             continue
-        got = fbl.proj(op, a, b, tile=_tile(fbl, tile))
+        got = fbl.proj(op, a, b, tile=t)
         torch.cuda.synchronize()
         assert got.shape == ref.shape
         e = rel_err(to_np(got), ref)
-        assert e <= TOL, f"op {op}: rel err {e}"
+        assert e <= TOL, f"op {op} tile {tile}: rel err {e}"
 
 
 def test_proj_strided_operands_and_packed_output():
@@ -110,3 +112,47 @@ def test_proj_paper_shape_sampled_rows():
     assert rel_err(to_np(dx[rows]), oracle.proj_bwd_data(dy[rows], w)) <= TOL
     krows = np.arange(0, K, 32)
     assert rel_err(to_np(dw[krows]), oracle.proj_bwd_weight(x[:, krows], dy)) <= TOL
+
+
+@pytest.mark.parametrize("objective", [0, 1])
+def test_proj_tune_picks_a_measured_candidate(objective):
+    """fbl_proj_tune times exactly the candidate tiles, picks the one its
+    objective ranks first (recomputed here from the returned times and the
+    staged-bytes model), leaves the product in `out`, and FBL_GEMM_TILE_AUTO
+    then runs the chosen tile (bit-identical output to the explicit id)."""
+    import torch
+    fbl = _lib()
+    M, K, N = 256, 256, 512
+    x, w, dy = _inputs(M, K, N, 99 + objective)
+    X, W, dY = to_dev(x, "bf16"), to_dev(w, "bf16"), to_dev(dy, "bf16")
+    tiles = fbl.gemm_tiles()
+    fbl.proj_tune_reset()
+    for op, a, b, ref, (rows, cols, kc) in [
+            (fbl.FBL_PROJ_FWD, X, W, oracle.proj_fwd(x, w), (M, N, K)),
+            (fbl.FBL_PROJ_BWD_DATA, dY, W, oracle.proj_bwd_data(dy, w), (M, K, N)),
+            (fbl.FBL_PROJ_BWD_WEIGHT, X, dY, oracle.proj_bwd_weight(x, dy), (K, N, M))]:
+        note(f"proj_tune op={op} objective={objective}")
+        out = torch.empty(ref.shape, dtype=torch.bfloat16, device="cuda")
+        assert fbl.proj_tuned_tile(op, M, K, N) == -1
+        best, ms = fbl.proj_tune(op, a, b, out, objective=objective, reps=3)
+        torch.cuda.synchronize()
+        assert sorted(ms) == fbl.proj_candidates(op, M, K, N)
+        assert all(v > 0 for v in ms.values())
+        flops = 2.0 * rows * cols * kc
+        min_bytes = 2.0 * (rows * kc + kc * cols + rows * cols)
+
+        def score(t):
+            if objective == 0:
+                return 1.0 / ms[t]
+            g = tiles[t]
+            staged = 2.0 * (rows * kc * (cols // g["bn"]) + kc * cols * (rows // g["bm"]) + rows * cols)
+            return flops / (ms[t] * 1e-3) * (min_bytes / staged)
+        assert best == max(sorted(ms), key=score)
+        assert fbl.proj_tuned_tile(op, M, K, N) == best
+        assert rel_err(to_np(out), ref) <= TOL
+        auto = fbl.proj(op, a, b)
+        explicit = fbl.proj(op, a, b, tile=best)
+        torch.cuda.synchronize()
+        assert torch.equal(auto, explicit)
+    fbl.proj_tune_reset()
+    assert fbl.proj_tuned_tile(fbl.FBL_PROJ_FWD, M, K, N) == -1
