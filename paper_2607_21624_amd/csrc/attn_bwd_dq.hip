@@ -6,13 +6,13 @@
 // stored it in the workspace, so this pass only streams dS and K:
 //   dQ^T(32 queries) += K_kb^T dS_kb^T       for the key blocks kb of the row
 // It is bound by HBM (2 bytes of dS per allowed pair against 2*d MFMA flops),
-// so the design goal is a full memory pipe, not MFMA issue: a workgroup
-// covers 128-query blocks of one (batch, query head), four wavefronts of one
-// 32-query tile; per 32-key step it brings the K tile (shared) and each
-// wavefront's dS block into LDS by DMA, with three steps in flight, and two
-// workgroups share a CU so that one computes while the other waits.  Under a
-// causal mask block q reads 4(q+1) key blocks, so a workgroup takes the pair
-// (nqb-1-r, r): every workgroup streams the same number of steps.
+// so the design goal is a full memory pipe, not MFMA issue: a workgroup of
+// NW wavefronts covers blocks of 32*NW queries of one (batch, query head), one
+// 32-query tile per wavefront; per 32-key step it brings the K tile (shared)
+// and each wavefront's dS block into LDS by DMA, with NBUF - 1 steps in
+// flight.  Under a causal mask block q reads NW(q+1) key blocks, so a
+// workgroup takes the pair (nqb-1-r, r): every workgroup streams the same
+// number of steps.
 //
 // dS block layout (written by the key/value-major pass): block (qb32, kb32)
 // of query head h is 1024 bf16 at ((b*Hq + h)*nk32 + kb32)*nq32*1024 +
@@ -38,32 +38,38 @@ namespace fbl {
 
 namespace {
 
-constexpr int kDqWaves = 4;
-constexpr int kDqTiles = 1;                        // 32-query tiles per wavefront
-constexpr int kDqRows = 32 * kDqTiles * kDqWaves;  // queries per block
-constexpr int kDqTilesPerBlock = kDqRows / 32;
+constexpr int kDqTiles = 1;  // 32-query tiles per wavefront
 
-template <int D>
+// NW wavefronts, NBUF LDS buffers (NBUF - 1 steps in flight)
+template <int D, int NW, int NBUF_>
 struct DqPipe {
-    static constexpr int NBUF = 4;
+    static constexpr int NBUF = NBUF_;
+    static constexpr int ROWS = 32 * kDqTiles * NW;       // queries per block
+    static constexpr int TPB = ROWS / 32;                 // 32-query tiles per block
     static constexpr int KT = 32 * D * 2;                 // bytes of a 32-key K tile
     static constexpr int KINST = KT / 1024;               // 1 KB DMA loads per K tile
-    static constexpr int KPW = KINST >= kDqWaves ? KINST / kDqWaves : 1;  // per wavefront
+    static constexpr int KPW = KINST >= NW ? KINST / NW : 1;  // per wavefront
     static constexpr int DSW = kDqTiles * 2048;           // one wavefront's dS blocks per step
-    static constexpr int DSBUF = kDqWaves * DSW;
+    static constexpr int DSBUF = NW * DSW;
     static constexpr int OFF_K = NBUF * DSBUF;
-    static constexpr int SPARE = OFF_K + NBUF * KT;       // sink of the K loads of idle wavefronts (d = 32)
-    static constexpr int BYTES = SPARE + 1024;
+    static constexpr int SPARE = OFF_K + NBUF * KT;       // sink of the K loads of idle wavefronts
+    static constexpr int BYTES = SPARE + (KINST < NW ? 1024 : 0);
     static constexpr int LOADS = 2 * kDqTiles + KPW;      // DMA loads per wavefront per step
-    static_assert(KINST % kDqWaves == 0 || KINST < kDqWaves, "K tile loads spread evenly");
-    static_assert((NBUF - 1) * DSBUF + (kDqTiles - 1) * 2048 + 384 < 65536 && (NBUF - 1) * KT + KT < 65536,
+    static constexpr int OCC = 2 * BYTES <= 160 * 1024 && NW == 4 ? 2 : 1;  // workgroups per CU
+    static_assert(KINST % NW == 0 || KINST < NW, "K tile loads spread evenly");
+    static_assert(NBUF >= 3 && NBUF <= 6 && (NBUF - 1) * LOADS < 64, "pipeline depth, vmcnt range");
+    // dS buffers are read from two bases (buffers 0-2 and 3-5), K from one
+    static_assert(2 * DSBUF + (kDqTiles - 1) * 2048 + 384 < 65536 && (NBUF - 1) * KT + KT < 65536,
                   "buffer offsets fit the 16-bit LDS immediate");
-    static_assert(2 * BYTES <= 160 * 1024, "two workgroups per CU");
+    static_assert(BYTES <= 160 * 1024, "LDS of one workgroup");
 };
 
-template <int D>
-__global__ __launch_bounds__(256, 2) void attn_bwd_dq_bf16(BwdArgs a) {
-    using P = DqPipe<D>;
+template <int D, int NW, int NBUF>
+__global__ __launch_bounds__(64 * NW, (DqPipe<D, NW, NBUF>::OCC)) void attn_bwd_dq_bf16(BwdArgs a) {
+    using P = DqPipe<D, NW, NBUF>;
+    constexpr int kDqWaves = NW;
+    constexpr int kDqRows = P::ROWS;
+    constexpr int kDqTilesPerBlock = P::TPB;
     using u32x4 = uint32_t __attribute__((ext_vector_type(4)));
     constexpr int ND = D / 32;
     constexpr int NT = kDqTiles;
@@ -142,10 +148,11 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_bf16(BwdArgs a) {
     // dS^T fragment: lane <-> query lane % 32, keys 8h + 4g + [0..3] of a
     // 16-key chunk; source lane s = 4j + m of its 16-lane group fetches the
     // four queries 16*(grp&1) + 4m + [0..3] at key 4*(grp>>1) + j.
-    uint32_t ds_lane;
+    uint32_t ds_lane[2];  // buffers 0-2, buffers 3-5
     {
         const int grp = lane >> 4, s = lane & 15, j = s >> 2, m = s & 3;
-        ds_lane = lds + wave * P::DSW + (grp & 1) * 1024 + (32 * (m & 1) + 4 * (grp >> 1) + j) * 16 + (m >> 1) * 8;
+        ds_lane[0] = lds + wave * P::DSW + (grp & 1) * 1024 + (32 * (m & 1) + 4 * (grp >> 1) + j) * 16 + (m >> 1) * 8;
+        ds_lane[1] = ds_lane[0] + 3 * P::DSBUF;
     }
     // Mask of the last key block when kv_end is not a multiple of 32: fragment
     // element e of chunk kc is key 16kc + 8(e/4) + 4g + e%4 of the block.
@@ -206,8 +213,8 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_bf16(BwdArgs a) {
             if (!tile_ok(tile0 + qt, kb)) continue;
 #pragma unroll
             for (int kc = 0; kc < 2; ++kc) {
-                const uint32_t off = B * P::DSBUF + qt * 2048 + kc * 256;
-                const bf16x4 x = lds_tr(ds_lane, off), y = lds_tr(ds_lane, off + 128);
+                const uint32_t off = (B % 3) * P::DSBUF + qt * 2048 + kc * 256;
+                const bf16x4 x = lds_tr(ds_lane[B / 3], off), y = lds_tr(ds_lane[B / 3], off + 128);
                 Frag<bf16> f;
                 f.v = bf16x8{x[0], x[1], x[2], x[3], y[0], y[1], y[2], y[3]};
                 if (tail) f.v = __builtin_bit_cast(bf16x8, __builtin_bit_cast(u32x4, f.v) & tail_mask[kc]);
@@ -220,52 +227,56 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_bf16(BwdArgs a) {
             reset();
         }
     };
-    // One step s, held in buffer B: its loads landed in every wavefront, then
-    // the buffer of step s-1 takes step s+3.
+    // One step s, held in buffer B: its loads landed in every wavefront (the
+    // NBUF - 2 later steps may still be in flight), then the buffer of step
+    // s-1 takes step s + NBUF - 1.
     auto step = [&](auto buf_c, int s) __attribute__((always_inline)) {
         constexpr int B = decltype(buf_c)::value;
-        if (s + 2 < n) wait_vmcnt<2 * P::LOADS>();
-        else if (s + 1 < n) wait_vmcnt<P::LOADS>();
+        const int later = min(NBUF - 2, n - 1 - s);  // steps issued after step s
+        if (later >= 4) wait_vmcnt<(NBUF >= 6 ? 4 : 0) * P::LOADS>();
+        else if (later == 3) wait_vmcnt<(NBUF >= 5 ? 3 : 0) * P::LOADS>();
+        else if (later == 2) wait_vmcnt<2 * P::LOADS>();
+        else if (later == 1) wait_vmcnt<P::LOADS>();
         else wait_vmcnt<0>();
         __syncthreads();
-        if (s + 3 < n) issue(s + 3, (B + 3) % P::NBUF);
+        if (s + NBUF - 1 < n) issue(s + NBUF - 1, (B + NBUF - 1) % NBUF);
         compute(buf_c, s);
     };
 
-    using C0 = std::integral_constant<int, 0>;
-    using C1 = std::integral_constant<int, 1>;
-    using C2 = std::integral_constant<int, 2>;
-    using C3 = std::integral_constant<int, 3>;
-    if (n > 0) issue(0, 0);
-    if (n > 1) issue(1, 1);
-    if (n > 2) issue(2, 2);
-    for (int s = 0; s < n; s += 4) {
-        step(C0{}, s);
-        if (s + 1 < n) step(C1{}, s + 1);
-        if (s + 2 < n) step(C2{}, s + 2);
-        if (s + 3 < n) step(C3{}, s + 3);
-    }
+    for (int s = 0; s < NBUF - 1 && s < n; ++s) issue(s, s);
+    // steps in order, NBUF per trip (one per LDS buffer, so every LDS address
+    // is a per-lane base plus an immediate)
+    for (int s = 0; s < n; s += NBUF)
+        unroll_steps(std::make_integer_sequence<int, NBUF>{}, [&](auto buf_c) __attribute__((always_inline)) {
+            if (s + decltype(buf_c)::value < n) step(buf_c, s + decltype(buf_c)::value);
+        });
     if (n == 0) {  // no allowed key at all: dQ = 0
         store_block(qa * kDqTilesPerBlock + wave * NT);
         if (qz >= 0) store_block(qz * kDqTilesPerBlock + wave * NT);
     }
 }
 
-template __global__ void attn_bwd_dq_bf16<32>(BwdArgs);
-template __global__ void attn_bwd_dq_bf16<64>(BwdArgs);
-template __global__ void attn_bwd_dq_bf16<128>(BwdArgs);
+template <int D, int NW, int NBUF>
+hipError_t launch_dq(const BwdArgs& a, hipStream_t stream) {
+    using P = DqPipe<D, NW, NBUF>;
+    static const hipError_t once = hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_bwd_dq_bf16<D, NW, NBUF>),
+                                                       hipFuncAttributeMaxDynamicSharedMemorySize, P::BYTES);
+    if (once != hipSuccess) return once;
+    const int nqb = (a.S + P::ROWS - 1) / P::ROWS;
+    const int n = (a.mask.causal ? (nqb + 1) / 2 : nqb) * a.Hq * a.B;
+    hipLaunchKernelGGL((attn_bwd_dq_bf16<D, NW, NBUF>), dim3((n + 7) / 8 * 8), dim3(64 * NW), P::BYTES, stream, a);
+    return hipGetLastError();
+}
+
+// Workgroup shape of the dQ pass.
+constexpr int kDqWaves = 4;
+constexpr int kDqBufs = 4;
 
 }  // namespace
 
 template <int D>
 hipError_t launch_attn_bwd_dq_bf16(const BwdArgs& a, hipStream_t stream) {
-    static const hipError_t once = hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_bwd_dq_bf16<D>),
-                                                       hipFuncAttributeMaxDynamicSharedMemorySize, DqPipe<D>::BYTES);
-    if (once != hipSuccess) return once;
-    const int nqb = (a.S + kDqRows - 1) / kDqRows;
-    const int n = (a.mask.causal ? (nqb + 1) / 2 : nqb) * a.Hq * a.B;
-    hipLaunchKernelGGL((attn_bwd_dq_bf16<D>), dim3((n + 7) / 8 * 8), dim3(256), DqPipe<D>::BYTES, stream, a);
-    return hipGetLastError();
+    return launch_dq<D, kDqWaves, kDqBufs>(a, stream);
 }
 
 template hipError_t launch_attn_bwd_dq_bf16<32>(const BwdArgs&, hipStream_t);

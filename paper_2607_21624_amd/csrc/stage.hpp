@@ -22,6 +22,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <utility>
+
 #include "cdna4.hpp"
 
 namespace fbl {
@@ -250,6 +252,14 @@ FBL_DEV int xcd_logical_id(int id, int total, int padded_total) {
     const int per_xcd = padded_total / 8;
     const int logical = (id % 8) * per_xcd + id / 8;
     return logical < total ? logical : -1;
+}
+
+// f(integral_constant<int, I>) for I = 0, 1, ..., in order: a loop over LDS
+// buffers whose index stays a compile-time constant (buffer offsets become
+// instruction immediates).
+template <int... I, typename F>
+FBL_DEV __attribute__((always_inline)) void unroll_steps(std::integer_sequence<int, I...>, F&& f) {
+    (f(std::integral_constant<int, I>{}), ...);
 }
 
 }  // namespace fbl
