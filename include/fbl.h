@@ -261,9 +261,12 @@ fbl_status fbl_attn_bwd_phases(uint32_t phases, const fbl_layout* lq, const void
  *            (>= 1024: 4-wavefront tiles with small LDS; >= 256: the
  *            8-wavefront 128 x 128 tile; fewer: 64 x 64 tiles whose
  *            wavefronts split the contraction).
- * Supported: the output's row and column counts multiples of 64 and the
- * contraction length a multiple of 32; an explicit tile must divide them
- * exactly (else FBL_ERR_UNSUPPORTED).  Checks: non-NULL pointers, positive
+ * Supported: any number of output rows, output columns a multiple of 4 and
+ * a contraction length a multiple of 8 (else FBL_ERR_UNSUPPORTED) -- so
+ * ragged token counts and LoRA ranks (8, 16, ...) as the narrow side or the
+ * contraction.  Any tile runs any shape: partial tiles are masked, and the
+ * contraction positions of a partial last step are zeroed before use.
+ * Checks: non-NULL pointers, positive
  * extents, leading dimensions >= widths, 16-byte aligned pointers and rows,
  * each operand's span below 2 GiB, c not overlapping a or b.  The caller owns
  * all memory; enqueued on `stream`; c is fully overwritten.
@@ -300,8 +303,11 @@ fbl_status fbl_gemm_tile_info(int32_t tile, int32_t* info);
  *   C1 compute alignment: wavefront tiles of whole 32x32 MFMA blocks, whole
  *      16-deep MFMA chunks per wavefront and step;
  *   C2 memory alignment: the workgroup's LDS fits the 160 KB of a CU and
- *      every staged row is a whole number of 128-byte cache lines;
- *   C3 shape: the tile divides the output and the contraction exactly.
+ *      every staged row is a whole number of 128-byte cache lines or spans
+ *      the operand's whole (narrower) stored row;
+ *   C3 shape: padding the output rows, the output columns and the
+ *      contraction to whole tiles adds at most 10% to each; if no tile
+ *      qualifies, the C1/C2 survivors of least padded volume.
  * Writes up to `cap` ids in increasing order to `tiles` and the number of
  * candidates to *count (which may exceed cap).  Host only, no GPU work.
  */

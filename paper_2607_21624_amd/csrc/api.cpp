@@ -386,13 +386,25 @@ fbl_status fbl_attn_bwd(const fbl_layout* lq, const void* q, const fbl_layout* l
 
 namespace {
 
-// A projection product, validated: kernel arguments, operand orientation and
-// the output/contraction extents the tile must divide.
+// A projection product, validated: kernel arguments, operand orientation,
+// the output/contraction extents and the operands' stored row widths.
 struct ProjPlan {
     fbl::GemmArgs p;
     int a_kmajor = 0, b_nmajor = 0;
     int64_t orows = 0, ocols = 0, kc = 0;
+    int64_t a_width = 0, b_width = 0;
 };
+
+// Orientation and extents of a product from (op, M, K, N) alone.
+void proj_shape(uint32_t op, int64_t M, int64_t K, int64_t N, ProjPlan& pl) {
+    pl.a_kmajor = op == FBL_PROJ_BWD_WEIGHT;
+    pl.b_nmajor = op == FBL_PROJ_BWD_DATA;
+    pl.orows = op == FBL_PROJ_BWD_WEIGHT ? K : M;
+    pl.ocols = op == FBL_PROJ_BWD_DATA ? K : N;
+    pl.kc = op == FBL_PROJ_FWD ? K : (op == FBL_PROJ_BWD_DATA ? N : M);
+    pl.a_width = op == FBL_PROJ_BWD_DATA ? N : K;  // X [M, K] or dY [M, N]
+    pl.b_width = N;                                // W [K, N] or dY [M, N]
+}
 
 fbl_status proj_plan(uint32_t op, int64_t M, int64_t K, int64_t N, const void* a, int64_t lda, const void* b,
                      int64_t ldb, void* c, int64_t ldc, ProjPlan& pl) {
@@ -414,7 +426,9 @@ fbl_status proj_plan(uint32_t op, int64_t M, int64_t K, int64_t N, const void* a
     if (lda < wa || ldb < wb || ldc < wc) return FBL_ERR_LAYOUT;
     if (!aligned16(a) || !aligned16(b) || !aligned16(c) || (lda * 2) % 16 || (ldb * 2) % 16 || (ldc * 2) % 16)
         return FBL_ERR_ALIGN;
-    if (pl.orows % 64 || pl.ocols % 64 || pl.kc % 32) return FBL_ERR_UNSUPPORTED;
+    pl.a_width = wa;
+    pl.b_width = wb;
+    if (pl.ocols % 4 || pl.kc % 8) return FBL_ERR_UNSUPPORTED;
     const int64_t sa = ((ra - 1) * lda + wa) * 2, sb = ((rb - 1) * ldb + wb) * 2, sc = ((rc - 1) * ldc + wc) * 2;
     if (sa >= ((int64_t)1 << 31) || sb >= ((int64_t)1 << 31) || sc >= ((int64_t)1 << 31)) return FBL_ERR_UNSUPPORTED;
     if (overlaps(c, sc, a, sa) || overlaps(c, sc, b, sb)) return FBL_ERR_ARG;
@@ -430,15 +444,31 @@ fbl_status proj_plan(uint32_t op, int64_t M, int64_t K, int64_t N, const void* a
     p.K = (int)pl.kc;
     p.a_bytes = (uint32_t)sa;
     p.b_bytes = (uint32_t)sb;
+    p.c_bytes = (uint32_t)sc;
     return FBL_OK;
 }
 
-bool tile_runs(int tile, const ProjPlan& pl) {
-    return fbl::gemm_c3(fbl::kGemmTiles[tile], pl.orows, pl.ocols, pl.kc);
-}
-bool tile_candidate(int tile, const ProjPlan& pl) {
-    const fbl::GemmTile& t = fbl::kGemmTiles[tile];
-    return fbl::gemm_c1(t) && fbl::gemm_c2(t, pl.a_kmajor, pl.b_nmajor) && tile_runs(tile, pl);
+// Candidate tiles (C1, C2, C3 of gemm_tiles.hpp) as a bit set over the ids:
+// when no tile keeps the padding within 10%, the C1/C2 survivors of least
+// padded volume.
+uint64_t candidate_set(const ProjPlan& pl) {
+    static_assert(fbl::kGemmTileCount <= 64, "tile ids fit the bit set");
+    uint64_t c12 = 0, all = 0;
+    for (int i = 0; i < fbl::kGemmTileCount; ++i) {
+        const fbl::GemmTile& t = fbl::kGemmTiles[i];
+        if (!fbl::gemm_c1(t) || !fbl::gemm_c2(t, pl.a_kmajor, pl.b_nmajor, pl.a_width, pl.b_width)) continue;
+        c12 |= uint64_t(1) << i;
+        if (fbl::gemm_c3(t, pl.orows, pl.ocols, pl.kc)) all |= uint64_t(1) << i;
+    }
+    if (all || !c12) return all;
+    double best = 0;
+    for (int i = 0; i < fbl::kGemmTileCount; ++i)
+        if (c12 >> i & 1) {
+            const double v = fbl::gemm_padded_volume(fbl::kGemmTiles[i], pl.orows, pl.ocols, pl.kc);
+            if (!all || v < best) all = uint64_t(1) << i, best = v;
+            else if (v == best) all |= uint64_t(1) << i;
+        }
+    return all;
 }
 
 // Per-shape table of measured choices (fbl_proj_tune), the run-time analogue
@@ -467,26 +497,24 @@ int32_t tuned_tile(uint32_t op, int64_t M, int64_t K, int64_t N) {
 // contraction.  The first candidate of the order that gives at least one
 // workgroup per CU (256) wins, else the first candidate.
 int32_t default_tile(const ProjPlan& pl) {
-    static const int many[] = {0, 4, 8, 1, 2, 5, 6, 11, 12, 10, 9, 7, 3};
-    static const int some[] = {8, 4, 6, 5, 11, 12, 0, 2, 1, 10, 9, 7, 3};
-    static const int few[] = {9, 10, 7, 6, 5, 8, 4, 3, 2, 1, 0, 11, 12};
+    static const int many[] = {0, 4, 8, 1, 2, 5, 6, 11, 12, 10, 9, 7, 3, 13, 15, 14, 16};
+    static const int some[] = {8, 4, 6, 5, 11, 12, 0, 2, 1, 10, 9, 7, 3, 13, 15, 14, 16};
+    static const int few[] = {9, 10, 7, 6, 5, 8, 4, 3, 2, 1, 0, 11, 12, 14, 13, 15, 16};
     static_assert(sizeof(many) == sizeof(int) * fbl::kGemmTileCount && sizeof(some) == sizeof(many) &&
                       sizeof(few) == sizeof(many),
                   "every tile ranked once");
-    const int64_t n128 = (pl.orows / 128) * (pl.ocols / 128);
+    const uint64_t cand = candidate_set(pl);
+    const int64_t n128 = ((pl.orows + 127) / 128) * ((pl.ocols + 127) / 128);
     const int* order = n128 >= 1024 ? many : (n128 >= 256 ? some : few);
     int32_t first = -1;
     for (int i = 0; i < fbl::kGemmTileCount; ++i) {
         const int t = order[i];
-        if (!tile_candidate(t, pl)) continue;
+        if (!(cand >> t & 1)) continue;
         const fbl::GemmTile& g = fbl::kGemmTiles[t];
-        if ((pl.orows / g.bm) * (pl.ocols / g.bn) >= 256) return t;
+        if (((pl.orows + g.bm - 1) / g.bm) * ((pl.ocols + g.bn - 1) / g.bn) >= 256) return t;
         if (first < 0) first = t;
     }
-    if (first >= 0) return first;
-    for (int t = 0; t < fbl::kGemmTileCount; ++t)
-        if (tile_runs(t, pl)) return t;
-    return -1;
+    return first >= 0 ? first : order[0];
 }
 
 }  // namespace
@@ -510,14 +538,11 @@ fbl_status fbl_proj_candidates(uint32_t op, int64_t M, int64_t K, int64_t N, int
     if (op > FBL_PROJ_BWD_WEIGHT) return FBL_ERR_ARG;
     if (M <= 0 || K <= 0 || N <= 0 || M > INT32_MAX || K > INT32_MAX || N > INT32_MAX) return FBL_ERR_SHAPE;
     ProjPlan pl;
-    pl.a_kmajor = op == FBL_PROJ_BWD_WEIGHT;
-    pl.b_nmajor = op == FBL_PROJ_BWD_DATA;
-    pl.orows = op == FBL_PROJ_BWD_WEIGHT ? K : M;
-    pl.ocols = op == FBL_PROJ_BWD_DATA ? K : N;
-    pl.kc = op == FBL_PROJ_FWD ? K : (op == FBL_PROJ_BWD_DATA ? N : M);
+    proj_shape(op, M, K, N, pl);
+    const uint64_t cand = candidate_set(pl);
     int32_t n = 0;
     for (int t = 0; t < fbl::kGemmTileCount; ++t)
-        if (tile_candidate(t, pl)) {
+        if (cand >> t & 1) {
             if (n < cap) tiles[n] = t;
             ++n;
         }
@@ -534,9 +559,7 @@ fbl_status fbl_proj(uint32_t op, int64_t M, int64_t K, int64_t N, const void* a,
     if (tile == FBL_GEMM_TILE_AUTO) {
         tile = tuned_tile(op, M, K, N);
         if (tile < 0) tile = default_tile(pl);
-        if (tile < 0) return FBL_ERR_UNSUPPORTED;
     }
-    if (!tile_runs(tile, pl)) return FBL_ERR_UNSUPPORTED;
     const hipError_t e = fbl::launch_proj_gemm(pl.a_kmajor, pl.b_nmajor, tile, pl.p, static_cast<hipStream_t>(stream));
     return e == hipSuccess ? FBL_OK : FBL_ERR_HIP;
 }
@@ -562,8 +585,9 @@ fbl_status fbl_proj_tune(uint32_t op, int64_t M, int64_t K, int64_t N, const voi
     int32_t pick = -1;
     double pick_score = 0;
     fbl_status out = FBL_OK;
+    const uint64_t cand = candidate_set(pl);
     for (int t = 0; t < fbl::kGemmTileCount && out == FBL_OK; ++t) {
-        if (!tile_candidate(t, pl)) continue;
+        if (!(cand >> t & 1)) continue;
         hipError_t e = fbl::launch_proj_gemm(pl.a_kmajor, pl.b_nmajor, t, pl.p, s);  // warm-up
         if (e == hipSuccess) e = hipEventRecord(e0, s);
         for (int r = 0; r < reps && e == hipSuccess; ++r) e = fbl::launch_proj_gemm(pl.a_kmajor, pl.b_nmajor, t, pl.p, s);
@@ -582,9 +606,9 @@ fbl_status fbl_proj_tune(uint32_t op, int64_t M, int64_t K, int64_t N, const voi
             // staged bytes: each row block of A is read once per column block
             // of the output and each column block of B once per row block
             const fbl::GemmTile& g = fbl::kGemmTiles[t];
-            const double staged = 2.0 * ((double)pl.orows * pl.kc * (double)(pl.ocols / g.bn) +
-                                         (double)pl.kc * pl.ocols * (double)(pl.orows / g.bm) +
-                                         (double)pl.orows * pl.ocols);
+            const double staged =
+                2.0 * ((double)pl.orows * pl.kc * (double)((pl.ocols + g.bn - 1) / g.bn) +
+                       (double)pl.kc * pl.ocols * (double)((pl.orows + g.bm - 1) / g.bm) + (double)pl.orows * pl.ocols);
             score = flops / (avg * 1e-3) * (min_bytes / staged);
         }
         if (pick < 0 || score > pick_score) pick = t, pick_score = score;

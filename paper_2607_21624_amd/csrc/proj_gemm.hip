@@ -20,6 +20,13 @@
 // 8g .. 8g+7 of a 16-element chunk, in order, so any pair of them forms a
 // consistent MFMA operand pair.
 //
+// Extents need not be multiples of the tile.  Operand rows past the end of
+// an operand read as zeros (buffer resources bound each operand's span);
+// columns past an operand's width read whatever follows in memory, which
+// only ever meets output rows/columns that are not stored -- and, along the
+// contraction, the positions of a partial last step, which are zeroed in LDS
+// before that step's products.
+//
 // Workgroup (gemm_tiles.hpp): a WM x WN grid of wavefront tiles over a
 // BM x BN output tile, each computed by WK wavefronts that split every step's
 // contraction; BK-deep steps through NS LDS stages (NS - 1 in flight).  The
@@ -27,6 +34,7 @@
 // fixed order.  The products accumulate C^T tiles (lane <-> m, in-lane n), so
 // each lane stores four consecutive outputs of a row.
 #include <array>
+#include <type_traits>
 #include <utility>
 
 #include "cdna4.hpp"
@@ -99,12 +107,12 @@ proj_gemm_bf16(GemmArgs p) {
     const int g = lane >> 5;
     // wavefront position: (wm, wn) in the tile grid, wk = its share of each step
     const int wm = wave % WM, wn = (wave / WM) % WN, wk = wave / (WM * WN);
-    const int mt = p.M / BM, nt = p.N / BN;
+    const int mt = (p.M + BM - 1) / BM, nt = (p.N + BN - 1) / BN;
     // consecutive ids share a column block of B (the weight) and land on one XCD
     const int logical = xcd_logical_id(blockIdx.x, mt * nt, gridDim.x);
     if (logical < 0) return;
     const int m0 = (logical % mt) * BM, n0 = (logical / mt) * BN;
-    const int nk = p.K / BK;
+    const int nk = (p.K + BK - 1) / BK;
 
     // ---- DMA: each stage holds the A and B tiles of one BK-deep step
     const Rsrc ra = make_rsrc(p.a, p.a_bytes), rb = make_rsrc(p.b, p.b_bytes);
@@ -194,12 +202,47 @@ proj_gemm_bf16(GemmArgs p) {
     };
     static_assert(NS <= 5, "wait_step covers at most three steps in flight behind the awaited one");
     for (int s = 0; s < NS - 1 && s < nk; ++s) issue(s, s);
+    // The last step may hold the end of the contraction (krem < BK elements
+    // left, a multiple of 8).  Once its tiles have landed, the workgroup
+    // zeroes their contraction positions krem .. BK-1 in LDS (whatever the
+    // loads brought there: zeros past an operand's last row, or the next
+    // row's elements past its width), so the products run unchanged.
+    auto zero_tail = [&](uint32_t stage, int krem) __attribute__((always_inline)) {
+        const int tid = threadIdx.x;
+        constexpr int NT = 64 * C::NW;
+        const f32x4 z = f32x4{};
+        // operand tile with the contraction along its stored rows (AT / not BT): whole rows
+        auto rows = [&](uint32_t tile, int cols) __attribute__((always_inline)) {
+            const int n16 = (BK - krem) * cols / 8;  // 16-byte chunks past row krem
+            for (int i = tid; i < n16; i += NT)
+                *(FBL_LDS f32x4*)(uintptr_t)(tile + (uint32_t)(krem * cols * 2 + i * 16)) = z;
+        };
+        // operand tile with the contraction along its stored columns: chunks krem/8 .. of every row
+        auto cols = [&](uint32_t tile, int nrows, auto geom) __attribute__((always_inline)) {
+            using G = decltype(geom);
+            const int per = (BK - krem) / 8;
+            for (int i = tid; i < nrows * per; i += NT) {
+                const int r = i / per, c = krem / 8 + i % per;
+                *(FBL_LDS f32x4*)(uintptr_t)(tile + 2u * (uint32_t)G::off(r, 8 * c)) = z;
+            }
+        };
+        const uint32_t ta = lds + stage, tb = lds + stage + C::SA;
+        if constexpr (AT) rows(ta, BM);
+        else cols(ta, BM, typename TA::G{});
+        if constexpr (BT) cols(tb, BN, typename TB::G{});
+        else rows(tb, BN);
+    };
     int buf = 0;
+    const int nfull = p.K / BK;  // steps wholly inside the contraction
     for (int s = 0; s < nk; ++s) {
         wait_step(s);
         __syncthreads();
         if (s + NS - 1 < nk) issue(s + NS - 1, buf == 0 ? NS - 1 : buf - 1);
         const uint32_t stage = (uint32_t)buf * C::STAGE;
+        if (s == nfull) {  // the partial last step (every load of it has landed: nothing is in flight)
+            zero_tail(stage, p.K - s * BK);
+            __syncthreads();
+        }
 #pragma unroll
         for (int j = 0; j < KCW; ++j) {
             Frag<bf16> fa[TM], fb[TN];
@@ -256,8 +299,12 @@ proj_gemm_bf16(GemmArgs p) {
         }
     }
 
-    // C[m][n .. n+3]: lane <-> m, four consecutive n per store
-    bf16* cbase = static_cast<bf16*>(p.c);
+    // C[m][n .. n+3]: lane <-> m, four consecutive n per store (N is a
+    // multiple of 4, so a store is wholly inside or wholly outside).  Stores
+    // outside the output go to an offset past the buffer's range, which the
+    // hardware drops -- no divergent branches around the stores.
+    using i32x2 = int __attribute__((ext_vector_type(2)));
+    const __amdgpu_buffer_rsrc_t crs = __builtin_amdgcn_make_buffer_rsrc(p.c, 0, (int)p.c_bytes, 0x00020000);
 #pragma unroll
     for (int tm = 0; tm < TM; ++tm) {
         const int m = m0 + (wm * TM + tm) * 32 + (lane & 31);
@@ -266,8 +313,10 @@ proj_gemm_bf16(GemmArgs p) {
 #pragma unroll
             for (int rr = 0; rr < 4; ++rr) {
                 const int n = n0 + (wn * TN + tn) * 32 + 8 * rr + 4 * g;
-                store4(cbase + (int64_t)m * p.ldc + n, acc[tn][tm][4 * rr], acc[tn][tm][4 * rr + 1],
-                       acc[tn][tm][4 * rr + 2], acc[tn][tm][4 * rr + 3]);
+                const uint32_t off = m < p.M && n < p.N ? (uint32_t)(((int64_t)m * p.ldc + n) * 2) : 0x80000000u;
+                const bf16x4 v = bf16x4{(bf16)acc[tn][tm][4 * rr], (bf16)acc[tn][tm][4 * rr + 1],
+                                        (bf16)acc[tn][tm][4 * rr + 2], (bf16)acc[tn][tm][4 * rr + 3]};
+                __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(i32x2, v), crs, off, 0, 0);
             }
     }
 }
@@ -280,7 +329,7 @@ hipError_t launch_id(const GemmArgs& p, hipStream_t stream) {
     static const hipError_t once = hipFuncSetAttribute(reinterpret_cast<const void*>(kernel),
                                                        hipFuncAttributeMaxDynamicSharedMemorySize, C::BYTES);
     if (once != hipSuccess) return once;
-    const int tiles = (p.M / t.bm) * (p.N / t.bn);
+    const int tiles = ((p.M + t.bm - 1) / t.bm) * ((p.N + t.bn - 1) / t.bn);
     hipLaunchKernelGGL(kernel, dim3((tiles + 7) / 8 * 8), dim3(64 * C::NW), C::BYTES, stream, p);
     return hipGetLastError();
 }

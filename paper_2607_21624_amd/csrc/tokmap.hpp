@@ -75,7 +75,7 @@ struct GemmArgs {
     void* c;
     int64_t lda, ldb, ldc;
     int M, N, K;
-    uint32_t a_bytes, b_bytes;
+    uint32_t a_bytes, b_bytes, c_bytes;  // spans of the operands and the result (< 2 GiB)
 };
 
 }  // namespace fbl

@@ -323,11 +323,11 @@ def test_proj_rejections():
     assert P(E.FBL_PROJ_BWD_DATA, 64, 64, 128, lda=64) == E.FBL_ERR_LAYOUT  # dY rows hold N
     assert P(E.FBL_PROJ_FWD, 64, 64, 64, a=FAKE + 2) == E.FBL_ERR_ALIGN
     assert P(E.FBL_PROJ_FWD, 64, 64, 64, lda=4100) == E.FBL_ERR_ALIGN  # row not 16-byte aligned
-    assert P(E.FBL_PROJ_FWD, 64, 48, 64) == E.FBL_ERR_UNSUPPORTED     # contraction not a multiple of 32
-    assert P(E.FBL_PROJ_FWD, 96, 64, 64) == E.FBL_ERR_UNSUPPORTED     # output rows not a multiple of 64
-    assert P(E.FBL_PROJ_FWD, 64, 64, 64, tile=E.FBL_GEMM_TILE_128x128) == E.FBL_ERR_UNSUPPORTED
-    assert P(E.FBL_PROJ_FWD, 64, 32, 64, tile=7) == E.FBL_ERR_UNSUPPORTED  # 64-deep steps, contraction 32
-    assert P(E.FBL_PROJ_FWD, 64, 64, 64, tile=13) == E.FBL_ERR_ARG    # no such tile id
+    assert P(E.FBL_PROJ_FWD, 64, 60, 64) == E.FBL_ERR_UNSUPPORTED     # contraction not a multiple of 8
+    assert P(E.FBL_PROJ_BWD_WEIGHT, 100, 64, 64) == E.FBL_ERR_UNSUPPORTED  # contraction M = 100
+    assert P(E.FBL_PROJ_FWD, 64, 64, 66, ldc=4104) == E.FBL_ERR_UNSUPPORTED  # output columns not a multiple of 4
+    assert P(E.FBL_PROJ_BWD_DATA, 64, 66, 64) == E.FBL_ERR_UNSUPPORTED  # dX columns K = 66
+    assert P(E.FBL_PROJ_FWD, 64, 64, 64, tile=17) == E.FBL_ERR_ARG    # no such tile id
     assert P(E.FBL_PROJ_FWD, 64, 64, 64, tile=-2) == E.FBL_ERR_ARG
     assert P(E.FBL_PROJ_FWD, 64, 64, 64, c=FAKE + 64) == E.FBL_ERR_ARG  # output overlaps an input
 
@@ -337,7 +337,7 @@ def test_gemm_tile_table():
     named output shapes, LDS within the 160 KB of a CU, and the contraction
     split and wavefront grid consistent with the output tile."""
     tiles = fbl.gemm_tiles()
-    assert len(tiles) == 13 and fbl.LIB.fbl_gemm_tile_count() == 13
+    assert len(tiles) == 17 and fbl.LIB.fbl_gemm_tile_count() == 17
     named = {F.FBL_GEMM_TILE_128x128: (128, 128), F.FBL_GEMM_TILE_128x64: (128, 64),
              F.FBL_GEMM_TILE_64x128: (64, 128), F.FBL_GEMM_TILE_64x64: (64, 64)}
     for t, (bm, bn) in named.items():
@@ -350,29 +350,35 @@ def test_gemm_tile_table():
         partial = (g["wk"] - 1) * g["bm"] * g["bn"] * 4
         assert g["lds_bytes"] == max(stages, partial) <= 160 * 1024
     info = (ctypes.c_int32 * 8)()
-    assert fbl.LIB.fbl_gemm_tile_info(13, info) == F.FBL_ERR_ARG
+    assert fbl.LIB.fbl_gemm_tile_info(17, info) == F.FBL_ERR_ARG
     assert fbl.LIB.fbl_gemm_tile_info(0, None) == F.FBL_ERR_NULL
 
 
 def test_proj_candidates_filters():
-    """C3 keeps only tiles that divide the product exactly; C2 drops staged
-    rows that are not whole 128-byte lines: a 32-deep step stages 64-byte rows
-    of a row-read operand, so the forward and data-gradient products (row-read
-    A) lose the 32-deep tiles while the weight gradient (both operands read
-    transposed, rows of bm or bn elements) keeps them."""
+    """C2 keeps staged rows that are whole 128-byte lines (or span the whole
+    stored row of a narrower operand); C3 keeps tiles that pad every extent by
+    at most 10%, and falls back to the least padded volume.  At 512 x 2048 x
+    8192: the forward (A row-read: bk elements per row; B row-read: bn) keeps
+    bk >= 64 and bn >= 64; the data gradient (both operands staged with bk
+    per row) keeps bk >= 64; the weight gradient (both transposed: bm, bn per
+    row) keeps bm >= 64 and bn >= 64."""
     tiles = fbl.gemm_tiles()
     M, K, N = 512, 2048, 8192
     fwd = fbl.proj_candidates(F.FBL_PROJ_FWD, M, K, N)
-    bwd_w = fbl.proj_candidates(F.FBL_PROJ_BWD_WEIGHT, M, K, N)
-    assert fwd == fbl.proj_candidates(F.FBL_PROJ_BWD_DATA, M, K, N)
-    assert fwd == [t for t in sorted(tiles) if tiles[t]["bk"] >= 64]
-    assert bwd_w == sorted(tiles)
-    # only the 64 x 64 output tile divides a 64 x 64 product; only 64-deep steps a contraction of 64
-    assert fbl.proj_candidates(F.FBL_PROJ_FWD, 64, 64, 64) == [7]
-    assert fbl.proj_candidates(F.FBL_PROJ_BWD_WEIGHT, 64, 64, 64) == [3, 7]
-    # 192 output rows: no 128-row tile; contraction 96: no 64- or 128-deep step, and 32-deep ones fail C2
-    assert all(tiles[t]["bm"] == 64 for t in fbl.proj_candidates(F.FBL_PROJ_FWD, 192, 128, 256))
-    assert fbl.proj_candidates(F.FBL_PROJ_FWD, 64, 96, 64) == []
+    assert fwd == [t for t in sorted(tiles) if tiles[t]["bk"] >= 64 and tiles[t]["bn"] >= 64]
+    assert fbl.proj_candidates(F.FBL_PROJ_BWD_DATA, M, K, N) == [t for t in sorted(tiles) if tiles[t]["bk"] >= 64]
+    assert fbl.proj_candidates(F.FBL_PROJ_BWD_WEIGHT, M, K, N) == \
+        [t for t in sorted(tiles) if tiles[t]["bm"] >= 64 and tiles[t]["bn"] >= 64]
+    # 192 output rows: 128-row tiles pad by 33%
+    assert all(tiles[t]["bm"] <= 64 for t in fbl.proj_candidates(F.FBL_PROJ_FWD, 192, 128, 256))
+    # contraction 96: every depth pads by 33%; least padded volume among C1/C2 survivors (bk 64 or 128 with
+    # 64 x 64 output; 32-deep steps fail C2 and 32-column tiles stage 64-byte rows of a 128-byte-wide B)
+    assert fbl.proj_candidates(F.FBL_PROJ_FWD, 64, 96, 64) == [7, 9]
+    # LoRA, rank 16: X A (2048 -> 16), H B (16 -> 2048) and the gradients
+    assert fbl.proj_candidates(F.FBL_PROJ_FWD, 512, 2048, 16) == [13, 14, 16]      # narrow output columns
+    assert fbl.proj_candidates(F.FBL_PROJ_FWD, 512, 16, 2048) == [0, 1, 2, 3]      # contraction 16: 32-deep steps
+    assert fbl.proj_candidates(F.FBL_PROJ_BWD_WEIGHT, 512, 16, 2048) == [15]        # dB: 16 output rows
+    assert fbl.proj_candidates(F.FBL_PROJ_BWD_WEIGHT, 512, 2048, 16) == [13, 14]    # dA: 16 output columns
     n = ctypes.c_int32()
     assert fbl.LIB.fbl_proj_candidates(F.FBL_PROJ_FWD, M, K, N, None, 0, ctypes.byref(n)) == F.FBL_OK
     assert n.value == len(fwd)

@@ -27,39 +27,37 @@ def _inputs(M, K, N, seed):
             synth.round_to_bf16(rng.standard_normal((M, N))))
 
 
-SHAPES = [(64, 64, 64), (128, 192, 64), (192, 256, 128), (256, 128, 320), (256, 256, 256), (512, 128, 384)]
+# M, K, N: multiples of the tiles; ragged (no extent a multiple of 32: every tile masks rows and columns and
+# the last step holds a half chunk); LoRA ranks 16 and 8 as the narrow output or the contraction
+SHAPES = [(64, 64, 64), (128, 192, 64), (192, 256, 128), (256, 128, 320), (256, 256, 256), (512, 128, 384),
+          (104, 72, 40), (200, 136, 264), (512, 2048, 16), (512, 16, 2048), (256, 8, 512), (256, 512, 8)]
 
 
-NTILES = 13  # fbl_gemm_tile_count(); tests/test_boundary.py pins it
-
-
-def _runs(info, rows, cols, kc):
-    return rows % info["bm"] == 0 and cols % info["bn"] == 0 and kc % info["bk"] == 0
+NTILES = 17  # fbl_gemm_tile_count(); tests/test_boundary.py pins it
 
 
 @pytest.mark.parametrize("tile", ["auto"] + list(range(NTILES)))
 @pytest.mark.parametrize("M,K,N", SHAPES)
 def test_proj_products_match_oracle(M, K, N, tile):
     """Every tile configuration (output tile, staged depth, wavefront grid and
-    contraction split) on every product; a tile that does not divide the
-    product is refused with FBL_ERR_UNSUPPORTED."""
+    contraction split) on every product and shape, whether or not the tile
+    divides the extents (partial tiles are masked)."""
     import torch
     fbl = _lib()
-    tiles = fbl.gemm_tiles()
     x, w, dy = _inputs(M, K, N, M + 3 * K + 7 * N)
     X, W, dY = to_dev(x, "bf16"), to_dev(w, "bf16"), to_dev(dy, "bf16")
     note(f"proj M={M} K={K} N={N} tile={tile}")
-    cases = [(fbl.FBL_PROJ_FWD, X, W, oracle.proj_fwd(x, w), K),
-             (fbl.FBL_PROJ_BWD_DATA, dY, W, oracle.proj_bwd_data(dy, w), N),
-             (fbl.FBL_PROJ_BWD_WEIGHT, X, dY, oracle.proj_bwd_weight(x, dy), M)]
+    cases = [(fbl.FBL_PROJ_FWD, X, W, oracle.proj_fwd(x, w)),
+             (fbl.FBL_PROJ_BWD_DATA, dY, W, oracle.proj_bwd_data(dy, w)),
+             (fbl.FBL_PROJ_BWD_WEIGHT, X, dY, oracle.proj_bwd_weight(x, dy))]
     t = fbl.FBL_GEMM_TILE_AUTO if tile == "auto" else tile
-    for op, a, b, ref, kc in cases:
-        if tile != "auto" and not _runs(tiles[tile], *ref.shape, kc):
-            with pytest.raises(fbl.FblError) as err:
-                fbl.proj(op, a, b, tile=t)
-            assert err.value.status == fbl.fbl.FBL_ERR_UNSUPPORTED
-            continue
-        got = fbl.proj(op, a, b, tile=t)
+    for op, a, b, ref in cases:
+        # the output, poisoned, also checks that nothing is written past its extent
+        out = torch.full((ref.shape[0] + 8, ref.shape[1] + 8), float("nan"), dtype=torch.bfloat16, device="cuda")
+        got = fbl.proj(op, a, b, out=out[:ref.shape[0], :ref.shape[1]], tile=t)
+        torch.cuda.synchronize()
+        rest = torch.cat([out[ref.shape[0]:].flatten(), out[:ref.shape[0], ref.shape[1]:].flatten()])
+        assert torch.isnan(rest.float()).all(), f"op {op} tile {tile}: wrote outside the output"
         torch.cuda.synchronize()
         assert got.shape == ref.shape
         e = rel_err(to_np(got), ref)
@@ -156,3 +154,36 @@ def test_proj_tune_picks_a_measured_candidate(objective):
         assert torch.equal(auto, explicit)
     fbl.proj_tune_reset()
     assert fbl.proj_tuned_tile(fbl.FBL_PROJ_FWD, M, K, N) == -1
+
+
+@pytest.mark.parametrize("r", [8, 16, 64])
+def test_lora_chain(r):
+    """A LoRA adapter on a frozen projection (section 2.2's example): H = X A,
+    Y = X W + H B, and the backward dB = H^T dY, dH = dY B^T, dA = X^T dH,
+    dX = dY W^T + dH A^T -- eight products at rank r on token-major operands,
+    against the fp64 oracle's chain (the GPU rounds H and dH to bf16 between
+    products)."""
+    import torch
+    fbl = _lib()
+    M, K, N = 512, 1024, 1536
+    rng = np.random.default_rng(300 + r)
+    bf = lambda *s: synth.round_to_bf16(rng.standard_normal(s))
+    x, w, a_, b_, dy = bf(M, K), bf(K, N), bf(K, r), bf(r, N), bf(M, N)
+    X, W, A, B, dY = (to_dev(t, "bf16") for t in (x, w, a_, b_, dy))
+    note(f"lora chain r={r}")
+    H = fbl.proj(fbl.FBL_PROJ_FWD, X, A)
+    Y = fbl.proj(fbl.FBL_PROJ_FWD, X, W).float() + fbl.proj(fbl.FBL_PROJ_FWD, H, B).float()
+    dB = fbl.proj(fbl.FBL_PROJ_BWD_WEIGHT, H, dY)
+    dH = fbl.proj(fbl.FBL_PROJ_BWD_DATA, dY, B)
+    dA = fbl.proj(fbl.FBL_PROJ_BWD_WEIGHT, X, dH)
+    dX = fbl.proj(fbl.FBL_PROJ_BWD_DATA, dY, W).float() + fbl.proj(fbl.FBL_PROJ_BWD_DATA, dH, A).float()
+    torch.cuda.synchronize()
+    h = oracle.proj_fwd(x, a_)
+    dh = oracle.proj_bwd_data(dy, b_)
+    refs = {"H": (H, h), "Y": (Y, oracle.proj_fwd(x, w) + oracle.proj_fwd(h, b_)),
+            "dB": (dB, oracle.proj_bwd_weight(h, dy)), "dH": (dH, dh),
+            "dA": (dA, oracle.proj_bwd_weight(x, dh)),
+            "dX": (dX, oracle.proj_bwd_data(dy, w) + oracle.proj_bwd_data(dh, a_))}
+    for name, (got, ref) in refs.items():
+        assert got.shape == ref.shape, name
+        assert rel_err(to_np(got), ref) <= TOL, name
