@@ -26,6 +26,10 @@ if ROOT not in sys.path:
 
 PEAK_BF16_TFLOPS = 2516.6   # dense MFMA, 256 CU x 4096 flop/clk x 2.4 GHz
 PEAK_F32_TFLOPS = 157.3
+# bf16 32x32x16 MFMA rate measured by a probe kernel on this part (4+ independent
+# accumulators, operands held constant); with random operands the chip's power
+# limit lowers the clock (a large library GEMM runs about 30% slower than on zeros)
+MEASURED_BF16_TFLOPS = 2450.0
 PEAK_HBM_GBS = 8000.0
 
 
@@ -194,6 +198,95 @@ def bench_proj(args, fbl, torch, np):
     }), flush=True)
 
 
+def bench_block(args, fbl, torch, np):
+    """A whole attention block, forward and backward, with no layout copy: the
+    QKV projection writes one packed [B*S, (Hq + 2Hkv) d] buffer, attention
+    reads Q, K, V from it in place and writes dQ, dK, dV into a packed
+    gradient buffer, and the output projection and both weight gradients read
+    the token-major activations as they are.  Llama-7B-like layer (B=1,
+    S=4096, 32 heads of 128, causal) unless --workload names another
+    self-attention shape.  value = algorithmic FLOPs of the eight projection
+    products and the attention step, over the timed step."""
+    import synth
+    w = synth.WORKLOADS[args.workload]
+    if w.dtype != "bf16" or w.Skv != w.S or w.mask & synth.MASK_KEY_PADDING:
+        raise SystemExit("--op block takes a bf16 self-attention workload without key padding")
+    B, S, Hq, Hkv, d = w.B, w.S, w.Hq, w.Hkv, w.d
+    causal = bool(w.mask & synth.MASK_CAUSAL)
+    Dm, P, M = Hq * d, (Hq + 2 * Hkv) * d, B * S
+    g = torch.Generator(device="cpu").manual_seed(0)
+    mk = lambda r, c, sc=1.0: (sc * torch.randn(r, c, generator=g)).to(device="cuda", dtype=torch.bfloat16)
+    X, dY = mk(M, Dm), mk(M, Dm)
+    Wqkv, Wo = mk(Dm, P, 1 / math.sqrt(Dm)), mk(Hq * d, Dm, 1 / math.sqrt(Hq * d))
+    qkv = torch.empty(M, P, dtype=torch.bfloat16, device="cuda")
+    o3 = torch.empty(B, S, Hq * d, dtype=torch.bfloat16, device="cuda")
+    lse = torch.empty(B, Hq, S, dtype=torch.float32, device="cuda")
+    Y, dO = torch.empty(M, Dm, dtype=torch.bfloat16, device="cuda"), torch.empty(M, Hq * d, dtype=torch.bfloat16, device="cuda")
+    dWo, dqkv = torch.empty(Hq * d, Dm, dtype=torch.bfloat16, device="cuda"), torch.empty(M, P, dtype=torch.bfloat16, device="cuda")
+    dX, dWqkv = torch.empty(M, Dm, dtype=torch.bfloat16, device="cuda"), torch.empty(Dm, P, dtype=torch.bfloat16, device="cuda")
+    qkv3, dqkv3, o = qkv.view(B, S, P), dqkv.view(B, S, P), o3.view(M, Hq * d)
+    lq, lk, _, _, _, _ = fbl.fbl._packed(qkv3, Hq, Hkv)
+    ws = torch.empty(fbl.fbl_attn_bwd_workspace(lq, lk), dtype=torch.uint8, device="cuda")
+    stream = torch.cuda.current_stream()
+    stages = [
+        ("qkv_proj", lambda: fbl.proj(fbl.FBL_PROJ_FWD, X, Wqkv, out=qkv)),
+        ("attn_fwd", lambda: fbl.attn_fwd_packed(qkv3, Hq, Hkv, causal=causal, out=o3, lse=lse)),
+        ("out_proj", lambda: fbl.proj(fbl.FBL_PROJ_FWD, o, Wo, out=Y)),
+        ("out_proj_bwd", lambda: (fbl.proj(fbl.FBL_PROJ_BWD_DATA, dY, Wo, out=dO),
+                                  fbl.proj(fbl.FBL_PROJ_BWD_WEIGHT, o, dY, out=dWo))),
+        ("attn_bwd", lambda: fbl.attn_bwd_packed(qkv3, o3, dO.view(B, S, Hq * d), lse, Hq, Hkv, causal=causal,
+                                                 dqkv=dqkv3, workspace=ws)),
+        ("qkv_proj_bwd", lambda: (fbl.proj(fbl.FBL_PROJ_BWD_DATA, dqkv, Wqkv, out=dX),
+                                  fbl.proj(fbl.FBL_PROJ_BWD_WEIGHT, X, dqkv, out=dWqkv))),
+    ]
+
+    def step(ev=None):
+        for i, (_, f) in enumerate(stages):
+            if ev is not None:
+                ev[i].record(stream)
+            f()
+        if ev is not None:
+            ev[-1].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    mem_before = torch.cuda.memory_allocated()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(stages) + 1)] for _ in range(args.steps)]
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record(stream)
+    for i in range(args.steps):
+        step(evs[i])
+    stop.record(stream)
+    torch.cuda.synchronize()
+    assert torch.cuda.memory_allocated() == mem_before, "the timed steps allocated device memory"
+    ms_per_step = start.elapsed_time(stop) / args.steps
+    stage_ms = {n: round(float(np.mean([e[i].elapsed_time(e[i + 1]) for e in evs])), 4)
+                for i, (n, _) in enumerate(stages)}
+    pairs = B * Hq * (S * (S + 1) // 2 if causal else S * S)
+    proj_flops = 3 * 2.0 * M * Dm * P + 3 * 2.0 * M * (Hq * d) * Dm
+    attn_flops = 14.0 * d * pairs
+    flops = proj_flops + attn_flops
+    tflops = flops / (ms_per_step * 1e-3) / 1e12
+    kernels = None if args.no_kernel_list else dispatched_kernels(step)
+    foreign = None if kernels is None else [n for n in kernels if not any(t in n for t in ("attn_", "proj_gemm"))]
+    print(json.dumps({
+        "metric": "attention block fwd+bwd (QKV projection, attention, output projection) TFLOP/s at 1 GPU; "
+                  "layout-copy bytes (=0)",
+        "value": round(tflops, 2), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic (seeded N(0,1) activations and gradients, scaled N(0,1) weights)",
+        "config": {"workload": f"attention block, {w.name} shape", "B": B, "S": S, "Hq": Hq, "Hkv": Hkv, "d": d,
+                   "model_width": Dm, "qkv_width": P, "mask": "causal" if causal else "none",
+                   "layout": "token-major; packed QKV"},
+        "pct_peak": round(100 * tflops / PEAK_BF16_TFLOPS, 2),
+        "stage_ms": stage_ms,
+        "algorithmic_gflop": {"projections": round(proj_flops / 1e9, 2), "attention": round(attn_flops / 1e9, 2)},
+        "layout_copy_bytes": 0 if foreign == [] else None,
+        "dispatched_kernels": kernels,
+    }), flush=True)
+
+
 def dispatched_kernels(step):
     """Kernel names dispatched by one step (torch profiler; None if unavailable)."""
     try:
@@ -218,9 +311,10 @@ def main():
     ap.add_argument("--no-kernel-list", action="store_true",
                     help="skip the torch-profiler dispatch listing (use under rocprofv3)")
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle work for cpu_baseline")
-    ap.add_argument("--op", default="attention", choices=["attention", "proj"],
+    ap.add_argument("--op", default="attention", choices=["attention", "proj", "block"],
                     help="attention: the fwd+bwd step (default); proj: the projection products Y = X W, dX = dY W^T, "
-                         "dW = X^T dY on token-major activations, every tile shape")
+                         "dW = X^T dY on token-major activations, every tile shape; block: a whole attention block "
+                         "(QKV projection into a packed buffer, attention in place, output projection) fwd+bwd")
     ap.add_argument("--proj-shape", default="512,2048,8192", help="M,K,N for --op proj")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="instead of attention, run 5 plain device copies of this many MiB (calibrates the HBM "
@@ -250,6 +344,9 @@ def main():
 
     if args.op == "proj":
         bench_proj(args, fbl, torch, np)
+        return
+    if args.op == "block":
+        bench_block(args, fbl, torch, np)
         return
 
     w = {**synth.WORKLOADS, **synth.CROSS_WORKLOADS}[args.workload]
@@ -306,6 +403,9 @@ def main():
     k_stats = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
     k_kv = float(np.mean([e[2].elapsed_time(e[3]) for e in evs]))
     k_q = float(np.mean([e[3].elapsed_time(e[4]) for e in evs]))
+    step_each = np.array([e[0].elapsed_time(e[4]) for e in evs])   # each step, first to last launch
+    fwd_each = np.array([e[0].elapsed_time(e[1]) for e in evs])
+    bwd_each = step_each - fwd_each
     assert torch.cuda.memory_allocated() == mem_before, "the timed steps allocated device memory"
 
     pairs = allowed_pairs(w, inp["kv_len"])
@@ -334,7 +434,11 @@ def main():
     roofline = {"bound": "mfma", "achieved": round(ktf[dom], 2), "peak": peak, "unit": "TFLOP/s",
                 "frac": round(ktf[dom] / peak, 4), "traffic": dom_traffic, "kernel": dom,
                 "avg_launch_ms": round(t_dom, 4), "flops_per_launch": a_dom * w.d * pairs,
-                "algorithmic_bytes_per_launch": alg_bytes[dom]}
+                "algorithmic_bytes_per_launch": alg_bytes[dom],
+                # the paper's MemEfficiency (section 4.2): minimal over measured bytes
+                "mem_efficiency": None if dom_traffic is None else round(alg_bytes[dom] / dom_traffic, 3)}
+    stat = lambda x: {"median": round(float(np.median(x)), 4), "min": round(float(np.min(x)), 4),
+                      "max": round(float(np.max(x)), 4)}
 
     kernels = None if args.no_kernel_list else dispatched_kernels(step)
     foreign = None
@@ -362,6 +466,9 @@ def main():
                    "mask": {0: "none", 1: "causal", 2: "key_padding", 3: "causal+key_padding"}[w.mask],
                    "layout": "token-major [B,S,H*d]", "parallelism": "single GPU"},
         "pct_peak": round(100 * tflops / peak, 2),
+        # against the bf16 MFMA rate a probe kernel reaches on this part (operands held constant)
+        "pct_measured_mfma_peak": round(100 * tflops / MEASURED_BF16_TFLOPS, 2) if w.dtype == "bf16" else None,
+        "ms": {"step": stat(step_each), "fwd": stat(fwd_each), "bwd": stat(bwd_each)},
         "layout_copy_bytes": 0 if foreign == [] else None,
         "dispatched_kernels": kernels,
         "kernel_ms": {"attn_fwd": round(k_fwd, 4), "attn_bwd_stats": round(k_stats, 4), "attn_bwd_kv": round(k_kv, 4),
@@ -375,6 +482,7 @@ def main():
         "algorithmic_bytes": alg_bytes["total"],
         "roofline": roofline,
         "cpu_baseline": cpu,
+        "gpu_over_oracle": None if cpu is None else round(tflops / cpu["value"], 1),
     }
     print(json.dumps(line), flush=True)
 
