@@ -33,6 +33,9 @@ constexpr GemmTile kGemmTiles[] = {
     {64, 32, 128, 3, 2, 1, 2},   // 14: each wavefront 32 x 32 on half
     {32, 128, 64, 3, 1, 4, 1},   // 15
     {32, 32, 128, 3, 1, 1, 4},   // 16: each wavefront the whole 32 x 32 on a quarter
+    // large products: 4 wavefronts of 128 x 128 (the accumulators fill the AGPRs)
+    {256, 256, 32, 4, 2, 2, 1},  // 17
+    {256, 256, 64, 2, 2, 2, 1},  // 18
 };
 constexpr int kGemmTileCount = (int)(sizeof(kGemmTiles) / sizeof(kGemmTiles[0]));
 

@@ -86,7 +86,10 @@ struct GemmCfg {
     static_assert(BM % (32 * WM) == 0 && BN % (32 * WN) == 0, "wavefront tiles of whole 32x32 blocks");
     static_assert(BK % 32 == 0 && NKC % WK == 0 && NS >= 2, "whole chunks per wavefront, at least double buffered");
     static_assert(NW == 4 || NW == 8, "4 or 8 wavefronts");
-    static_assert(STAGE < 65536, "in-stage offsets fit the 16-bit LDS immediate");
+    // stage offsets are added at run time; the read immediates are tile offsets within a stage
+    static_assert((TM - 1) * 32 * BK * 2 < 65536 && (TN - 1) * 32 * BK * 2 < 65536 &&
+                      (KCW - 1) * 16 * (BM > BN ? BM : BN) * 2 + 128 < 65536,
+                  "LDS read immediates fit 16 bits");
     static_assert(BYTES <= 160 * 1024 && NS * STAGE <= BYTES && (WK - 1) * WM * WN * PART <= BYTES, "LDS");
     static_assert((NS - 1) * LOADS < 64, "vmcnt range");
     static constexpr int OCC = (NW == 4 && BYTES <= 80 * 1024) ? 2 : 1;

@@ -327,7 +327,7 @@ def test_proj_rejections():
     assert P(E.FBL_PROJ_BWD_WEIGHT, 100, 64, 64) == E.FBL_ERR_UNSUPPORTED  # contraction M = 100
     assert P(E.FBL_PROJ_FWD, 64, 64, 66, ldc=4104) == E.FBL_ERR_UNSUPPORTED  # output columns not a multiple of 4
     assert P(E.FBL_PROJ_BWD_DATA, 64, 66, 64) == E.FBL_ERR_UNSUPPORTED  # dX columns K = 66
-    assert P(E.FBL_PROJ_FWD, 64, 64, 64, tile=17) == E.FBL_ERR_ARG    # no such tile id
+    assert P(E.FBL_PROJ_FWD, 64, 64, 64, tile=19) == E.FBL_ERR_ARG    # no such tile id
     assert P(E.FBL_PROJ_FWD, 64, 64, 64, tile=-2) == E.FBL_ERR_ARG
     assert P(E.FBL_PROJ_FWD, 64, 64, 64, c=FAKE + 64) == E.FBL_ERR_ARG  # output overlaps an input
 
@@ -337,7 +337,7 @@ def test_gemm_tile_table():
     named output shapes, LDS within the 160 KB of a CU, and the contraction
     split and wavefront grid consistent with the output tile."""
     tiles = fbl.gemm_tiles()
-    assert len(tiles) == 17 and fbl.LIB.fbl_gemm_tile_count() == 17
+    assert len(tiles) == 19 and fbl.LIB.fbl_gemm_tile_count() == 19
     named = {F.FBL_GEMM_TILE_128x128: (128, 128), F.FBL_GEMM_TILE_128x64: (128, 64),
              F.FBL_GEMM_TILE_64x128: (64, 128), F.FBL_GEMM_TILE_64x64: (64, 64)}
     for t, (bm, bn) in named.items():
@@ -350,7 +350,7 @@ def test_gemm_tile_table():
         partial = (g["wk"] - 1) * g["bm"] * g["bn"] * 4
         assert g["lds_bytes"] == max(stages, partial) <= 160 * 1024
     info = (ctypes.c_int32 * 8)()
-    assert fbl.LIB.fbl_gemm_tile_info(17, info) == F.FBL_ERR_ARG
+    assert fbl.LIB.fbl_gemm_tile_info(19, info) == F.FBL_ERR_ARG
     assert fbl.LIB.fbl_gemm_tile_info(0, None) == F.FBL_ERR_NULL
 
 
@@ -376,7 +376,7 @@ def test_proj_candidates_filters():
     assert fbl.proj_candidates(F.FBL_PROJ_FWD, 64, 96, 64) == [7, 9]
     # LoRA, rank 16: X A (2048 -> 16), H B (16 -> 2048) and the gradients
     assert fbl.proj_candidates(F.FBL_PROJ_FWD, 512, 2048, 16) == [13, 14, 16]      # narrow output columns
-    assert fbl.proj_candidates(F.FBL_PROJ_FWD, 512, 16, 2048) == [0, 1, 2, 3]      # contraction 16: 32-deep steps
+    assert fbl.proj_candidates(F.FBL_PROJ_FWD, 512, 16, 2048) == [0, 1, 2, 3, 17]  # contraction 16: 32-deep steps
     assert fbl.proj_candidates(F.FBL_PROJ_BWD_WEIGHT, 512, 16, 2048) == [15]        # dB: 16 output rows
     assert fbl.proj_candidates(F.FBL_PROJ_BWD_WEIGHT, 512, 2048, 16) == [13, 14]    # dA: 16 output columns
     n = ctypes.c_int32()
