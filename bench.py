@@ -208,7 +208,7 @@ def bench_block(args, fbl, torch, np):
     self-attention shape.  value = algorithmic FLOPs of the eight projection
     products and the attention step, over the timed step."""
     import synth
-    w = synth.WORKLOADS[args.workload]
+    w = {**synth.WORKLOADS, **synth.PAPER_MHA_SHAPES}[args.workload]
     if w.dtype != "bf16" or w.Skv != w.S or w.mask & synth.MASK_KEY_PADDING:
         raise SystemExit("--op block takes a bf16 self-attention workload without key padding")
     B, S, Hq, Hkv, d = w.B, w.S, w.Hq, w.Hkv, w.d
@@ -349,7 +349,7 @@ def main():
         bench_block(args, fbl, torch, np)
         return
 
-    w = {**synth.WORKLOADS, **synth.CROSS_WORKLOADS}[args.workload]
+    w = {**synth.WORKLOADS, **synth.CROSS_WORKLOADS, **synth.PAPER_MHA_SHAPES}[args.workload]
     inp = synth.make_inputs(w)
     dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
     dev = lambda x: torch.from_numpy(x).to("cuda").to(dt)

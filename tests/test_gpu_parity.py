@@ -45,7 +45,7 @@ def test_device_index_map_bit_exact(B, S, H, D, row):
 
 # ---------------------------------------------------------- named workloads
 def _check_workload(name, kv_heads=None, seed=None):
-    w = synth.WORKLOADS[name]
+    w = {**synth.WORKLOADS, **synth.PAPER_MHA_SHAPES}[name]
     inp = synth.make_inputs(w, seed=seed)
     note(f"{name} seed={inp['seed']} B={w.B} S={w.S} Hq={w.Hq} Hkv={w.Hkv} d={w.d} {w.dtype} mask={w.mask}")
     got = select_heads(gpu_fwd_bwd(inp), w, kv_heads)
@@ -66,6 +66,13 @@ def test_bert_base_keypad(seed):
 
 def test_gpt2_medium_causal():
     _check_workload("gpt2_medium_causal")
+
+
+@pytest.mark.parametrize("name", list(synth.PAPER_MHA_SHAPES))
+def test_paper_mha_shapes(name):
+    """The three MHA shapes of the paper's own multi-head attention experiment
+    (S = 512, bf16): every head checked."""
+    _check_workload(name)
 
 
 def test_llama32_1b_gqa_sampled_groups():
