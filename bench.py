@@ -311,6 +311,8 @@ def main():
     ap.add_argument("--no-kernel-list", action="store_true",
                     help="skip the torch-profiler dispatch listing (use under rocprofv3)")
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle work for cpu_baseline")
+    ap.add_argument("--graph", action="store_true",
+                    help="time replays of the step captured in a HIP graph (per-kernel times stay eager)")
     ap.add_argument("--op", default="attention", choices=["attention", "proj", "block"],
                     help="attention: the fwd+bwd step (default); proj: the projection products Y = X W, dX = dY W^T, "
                          "dW = X^T dY on token-major activations, every tile shape; block: a whole attention block "
@@ -399,6 +401,7 @@ def main():
     torch.cuda.synchronize()
     total_ms = start.elapsed_time(stop)
     ms_per_step = total_ms / args.steps
+    eager_ms_per_step = ms_per_step
     k_fwd = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
     k_stats = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
     k_kv = float(np.mean([e[2].elapsed_time(e[3]) for e in evs]))
@@ -407,6 +410,25 @@ def main():
     fwd_each = np.array([e[0].elapsed_time(e[1]) for e in evs])
     bwd_each = step_each - fwd_each
     assert torch.cuda.memory_allocated() == mem_before, "the timed steps allocated device memory"
+    if args.graph:
+        # the step's four launches captured once and replayed: no host work per step
+        # (capture and its memory pool come after the eager timing and its no-allocation check)
+        side = torch.cuda.Stream()
+        with torch.cuda.stream(side):
+            step()
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            step()
+        for _ in range(args.warmup):
+            graph.replay()
+        torch.cuda.synchronize()
+        start.record(stream)
+        for _ in range(args.steps):
+            graph.replay()
+        stop.record(stream)
+        torch.cuda.synchronize()
+        ms_per_step = start.elapsed_time(stop) / args.steps
 
     pairs = allowed_pairs(w, inp["kv_len"])
     flops = 14 * w.d * pairs
@@ -460,6 +482,8 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
+        "launch": "hip graph replay" if args.graph else "eager (one host call per launch)",
+        "eager_ms_per_step": round(eager_ms_per_step, 4),
         "dtype": w.dtype,
         "data": "synthetic (seeded N(0,1) token-major Q,K,V,dO)",
         "config": {"workload": w.name, "B": w.B, "S": w.S, "S_kv": w.Skv, "Hq": w.Hq, "Hkv": w.Hkv, "d": w.d,

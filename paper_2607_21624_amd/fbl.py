@@ -247,6 +247,23 @@ def _dtype_code(t) -> int:
     raise FblError(FBL_ERR_DTYPE, f"unsupported tensor dtype {t.dtype}")
 
 
+_LAYOUTS = {}
+
+
+def _layout(t, H: int) -> Layout:
+    """layout_of for the calls below, cached per (dtype, shape, strides, H): the
+    descriptor only depends on those, and building it costs a library call per
+    tensor per launch.  The cached objects are passed read-only (const) and
+    never handed out."""
+    key = (t.dtype, tuple(t.shape), t.stride(), H)
+    l = _LAYOUTS.get(key)
+    if l is None:
+        l = layout_of(t, H)
+        if len(_LAYOUTS) < 4096:
+            _LAYOUTS[key] = l
+    return l
+
+
 def layout_of(t, H: int) -> Layout:
     """Descriptor of a token-major [B, S, H*D] tensor (or a strided view of one:
     inner stride 1, arbitrary row and batch strides).  No data is touched."""
@@ -266,7 +283,7 @@ def attn_fwd(q, k, v, Hq: int, Hkv: int, scale: Optional[float] = None, causal: 
     """Forward on token-major tensors.  Returns (O, LSE); O has q's shape and dtype
     (allocated contiguous unless `out` is given), LSE is float32 [B, Hq, S]."""
     import torch
-    lq, lk, lv = layout_of(q, Hq), layout_of(k, Hkv), layout_of(v, Hkv)
+    lq, lk, lv = _layout(q, Hq), _layout(k, Hkv), _layout(v, Hkv)
     if scale is None:
         scale = 1.0 / math.sqrt(lq.D)
     B, S = q.shape[0], q.shape[1]
@@ -274,7 +291,7 @@ def attn_fwd(q, k, v, Hq: int, Hkv: int, scale: Optional[float] = None, causal: 
         out = torch.empty((B, S, q.shape[2]), dtype=q.dtype, device=q.device)
     if lse is None:
         lse = torch.empty((B, Hq, S), dtype=torch.float32, device=q.device)
-    lo = layout_of(out, Hq)
+    lo = _layout(out, Hq)
     _check(fbl_attn_fwd_raw(lq, q, lk, k, lv, v, lo, out, lse, scale, _mask(causal, kv_len), stream),
            "fbl_attn_fwd")
     return out, lse
@@ -284,8 +301,8 @@ def attn_bwd(q, k, v, o, do, lse, Hq: int, Hkv: int, scale: Optional[float] = No
              kv_len=None, dq=None, dk=None, dv=None, workspace=None, stream=None, phases: int = FBL_BWD_ALL):
     """Backward.  Returns (dQ, dK, dV) with the shapes/dtypes of q, k, v."""
     import torch
-    lq, lk, lv = layout_of(q, Hq), layout_of(k, Hkv), layout_of(v, Hkv)
-    lo, ldo = layout_of(o, Hq), layout_of(do, Hq)
+    lq, lk, lv = _layout(q, Hq), _layout(k, Hkv), _layout(v, Hkv)
+    lo, ldo = _layout(o, Hq), _layout(do, Hq)
     if scale is None:
         scale = 1.0 / math.sqrt(lq.D)
     if dq is None:
@@ -297,7 +314,7 @@ def attn_bwd(q, k, v, o, do, lse, Hq: int, Hkv: int, scale: Optional[float] = No
     if workspace is None:
         need = fbl_attn_bwd_workspace(lq, lk)
         workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
-    ldq, ldk, ldv = layout_of(dq, Hq), layout_of(dk, Hkv), layout_of(dv, Hkv)
+    ldq, ldk, ldv = _layout(dq, Hq), _layout(dk, Hkv), _layout(dv, Hkv)
     _check(fbl_attn_bwd_raw(lq, q, lk, k, lv, v, lo, o, ldo, do, lse, scale, _mask(causal, kv_len), ldq, dq, ldk,
                             dk, ldv, dv, workspace, workspace.numel() * workspace.element_size(), stream,
                             phases), "fbl_attn_bwd")
@@ -334,7 +351,7 @@ def attn_fwd_packed(qkv, Hq: int, Hkv: int, scale: Optional[float] = None, causa
         out = torch.empty((B, S, Hq * lq.D), dtype=qkv.dtype, device=qkv.device)
     if lse is None:
         lse = torch.empty((B, Hq, S), dtype=torch.float32, device=qkv.device)
-    lo = layout_of(out, Hq)
+    lo = _layout(out, Hq)
     _check(fbl_attn_fwd_raw(lq, pq, lk, pk, lv, pv, lo, out, lse, scale, _mask(causal, kv_len), stream),
            "fbl_attn_fwd")
     return out, lse
@@ -353,7 +370,7 @@ def attn_bwd_packed(qkv, o, do, lse, Hq: int, Hkv: int, scale: Optional[float] =
     if dqkv.shape != qkv.shape or dqkv.stride() != qkv.stride() or dqkv.dtype != qkv.dtype:
         raise FblError(FBL_ERR_SHAPE, "dqkv must have qkv's shape, strides and dtype")
     _, _, _, gq, gk, gv = _packed(dqkv, Hq, Hkv)
-    lo, ldo = layout_of(o, Hq), layout_of(do, Hq)
+    lo, ldo = _layout(o, Hq), _layout(do, Hq)
     if workspace is None:
         workspace = torch.empty(fbl_attn_bwd_workspace(lq, lk), dtype=torch.uint8, device=qkv.device)
     _check(fbl_attn_bwd_raw(lq, pq, lk, pk, lv, pv, lo, o, ldo, do, lse, scale, _mask(causal, kv_len), lq, gq, lk,
