@@ -442,9 +442,15 @@ fbl_status proj_plan(uint32_t op, int64_t M, int64_t K, int64_t N, const void* a
     p.M = (int)pl.orows;
     p.N = (int)pl.ocols;
     p.K = (int)pl.kc;
-    p.a_bytes = (uint32_t)sa;
-    p.b_bytes = (uint32_t)sb;
-    p.c_bytes = (uint32_t)sc;
+    // The loads move 16-byte chunks and the hardware drops every dword that
+    // reaches past a resource's range, so a span ending inside a dword (an
+    // odd row width) would lose the operand's last element: the load spans
+    // end at the 16-byte chunk holding it.  Pointers and row strides are
+    // 16-byte aligned, so that chunk is aligned and never crosses a page.
+    const auto chunk_end = [](int64_t n) { return (uint32_t)((n + 15) / 16 * 16); };
+    p.a_bytes = chunk_end(sa);
+    p.b_bytes = chunk_end(sb);
+    p.c_bytes = (uint32_t)sc;  // stores are 4 elements wide and output widths a multiple of 4
     return FBL_OK;
 }
 

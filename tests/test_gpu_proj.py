@@ -187,3 +187,44 @@ def test_lora_chain(r):
     for name, (got, ref) in refs.items():
         assert got.shape == ref.shape, name
         assert rel_err(to_np(got), ref) <= TOL, name
+
+
+# the smallest extents each product accepts: output rows any, output columns a multiple of 4,
+# contraction a multiple of 8
+TINY = [(op, M, K, N) for op, (M, K, N) in
+        [(0, (1, 8, 4)), (0, (5, 24, 12)), (1, (1, 4, 8)), (1, (7, 12, 40)), (2, (8, 1, 4)), (2, (16, 9, 20))]]
+
+
+@pytest.mark.parametrize("tile", ["auto"] + list(range(NTILES)))
+@pytest.mark.parametrize("op,M,K,N", TINY)
+def test_proj_tiny_extents(op, M, K, N, tile):
+    """One token, a handful of columns, a contraction of 8: every tile masks
+    almost all of its rows and columns and zeroes most of its only step."""
+    import torch
+    fbl = _lib()
+    rng = np.random.default_rng(M * 7 + K * 3 + N + op)
+    bf = lambda *s: synth.round_to_bf16(rng.standard_normal(s))
+    if op == 0:
+        a, b = bf(M, K), bf(K, N)
+        ref = oracle.proj_fwd(a, b)
+    elif op == 1:
+        a, b = bf(M, N), bf(K, N)
+        ref = oracle.proj_bwd_data(a, b)
+    else:
+        a, b = bf(M, K), bf(M, N)
+        ref = oracle.proj_bwd_weight(a, b)
+    note(f"proj tiny op={op} M={M} K={K} N={N} tile={tile}")
+    pad8 = lambda n: (n + 7) // 8 * 8   # rows must start on 16-byte boundaries: views of padded buffers
+
+    def view_of(x):
+        buf = torch.zeros((x.shape[0], pad8(x.shape[1])), dtype=torch.bfloat16, device="cuda")
+        buf[:, :x.shape[1]] = to_dev(x, "bf16")
+        return buf[:, :x.shape[1]]
+    out = torch.full((ref.shape[0] + 8, pad8(ref.shape[1]) + 8), float("nan"), dtype=torch.bfloat16, device="cuda")
+    view = out[:ref.shape[0], :ref.shape[1]]
+    t = fbl.FBL_GEMM_TILE_AUTO if tile == "auto" else tile
+    fbl.proj(op, view_of(a), view_of(b), out=view, tile=t)
+    torch.cuda.synchronize()
+    rest = torch.cat([out[ref.shape[0]:].flatten(), out[:ref.shape[0], ref.shape[1]:].flatten()])
+    assert torch.isnan(rest.float()).all(), "wrote outside the output"
+    assert rel_err(to_np(view), ref) <= TOL
