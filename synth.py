@@ -56,7 +56,7 @@ class Workload:
         return self.S_kv or self.S
 
 
-# The five workload shapes the build is measured and checked on.  Names say what
+# The five workload shapes measured and checked.  Names say what
 # each one stands in for; the pretrained models themselves are not used.
 WORKLOADS = {
     "tiny_mha_f32": Workload("tiny_mha_f32", B=1, S=64, Hq=2, Hkv=2, d=32, dtype="f32",
