@@ -8,8 +8,8 @@ result, only without layout copies):
   explicit argument (1/sqrt(d) in every workload here).
 * Heads come from the token-major projection output by the reshape/transpose
   chain of section 4.3.1; query head h reads key/value head floor(h / G) with
-  G = Hq / Hkv (grouped-query attention, the "expansion" the paper names in
-  the same section), i.e. repeat-interleave semantics.
+  G = Hq / Hkv (grouped-query attention, whose K/V expansion the same
+  section mentions), i.e. repeat-interleave semantics.
 * The backward pass is the chain rule applied to these definitions.  The paper
   states the matrix-product gradients (section 4.1, FTD-D; section 4.2: the
   forward reduces along K, the gradients along M or N) and classes softmax as

@@ -14,13 +14,13 @@
 //                   (batch, kv head); each wavefront keeps its 32 K and V rows
 //                   and its dK^T, dV^T accumulators in registers and walks the
 //                   query blocks of every query head of its GQA group.  The
-//                   reductions over queries that build dK/dV (the "reduce
-//                   along M" direction of section 4.2) and the group sum over
+//                   reductions over queries that build dK/dV (the M direction
+//                   of section 4.2's naming) and the group sum over
 //                   the G query heads never leave registers.
 //   attn_bwd_q      query-major.  A workgroup owns 128 queries of one
 //                   (batch, query head) and walks the key tiles, recomputing S
-//                   and dP, and accumulates dQ^T in registers (the "reduce
-//                   along N" direction).
+//                   and dP, and accumulates dQ^T in registers (the N
+//                   direction).
 // Recomputing S and dP in the query-major pass costs two extra products per
 // (query, key) pair; it replaces fp32 atomics, which run at ~1.3 TB/s on this
 // part -- far slower than the 3 products they would save at these shapes.

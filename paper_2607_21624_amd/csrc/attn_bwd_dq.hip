@@ -1,6 +1,6 @@
 // attn_bwd_dq.hip -- dQ from the stored dS, bf16 storage, gfx950.
 //
-// dQ = scale dS K (section 4.1, the reduction over keys: "reduce along N" of
+// dQ = scale dS K (section 4.1, the reduction over keys: the N direction of
 // section 4.2) as a plain contraction: the key/value-major pass has already
 // produced every block of dS (bf16, the values its own dK product used) and
 // stored it in the workspace, so this pass only streams dS and K:

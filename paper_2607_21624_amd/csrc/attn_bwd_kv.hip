@@ -1,7 +1,7 @@
 // attn_bwd_kv.hip -- key/value-major backward pass for bf16 storage, gfx950.
 //
 // Computes dV = P^T dO and dK = scale dS^T Q (section 4.1, the reductions
-// over queries: "reduce along M" of section 4.2) for one workgroup of 128
+// over queries: the M direction of section 4.2) for one workgroup of 128
 // keys of one (batch, kv head), over the query blocks of every query head of
 // the GQA group.  Each wavefront keeps its 32 K and V rows as MFMA operands
 // and its dK^T, dV^T accumulators in registers for the whole pass.

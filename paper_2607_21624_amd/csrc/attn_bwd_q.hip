@@ -1,6 +1,6 @@
 // attn_bwd_q.hip -- query-major backward pass (dQ) for bf16 storage, gfx950.
 //
-// dQ = scale dS K (section 4.1; the reduction over keys, "reduce along N" of
+// dQ = scale dS K (section 4.1; the reduction over keys, the N direction of
 // section 4.2) for one workgroup of 128 queries of one (batch, query head);
 // each wavefront owns 32 queries and keeps their Q and dO rows (as MFMA
 // operands), their LSE and D and its dQ^T accumulator in registers, and walks
