@@ -458,7 +458,9 @@ def main():
                 "avg_launch_ms": round(t_dom, 4), "flops_per_launch": a_dom * w.d * pairs,
                 "algorithmic_bytes_per_launch": alg_bytes[dom],
                 # the paper's MemEfficiency (section 4.2): minimal over measured bytes
-                "mem_efficiency": None if dom_traffic is None else round(alg_bytes[dom] / dom_traffic, 3)}
+                "mem_efficiency": None if dom_traffic is None else round(alg_bytes[dom] / dom_traffic, 3),
+                # counted HBM bytes (FETCH_SIZE + WRITE_SIZE) over the launch time
+                "hbm_gbs_measured": None if dom_traffic is None else round(dom_traffic / (t_dom * 1e-3) / 1e9, 1)}
     stat = lambda x: {"median": round(float(np.median(x)), 4), "min": round(float(np.min(x)), 4),
                       "max": round(float(np.max(x)), 4)}
 
