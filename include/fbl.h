@@ -12,6 +12,10 @@
  * (section 4.3.2, the composed tile-index function f3 o f2 o f1), which the
  * kernels apply when they stage (tile_s x d) row tiles -- the R-Tile of
  * section 4.2 -- into LDS.  No layout-conversion kernel is ever launched.
+ * The projection products around attention (fbl_proj: Y = X W and its two
+ * gradients, also for LoRA adapters) read the same token-major activations
+ * in place, and Q, K, V can be views of one packed projection output
+ * (fbl_layout_packed_qkv).
  *
  * Conventions shared by every entry point.
  *  - Element (b, h, s, i) of a tensor described by an fbl_layout L is at
@@ -31,8 +35,10 @@
  *  - Storage type of Q, K, V, O, dO, dQ, dK, dV is one fbl_dtype for the whole
  *    call (fp32 or bf16); accumulation is fp32.
  *  - Ownership: the caller owns every buffer (device memory for tensors,
- *    host memory for descriptors).  The library never allocates, frees or
- *    synchronises.  Inputs are read-only; outputs are fully overwritten
+ *    host memory for descriptors).  The library never allocates or frees
+ *    device memory and never synchronises (except fbl_proj_tune, which
+ *    waits for its own timing events).  Inputs are read-only; outputs are
+ *    fully overwritten
  *    (no accumulate semantics) and must not alias inputs.
  *  - Errors: every check runs on the host before the first launch, so an
  *    error return means nothing was enqueued.  Return codes are the only
