@@ -289,6 +289,17 @@ fbl_status fbl_proj(uint32_t op, int64_t M, int64_t K, int64_t N, const void* a,
                     int64_t ldb, void* c, int64_t ldc, int32_t tile, void* stream);
 
 /*
+ * fbl_proj for either storage type: dtype FBL_BF16 is fbl_proj exactly;
+ * FBL_F32 runs the same three products on fp32 operands and result (fp32
+ * MFMAs, fp32 accumulation) with one tile shape -- tile must be
+ * FBL_GEMM_TILE_AUTO (else FBL_ERR_ARG) -- any extents and leading
+ * dimensions, and 4-byte (natural) alignment; the other checks are
+ * fbl_proj's.  FBL_ERR_DTYPE for another dtype.
+ */
+fbl_status fbl_proj_dt(uint32_t op, int32_t dtype, int64_t M, int64_t K, int64_t N, const void* a, int64_t lda,
+                       const void* b, int64_t ldb, void* c, int64_t ldc, int32_t tile, void* stream);
+
+/*
  * Tile configurations of the projection products.  fbl_gemm_tile_count gives
  * the number of ids; fbl_gemm_tile_info writes 8 values for one id:
  *   info[0..1]  bm, bn   output tile rows x cols of one workgroup

@@ -406,8 +406,12 @@ void proj_shape(uint32_t op, int64_t M, int64_t K, int64_t N, ProjPlan& pl) {
     pl.b_width = N;                                // W [K, N] or dY [M, N]
 }
 
+// es: element size (2: bf16, 4: fp32).  bf16 operands are staged by 16-byte
+// DMA loads (16-byte aligned pointers and rows, output widths a multiple of
+// 4, contraction a multiple of 8); fp32 operands by bounds-checked element
+// loads (natural alignment only).
 fbl_status proj_plan(uint32_t op, int64_t M, int64_t K, int64_t N, const void* a, int64_t lda, const void* b,
-                     int64_t ldb, void* c, int64_t ldc, ProjPlan& pl) {
+                     int64_t ldb, void* c, int64_t ldc, ProjPlan& pl, int es = 2) {
     if (op > FBL_PROJ_BWD_WEIGHT) return FBL_ERR_ARG;
     if (!a || !b || !c) return FBL_ERR_NULL;
     if (M <= 0 || K <= 0 || N <= 0 || M > INT32_MAX || K > INT32_MAX || N > INT32_MAX) return FBL_ERR_SHAPE;
@@ -424,12 +428,13 @@ fbl_status proj_plan(uint32_t op, int64_t M, int64_t K, int64_t N, const void* a
         pl.a_kmajor = 1;
     }
     if (lda < wa || ldb < wb || ldc < wc) return FBL_ERR_LAYOUT;
-    if (!aligned16(a) || !aligned16(b) || !aligned16(c) || (lda * 2) % 16 || (ldb * 2) % 16 || (ldc * 2) % 16)
-        return FBL_ERR_ALIGN;
+    const auto aligned = [es](const void* x) { return (reinterpret_cast<uintptr_t>(x) & (es == 2 ? 15u : 3u)) == 0; };
+    if (!aligned(a) || !aligned(b) || !aligned(c)) return FBL_ERR_ALIGN;
+    if (es == 2 && ((lda * 2) % 16 || (ldb * 2) % 16 || (ldc * 2) % 16)) return FBL_ERR_ALIGN;
     pl.a_width = wa;
     pl.b_width = wb;
-    if (pl.ocols % 4 || pl.kc % 8) return FBL_ERR_UNSUPPORTED;
-    const int64_t sa = ((ra - 1) * lda + wa) * 2, sb = ((rb - 1) * ldb + wb) * 2, sc = ((rc - 1) * ldc + wc) * 2;
+    if (es == 2 && (pl.ocols % 4 || pl.kc % 8)) return FBL_ERR_UNSUPPORTED;
+    const int64_t sa = ((ra - 1) * lda + wa) * es, sb = ((rb - 1) * ldb + wb) * es, sc = ((rc - 1) * ldc + wc) * es;
     if (sa >= ((int64_t)1 << 31) || sb >= ((int64_t)1 << 31) || sc >= ((int64_t)1 << 31)) return FBL_ERR_UNSUPPORTED;
     if (overlaps(c, sc, a, sa) || overlaps(c, sc, b, sb)) return FBL_ERR_ARG;
     fbl::GemmArgs& p = pl.p;
@@ -560,11 +565,17 @@ fbl_status fbl_proj_candidates(uint32_t op, int64_t M, int64_t K, int64_t N, int
     return FBL_OK;
 }
 
-fbl_status fbl_proj(uint32_t op, int64_t M, int64_t K, int64_t N, const void* a, int64_t lda, const void* b,
-                    int64_t ldb, void* c, int64_t ldc, int32_t tile, void* stream) {
+fbl_status fbl_proj_dt(uint32_t op, int32_t dtype, int64_t M, int64_t K, int64_t N, const void* a, int64_t lda,
+                       const void* b, int64_t ldb, void* c, int64_t ldc, int32_t tile, void* stream) {
+    if (dtype != FBL_BF16 && dtype != FBL_F32) return FBL_ERR_DTYPE;
     ProjPlan pl;
-    const fbl_status st = proj_plan(op, M, K, N, a, lda, b, ldb, c, ldc, pl);
+    const fbl_status st = proj_plan(op, M, K, N, a, lda, b, ldb, c, ldc, pl, dtype == FBL_BF16 ? 2 : 4);
     if (st != FBL_OK) return st;
+    if (dtype == FBL_F32) {  // one tile shape (64 x 64 outputs, 16-deep steps)
+        if (tile != FBL_GEMM_TILE_AUTO) return FBL_ERR_ARG;
+        const hipError_t e = fbl::launch_proj_gemm_f32(pl.a_kmajor, pl.b_nmajor, pl.p, static_cast<hipStream_t>(stream));
+        return e == hipSuccess ? FBL_OK : FBL_ERR_HIP;
+    }
     if (tile < FBL_GEMM_TILE_AUTO || tile >= fbl::kGemmTileCount) return FBL_ERR_ARG;
     if (tile == FBL_GEMM_TILE_AUTO) {
         tile = tuned_tile(op, M, K, N);
@@ -635,6 +646,11 @@ fbl_status fbl_proj_tune(uint32_t op, int64_t M, int64_t K, int64_t N, const voi
     // leave c holding the product computed with the chosen tile
     const hipError_t e = fbl::launch_proj_gemm(pl.a_kmajor, pl.b_nmajor, pick, pl.p, s);
     return e == hipSuccess ? FBL_OK : FBL_ERR_HIP;
+}
+
+fbl_status fbl_proj(uint32_t op, int64_t M, int64_t K, int64_t N, const void* a, int64_t lda, const void* b,
+                    int64_t ldb, void* c, int64_t ldc, int32_t tile, void* stream) {
+    return fbl_proj_dt(op, FBL_BF16, M, K, N, a, lda, b, ldb, c, ldc, tile, stream);
 }
 
 int32_t fbl_proj_tuned_tile(uint32_t op, int64_t M, int64_t K, int64_t N) { return tuned_tile(op, M, K, N); }

@@ -38,6 +38,8 @@ hipError_t launch_attn_bwd_dq_bf16(const BwdArgs& a, hipStream_t stream);
 // `tile` indexes kGemmTiles (gemm_tiles.hpp).
 // a_kmajor: A stored [K, M]; b_nmajor: B stored [N, K].
 hipError_t launch_proj_gemm(int a_kmajor, int b_nmajor, int tile, const GemmArgs& p, hipStream_t stream);
+// The same products for fp32 storage (proj_gemm_f32.hip): one tile shape.
+hipError_t launch_proj_gemm_f32(int a_kmajor, int b_nmajor, const GemmArgs& p, hipStream_t stream);
 
 // Diagnostic: offsets of a token-major tensor computed by the device index map.
 hipError_t launch_layout_map(const TokMap& m, int B, int H, int S, int D, int64_t* out, hipStream_t stream);

@@ -48,7 +48,7 @@ FBL_TUNE_TIME = 0
 FBL_TUNE_GFLOPS_X_MEMEFF = 1
 
 EXPORTED = ("fbl_layout_desc", "fbl_layout_packed_qkv", "fbl_layout_offset", "fbl_layout_map_device", "fbl_attn_fwd",
-            "fbl_attn_bwd_workspace", "fbl_attn_bwd_workspace_min", "fbl_attn_bwd", "fbl_attn_bwd_phases", "fbl_proj",
+            "fbl_attn_bwd_workspace", "fbl_attn_bwd_workspace_min", "fbl_attn_bwd", "fbl_attn_bwd_phases", "fbl_proj", "fbl_proj_dt",
             "fbl_gemm_tile_count", "fbl_gemm_tile_info", "fbl_proj_candidates", "fbl_proj_tune", "fbl_proj_tuned_tile",
             "fbl_proj_tune_reset", "fbl_status_str")
 
@@ -113,6 +113,10 @@ def _load() -> ctypes.CDLL:
     lib.fbl_proj.argtypes = [ctypes.c_uint32] + [ctypes.c_int64] * 3 + [vp, ctypes.c_int64, vp, ctypes.c_int64, vp,
                                                                         ctypes.c_int64, ctypes.c_int32, vp]
     lib.fbl_proj.restype = ctypes.c_int
+    lib.fbl_proj_dt.argtypes = [ctypes.c_uint32, ctypes.c_int32] + [ctypes.c_int64] * 3 + [vp, ctypes.c_int64, vp,
+                                                                                   ctypes.c_int64, vp, ctypes.c_int64,
+                                                                                   ctypes.c_int32, vp]
+    lib.fbl_proj_dt.restype = ctypes.c_int
     lib.fbl_gemm_tile_count.argtypes = []
     lib.fbl_gemm_tile_count.restype = ctypes.c_int32
     lib.fbl_gemm_tile_info.argtypes = [ctypes.c_int32, P(ctypes.c_int32)]
@@ -405,7 +409,7 @@ def _proj_shape(op, a, b):
 
 
 def proj(op: int, a, b, out=None, tile: int = FBL_GEMM_TILE_AUTO, stream=None):
-    """One projection product on 2-D bf16 tensors (row-major, any row stride):
+    """One projection product on 2-D bf16 or fp32 tensors (row-major, any row stride):
     FBL_PROJ_FWD (a = X [M, K], b = W [K, N]) -> Y [M, N];
     FBL_PROJ_BWD_DATA (a = dY [M, N], b = W [K, N]) -> dX [M, K];
     FBL_PROJ_BWD_WEIGHT (a = X [M, K], b = dY [M, N]) -> dW [K, N]."""
@@ -414,7 +418,11 @@ def proj(op: int, a, b, out=None, tile: int = FBL_GEMM_TILE_AUTO, stream=None):
     if out is None:
         out = torch.empty(shape, dtype=a.dtype, device=a.device)
     _, _, ldc = _rows(out, "out")
-    _check(fbl_proj_raw(op, M, K, N, a, lda, b, ldb, out, ldc, tile, stream), "fbl_proj")
+    if a.dtype == torch.float32:
+        _check(LIB.fbl_proj_dt(op, FBL_F32, M, K, N, _ptr(a), lda, _ptr(b), ldb, _ptr(out), ldc, tile,
+                               _stream(stream) if stream != 0 else None), "fbl_proj_dt")
+    else:
+        _check(fbl_proj_raw(op, M, K, N, a, lda, b, ldb, out, ldc, tile, stream), "fbl_proj")
     return out
 
 

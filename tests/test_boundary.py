@@ -398,3 +398,19 @@ def test_proj_tune_rejections():
     assert T(reps=0) == F.FBL_ERR_ARG
     assert T(reps=1001) == F.FBL_ERR_ARG
     assert fbl.proj_tuned_tile(F.FBL_PROJ_FWD, 64, 64, 64) == -1
+
+
+def test_proj_dt_rejections():
+    """fbl_proj_dt: the dtype, the single fp32 tile and fp32's natural alignment."""
+    D = lambda op=0, dt=F.FBL_F32, a=FAKE, lda=4096, tile=-1, M=64, K=64, N=64: fbl.LIB.fbl_proj_dt(
+        op, dt, M, K, N, ctypes.c_void_p(a), lda, ctypes.c_void_p(FAKE + (1 << 24)), 4096,
+        ctypes.c_void_p(FAKE + (1 << 26)), 4096, tile, None)
+    assert D(dt=7) == F.FBL_ERR_DTYPE
+    assert D(tile=0) == F.FBL_ERR_ARG                  # fp32 has one tile shape
+    assert D(a=FAKE + 2) == F.FBL_ERR_ALIGN            # fp32 needs 4-byte alignment
+    assert D(lda=32) == F.FBL_ERR_LAYOUT
+    assert D(op=3) == F.FBL_ERR_ARG
+    assert D(M=0) == F.FBL_ERR_SHAPE
+    # bf16 through fbl_proj_dt keeps fbl_proj's rules
+    assert D(dt=F.FBL_BF16, K=60) == F.FBL_ERR_UNSUPPORTED
+    assert D(dt=F.FBL_BF16, a=FAKE + 4) == F.FBL_ERR_ALIGN

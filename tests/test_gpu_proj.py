@@ -228,3 +228,25 @@ def test_proj_tiny_extents(op, M, K, N, tile):
     rest = torch.cat([out[ref.shape[0]:].flatten(), out[:ref.shape[0], ref.shape[1]:].flatten()])
     assert torch.isnan(rest.float()).all(), "wrote outside the output"
     assert rel_err(to_np(view), ref) <= TOL
+
+
+@pytest.mark.parametrize("M,K,N", [(64, 64, 64), (100, 37, 53), (1, 3, 5), (257, 130, 66), (512, 1024, 384)])
+def test_proj_fp32_matches_oracle(M, K, N):
+    """fp32 storage (fbl_proj_dt): any extents, odd widths, every product, to
+    1e-4 of max|ref|; outputs written into NaN-poisoned wider buffers."""
+    import torch
+    fbl = _lib()
+    rng = np.random.default_rng(M + 5 * K + 11 * N)
+    x, w, dy = rng.standard_normal((M, K)), rng.standard_normal((K, N)), rng.standard_normal((M, N))
+    X, W, dY = (torch.tensor(t, dtype=torch.float32, device="cuda") for t in (x, w, dy))
+    note(f"proj fp32 M={M} K={K} N={N}")
+    for op, a, b, ref in ((fbl.FBL_PROJ_FWD, X, W, oracle.proj_fwd(x, w)),
+                          (fbl.FBL_PROJ_BWD_DATA, dY, W, oracle.proj_bwd_data(dy, w)),
+                          (fbl.FBL_PROJ_BWD_WEIGHT, X, dY, oracle.proj_bwd_weight(x, dy))):
+        out = torch.full((ref.shape[0] + 3, ref.shape[1] + 5), float("nan"), dtype=torch.float32, device="cuda")
+        view = out[:ref.shape[0], :ref.shape[1]]
+        fbl.proj(op, a, b, out=view)
+        torch.cuda.synchronize()
+        rest = torch.cat([out[ref.shape[0]:].flatten(), out[:ref.shape[0], ref.shape[1]:].flatten()])
+        assert torch.isnan(rest).all(), f"op {op}: wrote outside the output"
+        assert rel_err(to_np(view), ref) <= 1e-4, f"op {op}"
