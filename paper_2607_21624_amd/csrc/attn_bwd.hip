@@ -544,20 +544,11 @@ FBL_BWD_KERNELS(bf16, 64)
 FBL_BWD_KERNELS(bf16, 128)
 #undef FBL_BWD_KERNELS
 
-template <typename K>
-hipError_t set_lds(K kernel, int bytes) {
-    return hipFuncSetAttribute(reinterpret_cast<const void*>(kernel), hipFuncAttributeMaxDynamicSharedMemorySize,
-                               bytes);
-}
-
 template <typename T, int D>
 hipError_t set_bwd_lds() {
-    static hipError_t once = [] {
-        const hipError_t e = set_lds(&attn_bwd_kv<T, D>, KvCfg<T, D>::BYTES);
-        if (e != hipSuccess) return e;
-        return set_lds(&attn_bwd_q<T, D>, QSmem<T, D>::BYTES);
-    }();
-    return once;
+    const hipError_t e = ensure_dynamic_lds<&attn_bwd_kv<T, D>>(KvCfg<T, D>::BYTES);
+    if (e != hipSuccess) return e;
+    return ensure_dynamic_lds<&attn_bwd_q<T, D>>(QSmem<T, D>::BYTES);
 }
 
 int padded8(int n) { return (n + 7) / 8 * 8; }

@@ -259,8 +259,7 @@ __global__ __launch_bounds__(64 * NW, (DqPipe<D, NW, NBUF>::OCC)) void attn_bwd_
 template <int D, int NW, int NBUF>
 hipError_t launch_dq(const BwdArgs& a, hipStream_t stream) {
     using P = DqPipe<D, NW, NBUF>;
-    static const hipError_t once = hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_bwd_dq_bf16<D, NW, NBUF>),
-                                                       hipFuncAttributeMaxDynamicSharedMemorySize, P::BYTES);
+    const hipError_t once = ensure_dynamic_lds<&attn_bwd_dq_bf16<D, NW, NBUF>>(P::BYTES);
     if (once != hipSuccess) return once;
     const int nqb = (a.S + P::ROWS - 1) / P::ROWS;
     const int n = (a.mask.causal ? (nqb + 1) / 2 : nqb) * a.Hq * a.B;

@@ -451,8 +451,7 @@ template __global__ void attn_bwd_kv_bf16<128, true>(BwdArgs);
 
 template <int D, bool DS>
 hipError_t launch_kv(const BwdArgs& a, hipStream_t stream) {
-    static const hipError_t once = hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_bwd_kv_bf16<D, DS>),
-                                                       hipFuncAttributeMaxDynamicSharedMemorySize, KvPipe<D>::BYTES);
+    const hipError_t once = ensure_dynamic_lds<&attn_bwd_kv_bf16<D, DS>>(KvPipe<D>::BYTES);
     if (once != hipSuccess) return once;
     constexpr int lds = KvPipe<D>::BYTES;
     hipLaunchKernelGGL((attn_bwd_kv_bf16<D, DS>), dim3(rank_major_grid((a.Skv + kPKeys - 1) / kPKeys, a.Hkv * a.B)),

@@ -295,8 +295,7 @@ template __global__ void attn_bwd_q_bf16<128>(BwdArgs);
 
 template <int D>
 hipError_t launch_attn_bwd_q_bf16(const BwdArgs& a, hipStream_t stream) {
-    static const hipError_t once = hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_bwd_q_bf16<D>),
-                                                       hipFuncAttributeMaxDynamicSharedMemorySize, QPipe<D>::BYTES);
+    const hipError_t once = ensure_dynamic_lds<&attn_bwd_q_bf16<D>>(QPipe<D>::BYTES);
     if (once != hipSuccess) return once;
     constexpr int lds = QPipe<D>::BYTES;
     hipLaunchKernelGGL((attn_bwd_q_bf16<D>), dim3(rank_major_grid((a.S + kQRows - 1) / kQRows, a.Hq * a.B)), dim3(256),

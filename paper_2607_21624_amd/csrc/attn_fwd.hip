@@ -391,9 +391,7 @@ constexpr int fwd_lds_bytes() {
 
 template <typename T, int D>
 hipError_t set_fwd_lds() {
-    static hipError_t once = hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_fwd_kernel<T, D>),
-                                                 hipFuncAttributeMaxDynamicSharedMemorySize, fwd_lds_bytes<T, D>());
-    return once;
+    return ensure_dynamic_lds<&attn_fwd_kernel<T, D>>(fwd_lds_bytes<T, D>());
 }
 
 }  // namespace

@@ -3,10 +3,29 @@
 
 #include <hip/hip_runtime.h>
 
+#include <atomic>
+#include <cstdint>
+
 #include "gemm_tiles.hpp"
 #include "tokmap.hpp"
 
 namespace fbl {
+
+// Raise a kernel's dynamic-LDS limit before its first launch on each device
+// (the attribute is held per device).  One flag word per kernel; devices 64
+// and up set the attribute on every launch.
+template <auto Kernel>
+hipError_t ensure_dynamic_lds(int bytes) {
+    static std::atomic<uint64_t> done{0};  // bit d: set on device d
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    const uint64_t bit = dev >= 0 && dev < 64 ? (uint64_t(1) << dev) : 0;
+    if (bit && (done.load(std::memory_order_acquire) & bit)) return hipSuccess;
+    e = hipFuncSetAttribute(reinterpret_cast<const void*>(Kernel), hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+    if (e == hipSuccess && bit) done.fetch_or(bit, std::memory_order_release);
+    return e;
+}
 
 typedef __bf16 bf16;
 

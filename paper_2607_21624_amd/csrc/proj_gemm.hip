@@ -328,9 +328,8 @@ template <int I, bool AT, bool BT>
 hipError_t launch_id(const GemmArgs& p, hipStream_t stream) {
     constexpr GemmTile t = kGemmTiles[I];
     using C = GemmCfg<t.bm, t.bn, t.bk, t.ns, t.wm, t.wn, t.wk, AT, BT>;
-    auto kernel = &proj_gemm_bf16<t.bm, t.bn, t.bk, t.ns, t.wm, t.wn, t.wk, AT, BT>;
-    static const hipError_t once = hipFuncSetAttribute(reinterpret_cast<const void*>(kernel),
-                                                       hipFuncAttributeMaxDynamicSharedMemorySize, C::BYTES);
+    constexpr auto kernel = &proj_gemm_bf16<t.bm, t.bn, t.bk, t.ns, t.wm, t.wn, t.wk, AT, BT>;
+    const hipError_t once = ensure_dynamic_lds<kernel>(C::BYTES);
     if (once != hipSuccess) return once;
     const int tiles = ((p.M + t.bm - 1) / t.bm) * ((p.N + t.bn - 1) / t.bn);
     hipLaunchKernelGGL(kernel, dim3((tiles + 7) / 8 * 8), dim3(64 * C::NW), C::BYTES, stream, p);
