@@ -165,8 +165,11 @@ fbl_status fbl_layout_map_device(const fbl_layout* l, int64_t* out, void* stream
  *   lse      float32 [B, Hq, S_q] contiguous, written (saved for the backward).
  *   scale    softmax scale (finite), e.g. 1/sqrt(D).
  *   mask     see fbl_mask.
- * Supported: D in {32, 64, 128}; Hq % Hkv == 0; S_q, S_kv up to 2^30; a
- * causal mask needs S_q == S_kv (else FBL_ERR_UNSUPPORTED).
+ * Supported: D in {32, 64, 128}; Hq % Hkv == 0; for every tensor
+ * (S + 128) * ss * element size at most 2^31 bytes -- rows are addressed
+ * from each (batch, head) base with 32-bit offsets, and tiles reach up to
+ * 128 rows past the last token; a causal mask needs S_q == S_kv.  Otherwise
+ * FBL_ERR_UNSUPPORTED.
  * Checks: non-NULL pointers; one dtype; lq.B == lk.B == lv.B == lo.B;
  * lk and lv extents equal (S_kv = lk.S); lq.D == lk.D;
  * lo extents equal lq's; sd == 1; tile_d divides D; base pointers and
@@ -210,8 +213,9 @@ fbl_status fbl_attn_bwd_workspace_min(const fbl_layout* lq, const fbl_layout* lk
  *                With at least fbl_attn_bwd_workspace bytes the key/value pass
  *                stores dS there for the dQ pass (see fbl_attn_bwd_workspace).
  * Same checks as fbl_attn_fwd for the shared arguments, plus: ldo/ldq
- * extents equal lq's, ldk/ldv extents equal lk's, outputs do not overlap
- * inputs, each other or the workspace.
+ * extents equal lq's, ldk/ldv extents equal lk's, the row-offset limit of
+ * fbl_attn_fwd for every layout, outputs do not overlap inputs, each other or
+ * the workspace.
  */
 fbl_status fbl_attn_bwd(const fbl_layout* lq, const void* q, const fbl_layout* lk, const void* k,
                         const fbl_layout* lv, const void* v, const fbl_layout* lo, const void* o,

@@ -54,6 +54,15 @@ int64_t span_bytes(const fbl_layout* l) {
     return (last + 1) * elem_size(l->dtype);
 }
 
+// The attention kernels address a tensor from each (batch, head) base with
+// 32-bit byte offsets, and their tiles run up to 128 rows past the last token
+// (those rows read as zeros and are never stored): every such offset must stay
+// below 2^31, the largest range of a buffer resource.
+constexpr int64_t kTileRowPad = 128;
+bool rows_fit(const fbl_layout* l) {
+    return (l->S + kTileRowPad) * l->ss * elem_size(l->dtype) <= ((int64_t)1 << 31);
+}
+
 bool overlaps(const void* a, int64_t na, const void* b, int64_t nb) {
     const uintptr_t pa = reinterpret_cast<uintptr_t>(a), pb = reinterpret_cast<uintptr_t>(b);
     return pa < pb + (uintptr_t)nb && pb < pa + (uintptr_t)na;
@@ -99,9 +108,8 @@ fbl_status check_qkv(const fbl_layout* lq, const void* q, const fbl_layout* lk, 
     if (lq->D != lk->D) return FBL_ERR_SHAPE;
     if (lq->H % lk->H != 0) return FBL_ERR_SHAPE;
     if (lq->D != 32 && lq->D != 64 && lq->D != 128) return FBL_ERR_UNSUPPORTED;
-    // tiles are fetched through 32-bit buffer offsets from each (batch, head) base
     for (const fbl_layout* l : {lq, lk, lv})
-        if (((l->S - 1) * l->ss + l->D) * elem_size(l->dtype) >= ((int64_t)1 << 31)) return FBL_ERR_UNSUPPORTED;
+        if (!rows_fit(l)) return FBL_ERR_UNSUPPORTED;
     if (!aligned16(q) || !aligned16(k) || !aligned16(v)) return FBL_ERR_ALIGN;
     if (mask.kind & ~(FBL_MASK_CAUSAL | FBL_MASK_KEY_PADDING)) return FBL_ERR_ARG;
     if ((mask.kind & FBL_MASK_KEY_PADDING) && !mask.kv_len) return FBL_ERR_NULL;
@@ -247,6 +255,7 @@ fbl_status fbl_attn_fwd(const fbl_layout* lq, const void* q, const fbl_layout* l
     if (!lo || !o || !lse) return FBL_ERR_NULL;
     if ((st = check_layout(lo)) != FBL_OK) return st;
     if (!same_extents(lo, lq)) return lo->dtype != lq->dtype ? FBL_ERR_DTYPE : FBL_ERR_SHAPE;
+    if (!rows_fit(lo)) return FBL_ERR_UNSUPPORTED;
     if (!aligned16(o) || !aligned16(lse)) return FBL_ERR_ALIGN;
     const int64_t lse_bytes = lq->B * lq->H * lq->S * 4;
     const void* ins[3] = {q, k, v};
@@ -314,6 +323,8 @@ fbl_status fbl_attn_bwd_phases(uint32_t phases, const fbl_layout* lq, const void
         if (!same_extents(l, lq)) return l->dtype != lq->dtype ? FBL_ERR_DTYPE : FBL_ERR_SHAPE;
     for (const fbl_layout* l : {ldk, ldv})
         if (!same_extents(l, lk)) return l->dtype != lq->dtype ? FBL_ERR_DTYPE : FBL_ERR_SHAPE;
+    for (const fbl_layout* l : all)
+        if (!rows_fit(l)) return FBL_ERR_UNSUPPORTED;
     if (!aligned16(o) || !aligned16(dO) || !aligned16(lse) || !aligned16(dq) || !aligned16(dk) || !aligned16(dv))
         return FBL_ERR_ALIGN;
     if (!ws) return FBL_ERR_WORKSPACE;

@@ -208,6 +208,26 @@ def _bwd(lq, lk, lv, lo, p, ws_bytes, ldo=None, ldq=None, ldk=None, ldv=None, ki
                                 ws_bytes, stream=0)
 
 
+def test_row_offset_limit():
+    """Every attention tensor's rows are addressed with 32-bit offsets from
+    its (batch, head) base, tiles reaching 128 rows past the last token:
+    (S + 128) * ss * element size must stay within 2^31 bytes, for inputs and
+    outputs alike (each layout carries its own row stride)."""
+    E = F
+    S = 16
+    big = 1 << 23    # (16 + 128) * 2^23 * 2 bytes > 2^31, yet the 16 rows span only 0.25 GB
+    lq, lk, lv, lo, p = _fwd_setup(S=S)
+    wide = lambda l: _copy(l, ss=big, sb=S * big)
+    for role in ("q", "k", "v", "o"):
+        ls = {"q": lq, "k": lk, "v": lv, "o": lo}
+        ls[role] = wide(ls[role])
+        assert _fwd(ls["q"], ls["k"], ls["v"], ls["o"], p) == E.FBL_ERR_UNSUPPORTED, role
+    lq, lk, lv, lo, p, ws = _bwd_setup()
+    for kw in ({"ldo": wide(lo)}, {"ldq": wide(lq)}, {"ldk": wide(lk)}, {"ldv": wide(lv)}):
+        assert _bwd(lq, lk, lv, lo, p, ws, **kw) == E.FBL_ERR_UNSUPPORTED, kw
+    assert _bwd(lq, lk, lv, wide(lo), p, ws, ldo=lo) == E.FBL_ERR_UNSUPPORTED
+
+
 def test_bwd_workspace_size():
     """Minimum: the row statistics, [B, Hq, 2, S] fp32 rounded up to 256 bytes.
     Full (bf16): plus B*Hq*ceil(S/32)^2 dS blocks of 2 KB; fp32: statistics only."""

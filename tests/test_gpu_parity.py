@@ -262,6 +262,48 @@ def test_strided_views_of_packed_projection():
     assert not bad, bad
 
 
+def test_largest_row_stride():
+    """At the largest accepted row stride, (S + 128) * ss * 2 = 2^31 bytes:
+    every tensor (inputs, O, dO and the gradients) is a view with 8 MB between
+    consecutive tokens, the gaps filled with NaN.  The tiles' row offsets reach
+    the top of the 32-bit range; any read of a gap or any wrapped offset would
+    bring NaN into the results."""
+    import torch
+    fbl = _lib()
+    B, S, Hq, Hkv, d = 1, 128, 2, 1, 128
+    ss = (1 << 31) // ((S + 128) * 2)
+    assert ss == 1 << 22
+    w = synth.Workload("stride", B=B, S=S, Hq=Hq, Hkv=Hkv, d=d, dtype="bf16", mask=synth.MASK_CAUSAL, seed=77)
+    inp = synth.make_inputs(w)
+    note(f"largest row stride ss={ss} S={S} d={d}")
+
+    def view(cols, data=None):
+        buf = torch.full((S * ss,), float("nan"), dtype=torch.bfloat16, device="cuda")
+        t = torch.as_strided(buf, (B, S, cols), (S * ss, ss, 1))
+        if data is not None:
+            t.copy_(to_dev(data, "bf16"))
+        return t
+
+    q, k, v, do = view(Hq * d, inp["q"]), view(Hkv * d, inp["k"]), view(Hkv * d, inp["v"]), view(Hq * d, inp["do"])
+    o, dq, dk, dv = view(Hq * d), view(Hq * d), view(Hkv * d), view(Hkv * d)
+    assert fbl.layout_of(q, Hq).ss == ss and fbl.layout_of(dk, Hkv).ss == ss
+    scale = 1.0 / math.sqrt(d)
+    _, lse = fbl.attn_fwd(q, k, v, Hq, Hkv, scale, True, out=o)
+    fbl.attn_bwd(q, k, v, o, do, lse, Hq, Hkv, scale, True, None, dq=dq, dk=dk, dv=dv)
+    torch.cuda.synchronize()
+    got = {"o": to_np(o), "lse": to_np(lse), "dq": to_np(dq), "dk": to_np(dk), "dv": to_np(dv)}
+    errs, bad = compare(got, oracle_fwd_bwd(inp), "bf16")
+    note(f"largest row stride rel errs {errs}")
+    assert not bad, bad
+    del q, k, v, do, o, dq, dk, dv
+    # one 16-byte step further is refused before any launch
+    wide = torch.as_strided(torch.empty(S * (ss + 8), dtype=torch.bfloat16, device="cuda"), (B, S, Hq * d),
+                            (S * (ss + 8), ss + 8, 1))
+    with pytest.raises(fbl.FblError, match="UNSUPPORTED"):
+        fbl.attn_fwd(wide, wide[:, :, :Hkv * d], wide[:, :, :Hkv * d], Hq, Hkv, scale, True)
+    torch.cuda.empty_cache()
+
+
 @pytest.mark.parametrize("causal,Hq,Hkv,d,S", [(True, 8, 2, 64, 200), (False, 4, 4, 128, 131), (True, 6, 3, 32, 97)])
 def test_packed_qkv_entry_points(causal, Hq, Hkv, d, S):
     """attn_fwd_packed / attn_bwd_packed: Q, K, V read in place from one packed
