@@ -515,23 +515,27 @@ int32_t tuned_tile(uint32_t op, int64_t M, int64_t K, int64_t N) {
 // product has and how long its contraction is (measured on the 512 x 2048 x
 // 8192 and 4096 x 4096 x {4096, 12288} products and their transposes): with at
 // least four per CU (1024) and a contraction of 2048 or more, the 256 x 256
-// tiles, then the 8-wavefront 256 x 128 ones; with at least four per CU and a
+// tiles (8 wavefronts first when A is read along its rows, 4 first for the
+// weight gradient's transposed A), then the 8-wavefront 256 x 128 ones; with
+// at least four per CU and a
 // short contraction, 4-wavefront tiles with small LDS, several workgroups per
 // CU; with at least one per CU, the 8-wavefront 128 x 128 tile; below that,
 // 64 x 64 tiles whose four wavefronts split the contraction.  The first
 // candidate of the order that gives at least one workgroup per CU (256) wins,
 // else the first candidate.
 int32_t default_tile(const ProjPlan& pl) {
-    static const int big[] = {18, 17, 11, 12, 8, 4, 0, 6, 5, 2, 1, 10, 9, 7, 3, 13, 15, 14, 16};
-    static const int many[] = {0, 4, 8, 1, 2, 5, 6, 11, 12, 10, 9, 7, 3, 13, 15, 14, 16, 17, 18};
-    static const int some[] = {8, 4, 6, 5, 11, 12, 0, 2, 1, 10, 9, 7, 3, 13, 15, 14, 16, 17, 18};
-    static const int few[] = {9, 10, 7, 6, 5, 8, 4, 3, 2, 1, 0, 11, 12, 14, 13, 15, 16, 17, 18};
+    static const int big[] = {19, 18, 20, 17, 11, 12, 8, 4, 0, 6, 5, 2, 1, 10, 9, 7, 3, 13, 15, 14, 16};
+    static const int big_t[] = {18, 20, 19, 17, 11, 12, 8, 4, 0, 6, 5, 2, 1, 10, 9, 7, 3, 13, 15, 14, 16};
+    static const int many[] = {0, 4, 8, 1, 2, 5, 6, 11, 12, 10, 9, 7, 3, 13, 15, 14, 16, 17, 18, 19, 20};
+    static const int some[] = {8, 4, 6, 5, 11, 12, 0, 2, 1, 10, 9, 7, 3, 13, 15, 14, 16, 17, 18, 19, 20};
+    static const int few[] = {9, 10, 7, 6, 5, 8, 4, 3, 2, 1, 0, 11, 12, 14, 13, 15, 16, 17, 18, 19, 20};
     static_assert(sizeof(many) == sizeof(int) * fbl::kGemmTileCount && sizeof(some) == sizeof(many) &&
-                      sizeof(few) == sizeof(many) && sizeof(big) == sizeof(many),
+                      sizeof(few) == sizeof(many) && sizeof(big) == sizeof(many) && sizeof(big_t) == sizeof(many),
                   "every tile ranked once");
     const uint64_t cand = candidate_set(pl);
     const int64_t n128 = ((pl.orows + 127) / 128) * ((pl.ocols + 127) / 128);
-    const int* order = n128 >= 1024 ? (pl.kc >= 2048 ? big : many) : (n128 >= 256 ? some : few);
+    const int* order =
+        n128 >= 1024 ? (pl.kc >= 2048 ? (pl.a_kmajor ? big_t : big) : many) : (n128 >= 256 ? some : few);
     int32_t first = -1;
     for (int i = 0; i < fbl::kGemmTileCount; ++i) {
         const int t = order[i];

@@ -36,6 +36,9 @@ constexpr GemmTile kGemmTiles[] = {
     // large products: 4 wavefronts of 128 x 128 (the accumulators fill the AGPRs)
     {256, 256, 32, 4, 2, 2, 1},  // 17
     {256, 256, 64, 2, 2, 2, 1},  // 18
+    // large products, 8 wavefronts (two per SIMD) of 128 x 64 or 64 x 128
+    {256, 256, 64, 2, 2, 4, 1},  // 19
+    {256, 256, 64, 2, 4, 2, 1},  // 20
 };
 constexpr int kGemmTileCount = (int)(sizeof(kGemmTiles) / sizeof(kGemmTiles[0]));
 

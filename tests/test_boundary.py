@@ -347,17 +347,17 @@ def test_proj_rejections():
     assert P(E.FBL_PROJ_BWD_WEIGHT, 100, 64, 64) == E.FBL_ERR_UNSUPPORTED  # contraction M = 100
     assert P(E.FBL_PROJ_FWD, 64, 64, 66, ldc=4104) == E.FBL_ERR_UNSUPPORTED  # output columns not a multiple of 4
     assert P(E.FBL_PROJ_BWD_DATA, 64, 66, 64) == E.FBL_ERR_UNSUPPORTED  # dX columns K = 66
-    assert P(E.FBL_PROJ_FWD, 64, 64, 64, tile=19) == E.FBL_ERR_ARG    # no such tile id
+    assert P(E.FBL_PROJ_FWD, 64, 64, 64, tile=21) == E.FBL_ERR_ARG    # no such tile id
     assert P(E.FBL_PROJ_FWD, 64, 64, 64, tile=-2) == E.FBL_ERR_ARG
     assert P(E.FBL_PROJ_FWD, 64, 64, 64, c=FAKE + 64) == E.FBL_ERR_ARG  # output overlaps an input
 
 
 def test_gemm_tile_table():
-    """The tile table the GPU tests enumerate: 13 configurations, ids 0-3 the
+    """The tile table the GPU tests enumerate: 21 configurations, ids 0-3 the
     named output shapes, LDS within the 160 KB of a CU, and the contraction
     split and wavefront grid consistent with the output tile."""
     tiles = fbl.gemm_tiles()
-    assert len(tiles) == 19 and fbl.LIB.fbl_gemm_tile_count() == 19
+    assert len(tiles) == 21 and fbl.LIB.fbl_gemm_tile_count() == 21
     named = {F.FBL_GEMM_TILE_128x128: (128, 128), F.FBL_GEMM_TILE_128x64: (128, 64),
              F.FBL_GEMM_TILE_64x128: (64, 128), F.FBL_GEMM_TILE_64x64: (64, 64)}
     for t, (bm, bn) in named.items():
@@ -370,7 +370,7 @@ def test_gemm_tile_table():
         partial = (g["wk"] - 1) * g["bm"] * g["bn"] * 4
         assert g["lds_bytes"] == max(stages, partial) <= 160 * 1024
     info = (ctypes.c_int32 * 8)()
-    assert fbl.LIB.fbl_gemm_tile_info(19, info) == F.FBL_ERR_ARG
+    assert fbl.LIB.fbl_gemm_tile_info(21, info) == F.FBL_ERR_ARG
     assert fbl.LIB.fbl_gemm_tile_info(0, None) == F.FBL_ERR_NULL
 
 
