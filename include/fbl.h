@@ -191,6 +191,14 @@ fbl_status fbl_attn_fwd(const fbl_layout* lq, const void* q, const fbl_layout* l
  * dQ pass then does not recompute S and dP.  Part 2 is omitted (the size
  * equals fbl_attn_bwd_workspace_min) for fp32 storage and when one head's
  * blocks would reach 2 GiB (S_q = S_kv above 32736).
+ * Part 3, with part 2, where the key/value pass has fewer than 512 blocks of
+ * 128 keys (B * Hkv * ceil(S_kv/128)) and the first block at least 16 query
+ * iterations per share (Hq/Hkv * ceil(S_q/32) at D = 128, ceil(S_q/64)
+ * otherwise): the pass splits each key block's iterations among 2, or 4, workgroups
+ * (4 below 128 blocks when the iterations allow), and this part holds their
+ * fp32 partial dK and dV, 2 * split * B*S_kv*Hkv*D floats, which a
+ * reduction adds in a fixed order.  Without a causal mask the split is used
+ * only while the split grid fits 256 compute units.
  */
 fbl_status fbl_attn_bwd_workspace(const fbl_layout* lq, const fbl_layout* lk, size_t* bytes);
 
@@ -210,8 +218,11 @@ fbl_status fbl_attn_bwd_workspace_min(const fbl_layout* lq, const fbl_layout* lk
  * must be the forward's outputs for q, k, v.
  *   ws/ws_bytes  device workspace of at least fbl_attn_bwd_workspace_min
  *                bytes, 256-byte aligned; its contents on entry do not matter.
- *                With at least fbl_attn_bwd_workspace bytes the key/value pass
- *                stores dS there for the dQ pass (see fbl_attn_bwd_workspace).
+ *                With parts 1 and 2 of fbl_attn_bwd_workspace the key/value
+ *                pass stores dS there for the dQ pass; with all of it the
+ *                key/value pass may also be split (see fbl_attn_bwd_workspace).
+ *                Each size gives bitwise repeatable results; sizes that select
+ *                different passes may differ in the last bits.
  * Same checks as fbl_attn_fwd for the shared arguments, plus: ldo/ldq
  * extents equal lq's, ldk/ldv extents equal lk's, the row-offset limit of
  * fbl_attn_fwd for every layout, outputs do not overlap inputs, each other or

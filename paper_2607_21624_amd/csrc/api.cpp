@@ -160,7 +160,40 @@ size_t ws_ds_bytes(const fbl_layout* lq, const fbl_layout* lk) {
     return (size_t)(heads * per_head);
 }
 
-size_t ws_bytes_for(const fbl_layout* lq, const fbl_layout* lk) { return ws_stats_bytes(lq) + ws_ds_bytes(lq, lk); }
+// Split of the key/value pass (bf16 with stored dS).  Its work items are key
+// blocks of 128 keys per (batch, kv head).  Under a causal mask the first key
+// blocks carry the most queries, and with fewer than two items per CU (512)
+// the pass waits on those few large items while other CUs idle; without a
+// mask the items are equal and only a grid of fewer items than CUs leaves CUs
+// idle.  Sharing each key block's query iterations among 2 (or 4) workgroups
+// gives the scheduler items of half (a quarter) the size; each writes fp32
+// partial dK and dV and a reduction adds them in a fixed order.  Causal: split
+// while below 512 items; otherwise while the split grid still fits the 256
+// CUs.  Only where the first key block has at least 16 iterations per share.
+// (Measured: splitting the 512 items of the GPT-2-medium-like causal shape,
+// or the Llama-3.2-1B-like GQA shape four ways, is slower.)  The causal
+// choice is never below the other, so it sizes the workspace.
+int kv_split_for(const fbl_layout* lq, const fbl_layout* lk, bool causal = true) {
+    if (lq->dtype != FBL_BF16 || lk->H <= 0 || lq->D <= 0) return 1;
+    const int64_t items = (lk->S + 127) / 128 * lk->H * lk->B;
+    const int64_t bq = lq->D == 128 ? 32 : 64;  // queries per iteration
+    const int64_t iters = lq->H / lk->H * ((lq->S + bq - 1) / bq);
+    int split = 1;
+    while (split < 4 && (causal ? items * split < 512 : items * split * 2 <= 256) && iters >= 16 * split) split *= 2;
+    return split;
+}
+
+// Workspace, part 3 (with part 2 only): the split key/value pass's fp32
+// partial dK and dV, [2][kv_split][B, S_kv, Hkv, D]; 0 without a split.
+size_t ws_part_bytes(const fbl_layout* lq, const fbl_layout* lk) {
+    const int split = kv_split_for(lq, lk);
+    if (split == 1 || ws_ds_bytes(lq, lk) == 0) return 0;
+    return align256((size_t)2 * split * lk->B * lk->S * lk->H * lk->D * sizeof(float));
+}
+
+size_t ws_bytes_for(const fbl_layout* lq, const fbl_layout* lk) {
+    return ws_stats_bytes(lq) + ws_ds_bytes(lq, lk) + ws_part_bytes(lq, lk);
+}
 
 }  // namespace
 
@@ -360,6 +393,12 @@ fbl_status fbl_attn_bwd_phases(uint32_t phases, const fbl_layout* lq, const void
     const size_t ds_bytes = ws_ds_bytes(lq, lk);
     a.ds = ds_bytes && ws_bytes >= ws_stats_bytes(lq) + ds_bytes ? static_cast<char*>(ws) + ws_stats_bytes(lq)
                                                                  : nullptr;
+    // and the split key/value pass when it also holds the partial sums
+    const size_t part_bytes = ws_part_bytes(lq, lk);
+    if (a.ds && part_bytes && ws_bytes >= ws_stats_bytes(lq) + ds_bytes + part_bytes) {
+        a.kv_split = kv_split_for(lq, lk, (mask.kind & FBL_MASK_CAUSAL) != 0);
+        a.dkv_part = reinterpret_cast<float*>(static_cast<char*>(ws) + ws_stats_bytes(lq) + ds_bytes);
+    }
     a.nq32 = (int)((lq->S + 31) / 32);
     a.nk32 = (int)((lk->S + 31) / 32);
     a.mq = tokmap(lq);

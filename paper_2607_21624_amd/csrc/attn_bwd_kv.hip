@@ -87,8 +87,9 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_kv_bf16(BwdArgs a) {
     const int c32 = lane & 31;
     const int S = a.S, Skv = a.Skv;  // query tokens, key tokens
     const int nkb = (Skv + kPKeys - 1) / kPKeys;
-    int kblk, bh;  // causal: key block 0 meets the most queries; start it first
-    if (!rank_major_item(blockIdx.x, nkb, a.Hkv * a.B, kblk, bh)) return;
+    int rank, bh;  // causal: key block 0 meets the most queries; start it first
+    if (!rank_major_item(blockIdx.x, nkb * a.kv_split, a.Hkv * a.B, rank, bh)) return;
+    const int kblk = rank / a.kv_split, split = rank % a.kv_split;
     const int hk = bh % a.Hkv;
     const int b = bh / a.Hkv;
     const int G_ = a.Hq / a.Hkv;
@@ -124,7 +125,13 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_kv_bf16(BwdArgs a) {
     const int qb_start = a.mask.causal ? (k0 / BQ) : 0;
     const int nqb = (S + BQ - 1) / BQ;
     const int per_head = nqb - qb_start;
-    const int n_iter = (k0 < kv_end) ? G_ * per_head : 0;
+    // this workgroup's share of the key block's iterations (G_ heads x
+    // per_head query blocks, head-major): [it_lo, it_hi) of split `split`
+    const int n_all = (k0 < kv_end) ? G_ * per_head : 0;
+    const int it_lo = (int)((int64_t)n_all * split / a.kv_split);
+    const int n_iter = (int)((int64_t)n_all * (split + 1) / a.kv_split) - it_lo;
+    const int h_lo = n_iter > 0 ? it_lo / per_head : 0;  // query head (within the group) of the first
+    const int j_lo = n_iter > 0 ? it_lo % per_head : 0;  // and its block index within that head
     // Blocks of each head whose scores need the causal mask: those holding a
     // query before one of the workgroup's keys.  Keys at or past kv_end need no
     // mask: a key's P and dS only reach that key's own dK and dV rows, which are
@@ -139,7 +146,8 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_kv_bf16(BwdArgs a) {
     const int kb32 = kw0 / 32;
     const bool ds_live = DS && kw0 < kv_end;  // keys past kv_end: never read
     const uint32_t ds_head_elems = (uint32_t)a.nq32 * (uint32_t)a.nk32 * 1024u;
-    const bf16* ds_head = DS ? static_cast<const bf16*>(a.ds) + ((int64_t)b * a.Hq + hk * G_) * ds_head_elems : nullptr;
+    const bf16* ds_head =
+        DS ? static_cast<const bf16*>(a.ds) + ((int64_t)b * a.Hq + hk * G_ + h_lo) * ds_head_elems : nullptr;
     __amdgpu_buffer_rsrc_t ds_rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16*>(ds_head), 0,
                                                                      (int)(ds_head_elems * 2u), 0x00020000);
 
@@ -150,17 +158,17 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_kv_bf16(BwdArgs a) {
     DmaPlan<bf16, D, BQ, kPWaves> pq, po;
     pq.init(qbytes, wave, lane);
     po.init(obytes, wave, lane);
-    const bf16* q_head = static_cast<const bf16*>(a.q) + a.mq.head_base(b, hk * G_);
-    const bf16* o_head = static_cast<const bf16*>(a.dout) + a.mdo.head_base(b, hk * G_);
+    const bf16* q_head = static_cast<const bf16*>(a.q) + a.mq.head_base(b, hk * G_ + h_lo);
+    const bf16* o_head = static_cast<const bf16*>(a.dout) + a.mdo.head_base(b, hk * G_ + h_lo);
     // wave 0 loads the LSE*log2e row, wave 1 the D row, waves 2 and 3 nothing
     // (no records) into a spare slot
-    const float* st_head = a.stats + (2 * ((int64_t)b * a.Hq + hk * G_) + (wave & 1)) * S;
+    const float* st_head = a.stats + (2 * ((int64_t)b * a.Hq + hk * G_ + h_lo) + (wave & 1)) * S;
     const uint32_t st_bytes = wave < 2 ? (uint32_t)S * 4u : 0u;
     const uint32_t st_lds0 = wave < 2 ? lds + P::OFF_ST + wave * 256 : lds + P::SPARE;
     const uint32_t st_step = wave < 2 ? P::STB : 0;
     Rsrc rq = make_rsrc(q_head, qspan), ro = make_rsrc(o_head, ospan), rst = make_rsrc(st_head, st_bytes);
-    uint32_t dma_q0 = (uint32_t)(qb_start * BQ);  // first query of the next block to stage
-    int dma_j = 0;                                // its index within its head
+    uint32_t dma_q0 = (uint32_t)((qb_start + j_lo) * BQ);  // first query of the next block to stage
+    int dma_j = j_lo;                                      // its index within its head
     // A block is staged in NPART loads per wave (Q tile, dO tile, statistics
     // row).
     constexpr int NPQ = DmaPlan<bf16, D, BQ, kPWaves>::PER_WAVE;
@@ -388,7 +396,7 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_kv_bf16(BwdArgs a) {
         for (int k = 0; k < NSDP; ++k) read_row(C1{}, k);  // stale when there is no block 1
     }
     // Blocks in order, four per trip (one per LDS buffer).
-    int j = 0;  // index of block `it` within its head's blocks
+    int j = j_lo;  // index of block `it` within its head's blocks
     auto next_j = [&]() {
         if (++j == per_head) {
             j = 0;
@@ -420,7 +428,28 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_kv_bf16(BwdArgs a) {
     // consecutive d per store.  Keys at or past kv_end take no part: their
     // accumulators hold unmasked (possibly non-finite) sums and are replaced
     // by zeros.
-    if (key < Skv) {
+    if (key < Skv && a.kv_split > 1) {
+        // fp32 partial sums of this split (zeros past kv_end)
+        const bool live = key < kv_end;
+        const int64_t plane = (int64_t)a.B * Skv * a.Hkv * D;
+        float* pk = a.dkv_part + (int64_t)split * plane + (((int64_t)b * Skv + key) * a.Hkv + hk) * D;
+        float* pv = pk + (int64_t)a.kv_split * plane;
+#pragma unroll
+        for (int t = 0; t < ND; ++t) {
+#pragma unroll
+            for (int rr = 0; rr < 4; ++rr) {
+                const int dcol = 32 * t + 8 * rr + 4 * g;
+                float k4[4], v4[4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    k4[e] = live ? dk[t][4 * rr + e] * a.scale : 0.f;
+                    v4[e] = live ? dv[t][4 * rr + e] : 0.f;
+                }
+                store4(pk + dcol, k4[0], k4[1], k4[2], k4[3]);
+                store4(pv + dcol, v4[0], v4[1], v4[2], v4[3]);
+            }
+        }
+    } else if (key < Skv) {
         const bool live = key < kv_end;
         bf16* dkrow = static_cast<bf16*>(a.dk) + a.mdk.head_base(b, hk) + (int64_t)key * a.mdk.ss;
         bf16* dvrow = static_cast<bf16*>(a.dv) + a.mdv.head_base(b, hk) + (int64_t)key * a.mdv.ss;
@@ -449,13 +478,43 @@ template __global__ void attn_bwd_kv_bf16<32, true>(BwdArgs);
 template __global__ void attn_bwd_kv_bf16<64, true>(BwdArgs);
 template __global__ void attn_bwd_kv_bf16<128, true>(BwdArgs);
 
+// dK and dV of a split key/value pass: the kv_split partial sums of each
+// element added in split order (deterministic), rounded once to bf16.  One
+// thread per 4 consecutive d of one (b, key, kv head) row; dK rows first.
+template <int D>
+__global__ __launch_bounds__(256) void attn_bwd_kv_reduce(BwdArgs a) {
+    constexpr int C4 = D / 4;
+    const int64_t rows = (int64_t)a.B * a.Skv * a.Hkv;
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i >= 2 * rows * C4) return;
+    const bool is_v = i >= rows * C4;
+    const int64_t r = is_v ? i - rows * C4 : i;
+    const int c4 = (int)(r % C4);
+    const int64_t row = r / C4;  // (b * Skv + key) * Hkv + hk
+    const int hk = (int)(row % a.Hkv);
+    const int key = (int)((row / a.Hkv) % a.Skv);
+    const int b = (int)(row / ((int64_t)a.Hkv * a.Skv));
+    const int64_t plane = rows * D;
+    const float* src = a.dkv_part + (is_v ? (int64_t)a.kv_split * plane : 0) + row * D + 4 * c4;
+    f32x4 acc = *reinterpret_cast<const f32x4*>(src);
+    for (int s = 1; s < a.kv_split; ++s) acc += *reinterpret_cast<const f32x4*>(src + s * plane);
+    const TokMap& m = is_v ? a.mdv : a.mdk;
+    bf16* dst = static_cast<bf16*>(is_v ? a.dv : a.dk) + m.head_base(b, hk) + (int64_t)key * m.ss + 4 * c4;
+    store4(dst, acc[0], acc[1], acc[2], acc[3]);
+}
+
 template <int D, bool DS>
 hipError_t launch_kv(const BwdArgs& a, hipStream_t stream) {
     const hipError_t once = ensure_dynamic_lds<&attn_bwd_kv_bf16<D, DS>>(KvPipe<D>::BYTES);
     if (once != hipSuccess) return once;
     constexpr int lds = KvPipe<D>::BYTES;
-    hipLaunchKernelGGL((attn_bwd_kv_bf16<D, DS>), dim3(rank_major_grid((a.Skv + kPKeys - 1) / kPKeys, a.Hkv * a.B)),
-                       dim3(256), lds, stream, a);
+    const int nkb = (a.Skv + kPKeys - 1) / kPKeys;
+    hipLaunchKernelGGL((attn_bwd_kv_bf16<D, DS>), dim3(rank_major_grid(nkb * a.kv_split, a.Hkv * a.B)), dim3(256),
+                       lds, stream, a);
+    if (a.kv_split > 1) {
+        const int64_t n = 2 * (int64_t)a.B * a.Skv * a.Hkv * (D / 4);
+        hipLaunchKernelGGL((attn_bwd_kv_reduce<D>), dim3((unsigned)((n + 255) / 256)), dim3(256), 0, stream, a);
+    }
     return hipGetLastError();
 }
 

@@ -63,6 +63,12 @@ struct BwdArgs {
     float scale;       // softmax scale
     float scale_log2;  // scale * log2(e)
     MaskArgs mask;
+    // Key/value pass split: each key block's query iterations are shared by
+    // kv_split workgroups, which write fp32 partial dK (times scale) and dV to
+    // dkv_part, [2][kv_split][B, Skv, Hkv, D] (dK planes, then dV); a reduction
+    // adds them in split order.  1: no split, dK and dV written directly.
+    float* dkv_part = nullptr;
+    int kv_split = 1;
 };
 
 // Matrix product C[M, N] = sum_k A(m, k) B(k, n), bf16 operands, row-major

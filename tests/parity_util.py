@@ -49,7 +49,9 @@ def rel_err(got: np.ndarray, ref: np.ndarray) -> float:
 def gpu_fwd_bwd(inp: dict, stream=None, dO=None, workspace: str = "full"):
     """Run fbl_attn_fwd then fbl_attn_bwd on the inputs of one workload.
     workspace "full" (fbl_attn_bwd_workspace bytes: dQ from the stored dS for
-    bf16) or "min" (fbl_attn_bwd_workspace_min bytes: dQ recomputes S and dP).
+    bf16, and the key/value pass split where the shape calls for it), "ds"
+    (statistics and dS only: stored dS, no split) or "min"
+    (fbl_attn_bwd_workspace_min bytes: dQ recomputes S and dP).
     Returns a dict of numpy float64 arrays (o, lse, dq, dk, dv)."""
     import torch
     import paper_2607_21624_amd as fbl
@@ -64,7 +66,12 @@ def gpu_fwd_bwd(inp: dict, stream=None, dO=None, workspace: str = "full"):
     scale = 1.0 / math.sqrt(w.d)
     o, lse = fbl.attn_fwd(q, k, v, w.Hq, w.Hkv, scale, causal, kv_len)
     lq, lk = fbl.layout_of(q, w.Hq), fbl.layout_of(k, w.Hkv)
-    size = fbl.fbl_attn_bwd_workspace(lq, lk) if workspace == "full" else fbl.fbl_attn_bwd_workspace_min(lq, lk)
+    if workspace == "full":
+        size = fbl.fbl_attn_bwd_workspace(lq, lk)
+    elif workspace == "ds":  # statistics and dS blocks only: stored dS, key/value pass not split
+        size = fbl.fbl_attn_bwd_workspace_min(lq, lk) + w.B * w.Hq * -(-w.S // 32) * -(-w.Skv // 32) * 2048
+    else:
+        size = fbl.fbl_attn_bwd_workspace_min(lq, lk)
     ws = torch.empty(size, dtype=torch.uint8, device="cuda")
     dq, dk, dv = fbl.attn_bwd(q, k, v, o, do, lse, w.Hq, w.Hkv, scale, causal, kv_len, workspace=ws)
     torch.cuda.synchronize()

@@ -228,9 +228,24 @@ def test_row_offset_limit():
     assert _bwd(lq, lk, lv, wide(lo), p, ws, ldo=lo) == E.FBL_ERR_UNSUPPORTED
 
 
+def kv_split(B, Sq, Skv, Hq, Hkv, D):
+    """The key/value pass split rule, restated: items are key blocks of 128
+    per (batch, kv head); split 2 (then 4) while there are fewer than 512
+    items and the first key block keeps 16 iterations (of 32 queries at
+    D = 128, else 64) per share."""
+    items = -(-Skv // 128) * Hkv * B
+    iters = Hq // Hkv * -(-Sq // (32 if D == 128 else 64))
+    split = 1
+    while split < 4 and items * split < 512 and iters >= 16 * split:
+        split *= 2
+    return split
+
+
 def test_bwd_workspace_size():
     """Minimum: the row statistics, [B, Hq, 2, S] fp32 rounded up to 256 bytes.
-    Full (bf16): plus B*Hq*ceil(S/32)^2 dS blocks of 2 KB; fp32: statistics only."""
+    Full (bf16): plus B*Hq*ceil(S/32)^2 dS blocks of 2 KB, plus, when the
+    key/value pass is split, the fp32 partial dK and dV [2][split][B, S, Hkv, D];
+    fp32: statistics only."""
     for dt, with_ds in ((BF16, True), (F32, False)):
         for S in (16, 100, 1024):
             lq = fbl.fbl_layout_desc(dt, 2, S, 6, 64)
@@ -238,7 +253,18 @@ def test_bwd_workspace_size():
             stats = (2 * 6 * S * 2 * 4 + 255) // 256 * 256
             assert fbl.fbl_attn_bwd_workspace_min(lq, lk) == stats
             nb = (S + 31) // 32
-            assert fbl.fbl_attn_bwd_workspace(lq, lk) == stats + (2 * 6 * nb * nb * 2048 if with_ds else 0)
+            split = kv_split(2, S, S, 6, 3, 64)
+            part = 2 * split * 2 * S * 3 * 64 * 4 if split > 1 else 0
+            assert fbl.fbl_attn_bwd_workspace(lq, lk) == stats + ((2 * 6 * nb * nb * 2048 + part) if with_ds else 0)
+    assert kv_split(2, 1024, 1024, 6, 3, 64) == 4 and kv_split(2, 100, 100, 6, 3, 64) == 1
+    # the Llama-3.2-1B-like GQA shape: 256 items, split in two; the Llama-7B-like shape: 1024 items, no split
+    assert kv_split(2, 2048, 2048, 32, 8, 64) == 2 and kv_split(1, 4096, 4096, 32, 32, 128) == 1
+    for (B, S, Hq, Hkv, D) in ((2, 2048, 32, 8, 64), (1, 4096, 32, 32, 128), (4, 1024, 16, 16, 64)):
+        lq, lk = fbl.fbl_layout_desc(BF16, B, S, Hq, D), fbl.fbl_layout_desc(BF16, B, S, Hkv, D)
+        nb = (S + 31) // 32
+        rest = fbl.fbl_attn_bwd_workspace(lq, lk) - fbl.fbl_attn_bwd_workspace_min(lq, lk) - B * Hq * nb * nb * 2048
+        split = kv_split(B, S, S, Hq, Hkv, D)
+        assert rest == (2 * split * B * S * Hkv * D * 4 if split > 1 else 0), (B, S, Hq, Hkv, D)
     # cross-attention: statistics per query row, dS blocks ceil(S_q/32) x ceil(S_kv/32)
     lq = fbl.fbl_layout_desc(BF16, 2, 100, 6, 64)
     lk = fbl.fbl_layout_desc(BF16, 2, 70, 3, 64)

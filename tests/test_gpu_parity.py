@@ -130,6 +130,32 @@ def test_recompute_dq_path(d, mask, S):
         assert not bad, f"workspace {ws}: {bad}"
 
 
+# ------------------------------------------- split key/value pass (GQA, few key blocks)
+@pytest.mark.parametrize("B,S,Hq,Hkv,d,mask", [(1, 1024, 8, 2, 128, synth.MASK_CAUSAL),
+                                               (2, 700, 8, 2, 64, synth.MASK_CAUSAL | synth.MASK_KEY_PADDING),
+                                               (1, 513, 4, 1, 128, synth.MASK_NONE),
+                                               (2, 2048, 32, 8, 64, synth.MASK_CAUSAL)])
+def test_split_kv_pass(B, S, Hq, Hkv, d, mask):
+    """Few key blocks per CU: the key/value pass shares each key block's query
+    iterations among 2 or 4 workgroups (fp32 partial dK/dV added in a fixed
+    order).  The split, the unsplit stored-dS pass and the recompute pass must
+    all meet the oracle, and the split run must be bitwise repeatable."""
+    w = synth.Workload(f"split{S}", B=B, S=S, Hq=Hq, Hkv=Hkv, d=d, dtype="bf16", mask=mask, seed=S + Hq + d)
+    inp = synth.make_inputs(w)
+    kv_heads = None if Hkv <= 2 else [0, Hkv - 1]
+    note(f"split kv B={B} S={S} Hq={Hq} Hkv={Hkv} d={d} mask={mask}")
+    ref = oracle_fwd_bwd(inp, kv_heads)
+    full = gpu_fwd_bwd(inp)
+    for ws in ("full", "ds", "min"):
+        got = full if ws == "full" else gpu_fwd_bwd(inp, workspace=ws)
+        errs, bad = compare(select_heads(got, w, kv_heads), ref, "bf16")
+        note(f"split kv workspace {ws}: {errs}")
+        assert not bad, f"workspace {ws}: {bad}"
+    again = gpu_fwd_bwd(inp)
+    for n in ("dq", "dk", "dv"):
+        assert np.array_equal(again[n], full[n]), n
+
+
 # ---------------------------------------------------------- cross-attention
 @pytest.mark.parametrize("name", list(synth.CROSS_WORKLOADS))
 def test_cross_attention_workloads(name):
