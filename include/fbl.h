@@ -193,12 +193,12 @@ fbl_status fbl_attn_fwd(const fbl_layout* lq, const void* q, const fbl_layout* l
  * blocks would reach 2 GiB (S_q = S_kv above 32736).
  * Part 3, with part 2, where the key/value pass has fewer than 512 blocks of
  * 128 keys (B * Hkv * ceil(S_kv/128)) and the first block at least 16 query
- * iterations per share (Hq/Hkv * ceil(S_q/32) at D = 128, ceil(S_q/64)
- * otherwise): the pass splits each key block's iterations among 2, or 4, workgroups
- * (4 below 128 blocks when the iterations allow), and this part holds their
- * fp32 partial dK and dV, 2 * split * B*S_kv*Hkv*D floats, which a
- * reduction adds in a fixed order.  Without a causal mask the split is used
- * only while the split grid fits 256 compute units.
+ * iterations per share (Hq/Hkv * ceil(S_q/32), ceil(S_q/64) at D = 32): the
+ * pass splits each key block's iterations among 2, or 4, workgroups (4 below
+ * 128 blocks when the iterations allow), and this part holds their fp32
+ * partial dK and dV, 2 * split * B*S_kv*Hkv*D floats, which a reduction adds
+ * in a fixed order.  Without a causal mask the split is used only while the
+ * split grid fits the resident workgroups (256, or 512 at D = 64).
  */
 fbl_status fbl_attn_bwd_workspace(const fbl_layout* lq, const fbl_layout* lk, size_t* bytes);
 

@@ -164,22 +164,23 @@ size_t ws_ds_bytes(const fbl_layout* lq, const fbl_layout* lk) {
 // blocks of 128 keys per (batch, kv head).  Under a causal mask the first key
 // blocks carry the most queries, and with fewer than two items per CU (512)
 // the pass waits on those few large items while other CUs idle; without a
-// mask the items are equal and only a grid of fewer items than CUs leaves CUs
-// idle.  Sharing each key block's query iterations among 2 (or 4) workgroups
+// mask the items are equal and only a grid of fewer items than workgroup
+// slots (256 CUs, two workgroups each at D = 64) leaves CUs idle.  Sharing each key block's query iterations among 2 (or 4) workgroups
 // gives the scheduler items of half (a quarter) the size; each writes fp32
 // partial dK and dV and a reduction adds them in a fixed order.  Causal: split
-// while below 512 items; otherwise while the split grid still fits the 256
-// CUs.  Only where the first key block has at least 16 iterations per share.
+// while below 512 items; otherwise while the split grid still fits the slots.
+// Only where the first key block has at least 16 iterations per share.
 // (Measured: splitting the 512 items of the GPT-2-medium-like causal shape,
 // or the Llama-3.2-1B-like GQA shape four ways, is slower.)  The causal
 // choice is never below the other, so it sizes the workspace.
 int kv_split_for(const fbl_layout* lq, const fbl_layout* lk, bool causal = true) {
     if (lq->dtype != FBL_BF16 || lk->H <= 0 || lq->D <= 0) return 1;
     const int64_t items = (lk->S + 127) / 128 * lk->H * lk->B;
-    const int64_t bq = lq->D == 128 ? 32 : 64;  // queries per iteration
+    const int64_t bq = lq->D == 32 ? 64 : 32;     // queries per iteration
+    const int64_t slots = lq->D == 64 ? 512 : 256;  // workgroups resident at once (two per CU at D = 64)
     const int64_t iters = lq->H / lk->H * ((lq->S + bq - 1) / bq);
     int split = 1;
-    while (split < 4 && (causal ? items * split < 512 : items * split * 2 <= 256) && iters >= 16 * split) split *= 2;
+    while (split < 4 && (causal ? items * split < 512 : items * split * 2 <= slots) && iters >= 16 * split) split *= 2;
     return split;
 }
 

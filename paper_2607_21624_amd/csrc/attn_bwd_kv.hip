@@ -10,9 +10,10 @@
 //   S_i  = Q_i K_w^T,  dP_i = dO_i V_w^T        (row reads of the Q/dO tiles)
 //   P_i  = exp2(S_i scale log2e - LSE_i log2e), dS_i = P_i (dP_i - D_i)
 //   dV^T += dO_i^T P_i,  dK^T += Q_i^T dS_i      (transposed reads)
-// With one wavefront per SIMD (the accumulators take half the register file)
-// nothing else hides latency, and every instruction the wavefront issues
-// besides the products costs time, so the loop is software-pipelined by hand:
+// At D = 128 there is one wavefront per SIMD (the accumulators take half the
+// register file; at D = 64 two workgroups share a CU) and little else hides
+// latency: every instruction the wavefront issues besides the products costs
+// time, so the loop is software-pipelined by hand:
 //   phase X(i): S/dP products of block i+1  |  elementwise step of block i
 //   barrier; DMA of block i+3
 //   phase Y(i): dV/dK products of block i   |  LDS reads of block i's
@@ -52,7 +53,10 @@ constexpr int kLead = 4;              // product slots between an operand read a
 
 template <int D>
 struct KvPipe {
-    static constexpr int BQ = D == 128 ? 32 : 64;  // queries per block (register budget)
+    // queries per block: 32 (64 at D = 32).  At D = 64 the wavefront's state
+    // fits 256 registers, so two workgroups share a CU (two waves per SIMD).
+    static constexpr int BQ = D == 32 ? 64 : 32;
+    static constexpr int OCC = D == 64 ? 2 : 1;
     static constexpr int NQT = BQ / 32;
     static constexpr int TB = BQ * D * 2;  // bytes of one bf16 Q or dO tile
     static constexpr int NBUF = 4;
@@ -70,7 +74,7 @@ struct KvPipe {
 };
 
 template <int D, bool DS>
-__global__ __launch_bounds__(256, 1) void attn_bwd_kv_bf16(BwdArgs a) {
+__global__ __launch_bounds__(256, KvPipe<D>::OCC) void attn_bwd_kv_bf16(BwdArgs a) {
     using P = KvPipe<D>;
     constexpr int NC = D / 16;
     constexpr int ND = D / 32;

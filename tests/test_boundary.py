@@ -229,12 +229,12 @@ def test_row_offset_limit():
 
 
 def kv_split(B, Sq, Skv, Hq, Hkv, D):
-    """The key/value pass split rule, restated: items are key blocks of 128
-    per (batch, kv head); split 2 (then 4) while there are fewer than 512
-    items and the first key block keeps 16 iterations (of 32 queries at
-    D = 128, else 64) per share."""
+    """The key/value pass split rule under a causal mask, restated: items are
+    key blocks of 128 per (batch, kv head); split 2 (then 4) while there are
+    fewer than 512 items and the first key block keeps 16 iterations (of 32
+    queries, 64 at D = 32) per share."""
     items = -(-Skv // 128) * Hkv * B
-    iters = Hq // Hkv * -(-Sq // (32 if D == 128 else 64))
+    iters = Hq // Hkv * -(-Sq // (64 if D == 32 else 32))
     split = 1
     while split < 4 and items * split < 512 and iters >= 16 * split:
         split *= 2
