@@ -288,6 +288,42 @@ def test_strided_views_of_packed_projection():
     assert not bad, bad
 
 
+@pytest.mark.parametrize("d,mask", [(64, synth.MASK_CAUSAL), (128, synth.MASK_KEY_PADDING)])
+def test_sequence_sliced_views(d, mask):
+    """Q, K, V, dO and the outputs as the first 200 tokens of 300-token buffers
+    (batch stride 300 rows, larger than S rows): the tail rows hold NaN and
+    must be neither read (a read would bring NaN into the results) nor
+    written (they must still hold NaN afterwards)."""
+    import torch
+    fbl = _lib()
+    B, S, S_full, Hq, Hkv = 3, 200, 300, 4, 2
+    w = synth.Workload("sliced", B=B, S=S, Hq=Hq, Hkv=Hkv, d=d, dtype="bf16", mask=mask, seed=d + 5)
+    inp = synth.make_inputs(w)
+    note(f"sequence-sliced views d={d} mask={mask}")
+
+    def view(cols, data=None):
+        full = torch.full((B, S_full, cols), float("nan"), dtype=torch.bfloat16, device="cuda")
+        if data is not None:
+            full[:, :S].copy_(to_dev(data, "bf16"))
+        return full, full[:, :S]
+
+    (qf, q), (kf, k), (vf, v), (dof, do) = (view(Hq * d, inp["q"]), view(Hkv * d, inp["k"]),
+                                            view(Hkv * d, inp["v"]), view(Hq * d, inp["do"]))
+    (of, o), (dqf, dq), (dkf, dk), (dvf, dv) = view(Hq * d), view(Hq * d), view(Hkv * d), view(Hkv * d)
+    assert q.stride(0) == S_full * Hq * d and not q.is_contiguous()
+    kv_len = None if inp["kv_len"] is None else torch.from_numpy(inp["kv_len"].astype(np.int32)).to("cuda")
+    causal = bool(mask & synth.MASK_CAUSAL)
+    scale = 1.0 / math.sqrt(d)
+    _, lse = fbl.attn_fwd(q, k, v, Hq, Hkv, scale, causal, kv_len, out=o)
+    fbl.attn_bwd(q, k, v, o, do, lse, Hq, Hkv, scale, causal, kv_len, dq=dq, dk=dk, dv=dv)
+    torch.cuda.synchronize()
+    got = {"o": to_np(o), "lse": to_np(lse), "dq": to_np(dq), "dk": to_np(dk), "dv": to_np(dv)}
+    errs, bad = compare(got, oracle_fwd_bwd(inp), "bf16")
+    assert not bad, bad
+    for name, full in (("o", of), ("dq", dqf), ("dk", dkf), ("dv", dvf)):
+        assert torch.isnan(full[:, S:].float()).all(), f"{name}: rows past S were written"
+
+
 def test_largest_row_stride():
     """At the largest accepted row stride, (S + 128) * ss * 2 = 2^31 bytes:
     every tensor (inputs, O, dO and the gradients) is a view with 8 MB between
