@@ -294,6 +294,11 @@ def test_bwd_rejections():
     assert _bwd(lq, lk, lv, lo, p, ws, kind=F.FBL_MASK_KEY_PADDING) == E.FBL_ERR_NULL
     assert _bwd(lq, lk, lv, lo, p, ws, scale=float("nan")) == E.FBL_ERR_ARG
     assert _bwd(lq, lk, lv, lo, dict(p, lse=p["lse"] + 4), ws) == E.FBL_ERR_ALIGN
+    # phase masks: none, or a bit outside FBL_BWD_ALL
+    for ph in (0, 8, F.FBL_BWD_ALL | 16):
+        assert fbl.fbl_attn_bwd_raw(lq, p["q"], lk, p["k"], lv, p["v"], lo, p["o"], lo, p["do"], p["lse"], 0.1,
+                                    F.Mask(0, 0, None), lq, p["dq"], lk, p["dk"], lv, p["dv"], p["ws"], ws,
+                                    stream=0, phases=ph) == E.FBL_ERR_ARG, ph
 
 
 def test_layout_map_device_rejects_null():

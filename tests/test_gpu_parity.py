@@ -324,6 +324,55 @@ def test_sequence_sliced_views(d, mask):
         assert torch.isnan(full[:, S:].float()).all(), f"{name}: rows past S were written"
 
 
+@pytest.mark.parametrize("name", ["gpt2_medium_causal", "llama32_1b_gqa", "bert_base_keypad"])
+def test_backward_phases_separately(name):
+    """fbl_attn_bwd_phases: the preprocessing, key/value and dQ phases as three
+    calls -- on one stream, then on two streams ordered by an event -- give the
+    bits of the single call (the Llama-3.2-1B-like shape with its split key/value
+    pass)."""
+    import torch
+    fbl = _lib()
+    w = synth.WORKLOADS[name]
+    inp = synth.make_inputs(w)
+    note(f"backward phases separately {name}")
+    q, k, v, do = (to_dev(inp[n], "bf16") for n in ("q", "k", "v", "do"))
+    kv_len = None if inp["kv_len"] is None else torch.from_numpy(inp["kv_len"].astype(np.int32)).to("cuda")
+    causal = bool(w.mask & synth.MASK_CAUSAL)
+    scale = 1.0 / math.sqrt(w.d)
+    o, lse = fbl.attn_fwd(q, k, v, w.Hq, w.Hkv, scale, causal, kv_len)
+    ws = torch.empty(fbl.fbl_attn_bwd_workspace(fbl.layout_of(q, w.Hq), fbl.layout_of(k, w.Hkv)),
+                     dtype=torch.uint8, device="cuda")
+    outs = [torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)]
+    run = lambda ph, stream=None: fbl.attn_bwd(q, k, v, o, do, lse, w.Hq, w.Hkv, scale, causal, kv_len,
+                                               dq=outs[0], dk=outs[1], dv=outs[2], workspace=ws, phases=ph,
+                                               stream=stream)
+    run(fbl.FBL_BWD_ALL)
+    torch.cuda.synchronize()
+    ref = [t.clone() for t in outs]
+    for t in outs:
+        t.fill_(float("nan"))
+    ws.fill_(0xFF)
+    for ph in (fbl.FBL_BWD_PREP, fbl.FBL_BWD_KV, fbl.FBL_BWD_Q):
+        run(ph)
+    torch.cuda.synchronize()
+    assert all(torch.equal(a, b) for a, b in zip(outs, ref)), "three calls on one stream"
+    for t in outs:
+        t.fill_(float("nan"))
+    ws.fill_(0xFF)
+    torch.cuda.synchronize()
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    with torch.cuda.stream(s1):
+        run(fbl.FBL_BWD_PREP, stream=s1)
+        done = torch.cuda.Event()
+        done.record(s1)
+    s2.wait_event(done)
+    with torch.cuda.stream(s2):
+        run(fbl.FBL_BWD_KV, stream=s2)
+        run(fbl.FBL_BWD_Q, stream=s2)
+    torch.cuda.synchronize()
+    assert all(torch.equal(a, b) for a, b in zip(outs, ref)), "phases on two streams"
+
+
 def test_largest_row_stride():
     """At the largest accepted row stride, (S + 128) * ss * 2 = 2^31 bytes:
     every tensor (inputs, O, dO and the gradients) is a view with 8 MB between
