@@ -551,35 +551,53 @@ int32_t tuned_tile(uint32_t op, int64_t M, int64_t K, int64_t N) {
     return it == g_tuned.end() ? -1 : it->second;
 }
 
-// Untuned choice among the candidates, by how many 128 x 128 output tiles the
-// product has and how long its contraction is (measured on the 512 x 2048 x
-// 8192 and 4096 x 4096 x {4096, 12288} products and their transposes): with at
-// least four per CU (1024) and a contraction of 2048 or more, the 256 x 256
-// tiles (8 wavefronts first when A is read along its rows, 4 first for the
-// weight gradient's transposed A), then the 8-wavefront 256 x 128 ones; with
-// at least four per CU and a
-// short contraction, 4-wavefront tiles with small LDS, several workgroups per
-// CU; with at least one per CU, the 8-wavefront 128 x 128 tile; below that,
-// 64 x 64 tiles whose four wavefronts split the contraction.  The first
-// candidate of the order that gives at least one workgroup per CU (256) wins,
-// else the first candidate.
+// Untuned choice among the candidates, by how many 128 x 128 output tiles
+// the product has (n128) and how long its contraction is -- measured on the
+// 512 x {2048, 4096} x {8192, 12288}, {1024, 2048} x 4096 x 4096 and 4096 x
+// 4096 x {4096, 12288} products and their transposes:
+//   n128 >= 1024, contraction >= 2048: the 256 x 256 tiles, 8 wavefronts
+//     first when A is read along its rows, 4 first for the weight gradient's
+//     transposed A;
+//   n128 >= 1024, shorter contraction: the weight gradient's 8-wavefront
+//     64 x 128-per-wave 256 x 256 tile, else 4-wavefront 128 x 128 tiles;
+//   384 <= n128 < 1024: the 8-wavefront 256 x 128 and 128 x 256 tiles, even
+//     below one workgroup per CU (two waves per SIMD do more for these than
+//     a full grid of 4-wavefront tiles);
+//   256 <= n128 < 384: 4-wavefront 64 x 128 and 128 x 64 tiles;
+//   below: the 8-wavefront 128 x 64 tile that splits a deep contraction four
+//     ways, then the 4-wavefront 64 x 64 one.
+// Orders marked `fill` take the first candidate that gives at least one
+// workgroup per CU (256), else the first candidate; the others take the
+// first candidate.
 int32_t default_tile(const ProjPlan& pl) {
     static const int big[] = {19, 18, 20, 17, 11, 12, 8, 4, 0, 6, 5, 2, 1, 10, 9, 7, 3, 13, 15, 14, 16};
     static const int big_t[] = {18, 20, 19, 17, 11, 12, 8, 4, 0, 6, 5, 2, 1, 10, 9, 7, 3, 13, 15, 14, 16};
     static const int many[] = {0, 4, 8, 1, 2, 5, 6, 11, 12, 10, 9, 7, 3, 13, 15, 14, 16, 17, 18, 19, 20};
-    static const int some[] = {8, 4, 6, 5, 11, 12, 0, 2, 1, 10, 9, 7, 3, 13, 15, 14, 16, 17, 18, 19, 20};
-    static const int few[] = {9, 10, 7, 6, 5, 8, 4, 3, 2, 1, 0, 11, 12, 14, 13, 15, 16, 17, 18, 19, 20};
+    static const int many_t[] = {20, 18, 19, 0, 4, 8, 1, 2, 5, 6, 11, 12, 10, 9, 7, 3, 13, 15, 14, 16, 17};
+    static const int wide[] = {11, 12, 8, 4, 0, 5, 6, 2, 1, 10, 9, 7, 3, 13, 15, 14, 16, 17, 18, 19, 20};
+    static const int some[] = {6, 5, 8, 4, 11, 12, 0, 2, 1, 10, 9, 7, 3, 13, 15, 14, 16, 17, 18, 19, 20};
+    static const int few[] = {10, 9, 7, 6, 5, 8, 4, 3, 2, 1, 0, 11, 12, 14, 13, 15, 16, 17, 18, 19, 20};
     static_assert(sizeof(many) == sizeof(int) * fbl::kGemmTileCount && sizeof(some) == sizeof(many) &&
-                      sizeof(few) == sizeof(many) && sizeof(big) == sizeof(many) && sizeof(big_t) == sizeof(many),
+                      sizeof(few) == sizeof(many) && sizeof(big) == sizeof(many) && sizeof(big_t) == sizeof(many) &&
+                      sizeof(many_t) == sizeof(many) && sizeof(wide) == sizeof(many),
                   "every tile ranked once");
     const uint64_t cand = candidate_set(pl);
     const int64_t n128 = ((pl.orows + 127) / 128) * ((pl.ocols + 127) / 128);
-    const int* order =
-        n128 >= 1024 ? (pl.kc >= 2048 ? (pl.a_kmajor ? big_t : big) : many) : (n128 >= 256 ? some : few);
+    const int* order;
+    bool fill = true;
+    if (n128 >= 1024) {
+        order = pl.kc >= 2048 ? (pl.a_kmajor ? big_t : big) : (pl.a_kmajor ? many_t : many);
+    } else if (n128 >= 384) {
+        order = wide;
+        fill = false;
+    } else {
+        order = n128 >= 256 ? some : few;
+    }
     int32_t first = -1;
     for (int i = 0; i < fbl::kGemmTileCount; ++i) {
         const int t = order[i];
         if (!(cand >> t & 1)) continue;
+        if (!fill) return t;
         const fbl::GemmTile& g = fbl::kGemmTiles[t];
         if (((pl.orows + g.bm - 1) / g.bm) * ((pl.ocols + g.bn - 1) / g.bn) >= 256) return t;
         if (first < 0) first = t;
