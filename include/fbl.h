@@ -375,6 +375,16 @@ fbl_status fbl_proj_tune(uint32_t op, int64_t M, int64_t K, int64_t N, const voi
 int32_t fbl_proj_tuned_tile(uint32_t op, int64_t M, int64_t K, int64_t N);
 void fbl_proj_tune_reset(void);
 
+/*
+ * The tile id FBL_GEMM_TILE_AUTO resolves to for a bf16 product (op, M, K,
+ * N): the tuned choice when the table holds one, else the untuned preference
+ * among the candidates -- by the number of 128 x 128 output tiles and the
+ * contraction length, measured on MI355X.  The untuned choice depends on the
+ * shape only (not on leading dimensions or pointers).  Pure host function.
+ * FBL_ERR_NULL, FBL_ERR_ARG (unknown op) or FBL_ERR_SHAPE on bad arguments.
+ */
+fbl_status fbl_proj_auto_tile(uint32_t op, int64_t M, int64_t K, int64_t N, int32_t* tile);
+
 /* Static, human-readable name of a status code. */
 const char* fbl_status_str(fbl_status s);
 

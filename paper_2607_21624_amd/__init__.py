@@ -10,6 +10,6 @@ from .fbl import (  # noqa: F401
     attn_bwd, attn_bwd_packed, attn_fwd, attn_fwd_packed, fbl_attn_bwd_raw, fbl_attn_bwd_workspace, fbl_attn_bwd_workspace_min, fbl_attn_fwd_raw,
     fbl_layout_desc, fbl_layout_packed_qkv, fbl_proj_raw, proj, FBL_PROJ_FWD, FBL_PROJ_BWD_DATA, FBL_PROJ_BWD_WEIGHT,
     FBL_GEMM_TILE_AUTO, FBL_GEMM_TILE_128x128, FBL_GEMM_TILE_128x64, FBL_GEMM_TILE_64x128, FBL_GEMM_TILE_64x64,
-    FBL_TUNE_TIME, FBL_TUNE_GFLOPS_X_MEMEFF, gemm_tiles, proj_candidates, proj_tune, proj_tuned_tile, proj_tune_reset,
+    FBL_TUNE_TIME, FBL_TUNE_GFLOPS_X_MEMEFF, gemm_tiles, proj_candidates, proj_tune, proj_tuned_tile, proj_auto_tile, proj_tune_reset,
     fbl_layout_desc_status, fbl_layout_map_device, fbl_layout_offset, layout_of, status_str,
 )

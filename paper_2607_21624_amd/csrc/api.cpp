@@ -728,6 +728,17 @@ fbl_status fbl_proj(uint32_t op, int64_t M, int64_t K, int64_t N, const void* a,
 
 int32_t fbl_proj_tuned_tile(uint32_t op, int64_t M, int64_t K, int64_t N) { return tuned_tile(op, M, K, N); }
 
+fbl_status fbl_proj_auto_tile(uint32_t op, int64_t M, int64_t K, int64_t N, int32_t* tile) {
+    if (!tile) return FBL_ERR_NULL;
+    if (op > FBL_PROJ_BWD_WEIGHT) return FBL_ERR_ARG;
+    if (M <= 0 || K <= 0 || N <= 0 || M > INT32_MAX || K > INT32_MAX || N > INT32_MAX) return FBL_ERR_SHAPE;
+    ProjPlan pl;
+    proj_shape(op, M, K, N, pl);
+    const int32_t t = tuned_tile(op, M, K, N);
+    *tile = t >= 0 ? t : default_tile(pl);
+    return FBL_OK;
+}
+
 void fbl_proj_tune_reset(void) {
     std::lock_guard<std::mutex> lock(g_tuned_mu);
     g_tuned.clear();

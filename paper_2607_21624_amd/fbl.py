@@ -49,7 +49,7 @@ FBL_TUNE_GFLOPS_X_MEMEFF = 1
 
 EXPORTED = ("fbl_layout_desc", "fbl_layout_packed_qkv", "fbl_layout_offset", "fbl_layout_map_device", "fbl_attn_fwd",
             "fbl_attn_bwd_workspace", "fbl_attn_bwd_workspace_min", "fbl_attn_bwd", "fbl_attn_bwd_phases", "fbl_proj", "fbl_proj_dt",
-            "fbl_gemm_tile_count", "fbl_gemm_tile_info", "fbl_proj_candidates", "fbl_proj_tune", "fbl_proj_tuned_tile",
+            "fbl_gemm_tile_count", "fbl_gemm_tile_info", "fbl_proj_candidates", "fbl_proj_tune", "fbl_proj_tuned_tile", "fbl_proj_auto_tile",
             "fbl_proj_tune_reset", "fbl_status_str")
 
 
@@ -129,6 +129,8 @@ def _load() -> ctypes.CDLL:
     lib.fbl_proj_tune.restype = ctypes.c_int
     lib.fbl_proj_tuned_tile.argtypes = [ctypes.c_uint32] + [ctypes.c_int64] * 3
     lib.fbl_proj_tuned_tile.restype = ctypes.c_int32
+    lib.fbl_proj_auto_tile.argtypes = [ctypes.c_uint32] + [ctypes.c_int64] * 3 + [ctypes.POINTER(ctypes.c_int32)]
+    lib.fbl_proj_auto_tile.restype = ctypes.c_int
     lib.fbl_proj_tune_reset.argtypes = []
     lib.fbl_proj_tune_reset.restype = None
     lib.fbl_status_str.argtypes = [ctypes.c_int]
@@ -463,6 +465,13 @@ def proj_tune(op: int, a, b, out, objective: int = FBL_TUNE_TIME, reps: int = 10
 def proj_tuned_tile(op: int, M: int, K: int, N: int) -> int:
     """The tile fbl_proj_tune chose for this shape in this process, or -1."""
     return LIB.fbl_proj_tuned_tile(op, M, K, N)
+
+
+def proj_auto_tile(op: int, M: int, K: int, N: int) -> int:
+    """The tile id FBL_GEMM_TILE_AUTO resolves to for this bf16 product."""
+    t = ctypes.c_int32(-1)
+    _check(LIB.fbl_proj_auto_tile(op, M, K, N, ctypes.byref(t)), "fbl_proj_auto_tile")
+    return t.value
 
 
 def proj_tune_reset() -> None:

@@ -438,6 +438,30 @@ def test_proj_candidates_filters():
     assert fbl.LIB.fbl_proj_candidates(F.FBL_PROJ_FWD, M, K, N, None, 4, ctypes.byref(n)) == F.FBL_ERR_NULL
 
 
+def test_proj_auto_tile_measured_regimes():
+    """FBL_GEMM_TILE_AUTO without a tuned entry follows the measured preference
+    orders: 256 x 256 tiles from 1024 output tiles of 128 x 128 with a long
+    contraction (8 wavefronts for row-read A, 4 for the weight gradient), the
+    8-wavefront 256 x 128 tile from 384, 64 x 128 from 256, the deep-contraction
+    split tile below; the choice is always a candidate."""
+    fbl.proj_tune_reset()
+    A = fbl.proj_auto_tile
+    FWD, BD, BW = F.FBL_PROJ_FWD, F.FBL_PROJ_BWD_DATA, F.FBL_PROJ_BWD_WEIGHT
+    assert A(FWD, 4096, 4096, 12288) == 19 and A(BD, 4096, 4096, 12288) == 19
+    assert A(BW, 4096, 4096, 12288) == 18 and A(BW, 2048, 4096, 4096) == 18
+    assert A(BW, 512, 4096, 12288) == 20                     # 3072 output tiles, contraction 512
+    assert A(FWD, 512, 4096, 12288) == 11 and A(FWD, 2048, 4096, 4096) == 11   # 384 and 512 output tiles
+    assert A(FWD, 512, 2048, 8192) == 6                      # 256 output tiles
+    assert A(BD, 512, 4096, 12288) == 10                     # 128 output tiles, a grid of 256
+    assert A(BD, 512, 2048, 8192) == 9                       # 64 output tiles: the 64 x 64 split tile fills the CUs
+    for op, M, K, N in ((FWD, 512, 2048, 16), (BW, 512, 16, 2048), (FWD, 64, 96, 64), (BD, 192, 128, 256)):
+        assert A(op, M, K, N) in fbl.proj_candidates(op, M, K, N)
+    t = ctypes.c_int32()
+    assert fbl.LIB.fbl_proj_auto_tile(FWD, 64, 64, 64, None) == F.FBL_ERR_NULL
+    assert fbl.LIB.fbl_proj_auto_tile(3, 64, 64, 64, ctypes.byref(t)) == F.FBL_ERR_ARG
+    assert fbl.LIB.fbl_proj_auto_tile(FWD, 0, 64, 64, ctypes.byref(t)) == F.FBL_ERR_SHAPE
+
+
 def test_proj_tune_rejections():
     """Argument checks that return before any GPU work."""
     T = lambda op=0, obj=0, reps=5, a=FAKE: fbl.LIB.fbl_proj_tune(
