@@ -250,3 +250,26 @@ def test_proj_fp32_matches_oracle(M, K, N):
         rest = torch.cat([out[ref.shape[0]:].flatten(), out[:ref.shape[0], ref.shape[1]:].flatten()])
         assert torch.isnan(rest).all(), f"op {op}: wrote outside the output"
         assert rel_err(to_np(view), ref) <= 1e-4, f"op {op}"
+
+
+@pytest.mark.parametrize("op,M,K,N", [(0, 512, 2048, 8192), (1, 512, 4096, 12288), (2, 512, 1024, 4096),
+                                      (0, 1024, 512, 4096), (1, 300, 1000, 2048)])
+def test_auto_tile_query_matches_dispatch(op, M, K, N):
+    """The id fbl_proj_auto_tile reports is the tile FBL_GEMM_TILE_AUTO runs:
+    the two products are equal bit for bit (each tile's summation order is
+    its own)."""
+    import torch
+    fbl = _lib()
+    fbl.proj_tune_reset()
+    g = torch.Generator(device="cpu").manual_seed(M + K + N + op)
+    rows_a, cols_a = {0: (M, K), 1: (M, N), 2: (M, K)}[op]
+    rows_b, cols_b = {0: (K, N), 1: (K, N), 2: (M, N)}[op]
+    a = torch.randn(rows_a, cols_a, generator=g).to(device="cuda", dtype=torch.bfloat16)
+    b = torch.randn(rows_b, cols_b, generator=g).to(device="cuda", dtype=torch.bfloat16)
+    t = fbl.proj_auto_tile(op, M, K, N)
+    note(f"auto tile query op={op} M={M} K={K} N={N} -> t{t}")
+    assert t in fbl.proj_candidates(op, M, K, N)
+    auto = fbl.proj(op, a, b)
+    named = fbl.proj(op, a, b, tile=t)
+    torch.cuda.synchronize()
+    assert torch.equal(auto, named)
