@@ -558,8 +558,8 @@ int32_t tuned_tile(uint32_t op, int64_t M, int64_t K, int64_t N) {
 //   n128 >= 1024, contraction >= 2048: the 256 x 256 tiles, 8 wavefronts
 //     first when A is read along its rows, 4 first for the weight gradient's
 //     transposed A;
-//   n128 >= 1024, shorter contraction: the weight gradient's 8-wavefront
-//     64 x 128-per-wave 256 x 256 tile, else 4-wavefront 128 x 128 tiles;
+//   n128 >= 1024, shorter contraction: 4-wavefront 128 x 128 tiles (for the
+//     weight gradient 3-4% ahead of the 256 x 256 tiles, timed interleaved);
 //   384 <= n128 < 1024: the 8-wavefront 256 x 128 and 128 x 256 tiles, even
 //     below one workgroup per CU (two waves per SIMD do more for these than
 //     a full grid of 4-wavefront tiles);
@@ -573,20 +573,19 @@ int32_t default_tile(const ProjPlan& pl) {
     static const int big[] = {19, 18, 20, 17, 11, 12, 8, 4, 0, 6, 5, 2, 1, 10, 9, 7, 3, 13, 15, 14, 16};
     static const int big_t[] = {18, 20, 19, 17, 11, 12, 8, 4, 0, 6, 5, 2, 1, 10, 9, 7, 3, 13, 15, 14, 16};
     static const int many[] = {0, 4, 8, 1, 2, 5, 6, 11, 12, 10, 9, 7, 3, 13, 15, 14, 16, 17, 18, 19, 20};
-    static const int many_t[] = {20, 18, 19, 0, 4, 8, 1, 2, 5, 6, 11, 12, 10, 9, 7, 3, 13, 15, 14, 16, 17};
     static const int wide[] = {11, 12, 8, 4, 0, 5, 6, 2, 1, 10, 9, 7, 3, 13, 15, 14, 16, 17, 18, 19, 20};
     static const int some[] = {6, 5, 8, 4, 11, 12, 0, 2, 1, 10, 9, 7, 3, 13, 15, 14, 16, 17, 18, 19, 20};
     static const int few[] = {10, 9, 7, 6, 5, 8, 4, 3, 2, 1, 0, 11, 12, 14, 13, 15, 16, 17, 18, 19, 20};
     static_assert(sizeof(many) == sizeof(int) * fbl::kGemmTileCount && sizeof(some) == sizeof(many) &&
                       sizeof(few) == sizeof(many) && sizeof(big) == sizeof(many) && sizeof(big_t) == sizeof(many) &&
-                      sizeof(many_t) == sizeof(many) && sizeof(wide) == sizeof(many),
+                      sizeof(wide) == sizeof(many),
                   "every tile ranked once");
     const uint64_t cand = candidate_set(pl);
     const int64_t n128 = ((pl.orows + 127) / 128) * ((pl.ocols + 127) / 128);
     const int* order;
     bool fill = true;
     if (n128 >= 1024) {
-        order = pl.kc >= 2048 ? (pl.a_kmajor ? big_t : big) : (pl.a_kmajor ? many_t : many);
+        order = pl.kc >= 2048 ? (pl.a_kmajor ? big_t : big) : many;
     } else if (n128 >= 384) {
         order = wide;
         fill = false;

@@ -441,7 +441,8 @@ def test_proj_candidates_filters():
 def test_proj_auto_tile_measured_regimes():
     """FBL_GEMM_TILE_AUTO without a tuned entry follows the measured preference
     orders: 256 x 256 tiles from 1024 output tiles of 128 x 128 with a long
-    contraction (8 wavefronts for row-read A, 4 for the weight gradient), the
+    contraction (8 wavefronts for row-read A, 4 for the weight gradient; 128 x
+    128 with a short one), the
     8-wavefront 256 x 128 tile from 384, 64 x 128 from 256, the deep-contraction
     split tile below; the choice is always a candidate."""
     fbl.proj_tune_reset()
@@ -449,7 +450,7 @@ def test_proj_auto_tile_measured_regimes():
     FWD, BD, BW = F.FBL_PROJ_FWD, F.FBL_PROJ_BWD_DATA, F.FBL_PROJ_BWD_WEIGHT
     assert A(FWD, 4096, 4096, 12288) == 19 and A(BD, 4096, 4096, 12288) == 19
     assert A(BW, 4096, 4096, 12288) == 18 and A(BW, 2048, 4096, 4096) == 18
-    assert A(BW, 512, 4096, 12288) == 20                     # 3072 output tiles, contraction 512
+    assert A(BW, 512, 4096, 12288) == 0                      # 3072 output tiles, contraction 512
     assert A(FWD, 512, 4096, 12288) == 11 and A(FWD, 2048, 4096, 4096) == 11   # 384 and 512 output tiles
     assert A(FWD, 512, 2048, 8192) == 6                      # 256 output tiles
     assert A(BD, 512, 4096, 12288) == 10                     # 128 output tiles, a grid of 256
