@@ -560,9 +560,11 @@ int32_t tuned_tile(uint32_t op, int64_t M, int64_t K, int64_t N) {
 //     transposed A;
 //   n128 >= 1024, shorter contraction: 4-wavefront 128 x 128 tiles (for the
 //     weight gradient 3-4% ahead of the 256 x 256 tiles, timed interleaved);
-//   384 <= n128 < 1024: the 8-wavefront 256 x 128 and 128 x 256 tiles, even
-//     below one workgroup per CU (two waves per SIMD do more for these than
-//     a full grid of 4-wavefront tiles);
+//   384 <= n128 < 1024: the 8-wavefront 256 x 128 (forward) or 128 x 256
+//     (data gradient) tile, even below one workgroup per CU (two waves per
+//     SIMD do more for these than a full grid of 4-wavefront tiles); for the
+//     weight gradient's transposed A the 4-wavefront 128 x 128 tile, then
+//     128 x 256;
 //   256 <= n128 < 384: 4-wavefront 64 x 128 and 128 x 64 tiles;
 //   below: the 8-wavefront 128 x 64 tile that splits a deep contraction four
 //     ways, then the 4-wavefront 64 x 64 one.
@@ -574,11 +576,13 @@ int32_t default_tile(const ProjPlan& pl) {
     static const int big_t[] = {18, 20, 19, 17, 11, 12, 8, 4, 0, 6, 5, 2, 1, 10, 9, 7, 3, 13, 15, 14, 16};
     static const int many[] = {0, 4, 8, 1, 2, 5, 6, 11, 12, 10, 9, 7, 3, 13, 15, 14, 16, 17, 18, 19, 20};
     static const int wide[] = {11, 12, 8, 4, 0, 5, 6, 2, 1, 10, 9, 7, 3, 13, 15, 14, 16, 17, 18, 19, 20};
+    static const int wide_d[] = {12, 11, 8, 4, 0, 5, 6, 2, 1, 10, 9, 7, 3, 13, 15, 14, 16, 17, 18, 19, 20};
+    static const int wide_t[] = {0, 12, 8, 11, 4, 5, 6, 2, 1, 10, 9, 7, 3, 13, 15, 14, 16, 17, 18, 19, 20};
     static const int some[] = {6, 5, 8, 4, 11, 12, 0, 2, 1, 10, 9, 7, 3, 13, 15, 14, 16, 17, 18, 19, 20};
     static const int few[] = {10, 9, 7, 6, 5, 8, 4, 3, 2, 1, 0, 11, 12, 14, 13, 15, 16, 17, 18, 19, 20};
     static_assert(sizeof(many) == sizeof(int) * fbl::kGemmTileCount && sizeof(some) == sizeof(many) &&
                       sizeof(few) == sizeof(many) && sizeof(big) == sizeof(many) && sizeof(big_t) == sizeof(many) &&
-                      sizeof(wide) == sizeof(many),
+                      sizeof(wide) == sizeof(many) && sizeof(wide_d) == sizeof(many) && sizeof(wide_t) == sizeof(many),
                   "every tile ranked once");
     const uint64_t cand = candidate_set(pl);
     const int64_t n128 = ((pl.orows + 127) / 128) * ((pl.ocols + 127) / 128);
@@ -587,7 +591,7 @@ int32_t default_tile(const ProjPlan& pl) {
     if (n128 >= 1024) {
         order = pl.kc >= 2048 ? (pl.a_kmajor ? big_t : big) : many;
     } else if (n128 >= 384) {
-        order = wide;
+        order = pl.a_kmajor ? wide_t : (pl.b_nmajor ? wide_d : wide);
         fill = false;
     } else {
         order = n128 >= 256 ? some : few;

@@ -452,6 +452,7 @@ def test_proj_auto_tile_measured_regimes():
     assert A(BW, 4096, 4096, 12288) == 18 and A(BW, 2048, 4096, 4096) == 18
     assert A(BW, 512, 4096, 12288) == 0                      # 3072 output tiles, contraction 512
     assert A(FWD, 512, 4096, 12288) == 11 and A(FWD, 2048, 4096, 4096) == 11   # 384 and 512 output tiles
+    assert A(BD, 2048, 4096, 4096) == 12 and A(BW, 4096, 2048, 4096) == 0     # 512 output tiles
     assert A(FWD, 512, 2048, 8192) == 6                      # 256 output tiles
     assert A(BD, 512, 4096, 12288) == 10                     # 128 output tiles, a grid of 256
     assert A(BD, 512, 2048, 8192) == 9                       # 64 output tiles: the 64 x 64 split tile fills the CUs
