@@ -13,6 +13,11 @@
  *       patterns of q, k, v, dO ([B, S, H*D] token-major each).  OUT receives
  *       the bf16 bit patterns of o, dq, dk, dv and the float32 lse, in that
  *       order.
+ *   fbl_c_caller proj IN OUT
+ *       the three projection products through fbl_proj (automatic tile),
+ *       row-major operands with no padding.  IN holds int32 M, K, N, then the
+ *       bf16 bit patterns of X [M, K], W [K, N], dY [M, N]; OUT receives those
+ *       of Y = X W [M, N], dX = dY W^T [M, K] and dW = X^T dY [K, N].
  * Exit status 0 on success; a message on stderr otherwise.
  */
 #include <stdint.h>
@@ -181,9 +186,64 @@ static int attn_run(const char* in_path, const char* out_path) {
     return 0;
 }
 
+static int proj_run(const char* in_path, const char* out_path) {
+    FILE* f = fopen(in_path, "rb");
+    if (!f) { fprintf(stderr, "cannot open %s\n", in_path); return 1; }
+    int32_t hdr[3];
+    if (!read_all(f, hdr, sizeof hdr)) { fclose(f); return 1; }
+    const int64_t M = hdr[0], K = hdr[1], N = hdr[2];
+    if (M <= 0 || K <= 0 || N <= 0 || M * K > ((int64_t)1 << 26) || K * N > ((int64_t)1 << 26) ||
+        M * N > ((int64_t)1 << 26)) {
+        fclose(f);
+        fprintf(stderr, "bad header\n");
+        return 1;
+    }
+    const size_t nx = (size_t)(M * K), nw = (size_t)(K * N), ny = (size_t)(M * N);
+    uint16_t* hx = malloc(2 * nx);
+    uint16_t* hw = malloc(2 * nw);
+    uint16_t* hdy = malloc(2 * ny);
+    if (!hx || !hw || !hdy) { fclose(f); return 1; }
+    const int ok = read_all(f, hx, 2 * nx) && read_all(f, hw, 2 * nw) && read_all(f, hdy, 2 * ny);
+    fclose(f);
+    if (!ok) { fprintf(stderr, "short input\n"); return 1; }
+    void *x, *w, *dy, *y, *dx, *dw;
+    HIP(hipMalloc(&x, 2 * nx));
+    HIP(hipMalloc(&w, 2 * nw));
+    HIP(hipMalloc(&dy, 2 * ny));
+    HIP(hipMalloc(&y, 2 * ny));
+    HIP(hipMalloc(&dx, 2 * nx));
+    HIP(hipMalloc(&dw, 2 * nw));
+    HIP(hipMemcpy(x, hx, 2 * nx, hipMemcpyHostToDevice));
+    HIP(hipMemcpy(w, hw, 2 * nw, hipMemcpyHostToDevice));
+    HIP(hipMemcpy(dy, hdy, 2 * ny, hipMemcpyHostToDevice));
+    /* leading dimensions: the stored row lengths */
+    FBL(fbl_proj(FBL_PROJ_FWD, M, K, N, x, K, w, N, y, N, FBL_GEMM_TILE_AUTO, NULL));
+    FBL(fbl_proj(FBL_PROJ_BWD_DATA, M, K, N, dy, N, w, N, dx, K, FBL_GEMM_TILE_AUTO, NULL));
+    FBL(fbl_proj(FBL_PROJ_BWD_WEIGHT, M, K, N, x, K, dy, N, dw, N, FBL_GEMM_TILE_AUTO, NULL));
+    HIP(hipDeviceSynchronize());
+    FILE* g = fopen(out_path, "wb");
+    if (!g) { fprintf(stderr, "cannot open %s\n", out_path); return 1; }
+    const void* outs[3] = {y, dx, dw};
+    const size_t sizes[3] = {2 * ny, 2 * nx, 2 * nw};
+    for (int i = 0; i < 3; ++i) {
+        void* h = malloc(sizes[i]);
+        if (!h) { fclose(g); return 1; }
+        HIP(hipMemcpy(h, outs[i], sizes[i], hipMemcpyDeviceToHost));
+        fwrite(h, 1, sizes[i], g);
+        free(h);
+    }
+    fclose(g);
+    void* bufs[6] = {x, w, dy, y, dx, dw};
+    for (int i = 0; i < 6; ++i) HIP(hipFree(bufs[i]));
+    free(hx); free(hw); free(hdy);
+    printf("projection products done (M=%d K=%d N=%d)\n", (int)M, (int)K, (int)N);
+    return 0;
+}
+
 int main(int argc, char** argv) {
     if (argc == 2 && strcmp(argv[1], "host") == 0) return host_checks();
     if (argc == 4 && strcmp(argv[1], "attn") == 0) return attn_run(argv[2], argv[3]);
-    fprintf(stderr, "usage: %s host | attn IN OUT\n", argv[0]);
+    if (argc == 4 && strcmp(argv[1], "proj") == 0) return proj_run(argv[2], argv[3]);
+    fprintf(stderr, "usage: %s host | attn IN OUT | proj IN OUT\n", argv[0]);
     return 2;
 }

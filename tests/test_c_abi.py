@@ -81,3 +81,45 @@ def test_attention_from_plain_c(tmp_path):
     for n, t in (("o", o), ("dq", dq), ("dk", dk), ("dv", dv)):
         assert np.array_equal(t.view(torch.int16).cpu().numpy(), got[n]), n
     assert np.array_equal(lse.cpu().numpy(), got["lse"])
+
+
+@pytest.mark.gpu
+def test_projection_products_from_plain_c(tmp_path):
+    """Y = X W, dX = dY W^T and dW = X^T dY through fbl_proj from plain C
+    (automatic tile, extents ragged against every tile): they meet the oracle
+    and equal, bit for bit, the Python binding's products on the same inputs."""
+    import torch
+    import oracle
+    import paper_2607_21624_amd as fbl
+    exe = c_build.OUT
+    assert os.path.exists(exe), "the C caller is not built (run __graft_entry__.build())"
+    M, K, N = 304, 520, 264
+    rng = np.random.default_rng(17)
+    mats = {"x": rng.standard_normal((M, K)), "w": rng.standard_normal((K, N)), "dy": rng.standard_normal((M, N))}
+    bits = {n: _bf16_bits(m) for n, m in mats.items()}
+    vals = {n: _from_bits(b) for n, b in bits.items()}  # the bf16-rounded operands, as the GPU sees them
+    note(f"plain-C caller: projection products M={M} K={K} N={N}")
+    src, dst = tmp_path / "in.bin", tmp_path / "out.bin"
+    with open(src, "wb") as f:
+        f.write(np.array([M, K, N], dtype=np.int32).tobytes())
+        for n in ("x", "w", "dy"):
+            f.write(bits[n].tobytes())
+    r = subprocess.run([exe, "proj", str(src), str(dst)], capture_output=True, text=True, timeout=120)
+    assert r.returncode == 0, r.stdout + r.stderr
+    raw = open(dst, "rb").read()
+    assert len(raw) == 2 * (M * N + M * K + K * N)
+    y = np.frombuffer(raw, dtype=np.int16, count=M * N).reshape(M, N)
+    dx = np.frombuffer(raw, dtype=np.int16, count=M * K, offset=2 * M * N).reshape(M, K)
+    dw = np.frombuffer(raw, dtype=np.int16, count=K * N, offset=2 * (M * N + M * K)).reshape(K, N)
+    refs = {"y": oracle.proj_fwd(vals["x"], vals["w"]), "dx": oracle.proj_bwd_data(vals["dy"], vals["w"]),
+            "dw": oracle.proj_bwd_weight(vals["x"], vals["dy"])}
+    for n, got in (("y", y), ("dx", dx), ("dw", dw)):
+        err = float(np.max(np.abs(_from_bits(got) - refs[n])) / np.max(np.abs(refs[n])))
+        assert err <= 2e-2, (n, err)
+    dev = {n: torch.from_numpy(b).view(torch.bfloat16).to("cuda") for n, b in bits.items()}
+    py = {"y": fbl.proj(fbl.FBL_PROJ_FWD, dev["x"], dev["w"]),
+          "dx": fbl.proj(fbl.FBL_PROJ_BWD_DATA, dev["dy"], dev["w"]),
+          "dw": fbl.proj(fbl.FBL_PROJ_BWD_WEIGHT, dev["x"], dev["dy"])}
+    torch.cuda.synchronize()
+    for n, got in (("y", y), ("dx", dx), ("dw", dw)):
+        assert np.array_equal(py[n].view(torch.int16).cpu().numpy(), got), n
