@@ -18,7 +18,8 @@ Modules
              tensor, built by the reshape-then-transpose chain itself, also
              for Q, K, V split out of one packed projection output.
 
-Pins (tests/test_oracle.py, tests/test_layout.py) tie each function to
+Pins (tests/test_oracle.py, tests/test_oracle_cross.py, tests/test_oracle_proj.py,
+tests/test_layout_oracle.py) tie each function to
 something other than itself: brute force, float64 torch SDPA with autograd,
 central finite differences, closed forms, invariants and the paper's own
 layout examples.  Each function's docstring names the pin(s).

@@ -9,7 +9,7 @@ map.  Here that map is produced by carrying out the chain on an array of flat
 indices with numpy's own reshape and transpose, so the result is, by
 construction, "where logical element (b, h, s, i) lives in memory".
 
-Pins: tests/test_layout.py checks it against the closed affine form for the
+Pins: tests/test_layout_oracle.py checks it against the closed affine form for the
 paper's hidden=768 / 12 heads x 64 example and against explicit per-element
 enumeration on ragged shapes.
 """

@@ -14,9 +14,11 @@ autograd graph.
       x [..., K] (rows contiguous), w [K, N]; gradients x and w by the data-
       and weight-gradient products, no transposed copy of either.
 
-An incoming gradient that is not contiguous (autograd can hand over
-broadcast or transposed views) is made contiguous first: the kernels read
-16-byte-aligned rows of unit stride.
+The incoming gradient is read in place, never copied: it must have unit
+inner stride (any row stride), like every tensor the kernels read.  Autograd
+can hand over a broadcast view (the gradient of a plain .sum(), inner stride
+0); such a gradient is rejected with FblError, and the caller makes it
+contiguous (or backpropagates a materialised tensor) instead.
 """
 import math
 
@@ -25,8 +27,12 @@ import torch
 from . import fbl as _f
 
 
-def _unit(t):
-    return t if t.is_contiguous() else t.contiguous()
+def _unit(t, what: str):
+    """The incoming gradient as it is, if its rows have unit inner stride."""
+    if t.dim() == 0 or t.stride(-1) != 1:
+        raise _f.FblError(_f.FBL_ERR_LAYOUT, f"{what}: the incoming gradient needs unit inner stride, got strides "
+                                             f"{tuple(t.stride())}; pass a contiguous gradient")
+    return t
 
 
 class _Attention(torch.autograd.Function):
@@ -41,7 +47,8 @@ class _Attention(torch.autograd.Function):
     def backward(ctx, do):
         q, k, v, o, lse, kv = ctx.saved_tensors
         Hq, Hkv, scale, causal, has_kv = ctx.cfg
-        dq, dk, dv = _f.attn_bwd(q, k, v, o, _unit(do), lse, Hq, Hkv, scale, causal, kv if has_kv else None)
+        dq, dk, dv = _f.attn_bwd(q, k, v, o, _unit(do, 'attention'), lse, Hq, Hkv, scale, causal,
+                                 kv if has_kv else None)
         return dq, dk, dv, None, None, None, None, None
 
 
@@ -63,7 +70,7 @@ class _AttentionPacked(torch.autograd.Function):
     def backward(ctx, do):
         qkv, o, lse = ctx.saved_tensors
         Hq, Hkv, scale, causal = ctx.cfg
-        dqkv = _f.attn_bwd_packed(qkv, o, _unit(do), lse, Hq, Hkv, scale, causal)
+        dqkv = _f.attn_bwd_packed(qkv, o, _unit(do, 'attention_packed'), lse, Hq, Hkv, scale, causal)
         return dqkv, None, None, None, None
 
 
@@ -85,7 +92,12 @@ class _Linear(torch.autograd.Function):
     @staticmethod
     def backward(ctx, dy):
         x2, w = ctx.saved_tensors
-        dy2 = _unit(dy).reshape(-1, dy.shape[-1])
+        dy = _unit(dy, "linear")
+        try:
+            dy2 = dy.view(-1, dy.shape[-1])  # a view: token rows of the incoming gradient
+        except RuntimeError as e:
+            raise _f.FblError(_f.FBL_ERR_LAYOUT, f"linear: the incoming gradient's rows are not one strided "
+                                                 f"matrix ({e}); pass a contiguous gradient") from None
         dx = dw = None
         if ctx.needs_input_grad[0]:
             dx = _f.proj(_f.FBL_PROJ_BWD_DATA, dy2, w).view(ctx.xshape)

@@ -1,9 +1,11 @@
 // api.cpp -- the C ABI: layout descriptors, validation and kernel dispatch.
 //
 // Every check runs on the host before the first launch; an error return
-// means nothing was enqueued.  The library holds no mutable global state
-// (the per-kernel LDS attribute is set once, thread-safely, by a function-
-// local static) and never allocates, frees or synchronises.
+// means nothing was enqueued.  Mutable global state is limited to the
+// per-kernel LDS attribute flags (set once per device, thread-safely) and the
+// per-process tables of measured tile choices (mutex-guarded), which only the
+// tuning calls write.  The library never allocates, frees or synchronises,
+// except that the tuning calls wait for their own timing events.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -370,6 +372,11 @@ fbl_status fbl_attn_bwd_phases(uint32_t phases, const fbl_layout* lq, const void
     const fbl_layout* in_l[5] = {lq, lk, lv, lo, ldo};
     void* outs[3] = {dq, dk, dv};
     const fbl_layout* out_l[3] = {ldq, ldk, ldv};
+    // the workspace is written (statistics, dS, partial sums) while every
+    // input is read: it may share no byte with an input or with lse
+    for (int j = 0; j < 5; ++j)
+        if (overlaps(ws, (int64_t)ws_bytes, ins[j], span_bytes(in_l[j]))) return FBL_ERR_ARG;
+    if (overlaps(ws, (int64_t)ws_bytes, lse, lse_bytes)) return FBL_ERR_ARG;
     for (int i = 0; i < 3; ++i) {
         for (int j = 0; j < 5; ++j)
             if (views_overlap(outs[i], out_l[i], ins[j], in_l[j])) return FBL_ERR_ARG;

@@ -531,24 +531,26 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) void attn_bwd_q(BwdArg
     }
 }
 
-// Explicit instantiations: the host-side launch stubs of every kernel used below.
-#define FBL_BWD_KERNELS(T, D)                                 \
-    template __global__ void attn_bwd_stats<T, D>(BwdArgs); \
-    template __global__ void attn_bwd_kv<T, D>(BwdArgs);    \
-    template __global__ void attn_bwd_q<T, D>(BwdArgs);
-FBL_BWD_KERNELS(float, 32)
-FBL_BWD_KERNELS(float, 64)
-FBL_BWD_KERNELS(float, 128)
-FBL_BWD_KERNELS(bf16, 32)
-FBL_BWD_KERNELS(bf16, 64)
-FBL_BWD_KERNELS(bf16, 128)
-#undef FBL_BWD_KERNELS
+// Explicit instantiations: the host-side launch stubs of every kernel used
+// below.  bf16 storage runs the software-pipelined passes of attn_bwd_kv.hip,
+// attn_bwd_dq.hip and attn_bwd_q.hip; the two passes here serve fp32.
+#define FBL_BWD_KERNELS_F32(D)                                   \
+    template __global__ void attn_bwd_stats<float, D>(BwdArgs); \
+    template __global__ void attn_bwd_kv<float, D>(BwdArgs);    \
+    template __global__ void attn_bwd_q<float, D>(BwdArgs);
+FBL_BWD_KERNELS_F32(32)
+FBL_BWD_KERNELS_F32(64)
+FBL_BWD_KERNELS_F32(128)
+#undef FBL_BWD_KERNELS_F32
+template __global__ void attn_bwd_stats<bf16, 32>(BwdArgs);
+template __global__ void attn_bwd_stats<bf16, 64>(BwdArgs);
+template __global__ void attn_bwd_stats<bf16, 128>(BwdArgs);
 
-template <typename T, int D>
-hipError_t set_bwd_lds() {
-    const hipError_t e = ensure_dynamic_lds<&attn_bwd_kv<T, D>>(KvCfg<T, D>::BYTES);
+template <int D>
+hipError_t set_bwd_lds_f32() {
+    const hipError_t e = ensure_dynamic_lds<&attn_bwd_kv<float, D>>(KvCfg<float, D>::BYTES);
     if (e != hipSuccess) return e;
-    return ensure_dynamic_lds<&attn_bwd_q<T, D>>(QSmem<T, D>::BYTES);
+    return ensure_dynamic_lds<&attn_bwd_q<float, D>>(QSmem<float, D>::BYTES);
 }
 
 int padded8(int n) { return (n + 7) / 8 * 8; }
@@ -559,8 +561,10 @@ template <typename T, int D>
 hipError_t launch_attn_bwd(const BwdArgs& a, unsigned phases, hipStream_t stream) {
     constexpr int LPR = D / (16 / (int)sizeof(T));
     constexpr int RPB = 256 / LPR;
-    const hipError_t e = set_bwd_lds<T, D>();
-    if (e != hipSuccess) return e;
+    if constexpr (sizeof(T) == 4) {
+        const hipError_t e = set_bwd_lds_f32<D>();
+        if (e != hipSuccess) return e;
+    }
     if (phases & 1u) {
         const int64_t nrows = (int64_t)a.B * a.S * a.Hq;
         hipLaunchKernelGGL((attn_bwd_stats<T, D>), dim3((unsigned)((nrows + RPB - 1) / RPB)), dim3(256), 0, stream, a);
@@ -570,9 +574,9 @@ hipError_t launch_attn_bwd(const BwdArgs& a, unsigned phases, hipStream_t stream
             const hipError_t ek = launch_attn_bwd_kv_bf16<D>(a, stream);
             if (ek != hipSuccess) return ek;
         } else {
-        const int n = (a.Skv + kKvBN - 1) / kKvBN * a.Hkv * a.B;
-        constexpr int lds = KvCfg<T, D>::BYTES;
-        hipLaunchKernelGGL((attn_bwd_kv<T, D>), dim3(padded8(n)), dim3(256), lds, stream, a);
+            const int n = (a.Skv + kKvBN - 1) / kKvBN * a.Hkv * a.B;
+            constexpr int lds = KvCfg<T, D>::BYTES;
+            hipLaunchKernelGGL((attn_bwd_kv<T, D>), dim3(padded8(n)), dim3(256), lds, stream, a);
         }
     }
     if (phases & 4u) {

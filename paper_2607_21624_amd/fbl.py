@@ -284,11 +284,50 @@ def layout_of(t, H: int) -> Layout:
                            batch_stride=t.stride(0) if B > 1 else 0)
 
 
+def _check_kv_len(kv_len, B: int, where: str) -> None:
+    """kv_len must be an int32 tensor of at least B entries with unit stride:
+    the kernels read kv_len[b] as a 32-bit integer from device memory."""
+    if kv_len is None:
+        return
+    import torch
+    if not isinstance(kv_len, torch.Tensor):
+        raise FblError(FBL_ERR_ARG, f"{where}: kv_len must be a torch tensor")
+    if kv_len.dtype != torch.int32:
+        raise FblError(FBL_ERR_DTYPE, f"{where}: kv_len must be int32, got {kv_len.dtype}")
+    if kv_len.dim() != 1 or (kv_len.numel() > 1 and kv_len.stride(0) != 1):
+        raise FblError(FBL_ERR_LAYOUT, f"{where}: kv_len must be a 1-D tensor with unit stride")
+    if kv_len.numel() < B:
+        raise FblError(FBL_ERR_SHAPE, f"{where}: kv_len has {kv_len.numel()} entries, needs {B}")
+
+
+def _check_device(where: str, stream, **tensors) -> None:
+    """Every tensor argument lives on one GPU, the device the launch stream
+    belongs to: the kernels dereference each pointer on that device."""
+    import torch
+    dev = None
+    for name, t in tensors.items():
+        if t is None:
+            continue
+        if not t.is_cuda:
+            raise FblError(FBL_ERR_ARG, f"{where}: {name} is on {t.device}, not on a GPU")
+        if dev is None:
+            dev = t.device
+        elif t.device != dev:
+            raise FblError(FBL_ERR_ARG, f"{where}: {name} is on {t.device}, the other tensors on {dev}")
+    if dev is None or isinstance(stream, int) or stream == 0:
+        return
+    sdev = torch.cuda.current_device() if stream is None else stream.device.index
+    if sdev != dev.index:
+        raise FblError(FBL_ERR_ARG, f"{where}: tensors are on {dev}, the stream on cuda:{sdev}")
+
+
 def attn_fwd(q, k, v, Hq: int, Hkv: int, scale: Optional[float] = None, causal: bool = False, kv_len=None,
              out=None, lse=None, stream=None):
     """Forward on token-major tensors.  Returns (O, LSE); O has q's shape and dtype
     (allocated contiguous unless `out` is given), LSE is float32 [B, Hq, S]."""
     import torch
+    _check_kv_len(kv_len, q.shape[0], "attn_fwd")
+    _check_device("attn_fwd", stream, q=q, k=k, v=v, kv_len=kv_len, out=out, lse=lse)
     lq, lk, lv = _layout(q, Hq), _layout(k, Hkv), _layout(v, Hkv)
     if scale is None:
         scale = 1.0 / math.sqrt(lq.D)
@@ -307,6 +346,9 @@ def attn_bwd(q, k, v, o, do, lse, Hq: int, Hkv: int, scale: Optional[float] = No
              kv_len=None, dq=None, dk=None, dv=None, workspace=None, stream=None, phases: int = FBL_BWD_ALL):
     """Backward.  Returns (dQ, dK, dV) with the shapes/dtypes of q, k, v."""
     import torch
+    _check_kv_len(kv_len, q.shape[0], "attn_bwd")
+    _check_device("attn_bwd", stream, q=q, k=k, v=v, o=o, do=do, lse=lse, kv_len=kv_len, dq=dq, dk=dk, dv=dv,
+                  workspace=workspace)
     lq, lk, lv = _layout(q, Hq), _layout(k, Hkv), _layout(v, Hkv)
     lo, ldo = _layout(o, Hq), _layout(do, Hq)
     if scale is None:
@@ -349,6 +391,8 @@ def attn_fwd_packed(qkv, Hq: int, Hkv: int, scale: Optional[float] = None, causa
     V are read in place through fbl_layout_packed_qkv descriptors.  Returns
     (O [B, S, Hq D], LSE [B, Hq, S])."""
     import torch
+    _check_kv_len(kv_len, qkv.shape[0], "attn_fwd_packed")
+    _check_device("attn_fwd_packed", stream, qkv=qkv, kv_len=kv_len, out=out, lse=lse)
     lq, lk, lv, pq, pk, pv = _packed(qkv, Hq, Hkv)
     if scale is None:
         scale = 1.0 / math.sqrt(lq.D)
@@ -368,6 +412,9 @@ def attn_bwd_packed(qkv, o, do, lse, Hq: int, Hkv: int, scale: Optional[float] =
     """Backward on a packed QKV projection output: dQ, dK, dV are written into
     one packed gradient tensor shaped like ``qkv`` (allocated unless given)."""
     import torch
+    _check_kv_len(kv_len, qkv.shape[0], "attn_bwd_packed")
+    _check_device("attn_bwd_packed", stream, qkv=qkv, o=o, do=do, lse=lse, kv_len=kv_len, dqkv=dqkv,
+                  workspace=workspace)
     lq, lk, lv, pq, pk, pv = _packed(qkv, Hq, Hkv)
     if scale is None:
         scale = 1.0 / math.sqrt(lq.D)
@@ -416,10 +463,13 @@ def proj(op: int, a, b, out=None, tile: int = FBL_GEMM_TILE_AUTO, stream=None):
     FBL_PROJ_BWD_DATA (a = dY [M, N], b = W [K, N]) -> dX [M, K];
     FBL_PROJ_BWD_WEIGHT (a = X [M, K], b = dY [M, N]) -> dW [K, N]."""
     import torch
+    _check_device("proj", stream, a=a, b=b, out=out)
     M, K, N, shape, lda, ldb = _proj_shape(op, a, b)
     if out is None:
         out = torch.empty(shape, dtype=a.dtype, device=a.device)
     _, _, ldc = _rows(out, "out")
+    if not (a.dtype == b.dtype == out.dtype):
+        raise FblError(FBL_ERR_DTYPE, f"proj: operand dtypes differ ({a.dtype}, {b.dtype}, {out.dtype})")
     if a.dtype == torch.float32:
         _check(LIB.fbl_proj_dt(op, FBL_F32, M, K, N, _ptr(a), lda, _ptr(b), ldb, _ptr(out), ldc, tile,
                                _stream(stream) if stream != 0 else None), "fbl_proj_dt")
@@ -452,6 +502,7 @@ def proj_tune(op: int, a, b, out, objective: int = FBL_TUNE_TIME, reps: int = 10
     """Measured tile selection for one product (fbl_proj_tune).  Returns
     (chosen id, {id: average ms} over the candidates); `out` then holds the
     product computed with the chosen tile."""
+    _check_device("proj_tune", stream, a=a, b=b, out=out)
     M, K, N, _, lda, ldb = _proj_shape(op, a, b)
     _, _, ldc = _rows(out, "out")
     cap = LIB.fbl_gemm_tile_count()

@@ -291,6 +291,10 @@ def test_bwd_rejections():
     assert _bwd(lq, lk, lv, lo, dict(p, dq=p["do"]), ws) == E.FBL_ERR_ARG      # output aliases input
     assert _bwd(lq, lk, lv, lo, dict(p, dv=p["dk"]), ws) == E.FBL_ERR_ARG      # outputs alias each other
     assert _bwd(lq, lk, lv, lo, dict(p, dq=p["ws"]), ws) == E.FBL_ERR_ARG      # output aliases workspace
+    # the workspace overlapping an input or the saved LSE
+    for name in ("q", "k", "v", "o", "do"):
+        assert _bwd(lq, lk, lv, lo, dict(p, ws=(p[name] + 255) // 256 * 256), ws) == E.FBL_ERR_ARG, name
+    assert _bwd(lq, lk, lv, lo, dict(p, ws=p["lse"] // 256 * 256), ws) == E.FBL_ERR_ARG
     assert _bwd(lq, lk, lv, lo, p, ws, kind=F.FBL_MASK_KEY_PADDING) == E.FBL_ERR_NULL
     assert _bwd(lq, lk, lv, lo, p, ws, scale=float("nan")) == E.FBL_ERR_ARG
     assert _bwd(lq, lk, lv, lo, dict(p, lse=p["lse"] + 4), ws) == E.FBL_ERR_ALIGN
@@ -491,3 +495,50 @@ def test_proj_dt_rejections():
     # bf16 through fbl_proj_dt keeps fbl_proj's rules
     assert D(dt=F.FBL_BF16, K=60) == F.FBL_ERR_UNSUPPORTED
     assert D(dt=F.FBL_BF16, a=FAKE + 4) == F.FBL_ERR_ALIGN
+
+
+# ---------------------------------------------- the Python binding's own checks
+def test_binding_rejects_kv_len_and_host_tensors():
+    """The binding hands raw pointers to the kernels, so it checks what the C
+    ABI cannot see: kv_len is int32 with unit stride and at least B entries,
+    and every tensor is on the GPU (a host pointer would be read on the
+    device).  All of this raises before any library call."""
+    import torch
+    B, S, H, D = 2, 16, 2, 64
+    q = torch.zeros(B, S, H * D, dtype=torch.bfloat16)
+    for bad, status in ((torch.tensor([100, 37], dtype=torch.int64), F.FBL_ERR_DTYPE),
+                        (torch.tensor([5], dtype=torch.int32), F.FBL_ERR_SHAPE),
+                        (torch.tensor([[5, 6]], dtype=torch.int32), F.FBL_ERR_LAYOUT),
+                        (torch.tensor([5, 0, 6, 0], dtype=torch.int32)[::2], F.FBL_ERR_LAYOUT),
+                        ([5, 6], F.FBL_ERR_ARG)):
+        with pytest.raises(F.FblError) as ei:
+            F.attn_fwd(q, q, q, H, H, kv_len=bad)
+        assert ei.value.status == status, bad
+        with pytest.raises(F.FblError) as ei:
+            F.attn_bwd(q, q, q, q, q, None, H, H, kv_len=bad)
+        assert ei.value.status == status, bad
+    # host tensors: q itself, or an int32 kv_len left on the host
+    ok_len = torch.tensor([5, 6], dtype=torch.int32)
+    for call in (lambda: F.attn_fwd(q, q, q, H, H),
+                 lambda: F.attn_fwd(q, q, q, H, H, kv_len=ok_len),
+                 lambda: F.attn_bwd(q, q, q, q, q, torch.zeros(B, H, S), H, H),
+                 lambda: F.attn_fwd_packed(torch.zeros(B, S, 3 * H * D, dtype=torch.bfloat16), H, H),
+                 lambda: F.proj(F.FBL_PROJ_FWD, torch.zeros(4, 8, dtype=torch.bfloat16),
+                                torch.zeros(8, 4, dtype=torch.bfloat16))):
+        with pytest.raises(F.FblError) as ei:
+            call()
+        assert ei.value.status == F.FBL_ERR_ARG
+
+
+def test_autograd_rejects_broadcast_gradient():
+    """The autograd wrappers read the incoming gradient in place; a broadcast
+    view (inner stride 0) is refused instead of silently copied."""
+    import torch
+    from paper_2607_21624_amd import autograd as ag
+    g = torch.zeros(1, dtype=torch.bfloat16).expand(2, 4, 64)
+    with pytest.raises(F.FblError) as ei:
+        ag._unit(g, "attention")
+    assert ei.value.status == F.FBL_ERR_LAYOUT
+    t = torch.zeros(2, 4, 64, dtype=torch.bfloat16)
+    assert ag._unit(t, "attention") is t
+    assert ag._unit(t[:, :, :32], "attention").data_ptr() == t.data_ptr()  # strided rows pass as views
