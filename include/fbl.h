@@ -260,6 +260,29 @@ fbl_status fbl_attn_bwd_phases(uint32_t phases, const fbl_layout* lq, const void
                                const fbl_layout* ldv, void* dv, void* ws, size_t ws_bytes, void* stream);
 
 /*
+ * fbl_attn_bwd for callers that cannot allocate device memory -- code under
+ * HIP graph capture, serving loops and harnesses that forbid hipMalloc.  The
+ * arguments are fbl_attn_bwd's without the workspace: the backward's scratch
+ * is one library-owned device array of FBL_NOALLOC_SCRATCH_BYTES per GPU,
+ * held from the library's first use on that GPU until the process ends, and
+ * used as the workspace of fbl_attn_bwd would be (so the stored-dS path and
+ * the split key/value pass run exactly when their parts fit in it; results
+ * equal fbl_attn_bwd's with a workspace of that size, bit for bit).  The
+ * call allocates and frees nothing.  Returns FBL_ERR_WORKSPACE when even
+ * fbl_attn_bwd_workspace_min exceeds the array (more than
+ * FBL_NOALLOC_SCRATCH_BYTES / 8 query rows, B*Hq*S_q, about 8 million), and
+ * fbl_attn_bwd's statuses otherwise.  All calls on one GPU share the array:
+ * calls that can run at the same time on one GPU (on streams with no order
+ * between them) race; calls on one stream, or ordered by events, do not.
+ */
+#define FBL_NOALLOC_SCRATCH_BYTES (64u << 20)
+fbl_status fbl_attn_bwd_noalloc(const fbl_layout* lq, const void* q, const fbl_layout* lk, const void* k,
+                                const fbl_layout* lv, const void* v, const fbl_layout* lo, const void* o,
+                                const fbl_layout* ldo, const void* dO, const float* lse, float scale, fbl_mask mask,
+                                const fbl_layout* ldq, void* dq, const fbl_layout* ldk, void* dk,
+                                const fbl_layout* ldv, void* dv, void* stream);
+
+/*
  * Projection matrix products of the linear layers around attention, on the
  * same token-major activations (bf16 operands and result, fp32 accumulation).
  * Section 4.1 classes matrix products as forward-tensor-dependent: the

@@ -12,4 +12,5 @@ from .fbl import (  # noqa: F401
     FBL_GEMM_TILE_AUTO, FBL_GEMM_TILE_128x128, FBL_GEMM_TILE_128x64, FBL_GEMM_TILE_64x128, FBL_GEMM_TILE_64x64,
     FBL_TUNE_TIME, FBL_TUNE_GFLOPS_X_MEMEFF, gemm_tiles, proj_candidates, proj_tune, proj_tuned_tile, proj_auto_tile, proj_tune_reset,
     fbl_layout_desc_status, fbl_layout_map_device, fbl_layout_offset, layout_of, status_str,
+    NOALLOC_SCRATCH_BYTES, attn_bwd_noalloc, fbl_attn_bwd_noalloc_raw,
 )

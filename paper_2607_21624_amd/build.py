@@ -12,7 +12,7 @@ CSRC = os.path.join(HERE, "csrc")
 OBJ = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libfbl.so")
 SOURCES = ["attn_fwd.hip", "attn_bwd.hip", "attn_bwd_kv.hip", "attn_bwd_q.hip", "attn_bwd_dq.hip", "proj_gemm.hip",
-           "proj_gemm_f32.hip", "layout_map.hip", "api.cpp"]
+           "proj_gemm_f32.hip", "layout_map.hip", "noalloc.hip", "api.cpp"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",

@@ -48,7 +48,8 @@ FBL_TUNE_TIME = 0
 FBL_TUNE_GFLOPS_X_MEMEFF = 1
 
 EXPORTED = ("fbl_layout_desc", "fbl_layout_packed_qkv", "fbl_layout_offset", "fbl_layout_map_device", "fbl_attn_fwd",
-            "fbl_attn_bwd_workspace", "fbl_attn_bwd_workspace_min", "fbl_attn_bwd", "fbl_attn_bwd_phases", "fbl_proj", "fbl_proj_dt",
+            "fbl_attn_bwd_workspace", "fbl_attn_bwd_workspace_min", "fbl_attn_bwd", "fbl_attn_bwd_phases",
+            "fbl_attn_bwd_noalloc", "fbl_proj", "fbl_proj_dt",
             "fbl_gemm_tile_count", "fbl_gemm_tile_info", "fbl_proj_candidates", "fbl_proj_tune", "fbl_proj_tuned_tile", "fbl_proj_auto_tile",
             "fbl_proj_tune_reset", "fbl_status_str")
 
@@ -110,6 +111,8 @@ def _load() -> ctypes.CDLL:
     lib.fbl_attn_bwd.restype = ctypes.c_int
     lib.fbl_attn_bwd_phases.argtypes = [ctypes.c_uint32] + lib.fbl_attn_bwd.argtypes
     lib.fbl_attn_bwd_phases.restype = ctypes.c_int
+    lib.fbl_attn_bwd_noalloc.argtypes = lib.fbl_attn_bwd.argtypes[:19] + [vp]
+    lib.fbl_attn_bwd_noalloc.restype = ctypes.c_int
     lib.fbl_proj.argtypes = [ctypes.c_uint32] + [ctypes.c_int64] * 3 + [vp, ctypes.c_int64, vp, ctypes.c_int64, vp,
                                                                         ctypes.c_int64, ctypes.c_int32, vp]
     lib.fbl_proj.restype = ctypes.c_int
@@ -366,6 +369,36 @@ def attn_bwd(q, k, v, o, do, lse, Hq: int, Hkv: int, scale: Optional[float] = No
     _check(fbl_attn_bwd_raw(lq, q, lk, k, lv, v, lo, o, ldo, do, lse, scale, _mask(causal, kv_len), ldq, dq, ldk,
                             dk, ldv, dv, workspace, workspace.numel() * workspace.element_size(), stream,
                             phases), "fbl_attn_bwd")
+    return dq, dk, dv
+
+
+NOALLOC_SCRATCH_BYTES = 64 << 20  # FBL_NOALLOC_SCRATCH_BYTES
+
+
+def fbl_attn_bwd_noalloc_raw(lq, q, lk, k, lv, v, lo, o, ldo, do, lse, scale, mask: Mask, ldq, dq, ldk, dk, ldv,
+                             dv, stream=None) -> int:
+    """Direct call of fbl_attn_bwd_noalloc; returns the status."""
+    ref = lambda l: ctypes.byref(l) if l is not None else None
+    return LIB.fbl_attn_bwd_noalloc(ref(lq), _ptr(q), ref(lk), _ptr(k), ref(lv), _ptr(v), ref(lo), _ptr(o), ref(ldo),
+                                    _ptr(do), _ptr(lse), float(scale), mask, ref(ldq), _ptr(dq), ref(ldk), _ptr(dk),
+                                    ref(ldv), _ptr(dv), _stream(stream) if stream != 0 else None)
+
+
+def attn_bwd_noalloc(q, k, v, o, do, lse, Hq: int, Hkv: int, dq, dk, dv, scale: Optional[float] = None,
+                     causal: bool = False, kv_len=None, stream=None):
+    """Backward through fbl_attn_bwd_noalloc: the library's own device scratch
+    replaces the workspace, so nothing is allocated; dq, dk, dv are the
+    caller's preallocated outputs (shapes and dtypes of q, k, v)."""
+    _check_kv_len(kv_len, q.shape[0], "attn_bwd_noalloc")
+    _check_device("attn_bwd_noalloc", stream, q=q, k=k, v=v, o=o, do=do, lse=lse, kv_len=kv_len, dq=dq, dk=dk,
+                  dv=dv)
+    lq, lk, lv = _layout(q, Hq), _layout(k, Hkv), _layout(v, Hkv)
+    lo, ldo = _layout(o, Hq), _layout(do, Hq)
+    ldq, ldk, ldv = _layout(dq, Hq), _layout(dk, Hkv), _layout(dv, Hkv)
+    if scale is None:
+        scale = 1.0 / math.sqrt(lq.D)
+    _check(fbl_attn_bwd_noalloc_raw(lq, q, lk, k, lv, v, lo, o, ldo, do, lse, scale, _mask(causal, kv_len), ldq, dq,
+                                    ldk, dk, ldv, dv, stream), "fbl_attn_bwd_noalloc")
     return dq, dk, dv
 
 

@@ -542,3 +542,17 @@ def test_autograd_rejects_broadcast_gradient():
     t = torch.zeros(2, 4, 64, dtype=torch.bfloat16)
     assert ag._unit(t, "attention") is t
     assert ag._unit(t[:, :, :32], "attention").data_ptr() == t.data_ptr()  # strided rows pass as views
+
+
+def test_noalloc_rejects_too_many_rows():
+    """fbl_attn_bwd_noalloc with more query rows than its scratch holds
+    statistics for: FBL_ERR_WORKSPACE, before any HIP call."""
+    macro = re.search(r"#define FBL_NOALLOC_SCRATCH_BYTES \((\d+)u << (\d+)\)", open(HEADER).read())
+    assert int(macro.group(1)) << int(macro.group(2)) == fbl.NOALLOC_SCRATCH_BYTES
+    rows = fbl.NOALLOC_SCRATCH_BYTES // 8 + 256
+    lq = fbl.fbl_layout_desc(fbl.FBL_BF16, 1, rows // 64, 64, 64)
+    lk = fbl.fbl_layout_desc(fbl.FBL_BF16, 1, rows // 64, 64, 64)
+    assert fbl.fbl_attn_bwd_workspace_min(lq, lk) > fbl.NOALLOC_SCRATCH_BYTES
+    st = F.fbl_attn_bwd_noalloc_raw(lq, FAKE, lk, FAKE, lk, FAKE, lq, FAKE, lq, FAKE, FAKE, 0.1, F.Mask(0, 0, None),
+                                    lq, FAKE, lk, FAKE, lk, FAKE, stream=0)
+    assert st == F.FBL_ERR_WORKSPACE
