@@ -325,6 +325,11 @@ def main():
                          "dW = X^T dY on token-major activations, every tile shape; block: a whole attention block "
                          "(QKV projection into a packed buffer, attention in place, output projection) fwd+bwd")
     ap.add_argument("--proj-shape", default="512,2048,8192", help="M,K,N for --op proj")
+    ap.add_argument("--tiles", default=None,
+                    help="explicit attention tile ids FWD,KV,DQ (bf16; -1 = automatic); default: the automatic choice")
+    ap.add_argument("--tune", action="store_true",
+                    help="run the measured tile selection (fbl_attn_tune) on the inputs before the warmup; the step "
+                         "then runs the tuned tiles")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="instead of attention, run 5 plain device copies of this many MiB (calibrates the HBM "
                          "byte counters FETCH_SIZE / WRITE_SIZE against a kernel of known traffic)")
@@ -372,15 +377,27 @@ def main():
     ws = torch.empty(fbl.fbl_attn_bwd_workspace(fbl.layout_of(q, w.Hq), fbl.layout_of(k, w.Hkv)),
                      dtype=torch.uint8, device="cuda")
     stream = torch.cuda.current_stream()
+    tiles = [fbl.FBL_ATTN_TILE_AUTO] * 3
+    if args.tiles:
+        tiles = [int(x) for x in args.tiles.split(",")]
+    tune = None
+    if args.tune:
+        best, tms, _ = fbl.attn_tune(q, k, v, do, w.Hq, w.Hkv, scale, causal, kv_len, o=o, lse=lse, dq=dq, dk=dk,
+                                     dv=dv, workspace=ws, reps=5)
+        torch.cuda.synchronize()
+        tune = {"chosen": list(best), "ms": {str(t): round(x, 4) for t, x in tms.items()}}
+    lq_, lk_ = fbl.layout_of(q, w.Hq), fbl.layout_of(k, w.Hkv)
+    auto = fbl.attn_auto_tiles(lq_, lk_, int(w.mask)) if w.dtype == "bf16" else None
+    run_tiles = None if auto is None else [a if t == fbl.FBL_ATTN_TILE_AUTO else t for t, a in zip(tiles, auto)]
 
     def bwd(phases):
         fbl.attn_bwd(q, k, v, o, do, lse, w.Hq, w.Hkv, scale, causal, kv_len, dq=dq, dk=dk, dv=dv, workspace=ws,
-                     phases=phases)
+                     phases=phases, kv_tile=tiles[1], dq_tile=tiles[2])
 
     def step(ev=None):
         if ev is not None:
             ev[0].record(stream)
-        fbl.attn_fwd(q, k, v, w.Hq, w.Hkv, scale, causal, kv_len, out=o, lse=lse)
+        fbl.attn_fwd(q, k, v, w.Hq, w.Hkv, scale, causal, kv_len, out=o, lse=lse, tile=tiles[0])
         if ev is not None:
             ev[1].record(stream)
         bwd(fbl.FBL_BWD_PREP)
@@ -514,6 +531,8 @@ def main():
         "algorithmic_gflop": round(flops / 1e9, 3),
         "algorithmic_bytes": alg_bytes["total"],
         "roofline": roofline,
+        "attn_tiles": run_tiles,
+        "tune": tune,
         "cpu_baseline": cpu,
         "gpu_over_oracle": None if cpu is None else round(tflops / cpu["value"], 1),
     }

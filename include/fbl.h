@@ -10,8 +10,10 @@
  * (B,H,S,HD) (section 4.3.1, the multi-head attention chain) are not carried
  * out as copies: they are folded into one affine index map per tensor
  * (section 4.3.2, the composed tile-index function f3 o f2 o f1), which the
- * kernels apply when they stage (tile_s x d) row tiles -- the R-Tile of
- * section 4.2 -- into LDS.  No layout-conversion kernel is ever launched.
+ * kernels apply when they stage (rows x d) row tiles -- the R-Tile of
+ * section 4.2 -- into LDS.  Which tile each kernel stages is chosen per
+ * shape from a filtered candidate set, by measurement (fbl_attn_tune) or a
+ * preference order.  No layout-conversion kernel is ever launched.
  * The projection products around attention (fbl_proj: Y = X W and its two
  * gradients, also for LoRA adapters) read the same token-major activations
  * in place, and Q, K, V can be views of one packed projection output
@@ -74,20 +76,22 @@ typedef enum { FBL_F32 = 0, FBL_BF16 = 1 } fbl_dtype;
 /*
  * Layout descriptor of one tensor with logical dims (B, H, S, D) -- the
  * logical shape S(t) and physical layout L(t) of a tensor in the paper's problem
- * statement (section 3.1) -- plus the R-Tile the kernels stage it in.
+ * statement (section 3.1) -- plus the tile-legality parameter of its R-Tile.
  *
  * Strides are in elements.  Token-major defaults: sd = 1, sh = D,
  * ss = H*D (row stride), sb = S*ss.  A row stride larger than H*D describes a
  * view into a wider packed projection output without copying it.
- * tile_s x tile_d is the R-Tile: tile_s token rows by tile_d head-dim
- * columns.  tile_d divides D (tile boundary preservation, section 4.3.1) and
- * sd == 1 (intra-tile continuity, section 4.3.1).
+ * tile_d is the R-Tile width in head-dim elements: it must divide D (tile
+ * boundary preservation, section 4.3.1), with sd == 1 (intra-tile
+ * continuity, section 4.3.1).  The kernels stage whole head rows; the number
+ * of rows per staged tile belongs to the kernel's tile configuration
+ * (fbl_attn_tile_info), not to the tensor.
  */
 typedef struct {
-    int32_t dtype;    /* fbl_dtype                                   */
-    int32_t tile_s;   /* R-Tile rows (tokens); set by fbl_layout_desc */
-    int32_t tile_d;   /* R-Tile columns (head-dim elements)          */
-    int32_t reserved; /* zero                                        */
+    int32_t dtype;     /* fbl_dtype                                   */
+    int32_t reserved0; /* zero                                        */
+    int32_t tile_d;    /* R-Tile columns (head-dim elements)          */
+    int32_t reserved1; /* zero                                        */
     int64_t B, S, H, D;
     int64_t sb, ss, sh, sd;
 } fbl_layout;
@@ -116,7 +120,6 @@ typedef struct {
  *                Must be >= S*row_stride when B > 1.
  *   tile_d       R-Tile width in head-dim elements; 0 means D.  Must divide D
  *                and span a multiple of 16 bytes.
- * tile_s is set from the library's tile table for (D, dtype).
  * Returns FBL_ERR_NULL, FBL_ERR_SHAPE, FBL_ERR_DTYPE or FBL_ERR_LAYOUT on
  * failure (then *out is left zeroed).  Pure host function.
  */
@@ -146,7 +149,10 @@ fbl_status fbl_layout_packed_qkv(fbl_layout* lq, fbl_layout* lk, fbl_layout* lv,
 
 /*
  * Host evaluation of the index map: element offset of logical (b, h, s, i),
- * or -1 when the descriptor is NULL or an index is out of range.
+ * or -1 when the descriptor is NULL or an index is out of range.  This is
+ * the composition of the head split and transpose of the multi-head
+ * attention chain (section 4.3.1) into one coordinate map (section 4.3.2,
+ * f3 o f2 o f1), evaluated for one element.
  */
 int64_t fbl_layout_offset(const fbl_layout* l, int64_t b, int64_t h, int64_t s, int64_t i);
 
@@ -159,7 +165,12 @@ int64_t fbl_layout_offset(const fbl_layout* l, int64_t b, int64_t h, int64_t s, 
 fbl_status fbl_layout_map_device(const fbl_layout* l, int64_t* out, void* stream);
 
 /*
- * Attention forward.
+ * Attention forward: O = softmax(scale Q K^T) V per query head, the attention
+ * module of section 2.2 (the LoRA fine-tuning example), with the masks and
+ * grouped-query head map described above, and the row log-sum-exp saved for
+ * the backward.  QK^T and the product with V are the consecutive
+ * matrix-product pair of section 4.4.2, fused in one kernel.  bf16 storage
+ * runs the forward tile FBL_ATTN_TILE_AUTO resolves to (fbl_attn_auto_tiles).
  *   lq/q     queries, Hq heads.       lk/k, lv/v  keys and values, Hkv heads.
  *   lo/o     output, same extents as q.
  *   lse      float32 [B, Hq, S_q] contiguous, written (saved for the backward).
@@ -212,7 +223,11 @@ fbl_status fbl_attn_bwd_workspace_min(const fbl_layout* lq, const fbl_layout* lk
 
 /*
  * Attention backward of L = sum(O * dO): writes dQ (Hq heads), dK and dV
- * (Hkv heads; each the sum over the query heads of its group).  The softmax
+ * (Hkv heads; each the sum over the query heads of its group) -- the chain
+ * rule through the matrix-product gradients of section 4.1 (forward-tensor
+ * dependent: they read Q, K, V and dO along other axes than the forward,
+ * dK and dV reducing over queries, dQ over keys) and the softmax gradient
+ * (section 4.1's forward-dependent, consistent-access class).  The softmax
  * probabilities are recomputed from q, k and the saved lse.  No output is
  * accumulated atomically, so the results are bitwise repeatable.  o and lse
  * must be the forward's outputs for q, k, v.
@@ -226,7 +241,9 @@ fbl_status fbl_attn_bwd_workspace_min(const fbl_layout* lq, const fbl_layout* lk
  * Same checks as fbl_attn_fwd for the shared arguments, plus: ldo/ldq
  * extents equal lq's, ldk/ldv extents equal lk's, the row-offset limit of
  * fbl_attn_fwd for every layout, outputs do not overlap inputs, each other or
- * the workspace.
+ * the workspace, and the workspace does not overlap an input or lse (it is
+ * written while they are read).  bf16 storage runs the kv and dQ tiles
+ * FBL_ATTN_TILE_AUTO resolves to.
  */
 fbl_status fbl_attn_bwd(const fbl_layout* lq, const void* q, const fbl_layout* lk, const void* k,
                         const fbl_layout* lv, const void* v, const fbl_layout* lo, const void* o,
@@ -258,6 +275,117 @@ fbl_status fbl_attn_bwd_phases(uint32_t phases, const fbl_layout* lq, const void
                                const void* o, const fbl_layout* ldo, const void* dO, const float* lse, float scale,
                                fbl_mask mask, const fbl_layout* ldq, void* dq, const fbl_layout* ldk, void* dk,
                                const fbl_layout* ldv, void* dv, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Tile configurations of the attention kernels (bf16 storage).  Each pass
+ * stages one kind of row tile of a token-major tensor -- the R-Tile of
+ * section 4.2, whole head rows -- and gives every wavefront a block of rows
+ * it keeps in registers:
+ *   FBL_ATTN_FWD     the forward: K/V tiles of `cols` keys; each wavefront
+ *                    owns `per_wave` queries of a workgroup's `rows`;
+ *   FBL_ATTN_BWD_KV  the backward's key/value pass: Q/dO tiles of `cols`
+ *                    queries; each wavefront owns 32 of the workgroup's
+ *                    `rows` keys;
+ *   FBL_ATTN_BWD_DQ  the backward's dQ pass from stored dS: K tiles of 32
+ *                    keys; each wavefront owns 32 of the `rows` queries.
+ * fbl_attn_tile_count gives the number of ids; fbl_attn_tile_info writes 8
+ * values for one id at head dim D (32, 64 or 128):
+ *   info[0] pass   info[1] rows   info[2] cols   info[3] wavefronts
+ *   info[4] per_wave   info[5] workgroups per CU   info[6] LDS bytes
+ *   info[7] 1 if the tile passes C1 and C2 at this head dim (runs), else 0.
+ * FBL_ERR_NULL, FBL_ERR_ARG (id out of range), FBL_ERR_UNSUPPORTED (D).
+ */
+#define FBL_ATTN_FWD 0u
+#define FBL_ATTN_BWD_KV 1u
+#define FBL_ATTN_BWD_DQ 2u
+#define FBL_ATTN_TILE_AUTO (-1)
+int32_t fbl_attn_tile_count(void);
+fbl_status fbl_attn_tile_info(int32_t tile, int64_t D, int32_t* info);
+
+/*
+ * Candidate tiles of one pass for the shapes lq (queries) and lk (keys):
+ * the three progressive filters of the R-Tile candidate generation (section
+ * 4.2, step 1, and the supplementary algorithm), read for gfx950 --
+ *   C1 compute alignment: whole 32x32 MFMA blocks per wavefront and per
+ *      staged tile, whole 16-deep chunks over the head dim, 2-8 wavefronts;
+ *   C2 memory alignment and capacity: the workgroups a CU holds fit its
+ *      160 KB of LDS; staged rows whole 16-byte loads and staged tiles whole
+ *      1 KB wavefront loads spread evenly over the wavefronts; the per-lane
+ *      registers fit a wavefront's share of the register file;
+ *   C3 shape: padding the sequence to whole workgroup row blocks and whole
+ *      staged tiles adds at most 10%; if no tile qualifies, the C1/C2
+ *      survivors of least padded volume.
+ * Writes up to `cap` ids in increasing order and the count (which may exceed
+ * cap).  bf16 descriptors only (FBL_ERR_DTYPE otherwise: fp32 storage has
+ * one configuration per pass).  Host only.
+ */
+fbl_status fbl_attn_candidates(uint32_t pass, const fbl_layout* lq, const fbl_layout* lk, int32_t* tiles,
+                               int32_t cap, int32_t* count);
+
+/*
+ * The ids FBL_ATTN_TILE_AUTO resolves to for (lq, lk, mask kind): tiles[0]
+ * forward, tiles[1] kv pass, tiles[2] dQ pass -- the measured choice of
+ * fbl_attn_tune for this shape when the process holds one, else the first
+ * candidate in a preference order measured on MI355X.  Host only.
+ */
+fbl_status fbl_attn_auto_tiles(const fbl_layout* lq, const fbl_layout* lk, uint32_t mask_kind, int32_t* tiles);
+
+/*
+ * fbl_attn_fwd and fbl_attn_bwd_phases with explicit tiles (fbl_attn_bwd is
+ * fbl_attn_bwd_tiled(FBL_BWD_ALL, ..., FBL_ATTN_TILE_AUTO, FBL_ATTN_TILE_AUTO,
+ * stream)): `tile`, `kv_tile`, `dq_tile` are ids of the right pass that pass
+ * C1 and C2 at this head dim
+ * (FBL_ERR_ARG for an id of another pass or out of range, FBL_ERR_UNSUPPORTED
+ * for one the filters exclude at this head dim), or FBL_ATTN_TILE_AUTO.  Any
+ * legal tile runs any shape (C3 only ranks them); every tile gives results
+ * within the same tolerance, and one tile is bitwise repeatable.  fp32
+ * storage takes FBL_ATTN_TILE_AUTO only.  dq_tile applies when the dQ pass
+ * reads stored dS (the workspace holds it).  Otherwise as fbl_attn_fwd /
+ * fbl_attn_bwd.
+ */
+fbl_status fbl_attn_fwd_tiled(const fbl_layout* lq, const void* q, const fbl_layout* lk, const void* k,
+                              const fbl_layout* lv, const void* v, const fbl_layout* lo, void* o, float* lse,
+                              float scale, fbl_mask mask, int32_t tile, void* stream);
+fbl_status fbl_attn_bwd_tiled(uint32_t phases, const fbl_layout* lq, const void* q, const fbl_layout* lk,
+                              const void* k, const fbl_layout* lv, const void* v, const fbl_layout* lo, const void* o,
+                              const fbl_layout* ldo, const void* dO, const float* lse, float scale, fbl_mask mask,
+                              const fbl_layout* ldq, void* dq, const fbl_layout* ldk, void* dk, const fbl_layout* ldv,
+                              void* dv, void* ws, size_t ws_bytes, int32_t kv_tile, int32_t dq_tile, void* stream);
+
+/*
+ * Measured tile selection for one attention shape (section 4.2's unified
+ * selection, per pass; the per-shape table is the analogue of the paper's
+ * lookup table for dynamic shapes).  Runs the forward, then the backward, on
+ * the caller's buffers (the arguments of fbl_attn_fwd and fbl_attn_bwd
+ * together); times every candidate of each pass (fbl_attn_candidates) once
+ * untimed and `reps` (1..1000) times with HIP events on `stream` -- the kv
+ * pass with the backward's statistics phase done once before, the dQ pass
+ * (only when the workspace holds stored dS) on the dS the kv pass left --
+ * and keeps, per pass, the id maximising
+ *   FBL_TUNE_TIME              1 / average time, or
+ *   FBL_TUNE_GFLOPS_X_MEMEFF   GFLOP/s x MemEfficiency (section 4.2): the
+ *                              pass's minimal bytes over the bytes its tile
+ *                              schedule stages (the forward re-reads a
+ *                              query block's K/V rows once per block of
+ *                              `rows` queries, the dQ pass its K rows).
+ * The choices go to a per-process table keyed by pass, dtype, extents, heads,
+ * head dim and mask kind, which FBL_ATTN_TILE_AUTO consults (thread-safe;
+ * fbl_attn_tuned_tile reads it, -1 if absent; fbl_attn_tune_reset clears
+ * it).  ms (optional, fbl_attn_tile_count() floats): each timed id's average
+ * milliseconds, -1 for the others; best (optional, 3 int32): the chosen
+ * forward, kv and dQ ids (-1 for dQ when it was not tuned).  Blocks until the
+ * timed launches finish; on return o, lse, dq, dk, dv hold the results of
+ * the chosen tiles.  bf16 only (FBL_ERR_DTYPE); FBL_ERR_ARG for an unknown
+ * objective or reps out of range; otherwise the statuses of fbl_attn_fwd and
+ * fbl_attn_bwd.
+ */
+fbl_status fbl_attn_tune(const fbl_layout* lq, const void* q, const fbl_layout* lk, const void* k,
+                         const fbl_layout* lv, const void* v, const fbl_layout* lo, void* o, float* lse,
+                         const fbl_layout* ldo, const void* dO, float scale, fbl_mask mask, const fbl_layout* ldq,
+                         void* dq, const fbl_layout* ldk, void* dk, const fbl_layout* ldv, void* dv, void* ws,
+                         size_t ws_bytes, uint32_t objective, int32_t reps, float* ms, int32_t* best, void* stream);
+int32_t fbl_attn_tuned_tile(uint32_t pass, const fbl_layout* lq, const fbl_layout* lk, uint32_t mask_kind);
+void fbl_attn_tune_reset(void);
 
 /*
  * fbl_attn_bwd for callers that cannot allocate device memory -- code under

@@ -14,10 +14,11 @@
 #include <map>
 #include <mutex>
 #include <tuple>
+#include <vector>
 
 #include "../../include/fbl.h"
+#include "attn_tiles.hpp"
 #include "kernels.hpp"
-#include "tiles.hpp"
 
 using fbl::bf16;
 
@@ -121,12 +122,18 @@ fbl_status check_qkv(const fbl_layout* lq, const void* q, const fbl_layout* lk, 
     return FBL_OK;
 }
 
-template <typename T>
-hipError_t dispatch_fwd(int D, const fbl::FwdArgs& a, hipStream_t s) {
+hipError_t dispatch_fwd(int32_t dtype, int D, int tile, const fbl::FwdArgs& a, hipStream_t s) {
+    if (dtype == FBL_BF16) {
+        switch (D) {
+            case 32: return fbl::launch_attn_fwd_bf16<32>(a, tile, s);
+            case 64: return fbl::launch_attn_fwd_bf16<64>(a, tile, s);
+            default: return fbl::launch_attn_fwd_bf16<128>(a, tile, s);
+        }
+    }
     switch (D) {
-        case 32: return fbl::launch_attn_fwd<T, 32>(a, s);
-        case 64: return fbl::launch_attn_fwd<T, 64>(a, s);
-        default: return fbl::launch_attn_fwd<T, 128>(a, s);
+        case 32: return fbl::launch_attn_fwd_f32<32>(a, s);
+        case 64: return fbl::launch_attn_fwd_f32<64>(a, s);
+        default: return fbl::launch_attn_fwd_f32<128>(a, s);
     }
 }
 
@@ -137,6 +144,101 @@ hipError_t dispatch_bwd(int D, const fbl::BwdArgs& a, unsigned phases, hipStream
         case 64: return fbl::launch_attn_bwd<T, 64>(a, phases, s);
         default: return fbl::launch_attn_bwd<T, 128>(a, phases, s);
     }
+}
+
+// ---------------------------------------------------------- attention tiles
+// Candidate tiles of one pass at one shape (C1, C2, C3 of attn_tiles.hpp) as
+// a bit set over the ids: when no tile keeps the padding within 10%, the
+// C1/C2 survivors of least padded volume.
+uint64_t attn_candidate_set(uint32_t pass, int64_t D, int64_t Sq, int64_t Skv) {
+    static_assert(fbl::kAttnTileCount <= 64, "tile ids fit the bit set");
+    uint64_t c12 = 0, all = 0;
+    for (int i = 0; i < fbl::kAttnTileCount; ++i) {
+        const fbl::AttnTile& t = fbl::kAttnTiles[i];
+        if ((uint32_t)t.pass != pass || !fbl::attn_c1(t, (int)D) || !fbl::attn_c2(t, (int)D)) continue;
+        c12 |= uint64_t(1) << i;
+        if (fbl::attn_c3(t, Sq, Skv)) all |= uint64_t(1) << i;
+    }
+    if (all || !c12) return all;
+    double best = 0;
+    for (int i = 0; i < fbl::kAttnTileCount; ++i)
+        if (c12 >> i & 1) {
+            const double v = fbl::attn_padded_volume(fbl::kAttnTiles[i], Sq, Skv);
+            if (!all || v < best) all = uint64_t(1) << i, best = v;
+            else if (v == best) all |= uint64_t(1) << i;
+        }
+    return all;
+}
+
+bool attn_tile_legal(uint32_t pass, int32_t tile, int64_t D) {
+    if (tile < 0 || tile >= fbl::kAttnTileCount) return false;
+    const fbl::AttnTile& t = fbl::kAttnTiles[tile];
+    return (uint32_t)t.pass == pass && fbl::attn_c1(t, (int)D) && fbl::attn_c2(t, (int)D);
+}
+
+// Per-shape table of measured choices (fbl_attn_tune), keyed by the pass and
+// everything that sets its work: storage type, extents, heads, head dim and
+// mask kind.
+struct AttnKey {
+    uint32_t pass;
+    int32_t dtype;
+    int64_t B, Sq, Skv, Hq, Hkv, D;
+    uint32_t mask;
+    bool operator<(const AttnKey& o) const {
+        return std::tie(pass, dtype, B, Sq, Skv, Hq, Hkv, D, mask) <
+               std::tie(o.pass, o.dtype, o.B, o.Sq, o.Skv, o.Hq, o.Hkv, o.D, o.mask);
+    }
+};
+std::mutex g_attn_mu;
+std::map<AttnKey, int32_t> g_attn_tuned;
+
+AttnKey attn_key(uint32_t pass, const fbl_layout* lq, const fbl_layout* lk, uint32_t mask_kind) {
+    return AttnKey{pass, lq->dtype, lq->B, lq->S, lk->S, lq->H, lk->H, lq->D, mask_kind};
+}
+
+// Untuned choice: the first candidate in a preference order per pass, else
+// the first legal tile of the pass.  The forward's order is the measured one
+// on the Llama-7B-like, Llama-3.2-1B-like GQA and GPT-2-medium-like causal
+// shapes (the same at d = 128 and 64): 128 queries in 64-key tiles first, the
+// 64-queries-per-wavefront tiles last.
+int32_t attn_default_tile(uint32_t pass, int64_t D, int64_t Sq, int64_t Skv) {
+    static const int fwd[] = {0, 2, 3, 4, 1};
+    static const int kv[] = {5, 6};
+    static const int dq[] = {7, 8, 9};
+    const int* order;
+    int n;
+    if (pass == FBL_ATTN_FWD) order = fwd, n = 5;
+    else if (pass == FBL_ATTN_BWD_KV) order = kv, n = 2;
+    else order = dq, n = 3;
+    const uint64_t cand = attn_candidate_set(pass, D, Sq, Skv);
+    for (int i = 0; i < n; ++i)
+        if (cand >> order[i] & 1) return order[i];
+    for (int i = 0; i < n; ++i)
+        if (attn_tile_legal(pass, order[i], D)) return order[i];
+    return -1;
+}
+
+// The tile a launch runs: an explicit id (legal for the pass at this head
+// dim), else the measured choice for the shape, else the untuned default.
+fbl_status attn_resolve(uint32_t pass, const fbl_layout* lq, const fbl_layout* lk, uint32_t mask_kind,
+                        int32_t requested, int32_t* out) {
+    if (requested != FBL_ATTN_TILE_AUTO) {
+        if (requested < 0 || requested >= fbl::kAttnTileCount || (uint32_t)fbl::kAttnTiles[requested].pass != pass)
+            return FBL_ERR_ARG;
+        if (!attn_tile_legal(pass, requested, lq->D)) return FBL_ERR_UNSUPPORTED;
+        *out = requested;
+        return FBL_OK;
+    }
+    {
+        std::lock_guard<std::mutex> lock(g_attn_mu);
+        const auto it = g_attn_tuned.find(attn_key(pass, lq, lk, mask_kind));
+        if (it != g_attn_tuned.end()) {
+            *out = it->second;
+            return FBL_OK;
+        }
+    }
+    *out = attn_default_tile(pass, lq->D, lq->S, lk->S);
+    return *out >= 0 ? FBL_OK : FBL_ERR_UNSUPPORTED;
 }
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -175,10 +277,12 @@ size_t ws_ds_bytes(const fbl_layout* lq, const fbl_layout* lk) {
 // (Measured: splitting the 512 items of the GPT-2-medium-like causal shape,
 // or the Llama-3.2-1B-like GQA shape four ways, is slower.)  The causal
 // choice is never below the other, so it sizes the workspace.
-int kv_split_for(const fbl_layout* lq, const fbl_layout* lk, bool causal = true) {
+// bq: the kv tile's queries per iteration (0: the smallest a kv tile at this
+// head dim stages, which gives the largest split and so sizes the workspace).
+int kv_split_for(const fbl_layout* lq, const fbl_layout* lk, bool causal = true, int64_t bq = 0) {
     if (lq->dtype != FBL_BF16 || lk->H <= 0 || lq->D <= 0) return 1;
     const int64_t items = (lk->S + 127) / 128 * lk->H * lk->B;
-    const int64_t bq = lq->D == 32 ? 64 : 32;     // queries per iteration
+    if (bq == 0) bq = lq->D == 32 ? 64 : 32;
     const int64_t slots = lq->D == 64 ? 512 : 256;  // workgroups resident at once (two per CU at D = 64)
     const int64_t iters = lq->H / lk->H * ((lq->S + bq - 1) / bq);
     int split = 1;
@@ -237,7 +341,6 @@ fbl_status fbl_layout_desc(fbl_layout* out, int32_t dtype, int64_t B, int64_t S,
     l.sb = batch_stride ? batch_stride : S * l.ss;
     if (tile_d > INT32_MAX) return FBL_ERR_LAYOUT;
     l.tile_d = (int32_t)(tile_d ? tile_d : D);
-    l.tile_s = fbl::tile_rows(D, dtype);
     const fbl_status st = check_layout(&l);
     if (st != FBL_OK) return st;
     *out = l;
@@ -283,9 +386,9 @@ fbl_status fbl_layout_map_device(const fbl_layout* l, int64_t* out, void* stream
     return e == hipSuccess ? FBL_OK : FBL_ERR_HIP;
 }
 
-fbl_status fbl_attn_fwd(const fbl_layout* lq, const void* q, const fbl_layout* lk, const void* k,
-                        const fbl_layout* lv, const void* v, const fbl_layout* lo, void* o, float* lse, float scale,
-                        fbl_mask mask, void* stream) {
+fbl_status fbl_attn_fwd_tiled(const fbl_layout* lq, const void* q, const fbl_layout* lk, const void* k,
+                              const fbl_layout* lv, const void* v, const fbl_layout* lo, void* o, float* lse,
+                              float scale, fbl_mask mask, int32_t tile, void* stream) {
     fbl_status st = check_qkv(lq, q, lk, k, lv, v, scale, mask);
     if (st != FBL_OK) return st;
     if (!lo || !o || !lse) return FBL_ERR_NULL;
@@ -301,6 +404,12 @@ fbl_status fbl_attn_fwd(const fbl_layout* lq, const void* q, const fbl_layout* l
         if (overlaps(lse, lse_bytes, ins[i], span_bytes(in_l[i]))) return FBL_ERR_ARG;
     }
     if (overlaps(o, span_bytes(lo), lse, lse_bytes)) return FBL_ERR_ARG;
+    int32_t t = -1;
+    if (lq->dtype == FBL_BF16) {
+        if ((st = attn_resolve(FBL_ATTN_FWD, lq, lk, mask.kind, tile, &t)) != FBL_OK) return st;
+    } else if (tile != FBL_ATTN_TILE_AUTO) {
+        return FBL_ERR_ARG;  // fp32 storage has one configuration
+    }
 
     fbl::FwdArgs a;
     a.q = q;
@@ -319,10 +428,14 @@ fbl_status fbl_attn_fwd(const fbl_layout* lq, const void* q, const fbl_layout* l
     a.Hkv = (int)lk->H;
     a.scale_log2 = scale * 1.4426950408889634f;
     a.mask = mask_args(mask);
-    const hipStream_t s = static_cast<hipStream_t>(stream);
-    const hipError_t e = lq->dtype == FBL_BF16 ? dispatch_fwd<bf16>((int)lq->D, a, s)
-                                               : dispatch_fwd<float>((int)lq->D, a, s);
+    const hipError_t e = dispatch_fwd(lq->dtype, (int)lq->D, t, a, static_cast<hipStream_t>(stream));
     return e == hipSuccess ? FBL_OK : FBL_ERR_HIP;
+}
+
+fbl_status fbl_attn_fwd(const fbl_layout* lq, const void* q, const fbl_layout* lk, const void* k,
+                        const fbl_layout* lv, const void* v, const fbl_layout* lo, void* o, float* lse, float scale,
+                        fbl_mask mask, void* stream) {
+    return fbl_attn_fwd_tiled(lq, q, lk, k, lv, v, lo, o, lse, scale, mask, FBL_ATTN_TILE_AUTO, stream);
 }
 
 fbl_status fbl_attn_bwd_workspace(const fbl_layout* lq, const fbl_layout* lk, size_t* bytes) {
@@ -343,11 +456,15 @@ fbl_status fbl_attn_bwd_workspace_min(const fbl_layout* lq, const fbl_layout* lk
     return FBL_OK;
 }
 
-fbl_status fbl_attn_bwd_phases(uint32_t phases, const fbl_layout* lq, const void* q, const fbl_layout* lk,
-                               const void* k, const fbl_layout* lv, const void* v, const fbl_layout* lo,
-                               const void* o, const fbl_layout* ldo, const void* dO, const float* lse, float scale,
-                               fbl_mask mask, const fbl_layout* ldq, void* dq, const fbl_layout* ldk, void* dk,
-                               const fbl_layout* ldv, void* dv, void* ws, size_t ws_bytes, void* stream) {
+}  // extern "C"
+
+namespace {
+
+fbl_status bwd_run(uint32_t phases, const fbl_layout* lq, const void* q, const fbl_layout* lk, const void* k,
+                   const fbl_layout* lv, const void* v, const fbl_layout* lo, const void* o, const fbl_layout* ldo,
+                   const void* dO, const float* lse, float scale, fbl_mask mask, const fbl_layout* ldq, void* dq,
+                   const fbl_layout* ldk, void* dk, const fbl_layout* ldv, void* dv, void* ws, size_t ws_bytes,
+                   int32_t kv_tile, int32_t dq_tile, void* stream) {
     if (phases == 0 || (phases & ~FBL_BWD_ALL)) return FBL_ERR_ARG;
     fbl_status st = check_qkv(lq, q, lk, k, lv, v, scale, mask);
     if (st != FBL_OK) return st;
@@ -401,10 +518,17 @@ fbl_status fbl_attn_bwd_phases(uint32_t phases, const fbl_layout* lq, const void
     const size_t ds_bytes = ws_ds_bytes(lq, lk);
     a.ds = ds_bytes && ws_bytes >= ws_stats_bytes(lq) + ds_bytes ? static_cast<char*>(ws) + ws_stats_bytes(lq)
                                                                  : nullptr;
+    // tiles of the bf16 passes (fp32 storage has one configuration per pass)
+    if (lq->dtype == FBL_BF16) {
+        if ((st = attn_resolve(FBL_ATTN_BWD_KV, lq, lk, mask.kind, kv_tile, &a.kv_tile)) != FBL_OK) return st;
+        if ((st = attn_resolve(FBL_ATTN_BWD_DQ, lq, lk, mask.kind, dq_tile, &a.dq_tile)) != FBL_OK) return st;
+    } else if (kv_tile != FBL_ATTN_TILE_AUTO || dq_tile != FBL_ATTN_TILE_AUTO) {
+        return FBL_ERR_ARG;
+    }
     // and the split key/value pass when it also holds the partial sums
     const size_t part_bytes = ws_part_bytes(lq, lk);
     if (a.ds && part_bytes && ws_bytes >= ws_stats_bytes(lq) + ds_bytes + part_bytes) {
-        a.kv_split = kv_split_for(lq, lk, (mask.kind & FBL_MASK_CAUSAL) != 0);
+        a.kv_split = kv_split_for(lq, lk, (mask.kind & FBL_MASK_CAUSAL) != 0, fbl::kAttnTiles[a.kv_tile].cols);
         a.dkv_part = reinterpret_cast<float*>(static_cast<char*>(ws) + ws_stats_bytes(lq) + ds_bytes);
     }
     a.nq32 = (int)((lq->S + 31) / 32);
@@ -431,13 +555,200 @@ fbl_status fbl_attn_bwd_phases(uint32_t phases, const fbl_layout* lq, const void
     return e == hipSuccess ? FBL_OK : FBL_ERR_HIP;
 }
 
+}  // namespace
+
+extern "C" {
+
+fbl_status fbl_attn_bwd_phases(uint32_t phases, const fbl_layout* lq, const void* q, const fbl_layout* lk,
+                               const void* k, const fbl_layout* lv, const void* v, const fbl_layout* lo,
+                               const void* o, const fbl_layout* ldo, const void* dO, const float* lse, float scale,
+                               fbl_mask mask, const fbl_layout* ldq, void* dq, const fbl_layout* ldk, void* dk,
+                               const fbl_layout* ldv, void* dv, void* ws, size_t ws_bytes, void* stream) {
+    return bwd_run(phases, lq, q, lk, k, lv, v, lo, o, ldo, dO, lse, scale, mask, ldq, dq, ldk, dk, ldv, dv, ws,
+                   ws_bytes, FBL_ATTN_TILE_AUTO, FBL_ATTN_TILE_AUTO, stream);
+}
+
 fbl_status fbl_attn_bwd(const fbl_layout* lq, const void* q, const fbl_layout* lk, const void* k,
                         const fbl_layout* lv, const void* v, const fbl_layout* lo, const void* o,
                         const fbl_layout* ldo, const void* dO, const float* lse, float scale, fbl_mask mask,
                         const fbl_layout* ldq, void* dq, const fbl_layout* ldk, void* dk, const fbl_layout* ldv,
                         void* dv, void* ws, size_t ws_bytes, void* stream) {
-    return fbl_attn_bwd_phases(FBL_BWD_ALL, lq, q, lk, k, lv, v, lo, o, ldo, dO, lse, scale, mask, ldq, dq, ldk, dk,
-                               ldv, dv, ws, ws_bytes, stream);
+    return bwd_run(FBL_BWD_ALL, lq, q, lk, k, lv, v, lo, o, ldo, dO, lse, scale, mask, ldq, dq, ldk, dk, ldv, dv, ws,
+                   ws_bytes, FBL_ATTN_TILE_AUTO, FBL_ATTN_TILE_AUTO, stream);
+}
+
+fbl_status fbl_attn_bwd_tiled(uint32_t phases, const fbl_layout* lq, const void* q, const fbl_layout* lk,
+                              const void* k, const fbl_layout* lv, const void* v, const fbl_layout* lo, const void* o,
+                              const fbl_layout* ldo, const void* dO, const float* lse, float scale, fbl_mask mask,
+                              const fbl_layout* ldq, void* dq, const fbl_layout* ldk, void* dk, const fbl_layout* ldv,
+                              void* dv, void* ws, size_t ws_bytes, int32_t kv_tile, int32_t dq_tile, void* stream) {
+    return bwd_run(phases, lq, q, lk, k, lv, v, lo, o, ldo, dO, lse, scale, mask, ldq, dq, ldk, dk, ldv, dv, ws,
+                   ws_bytes, kv_tile, dq_tile, stream);
+}
+
+int32_t fbl_attn_tile_count(void) { return fbl::kAttnTileCount; }
+
+fbl_status fbl_attn_tile_info(int32_t tile, int64_t D, int32_t* info) {
+    if (!info) return FBL_ERR_NULL;
+    if (tile < 0 || tile >= fbl::kAttnTileCount) return FBL_ERR_ARG;
+    if (D != 32 && D != 64 && D != 128) return FBL_ERR_UNSUPPORTED;
+    const fbl::AttnTile& t = fbl::kAttnTiles[tile];
+    const int32_t v[8] = {t.pass,
+                          fbl::attn_rows(t),
+                          t.cols,
+                          t.waves,
+                          t.per_wave,
+                          fbl::attn_occ(t, (int)D),
+                          fbl::attn_lds_bytes(t, (int)D),
+                          (fbl::attn_c1(t, (int)D) && fbl::attn_c2(t, (int)D)) ? 1 : 0};
+    std::memcpy(info, v, sizeof(v));
+    return FBL_OK;
+}
+
+fbl_status fbl_attn_candidates(uint32_t pass, const fbl_layout* lq, const fbl_layout* lk, int32_t* tiles,
+                               int32_t cap, int32_t* count) {
+    if (!lq || !lk || !count || (cap > 0 && !tiles)) return FBL_ERR_NULL;
+    if (pass > FBL_ATTN_BWD_DQ) return FBL_ERR_ARG;
+    fbl_status st;
+    if ((st = check_layout(lq)) != FBL_OK) return st;
+    if ((st = check_layout(lk)) != FBL_OK) return st;
+    if (lq->dtype != FBL_BF16) return FBL_ERR_DTYPE;  // fp32 storage: one configuration per pass
+    if (lq->D != 32 && lq->D != 64 && lq->D != 128) return FBL_ERR_UNSUPPORTED;
+    const uint64_t cand = attn_candidate_set(pass, lq->D, lq->S, lk->S);
+    int32_t n = 0;
+    for (int t = 0; t < fbl::kAttnTileCount; ++t)
+        if (cand >> t & 1) {
+            if (n < cap) tiles[n] = t;
+            ++n;
+        }
+    *count = n;
+    return FBL_OK;
+}
+
+fbl_status fbl_attn_auto_tiles(const fbl_layout* lq, const fbl_layout* lk, uint32_t mask_kind, int32_t* tiles) {
+    if (!lq || !lk || !tiles) return FBL_ERR_NULL;
+    fbl_status st;
+    if ((st = check_layout(lq)) != FBL_OK) return st;
+    if ((st = check_layout(lk)) != FBL_OK) return st;
+    if (lq->dtype != FBL_BF16) return FBL_ERR_DTYPE;
+    if (lq->D != 32 && lq->D != 64 && lq->D != 128) return FBL_ERR_UNSUPPORTED;
+    for (uint32_t pass = 0; pass <= FBL_ATTN_BWD_DQ; ++pass)
+        if ((st = attn_resolve(pass, lq, lk, mask_kind, FBL_ATTN_TILE_AUTO, &tiles[pass])) != FBL_OK) return st;
+    return FBL_OK;
+}
+
+fbl_status fbl_attn_tune(const fbl_layout* lq, const void* q, const fbl_layout* lk, const void* k,
+                         const fbl_layout* lv, const void* v, const fbl_layout* lo, void* o, float* lse,
+                         const fbl_layout* ldo, const void* dO, float scale, fbl_mask mask, const fbl_layout* ldq,
+                         void* dq, const fbl_layout* ldk, void* dk, const fbl_layout* ldv, void* dv, void* ws,
+                         size_t ws_bytes, uint32_t objective, int32_t reps, float* ms, int32_t* best, void* stream) {
+    if (objective > FBL_TUNE_GFLOPS_X_MEMEFF || reps < 1 || reps > 1000) return FBL_ERR_ARG;
+    // every argument check, once, before anything is timed
+    fbl_status st = fbl_attn_fwd_tiled(lq, q, lk, k, lv, v, lo, o, lse, scale, mask, FBL_ATTN_TILE_AUTO, stream);
+    if (st != FBL_OK) return st;
+    if (lq->dtype != FBL_BF16) return FBL_ERR_DTYPE;  // fp32 storage: one configuration per pass
+    auto bwd = [&](uint32_t phases, int32_t kv_tile, int32_t dq_tile) {
+        return bwd_run(phases, lq, q, lk, k, lv, v, lo, o, ldo, dO, lse, scale, mask, ldq, dq, ldk, dk, ldv, dv, ws,
+                       ws_bytes, kv_tile, dq_tile, stream);
+    };
+    if ((st = bwd(FBL_BWD_ALL, FBL_ATTN_TILE_AUTO, FBL_ATTN_TILE_AUTO)) != FBL_OK) return st;
+    if (ms)
+        for (int t = 0; t < fbl::kAttnTileCount; ++t) ms[t] = -1.0f;
+    const hipStream_t s = static_cast<hipStream_t>(stream);
+    hipEvent_t e0 = nullptr, e1 = nullptr;
+    if (hipEventCreate(&e0) != hipSuccess || hipEventCreate(&e1) != hipSuccess) {
+        if (e0) hipEventDestroy(e0);
+        return FBL_ERR_HIP;
+    }
+    // average milliseconds of `reps` launches after one untimed launch
+    auto timed = [&](auto&& launch, float* out) -> fbl_status {
+        fbl_status r = launch();
+        if (r != FBL_OK) return r;
+        if (hipEventRecord(e0, s) != hipSuccess) return FBL_ERR_HIP;
+        for (int i = 0; i < reps; ++i)
+            if ((r = launch()) != FBL_OK) return r;
+        float total = 0;
+        if (hipEventRecord(e1, s) != hipSuccess || hipEventSynchronize(e1) != hipSuccess ||
+            hipEventElapsedTime(&total, e0, e1) != hipSuccess)
+            return FBL_ERR_HIP;
+        *out = total / (float)reps;
+        return FBL_OK;
+    };
+    // MemEfficiency of a tile (section 4.2): the pass's minimal bytes over the
+    // bytes its tile schedule stages.  Per (batch, query head), the forward
+    // stages the K and V rows a query block sees once per block of `rows`
+    // queries, the dQ pass the K rows once per block; the kv pass stages the
+    // same rows whatever its query tile, so its efficiency is 1.
+    const bool causal = (mask.kind & FBL_MASK_CAUSAL) != 0;
+    const double D = (double)lq->D, Sq = (double)lq->S, Skv = (double)lk->S;
+    const double bh = (double)lq->B * (double)lq->H;
+    auto keys_staged = [&](int rows) {  // keys read per (batch, query head) over its query blocks
+        double n = 0;
+        for (int64_t q0 = 0; q0 < lq->S; q0 += rows) n += causal ? std::min(Skv, (double)(q0 + rows)) : Skv;
+        return n;
+    };
+    auto mem_eff = [&](uint32_t pass, int tile) {
+        const int rows = fbl::attn_rows(fbl::kAttnTiles[tile]);
+        if (pass == FBL_ATTN_FWD) {
+            const double qo = 2.0 * bh * Sq * D * 2 + bh * Sq * 4;  // Q read, O written, LSE written
+            const double kv_min = 2.0 * (double)lk->B * (double)lk->H * Skv * D * 2;
+            return (qo + kv_min) / (qo + 2.0 * bh * keys_staged(rows) * D * 2);
+        }
+        if (pass == FBL_ATTN_BWD_DQ) {
+            const double ds = 2048.0 * bh * std::ceil(Sq / 32) * std::ceil(Skv / 32) * (causal ? 0.5 : 1.0);
+            const double fixed = ds + bh * Sq * D * 2;  // dS read, dQ written
+            return (fixed + (double)lk->B * (double)lk->H * Skv * D * 2) / (fixed + bh * keys_staged(rows) * D * 2);
+        }
+        return 1.0;
+    };
+    int32_t pick[3] = {-1, -1, -1};
+    const bool ds_path = ws_ds_bytes(lq, lk) && ws_bytes >= ws_stats_bytes(lq) + ws_ds_bytes(lq, lk);
+    for (uint32_t pass = 0; pass <= FBL_ATTN_BWD_DQ && st == FBL_OK; ++pass) {
+        if (pass == FBL_ATTN_BWD_DQ && !ds_path) break;  // the recompute pass has one configuration
+        const uint64_t cand = attn_candidate_set(pass, lq->D, lq->S, lk->S);
+        double pick_score = 0;
+        for (int t = 0; t < fbl::kAttnTileCount && st == FBL_OK; ++t) {
+            if (!(cand >> t & 1)) continue;
+            float avg = 0;
+            if (pass == FBL_ATTN_FWD)
+                st = timed([&] { return fbl_attn_fwd_tiled(lq, q, lk, k, lv, v, lo, o, lse, scale, mask, t, stream); },
+                           &avg);
+            else if (pass == FBL_ATTN_BWD_KV)
+                st = timed([&] { return bwd(FBL_BWD_KV, t, FBL_ATTN_TILE_AUTO); }, &avg);
+            else
+                st = timed([&] { return bwd(FBL_BWD_Q, pick[FBL_ATTN_BWD_KV], t); }, &avg);
+            if (st != FBL_OK) break;
+            if (ms) ms[t] = avg;
+            double score = 1.0 / (double)avg;
+            if (objective == FBL_TUNE_GFLOPS_X_MEMEFF) score *= mem_eff(pass, t);
+            if (pick[pass] < 0 || score > pick_score) pick[pass] = t, pick_score = score;
+        }
+        if (st == FBL_OK && pick[pass] < 0) st = FBL_ERR_UNSUPPORTED;
+    }
+    hipEventDestroy(e0);
+    hipEventDestroy(e1);
+    if (st != FBL_OK) return st;
+    {
+        std::lock_guard<std::mutex> lock(g_attn_mu);
+        for (uint32_t pass = 0; pass <= FBL_ATTN_BWD_DQ; ++pass)
+            if (pick[pass] >= 0) g_attn_tuned[attn_key(pass, lq, lk, mask.kind)] = pick[pass];
+    }
+    if (best) std::memcpy(best, pick, sizeof(pick));
+    // leave o, lse, dq, dk and dv holding the results of the chosen tiles
+    if ((st = fbl_attn_fwd_tiled(lq, q, lk, k, lv, v, lo, o, lse, scale, mask, pick[0], stream)) != FBL_OK) return st;
+    return bwd(FBL_BWD_ALL, pick[1], pick[2] >= 0 ? pick[2] : FBL_ATTN_TILE_AUTO);
+}
+
+int32_t fbl_attn_tuned_tile(uint32_t pass, const fbl_layout* lq, const fbl_layout* lk, uint32_t mask_kind) {
+    if (!lq || !lk || pass > FBL_ATTN_BWD_DQ) return -1;
+    std::lock_guard<std::mutex> lock(g_attn_mu);
+    const auto it = g_attn_tuned.find(attn_key(pass, lq, lk, mask_kind));
+    return it == g_attn_tuned.end() ? -1 : it->second;
+}
+
+void fbl_attn_tune_reset(void) {
+    std::lock_guard<std::mutex> lock(g_attn_mu);
+    g_attn_tuned.clear();
 }
 
 }  // extern "C"

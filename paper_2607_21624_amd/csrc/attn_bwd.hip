@@ -571,7 +571,7 @@ hipError_t launch_attn_bwd(const BwdArgs& a, unsigned phases, hipStream_t stream
     }
     if (phases & 2u) {
         if constexpr (sizeof(T) == 2) {
-            const hipError_t ek = launch_attn_bwd_kv_bf16<D>(a, stream);
+            const hipError_t ek = launch_attn_bwd_kv_bf16<D>(a, a.kv_tile, stream);
             if (ek != hipSuccess) return ek;
         } else {
             const int n = (a.Skv + kKvBN - 1) / kKvBN * a.Hkv * a.B;
@@ -581,7 +581,8 @@ hipError_t launch_attn_bwd(const BwdArgs& a, unsigned phases, hipStream_t stream
     }
     if (phases & 4u) {
         if constexpr (sizeof(T) == 2) {
-            const hipError_t eq = a.ds ? launch_attn_bwd_dq_bf16<D>(a, stream) : launch_attn_bwd_q_bf16<D>(a, stream);
+            const hipError_t eq =
+                a.ds ? launch_attn_bwd_dq_bf16<D>(a, a.dq_tile, stream) : launch_attn_bwd_q_bf16<D>(a, stream);
             if (eq != hipSuccess) return eq;
         } else {
             const int n = (a.S + kQBM - 1) / kQBM * a.Hq * a.B;

@@ -29,6 +29,7 @@
 // unmasked, and they may be non-finite).
 #include <type_traits>
 
+#include "attn_tiles.hpp"
 #include "cdna4.hpp"
 #include "kernels.hpp"
 #include "stage.hpp"
@@ -267,19 +268,30 @@ hipError_t launch_dq(const BwdArgs& a, hipStream_t stream) {
     return hipGetLastError();
 }
 
-// Workgroup shape of the dQ pass.
-constexpr int kDqWaves = 4;
-constexpr int kDqBufs = 4;
+template <int D, int TILE>
+hipError_t launch_dq_tile(const BwdArgs& a, hipStream_t stream) {
+    constexpr AttnTile t = kAttnTiles[TILE];
+    static_assert(t.pass == kAttnDq && t.per_wave == 32 * kDqTiles && t.cols == 32, "a dQ-pass tile");
+    using P = DqPipe<D, t.waves, t.bufs>;
+    static_assert(P::BYTES == attn_lds_bytes(t, D) && P::OCC == attn_occ(t, D),
+                  "the kernel's LDS layout and occupancy are the tile table's");
+    return launch_dq<D, t.waves, t.bufs>(a, stream);
+}
 
 }  // namespace
 
 template <int D>
-hipError_t launch_attn_bwd_dq_bf16(const BwdArgs& a, hipStream_t stream) {
-    return launch_dq<D, kDqWaves, kDqBufs>(a, stream);
+hipError_t launch_attn_bwd_dq_bf16(const BwdArgs& a, int tile, hipStream_t stream) {
+    switch (tile) {
+        case 7: return launch_dq_tile<D, 7>(a, stream);
+        case 8: return launch_dq_tile<D, 8>(a, stream);
+        case 9: return launch_dq_tile<D, 9>(a, stream);
+        default: return hipErrorInvalidValue;
+    }
 }
 
-template hipError_t launch_attn_bwd_dq_bf16<32>(const BwdArgs&, hipStream_t);
-template hipError_t launch_attn_bwd_dq_bf16<64>(const BwdArgs&, hipStream_t);
-template hipError_t launch_attn_bwd_dq_bf16<128>(const BwdArgs&, hipStream_t);
+template hipError_t launch_attn_bwd_dq_bf16<32>(const BwdArgs&, int, hipStream_t);
+template hipError_t launch_attn_bwd_dq_bf16<64>(const BwdArgs&, int, hipStream_t);
+template hipError_t launch_attn_bwd_dq_bf16<128>(const BwdArgs&, int, hipStream_t);
 
 }  // namespace fbl

@@ -38,6 +38,7 @@
 // stored (the dQ pass never reads them).
 #include <type_traits>
 
+#include "attn_tiles.hpp"
 #include "cdna4.hpp"
 #include "kernels.hpp"
 #include "stage.hpp"
@@ -51,12 +52,13 @@ constexpr int kPWaves = 4;
 constexpr int kPKeys = 32 * kPWaves;  // keys per workgroup
 constexpr int kLead = 4;              // product slots between an operand read and its use
 
-template <int D>
+// BQ_ queries per block (the staged Q/dO tile rows of the tile table).  At
+// D = 64 with 32-query blocks the wavefront's state fits 256 registers, so
+// two workgroups share a CU (two waves per SIMD).
+template <int D, int BQ_>
 struct KvPipe {
-    // queries per block: 32 (64 at D = 32).  At D = 64 the wavefront's state
-    // fits 256 registers, so two workgroups share a CU (two waves per SIMD).
-    static constexpr int BQ = D == 32 ? 64 : 32;
-    static constexpr int OCC = D == 64 ? 2 : 1;
+    static constexpr int BQ = BQ_;
+    static constexpr int OCC = (D == 64 && BQ == 32) ? 2 : 1;
     static constexpr int NQT = BQ / 32;
     static constexpr int TB = BQ * D * 2;  // bytes of one bf16 Q or dO tile
     static constexpr int NBUF = 4;
@@ -73,9 +75,9 @@ struct KvPipe {
     static_assert(BYTES <= 160 * 1024, "LDS of one workgroup");
 };
 
-template <int D, bool DS>
-__global__ __launch_bounds__(256, KvPipe<D>::OCC) void attn_bwd_kv_bf16(BwdArgs a) {
-    using P = KvPipe<D>;
+template <int D, int BQ_, bool DS>
+__global__ __launch_bounds__(256, (KvPipe<D, BQ_>::OCC)) void attn_bwd_kv_bf16(BwdArgs a) {
+    using P = KvPipe<D, BQ_>;
     constexpr int NC = D / 16;
     constexpr int ND = D / 32;
     constexpr int BQ = P::BQ;
@@ -475,12 +477,6 @@ __global__ __launch_bounds__(256, KvPipe<D>::OCC) void attn_bwd_kv_bf16(BwdArgs 
     }
 }
 
-template __global__ void attn_bwd_kv_bf16<32, false>(BwdArgs);
-template __global__ void attn_bwd_kv_bf16<64, false>(BwdArgs);
-template __global__ void attn_bwd_kv_bf16<128, false>(BwdArgs);
-template __global__ void attn_bwd_kv_bf16<32, true>(BwdArgs);
-template __global__ void attn_bwd_kv_bf16<64, true>(BwdArgs);
-template __global__ void attn_bwd_kv_bf16<128, true>(BwdArgs);
 
 // dK and dV of a split key/value pass: the kv_split partial sums of each
 // element added in split order (deterministic), rounded once to bf16.  One
@@ -507,14 +503,15 @@ __global__ __launch_bounds__(256) void attn_bwd_kv_reduce(BwdArgs a) {
     store4(dst, acc[0], acc[1], acc[2], acc[3]);
 }
 
-template <int D, bool DS>
+template <int D, int BQ, bool DS>
 hipError_t launch_kv(const BwdArgs& a, hipStream_t stream) {
-    const hipError_t once = ensure_dynamic_lds<&attn_bwd_kv_bf16<D, DS>>(KvPipe<D>::BYTES);
+    using P = KvPipe<D, BQ>;
+    const hipError_t once = ensure_dynamic_lds<&attn_bwd_kv_bf16<D, BQ, DS>>(P::BYTES);
     if (once != hipSuccess) return once;
-    constexpr int lds = KvPipe<D>::BYTES;
+    constexpr int lds = P::BYTES;
     const int nkb = (a.Skv + kPKeys - 1) / kPKeys;
-    hipLaunchKernelGGL((attn_bwd_kv_bf16<D, DS>), dim3(rank_major_grid(nkb * a.kv_split, a.Hkv * a.B)), dim3(256),
-                       lds, stream, a);
+    hipLaunchKernelGGL((attn_bwd_kv_bf16<D, BQ, DS>), dim3(rank_major_grid(nkb * a.kv_split, a.Hkv * a.B)),
+                       dim3(256), lds, stream, a);
     if (a.kv_split > 1) {
         const int64_t n = 2 * (int64_t)a.B * a.Skv * a.Hkv * (D / 4);
         hipLaunchKernelGGL((attn_bwd_kv_reduce<D>), dim3((unsigned)((n + 255) / 256)), dim3(256), 0, stream, a);
@@ -524,13 +521,32 @@ hipError_t launch_kv(const BwdArgs& a, hipStream_t stream) {
 
 }  // namespace
 
-template <int D>
-hipError_t launch_attn_bwd_kv_bf16(const BwdArgs& a, hipStream_t stream) {
-    return a.ds ? launch_kv<D, true>(a, stream) : launch_kv<D, false>(a, stream);
+// One tile of the table: its query block (the staged Q/dO rows); the split
+// is the launch's a.kv_split.
+template <int D, int TILE>
+hipError_t launch_kv_tile(const BwdArgs& a, hipStream_t stream) {
+    constexpr AttnTile t = kAttnTiles[TILE];
+    static_assert(t.pass == kAttnKv && t.per_wave == 32 && t.waves == kPWaves && t.bufs == 4, "a kv-pass tile");
+    if constexpr (!attn_c1(t, D) || !attn_c2(t, D)) {
+        return hipErrorInvalidValue;  // not built at this head dim (the filters exclude it)
+    } else {
+        static_assert(KvPipe<D, t.cols>::BYTES == attn_lds_bytes(t, D) && KvPipe<D, t.cols>::OCC == attn_occ(t, D),
+                      "the kernel's LDS layout and occupancy are the tile table's");
+        return a.ds ? launch_kv<D, t.cols, true>(a, stream) : launch_kv<D, t.cols, false>(a, stream);
+    }
 }
 
-template hipError_t launch_attn_bwd_kv_bf16<32>(const BwdArgs&, hipStream_t);
-template hipError_t launch_attn_bwd_kv_bf16<64>(const BwdArgs&, hipStream_t);
-template hipError_t launch_attn_bwd_kv_bf16<128>(const BwdArgs&, hipStream_t);
+template <int D>
+hipError_t launch_attn_bwd_kv_bf16(const BwdArgs& a, int tile, hipStream_t stream) {
+    switch (tile) {
+        case 5: return launch_kv_tile<D, 5>(a, stream);
+        case 6: return launch_kv_tile<D, 6>(a, stream);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+template hipError_t launch_attn_bwd_kv_bf16<32>(const BwdArgs&, int, hipStream_t);
+template hipError_t launch_attn_bwd_kv_bf16<64>(const BwdArgs&, int, hipStream_t);
+template hipError_t launch_attn_bwd_kv_bf16<128>(const BwdArgs&, int, hipStream_t);
 
 }  // namespace fbl

@@ -1,4 +1,5 @@
-// attn_fwd.hip -- attention forward on token-major Q/K/V, gfx950.
+// attn_fwd.hip -- attention forward for fp32 storage on token-major Q/K/V,
+// gfx950.  (bf16 storage: attn_fwd_bf16.hip, templated on its tile.)
 //
 // One workgroup = 4 wavefronts = 128 queries of one (batch, query head); each
 // wavefront owns 32 queries.  Key/value tiles of 64 rows (the R-Tile, paper
@@ -16,15 +17,13 @@
 //                   accumulator holds one query per lane column, so the
 //                   softmax row max/sum over keys is an in-lane reduction
 //                   plus one exchange between the two 32-lane halves;
-//   O^T += V^T P^T  A = V^T via LDS transposed reads (ds_read_b64_tr_b16),
-//                   B = P^T straight from the S^T accumulator registers.
-// QK^T followed by PV is the consecutive matrix-product pair of section 4.4.2;
-// both share one tile configuration inside one kernel.
-// Online softmax in base 2 with scale*log2(e) folded into one FMA per score.
-// The running maximum is raised only when a tile exceeds it by more than
-// 2^8 (a stale maximum leaves every probability <= 256 and cancels in O/l),
-// which skips almost all rescales of the O accumulator.  The saved LSE is
-// converted to natural log at the store.
+//   O^T += V^T P^T  A = V^T from LDS column reads, B = P^T straight from the
+//                   S^T accumulator registers.
+// fp32 MFMAs (v_mfma_f32_32x32x2_f32, eight per 16-deep chunk).  Online
+// softmax in base 2 with scale*log2(e) folded into one FMA per score; the
+// running maximum is raised only when a tile exceeds it by more than 2^8 (a
+// stale maximum leaves every probability <= 256 and cancels in O/l).  The
+// saved LSE is converted to natural log at the store.
 #include <type_traits>
 
 #include "cdna4.hpp"
@@ -41,13 +40,13 @@ constexpr int kFwdBM = 32 * kFwdWaves;  // queries per workgroup
 constexpr int kFwdBN = 64;              // keys per tile
 constexpr float kRescaleSlack = 8.0f;   // log2 of the largest unnormalised probability
 
-template <typename T, int D>
-__global__ __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) void attn_fwd_kernel(FwdArgs a) {
+template <int D>
+__global__ __launch_bounds__(256, 1) void attn_fwd_f32(FwdArgs a) {
+    using T = float;
     constexpr int NC = D / 16;  // k-chunks over the head dim
     constexpr int ND = D / 32;  // 32-wide output column blocks
     constexpr int TILE = kFwdBN * D;
     constexpr uint32_t TB = TILE * sizeof(T);  // tile bytes
-    constexpr bool kBf16 = sizeof(T) == 2;
     extern __shared__ __attribute__((aligned(1024))) unsigned char fwd_smem[];
     T* smem = reinterpret_cast<T*>(fwd_smem);  // K0 K1 V0 V1, TILE elements each
     const uint32_t lds = lds_addr(fwd_smem);  // LDS byte address of the tiles
@@ -88,17 +87,10 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) void attn_fwd_kernel(F
         for (int cc = 0; cc < NC; ++cc) {
             float z[8] = {0, 0, 0, 0, 0, 0, 0, 0};
             if (qi < S) {
-                if constexpr (kBf16) {
-                    uint4 x = load16(qrow + 16 * cc + 8 * g);
-                    if (neg) { x.x ^= 0x80008000u; x.y ^= 0x80008000u; x.z ^= 0x80008000u; x.w ^= 0x80008000u; }
-                    qf[cc].v = __builtin_bit_cast(bf16x8, x);
-                    continue;
-                } else {
-                    const f32x4 x0 = __builtin_bit_cast(f32x4, load16(qrow + 16 * cc + 8 * g));
-                    const f32x4 x1 = __builtin_bit_cast(f32x4, load16(qrow + 16 * cc + 8 * g + 4));
+                const f32x4 x0 = __builtin_bit_cast(f32x4, load16(qrow + 16 * cc + 8 * g));
+                const f32x4 x1 = __builtin_bit_cast(f32x4, load16(qrow + 16 * cc + 8 * g + 4));
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) { z[e] = neg ? -x0[e] : x0[e]; z[4 + e] = neg ? -x1[e] : x1[e]; }
-                }
+                for (int e = 0; e < 4; ++e) { z[e] = neg ? -x0[e] : x0[e]; z[4 + e] = neg ? -x1[e] : x1[e]; }
             }
             pack_frag(qf[cc], z);
         }
@@ -119,8 +111,6 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) void attn_fwd_kernel(F
     DmaPlan<T, D, kFwdBN, kFwdWaves> dk, dv;
     dk.init(kbytes, wave, lane);
     dv.init(vbytes, wave, lane);
-    LaneOffsets<D> lo;
-    if constexpr (kBf16) lo.init(lds_addr(fwd_smem), lane);
 
     // Software pipeline over key tiles j: while the softmax of tile j runs on
     // the vector ALUs, the scores of tile j+1 are already in the matrix
@@ -140,8 +130,7 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) void attn_fwd_kernel(F
 #pragma unroll
             for (int cc = 0; cc < NC; ++cc) {
                 Frag<T> kf;
-                if constexpr (kBf16) kf.v = lds_b128(lo.row[cc], kbuf * TB + kt * 32 * D * 2);
-                else tile_row_frag<D>(kf, smem + kbuf * TILE, kt * 32 + c32, 16 * cc + 8 * g);
+                tile_row_frag<D>(kf, smem + kbuf * TILE, kt * 32 + c32, 16 * cc + 8 * g);
                 mma(sc[P][kt], kf, qf[cc]);
             }
         }
@@ -201,124 +190,15 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) void attn_fwd_kernel(F
 #pragma unroll
                 for (int t = 0; t < ND; ++t) {
                     Frag<T> vf;
-                    if constexpr (kBf16) {
-                        const uint32_t rb = (2 + P) * TB + (kt * 32 + 16 * cc) * D * 2;
-                        const bf16x4 x0 = lds_tr(lo.tr[t][0], rb), x1 = lds_tr(lo.tr[t][1], rb);
-                        vf.v = bf16x8{x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
-                    } else {
-                        const int row0 = kt * 32 + 16 * cc + 4 * g;
-                        tile_tr_frag<D>(vf, smem + (2 + P) * TILE, row0, row0 + 8, 32 * t, lane);
-                    }
+                    const int row0 = kt * 32 + 16 * cc + 4 * g;
+                    tile_tr_frag<D>(vf, smem + (2 + P) * TILE, row0, row0 + 8, 32 * t, lane);
                     mma(oacc[t], vf, pf);
                 }
             }
     };
 
-    // bf16 iteration j (parity P): the products of S_{j+1} interleaved with the
-    // softmax of tile j, operands read from LDS kLead product slots ahead of
-    // their use, then O += P_j V_j.
-    constexpr int kLead = 4;
-    constexpr int NQK = 2 * NC;      // S^T products per tile: key half kt = k / NC, d-chunk k % NC
-    constexpr int NPV = 2 * 2 * ND;  // O^T products: d-block n % ND, chunk (n / ND) % 2, half n / (2 ND)
-    Frag<T> fk[NQK];
-    auto read_k = [&](int kbuf, int k) __attribute__((always_inline)) {
-        if constexpr (kBf16) fk[k].v = lds_b128(lo.row[k % NC], kbuf * TB + (k / NC) * 32 * D * 2);
-    };
-    bf16x4 vv[2 * NPV];
-    auto read_v = [&](int vbuf, int n) __attribute__((always_inline)) {
-        if constexpr (kBf16) {
-            const int t = n % ND, cc = (n / ND) % 2, kt = n / (2 * ND);
-            const uint32_t off = (2 + vbuf) * TB + (kt * 32 + 16 * cc) * D * 2;
-            vv[2 * n] = lds_tr(lo.tr[t][0], off);
-            vv[2 * n + 1] = lds_tr(lo.tr[t][1], off);
-        }
-    };
-    auto step_bf16 = [&](auto par_c, auto mask_c, int j) __attribute__((always_inline)) {
-        constexpr int P = decltype(par_c)::value;
-        constexpr int NP = 1 - P;
-        constexpr bool MASK = decltype(mask_c)::value;
-        wait_vmcnt<0>();
-        __syncthreads();  // K_{j+1} and V_j landed; iteration j-1 is done everywhere
-        if (j + 2 < nkb) dk.issue(lds + P * TB, rk, (uint32_t)((j + 2) * kFwdBN) * kbytes, wave);
-        const bool more = j + 1 < nkb;
-        if (more) dv.issue(lds + (2 + NP) * TB, rv, (uint32_t)((j + 1) * kFwdBN) * vbytes, wave);
-        f32x16* s = sc[P];
-        const int k0 = j * kFwdBN;
-        if constexpr (MASK) {
-#pragma unroll
-            for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-                for (int r = 0; r < 16; ++r) {
-                    const int key = k0 + kt * 32 + acc_row(r, g);
-                    if (key >= kv_end || (a.mask.causal && key > qi)) s[kt][r] = -INFINITY;
-                }
-        }
-#pragma unroll
-        for (int k = 0; k < kLead; ++k) read_k(NP, k);
-        __builtin_amdgcn_sched_barrier(0);
-        // slots 0..3: products of S_{j+1} with the row maximum of tile j
-        float mx = -INFINITY;
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            if (k % NC == 0) sc[NP][k / NC] = f32x16{};
-            mma(sc[NP][k / NC], fk[k], qf[k % NC]);
-            read_k(NP, k + kLead);
-#pragma unroll
-            for (int e = 8 * k; e < 8 * k + 8; ++e) mx = fmaxf(mx, s[e / 16][e % 16]);
-            __builtin_amdgcn_sched_barrier(0);
-        }
-        mx = fmaxf(mx, other_half(mx)) * c;
-        if (__any(mx > m + kRescaleSlack)) {
-            const float m_new = fmaxf(m, mx);
-            const float alpha = (m_new == -INFINITY) ? 1.f : fast_exp2(m - m_new);  // 0 when m was -inf
-            l *= alpha;
-#pragma unroll
-            for (int t = 0; t < ND; ++t) oacc[t] *= alpha;
-            m = m_new;
-        }
-        const float nm = (m == -INFINITY) ? 0.f : -m;
-        __builtin_amdgcn_sched_barrier(0);
-        // slots 4..NQK-1: the remaining products with exp2, row sum and packing
-        constexpr int NSL = NQK - 4;
-        float pv[32];
-        Frag<T> pf[2][2];
-#pragma unroll
-        for (int k = 4; k < NQK; ++k) {
-            if (k % NC == 0) sc[NP][k / NC] = f32x16{};
-            mma(sc[NP][k / NC], fk[k], qf[k % NC]);
-            if (k + kLead < NQK) read_k(NP, k + kLead);
-#pragma unroll
-            for (int e = (k - 4) * 32 / NSL; e < (k - 3) * 32 / NSL; ++e) {
-                const float x = s[e / 16][e % 16];
-                float p = fast_exp2(__builtin_fmaf(x, c, nm));
-                if constexpr (MASK) p = x == -INFINITY ? 0.f : p;
-                asm volatile("" : "+v"(p));
-                pv[e] = p;
-                l += p;
-                if (e % 8 == 7) pack_frag(pf[e / 16][(e % 16) / 8], pv + e - 7);
-            }
-            __builtin_amdgcn_sched_barrier(0);
-        }
-        // O^T += V^T P^T over the 64 keys
-#pragma unroll
-        for (int n = 0; n < kLead; ++n) read_v(P, n);
-        __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-        for (int n = 0; n < NPV; ++n) {
-            const int t = n % ND, cc = (n / ND) % 2, kt = n / (2 * ND);
-            Frag<T> vf;
-            if constexpr (kBf16)
-                vf.v = bf16x8{vv[2 * n][0], vv[2 * n][1], vv[2 * n][2], vv[2 * n][3],
-                              vv[2 * n + 1][0], vv[2 * n + 1][1], vv[2 * n + 1][2], vv[2 * n + 1][3]};
-            mma(oacc[t], vf, pf[kt][cc]);
-            if (n + kLead < NPV) read_v(P, n + kLead);
-            __builtin_amdgcn_sched_barrier(0);
-        }
-        (void)more;
-    };
-
     // iteration j (parity P = j % 2)
-    auto step_generic = [&](auto par_c, auto mask_c, int j) {
+    auto step = [&](auto par_c, auto mask_c, int j) {
         constexpr int P = decltype(par_c)::value;
         constexpr int NP = 1 - P;
         wait_vmcnt<0>();
@@ -329,10 +209,6 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) void attn_fwd_kernel(F
             qk(std::integral_constant<int, NP>{}, NP);
         }
         softmax_pv(par_c, mask_c, j * kFwdBN);
-    };
-    auto step = [&](auto par_c, auto mask_c, int j) __attribute__((always_inline)) {
-        if constexpr (kBf16 && D >= 64) step_bf16(par_c, mask_c, j);  // NQK >= 8: four max slots + exp slots
-        else step_generic(par_c, mask_c, j);
     };
 
     if (nkb > 0) {
@@ -377,40 +253,25 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) void attn_fwd_kernel(F
     }
 }
 
-template __global__ void attn_fwd_kernel<float, 32>(FwdArgs);
-template __global__ void attn_fwd_kernel<float, 64>(FwdArgs);
-template __global__ void attn_fwd_kernel<float, 128>(FwdArgs);
-template __global__ void attn_fwd_kernel<bf16, 32>(FwdArgs);
-template __global__ void attn_fwd_kernel<bf16, 64>(FwdArgs);
-template __global__ void attn_fwd_kernel<bf16, 128>(FwdArgs);
-
-template <typename T, int D>
+template <int D>
 constexpr int fwd_lds_bytes() {
-    return 4 * kFwdBN * D * (int)sizeof(T);
-}
-
-template <typename T, int D>
-hipError_t set_fwd_lds() {
-    return ensure_dynamic_lds<&attn_fwd_kernel<T, D>>(fwd_lds_bytes<T, D>());
+    return 4 * kFwdBN * D * (int)sizeof(float);
 }
 
 }  // namespace
 
-template <typename T, int D>
-hipError_t launch_attn_fwd(const FwdArgs& a, hipStream_t stream) {
-    const hipError_t e = set_fwd_lds<T, D>();
+template <int D>
+hipError_t launch_attn_fwd_f32(const FwdArgs& a, hipStream_t stream) {
+    const hipError_t e = ensure_dynamic_lds<&attn_fwd_f32<D>>(fwd_lds_bytes<D>());
     if (e != hipSuccess) return e;
     const int nqb = (a.S + kFwdBM - 1) / kFwdBM;
-    constexpr int lds = fwd_lds_bytes<T, D>();
-    hipLaunchKernelGGL((attn_fwd_kernel<T, D>), dim3(rank_major_grid(nqb, a.Hq * a.B)), dim3(256), lds, stream, a);
+    hipLaunchKernelGGL((attn_fwd_f32<D>), dim3(rank_major_grid(nqb, a.Hq * a.B)), dim3(256), fwd_lds_bytes<D>(),
+                       stream, a);
     return hipGetLastError();
 }
 
-template hipError_t launch_attn_fwd<float, 32>(const FwdArgs&, hipStream_t);
-template hipError_t launch_attn_fwd<float, 64>(const FwdArgs&, hipStream_t);
-template hipError_t launch_attn_fwd<float, 128>(const FwdArgs&, hipStream_t);
-template hipError_t launch_attn_fwd<bf16, 32>(const FwdArgs&, hipStream_t);
-template hipError_t launch_attn_fwd<bf16, 64>(const FwdArgs&, hipStream_t);
-template hipError_t launch_attn_fwd<bf16, 128>(const FwdArgs&, hipStream_t);
+template hipError_t launch_attn_fwd_f32<32>(const FwdArgs&, hipStream_t);
+template hipError_t launch_attn_fwd_f32<64>(const FwdArgs&, hipStream_t);
+template hipError_t launch_attn_fwd_f32<128>(const FwdArgs&, hipStream_t);
 
 }  // namespace fbl

@@ -6,6 +6,7 @@
 #include <atomic>
 #include <cstdint>
 
+#include "attn_tiles.hpp"
 #include "gemm_tiles.hpp"
 #include "tokmap.hpp"
 
@@ -29,9 +30,13 @@ hipError_t ensure_dynamic_lds(int bytes) {
 
 typedef __bf16 bf16;
 
-// Forward: O and LSE from Q, K, V.  T is float or __bf16; D in {32, 64, 128}.
-template <typename T, int D>
-hipError_t launch_attn_fwd(const FwdArgs& a, hipStream_t stream);
+// Forward for fp32 storage: O and LSE from Q, K, V; D in {32, 64, 128}.
+template <int D>
+hipError_t launch_attn_fwd_f32(const FwdArgs& a, hipStream_t stream);
+
+// Forward for bf16 storage with forward tile `tile` of kAttnTiles.
+template <int D>
+hipError_t launch_attn_fwd_bf16(const FwdArgs& a, int tile, hipStream_t stream);
 
 // Backward: per-row statistics (LSE * log2(e), D = rowsum(dO * O)), then the
 // key/value-major pass (dK, dV) and the query-major pass (dQ).
@@ -39,9 +44,10 @@ hipError_t launch_attn_fwd(const FwdArgs& a, hipStream_t stream);
 template <typename T, int D>
 hipError_t launch_attn_bwd(const BwdArgs& a, unsigned phases, hipStream_t stream);
 
-// Key/value-major backward pass for bf16 storage (software-pipelined kernel).
+// Key/value-major backward pass for bf16 storage (software-pipelined kernel)
+// with kv tile `tile` of kAttnTiles (its split is a.kv_split).
 template <int D>
-hipError_t launch_attn_bwd_kv_bf16(const BwdArgs& a, hipStream_t stream);
+hipError_t launch_attn_bwd_kv_bf16(const BwdArgs& a, int tile, hipStream_t stream);
 
 // Query-major backward pass (dQ) for bf16 storage (software-pipelined kernel),
 // recomputing S and dP.
@@ -49,9 +55,9 @@ template <int D>
 hipError_t launch_attn_bwd_q_bf16(const BwdArgs& a, hipStream_t stream);
 
 // dQ for bf16 storage from the dS blocks the key/value-major pass stored in
-// the workspace (a.ds != nullptr).
+// the workspace (a.ds != nullptr), with dQ tile `tile` of kAttnTiles.
 template <int D>
-hipError_t launch_attn_bwd_dq_bf16(const BwdArgs& a, hipStream_t stream);
+hipError_t launch_attn_bwd_dq_bf16(const BwdArgs& a, int tile, hipStream_t stream);
 
 // Projection matrix products (proj_gemm.hip).  Output tile shapes:
 // `tile` indexes kGemmTiles (gemm_tiles.hpp).

@@ -69,6 +69,9 @@ struct BwdArgs {
     // adds them in split order.  1: no split, dK and dV written directly.
     float* dkv_part = nullptr;
     int kv_split = 1;
+    // tile ids (attn_tiles.hpp) of the bf16 key/value and dQ passes
+    int kv_tile = 5;
+    int dq_tile = 7;
 };
 
 // Matrix product C[M, N] = sum_k A(m, k) B(k, n), bf16 operands, row-major

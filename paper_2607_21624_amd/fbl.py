@@ -47,23 +47,30 @@ FBL_GEMM_TILE_64x64 = 3
 FBL_TUNE_TIME = 0
 FBL_TUNE_GFLOPS_X_MEMEFF = 1
 
+FBL_ATTN_FWD = 0
+FBL_ATTN_BWD_KV = 1
+FBL_ATTN_BWD_DQ = 2
+FBL_ATTN_TILE_AUTO = -1
+
 EXPORTED = ("fbl_layout_desc", "fbl_layout_packed_qkv", "fbl_layout_offset", "fbl_layout_map_device", "fbl_attn_fwd",
             "fbl_attn_bwd_workspace", "fbl_attn_bwd_workspace_min", "fbl_attn_bwd", "fbl_attn_bwd_phases",
-            "fbl_attn_bwd_noalloc", "fbl_proj", "fbl_proj_dt",
+            "fbl_attn_bwd_noalloc", "fbl_attn_fwd_tiled", "fbl_attn_bwd_tiled", "fbl_attn_tile_count",
+            "fbl_attn_tile_info", "fbl_attn_candidates", "fbl_attn_auto_tiles", "fbl_attn_tune", "fbl_attn_tuned_tile",
+            "fbl_attn_tune_reset", "fbl_proj", "fbl_proj_dt",
             "fbl_gemm_tile_count", "fbl_gemm_tile_info", "fbl_proj_candidates", "fbl_proj_tune", "fbl_proj_tuned_tile", "fbl_proj_auto_tile",
             "fbl_proj_tune_reset", "fbl_status_str")
 
 
 class Layout(ctypes.Structure):
     """Mirror of fbl_layout."""
-    _fields_ = [("dtype", ctypes.c_int32), ("tile_s", ctypes.c_int32), ("tile_d", ctypes.c_int32),
-                ("reserved", ctypes.c_int32),
+    _fields_ = [("dtype", ctypes.c_int32), ("reserved0", ctypes.c_int32), ("tile_d", ctypes.c_int32),
+                ("reserved1", ctypes.c_int32),
                 ("B", ctypes.c_int64), ("S", ctypes.c_int64), ("H", ctypes.c_int64), ("D", ctypes.c_int64),
                 ("sb", ctypes.c_int64), ("ss", ctypes.c_int64), ("sh", ctypes.c_int64), ("sd", ctypes.c_int64)]
 
     def __repr__(self):
         return (f"Layout(dtype={self.dtype}, B={self.B}, S={self.S}, H={self.H}, D={self.D}, "
-                f"sb={self.sb}, ss={self.ss}, sh={self.sh}, sd={self.sd}, tile=({self.tile_s}x{self.tile_d}))")
+                f"sb={self.sb}, ss={self.ss}, sh={self.sh}, sd={self.sd}, tile_d={self.tile_d})")
 
 
 class Mask(ctypes.Structure):
@@ -113,6 +120,29 @@ def _load() -> ctypes.CDLL:
     lib.fbl_attn_bwd_phases.restype = ctypes.c_int
     lib.fbl_attn_bwd_noalloc.argtypes = lib.fbl_attn_bwd.argtypes[:19] + [vp]
     lib.fbl_attn_bwd_noalloc.restype = ctypes.c_int
+    lib.fbl_attn_fwd_tiled.argtypes = lib.fbl_attn_fwd.argtypes[:11] + [ctypes.c_int32, vp]
+    lib.fbl_attn_fwd_tiled.restype = ctypes.c_int
+    lib.fbl_attn_bwd_tiled.argtypes = [ctypes.c_uint32] + lib.fbl_attn_bwd.argtypes[:21] + [ctypes.c_int32,
+                                                                                         ctypes.c_int32, vp]
+    lib.fbl_attn_bwd_tiled.restype = ctypes.c_int
+    lib.fbl_attn_tile_count.argtypes = []
+    lib.fbl_attn_tile_count.restype = ctypes.c_int32
+    lib.fbl_attn_tile_info.argtypes = [ctypes.c_int32, ctypes.c_int64, P(ctypes.c_int32)]
+    lib.fbl_attn_tile_info.restype = ctypes.c_int
+    lib.fbl_attn_candidates.argtypes = [ctypes.c_uint32, P(Layout), P(Layout), P(ctypes.c_int32), ctypes.c_int32,
+                                        P(ctypes.c_int32)]
+    lib.fbl_attn_candidates.restype = ctypes.c_int
+    lib.fbl_attn_auto_tiles.argtypes = [P(Layout), P(Layout), ctypes.c_uint32, P(ctypes.c_int32)]
+    lib.fbl_attn_auto_tiles.restype = ctypes.c_int
+    lib.fbl_attn_tune.argtypes = ([P(Layout), vp, P(Layout), vp, P(Layout), vp, P(Layout), vp, vp, P(Layout), vp,
+                                   ctypes.c_float, Mask, P(Layout), vp, P(Layout), vp, P(Layout), vp, vp,
+                                   ctypes.c_size_t, ctypes.c_uint32, ctypes.c_int32, P(ctypes.c_float),
+                                   P(ctypes.c_int32), vp])
+    lib.fbl_attn_tune.restype = ctypes.c_int
+    lib.fbl_attn_tuned_tile.argtypes = [ctypes.c_uint32, P(Layout), P(Layout), ctypes.c_uint32]
+    lib.fbl_attn_tuned_tile.restype = ctypes.c_int32
+    lib.fbl_attn_tune_reset.argtypes = []
+    lib.fbl_attn_tune_reset.restype = None
     lib.fbl_proj.argtypes = [ctypes.c_uint32] + [ctypes.c_int64] * 3 + [vp, ctypes.c_int64, vp, ctypes.c_int64, vp,
                                                                         ctypes.c_int64, ctypes.c_int32, vp]
     lib.fbl_proj.restype = ctypes.c_int
@@ -212,13 +242,15 @@ def _mask(causal: bool, kv_len) -> Mask:
     return Mask(kind, 0, _ptr(kv_len))
 
 
-def fbl_attn_fwd_raw(lq, q, lk, k, lv, v, lo, o, lse, scale, mask: Mask, stream=None) -> int:
-    """Direct call; returns the status code (for boundary tests)."""
-    return LIB.fbl_attn_fwd(ctypes.byref(lq) if lq is not None else None, _ptr(q),
-                            ctypes.byref(lk) if lk is not None else None, _ptr(k),
-                            ctypes.byref(lv) if lv is not None else None, _ptr(v),
-                            ctypes.byref(lo) if lo is not None else None, _ptr(o), _ptr(lse), float(scale),
-                            mask, _stream(stream) if stream != 0 else None)
+def fbl_attn_fwd_raw(lq, q, lk, k, lv, v, lo, o, lse, scale, mask: Mask, stream=None,
+                     tile: int = FBL_ATTN_TILE_AUTO) -> int:
+    """Direct call of fbl_attn_fwd (tile AUTO) or fbl_attn_fwd_tiled; returns the status code."""
+    ref = lambda l: ctypes.byref(l) if l is not None else None
+    args = (ref(lq), _ptr(q), ref(lk), _ptr(k), ref(lv), _ptr(v), ref(lo), _ptr(o), _ptr(lse), float(scale), mask)
+    st = _stream(stream) if stream != 0 else None
+    if tile == FBL_ATTN_TILE_AUTO:
+        return LIB.fbl_attn_fwd(*args, st)
+    return LIB.fbl_attn_fwd_tiled(*args, int(tile), st)
 
 
 def fbl_attn_bwd_workspace(lq: Layout, lk: Layout) -> int:
@@ -235,15 +267,19 @@ def fbl_attn_bwd_workspace_min(lq: Layout, lk: Layout) -> int:
 
 
 def fbl_attn_bwd_raw(lq, q, lk, k, lv, v, lo, o, ldo, do, lse, scale, mask: Mask, ldq, dq, ldk, dk, ldv, dv,
-                     ws, ws_bytes, stream=None, phases: int = FBL_BWD_ALL) -> int:
-    """Direct call of fbl_attn_bwd (phases == FBL_BWD_ALL) or fbl_attn_bwd_phases; returns the status."""
+                     ws, ws_bytes, stream=None, phases: int = FBL_BWD_ALL, kv_tile: int = FBL_ATTN_TILE_AUTO,
+                     dq_tile: int = FBL_ATTN_TILE_AUTO) -> int:
+    """Direct call of fbl_attn_bwd (phases == FBL_BWD_ALL, AUTO tiles), fbl_attn_bwd_phases (AUTO
+    tiles) or fbl_attn_bwd_tiled (an explicit tile); returns the status."""
     ref = lambda l: ctypes.byref(l) if l is not None else None
     args = (ref(lq), _ptr(q), ref(lk), _ptr(k), ref(lv), _ptr(v), ref(lo), _ptr(o), ref(ldo), _ptr(do), _ptr(lse),
-            float(scale), mask, ref(ldq), _ptr(dq), ref(ldk), _ptr(dk), ref(ldv), _ptr(dv), _ptr(ws), int(ws_bytes),
-            _stream(stream) if stream != 0 else None)
+            float(scale), mask, ref(ldq), _ptr(dq), ref(ldk), _ptr(dk), ref(ldv), _ptr(dv), _ptr(ws), int(ws_bytes))
+    st = _stream(stream) if stream != 0 else None
+    if kv_tile != FBL_ATTN_TILE_AUTO or dq_tile != FBL_ATTN_TILE_AUTO:
+        return LIB.fbl_attn_bwd_tiled(phases, *args, int(kv_tile), int(dq_tile), st)
     if phases == FBL_BWD_ALL:
-        return LIB.fbl_attn_bwd(*args)
-    return LIB.fbl_attn_bwd_phases(phases, *args)
+        return LIB.fbl_attn_bwd(*args, st)
+    return LIB.fbl_attn_bwd_phases(phases, *args, st)
 
 
 # ------------------------------------------------------- torch-tensor helpers
@@ -325,7 +361,7 @@ def _check_device(where: str, stream, **tensors) -> None:
 
 
 def attn_fwd(q, k, v, Hq: int, Hkv: int, scale: Optional[float] = None, causal: bool = False, kv_len=None,
-             out=None, lse=None, stream=None):
+             out=None, lse=None, stream=None, tile: int = FBL_ATTN_TILE_AUTO):
     """Forward on token-major tensors.  Returns (O, LSE); O has q's shape and dtype
     (allocated contiguous unless `out` is given), LSE is float32 [B, Hq, S]."""
     import torch
@@ -340,13 +376,14 @@ def attn_fwd(q, k, v, Hq: int, Hkv: int, scale: Optional[float] = None, causal: 
     if lse is None:
         lse = torch.empty((B, Hq, S), dtype=torch.float32, device=q.device)
     lo = _layout(out, Hq)
-    _check(fbl_attn_fwd_raw(lq, q, lk, k, lv, v, lo, out, lse, scale, _mask(causal, kv_len), stream),
+    _check(fbl_attn_fwd_raw(lq, q, lk, k, lv, v, lo, out, lse, scale, _mask(causal, kv_len), stream, tile),
            "fbl_attn_fwd")
     return out, lse
 
 
 def attn_bwd(q, k, v, o, do, lse, Hq: int, Hkv: int, scale: Optional[float] = None, causal: bool = False,
-             kv_len=None, dq=None, dk=None, dv=None, workspace=None, stream=None, phases: int = FBL_BWD_ALL):
+             kv_len=None, dq=None, dk=None, dv=None, workspace=None, stream=None, phases: int = FBL_BWD_ALL,
+             kv_tile: int = FBL_ATTN_TILE_AUTO, dq_tile: int = FBL_ATTN_TILE_AUTO):
     """Backward.  Returns (dQ, dK, dV) with the shapes/dtypes of q, k, v."""
     import torch
     _check_kv_len(kv_len, q.shape[0], "attn_bwd")
@@ -368,8 +405,81 @@ def attn_bwd(q, k, v, o, do, lse, Hq: int, Hkv: int, scale: Optional[float] = No
     ldq, ldk, ldv = _layout(dq, Hq), _layout(dk, Hkv), _layout(dv, Hkv)
     _check(fbl_attn_bwd_raw(lq, q, lk, k, lv, v, lo, o, ldo, do, lse, scale, _mask(causal, kv_len), ldq, dq, ldk,
                             dk, ldv, dv, workspace, workspace.numel() * workspace.element_size(), stream,
-                            phases), "fbl_attn_bwd")
+                            phases, kv_tile, dq_tile), "fbl_attn_bwd")
     return dq, dk, dv
+
+
+# ------------------------------------------------------- attention tiles
+def attn_tiles(D: int):
+    """Every attention tile configuration at head dim D:
+    {id: dict(pass, rows, cols, waves, per_wave, occupancy, lds_bytes, legal)}."""
+    keys = ("pass", "rows", "cols", "waves", "per_wave", "occupancy", "lds_bytes", "legal")
+    out = {}
+    for t in range(LIB.fbl_attn_tile_count()):
+        info = (ctypes.c_int32 * 8)()
+        _check(LIB.fbl_attn_tile_info(t, D, info), "fbl_attn_tile_info")
+        out[t] = dict(zip(keys, list(info)))
+    return out
+
+
+def attn_candidates(pass_: int, lq: Layout, lk: Layout):
+    """Candidate tile ids of one attention pass for these shapes (C1/C2/C3)."""
+    n = ctypes.c_int32()
+    cap = LIB.fbl_attn_tile_count()
+    ids = (ctypes.c_int32 * cap)()
+    _check(LIB.fbl_attn_candidates(pass_, ctypes.byref(lq), ctypes.byref(lk), ids, cap, ctypes.byref(n)),
+           "fbl_attn_candidates")
+    return list(ids[:n.value])
+
+
+def attn_auto_tiles(lq: Layout, lk: Layout, mask_kind: int):
+    """(forward, kv, dQ) tile ids FBL_ATTN_TILE_AUTO resolves to."""
+    t = (ctypes.c_int32 * 3)()
+    _check(LIB.fbl_attn_auto_tiles(ctypes.byref(lq), ctypes.byref(lk), mask_kind, t), "fbl_attn_auto_tiles")
+    return tuple(t)
+
+
+def attn_tune(q, k, v, do, Hq: int, Hkv: int, scale: Optional[float] = None, causal: bool = False, kv_len=None,
+              o=None, lse=None, dq=None, dk=None, dv=None, workspace=None, objective: int = FBL_TUNE_TIME,
+              reps: int = 10, stream=None):
+    """Measured tile selection for this attention shape (fbl_attn_tune).  Returns
+    ((fwd, kv, dq) chosen ids, {id: average ms}, outputs (o, lse, dq, dk, dv)
+    computed with the chosen tiles)."""
+    import torch
+    _check_kv_len(kv_len, q.shape[0], "attn_tune")
+    _check_device("attn_tune", stream, q=q, k=k, v=v, do=do, kv_len=kv_len, o=o, lse=lse, dq=dq, dk=dk, dv=dv,
+                  workspace=workspace)
+    lq, lk, lv, ldo = _layout(q, Hq), _layout(k, Hkv), _layout(v, Hkv), _layout(do, Hq)
+    if scale is None:
+        scale = 1.0 / math.sqrt(lq.D)
+    B, S = q.shape[0], q.shape[1]
+    o = torch.empty(q.shape, dtype=q.dtype, device=q.device) if o is None else o
+    lse = torch.empty((B, Hq, S), dtype=torch.float32, device=q.device) if lse is None else lse
+    dq = torch.empty(q.shape, dtype=q.dtype, device=q.device) if dq is None else dq
+    dk = torch.empty(k.shape, dtype=k.dtype, device=k.device) if dk is None else dk
+    dv = torch.empty(v.shape, dtype=v.dtype, device=v.device) if dv is None else dv
+    if workspace is None:
+        workspace = torch.empty(fbl_attn_bwd_workspace(lq, lk), dtype=torch.uint8, device=q.device)
+    lo, ldq, ldk, ldv = _layout(o, Hq), _layout(dq, Hq), _layout(dk, Hkv), _layout(dv, Hkv)
+    cap = LIB.fbl_attn_tile_count()
+    ms = (ctypes.c_float * cap)()
+    best = (ctypes.c_int32 * 3)()
+    ref = ctypes.byref
+    _check(LIB.fbl_attn_tune(ref(lq), _ptr(q), ref(lk), _ptr(k), ref(lv), _ptr(v), ref(lo), _ptr(o), _ptr(lse),
+                             ref(ldo), _ptr(do), float(scale), _mask(causal, kv_len), ref(ldq), _ptr(dq), ref(ldk),
+                             _ptr(dk), ref(ldv), _ptr(dv), _ptr(workspace),
+                             workspace.numel() * workspace.element_size(), objective, reps, ms, best,
+                             _stream(stream) if stream != 0 else None), "fbl_attn_tune")
+    return tuple(best), {t: ms[t] for t in range(cap) if ms[t] >= 0}, (o, lse, dq, dk, dv)
+
+
+def attn_tuned_tile(pass_: int, lq: Layout, lk: Layout, mask_kind: int) -> int:
+    """The tile fbl_attn_tune chose for this pass and shape in this process, or -1."""
+    return LIB.fbl_attn_tuned_tile(pass_, ctypes.byref(lq), ctypes.byref(lk), mask_kind)
+
+
+def attn_tune_reset() -> None:
+    LIB.fbl_attn_tune_reset()
 
 
 NOALLOC_SCRATCH_BYTES = 64 << 20  # FBL_NOALLOC_SCRATCH_BYTES

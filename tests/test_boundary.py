@@ -44,7 +44,7 @@ def test_status_strings():
 def test_layout_desc_defaults_and_tile():
     l = fbl.fbl_layout_desc(BF16, 4, 1024, 16, 64)
     assert (l.sd, l.sh, l.ss, l.sb) == (1, 64, 1024, 1024 * 1024)
-    assert l.tile_d == 64 and l.tile_s in (32, 64)
+    assert l.tile_d == 64 and l.reserved0 == 0 and l.reserved1 == 0
 
 
 @pytest.mark.parametrize("args,status", [
@@ -556,3 +556,74 @@ def test_noalloc_rejects_too_many_rows():
     st = F.fbl_attn_bwd_noalloc_raw(lq, FAKE, lk, FAKE, lk, FAKE, lq, FAKE, lq, FAKE, FAKE, 0.1, F.Mask(0, 0, None),
                                     lq, FAKE, lk, FAKE, lk, FAKE, stream=0)
     assert st == F.FBL_ERR_WORKSPACE
+
+
+# ------------------------------------------------------ attention tile table
+def _attn_c123(t, D, Sq, Skv):
+    """The three candidate filters restated from their definitions: C1 whole
+    32x32 MFMA blocks per wavefront and staged tile, 16-deep chunks over d,
+    2-8 wavefronts; C2 LDS per CU, whole 1 KB loads spread evenly, registers
+    within a wavefront's share of the file; C3 padding at most 10%."""
+    c1 = t["per_wave"] % 32 == 0 and t["cols"] % 32 == 0 and D % 16 == 0 and 2 <= t["waves"] <= 8
+    pad = lambda n, m: -(-n // m) * m
+    rows_seq, cols_seq = (Skv, Sq) if t["pass"] == F.FBL_ATTN_BWD_KV else (Sq, Skv)
+    c3 = 10 * (pad(rows_seq, t["rows"]) - rows_seq) <= rows_seq and 10 * (pad(cols_seq, t["cols"]) - cols_seq) <= cols_seq
+    return c1 and t["legal"] == 1, c3, pad(rows_seq, t["rows"]) * pad(cols_seq, t["cols"])
+
+
+@pytest.mark.parametrize("D", [32, 64, 128])
+def test_attn_tile_table_and_filters(D):
+    tiles = fbl.attn_tiles(D)
+    assert len(tiles) == F.LIB.fbl_attn_tile_count()
+    for t, i in tiles.items():
+        assert i["rows"] == i["per_wave"] * i["waves"] and i["lds_bytes"] * i["occupancy"] <= 160 * 1024, (t, i)
+    # every pass has a runnable tile at every head dim
+    for p in (F.FBL_ATTN_FWD, F.FBL_ATTN_BWD_KV, F.FBL_ATTN_BWD_DQ):
+        assert any(i["pass"] == p and i["legal"] for i in tiles.values())
+    # kv tiles staging 64-query blocks do not fit the registers at d = 128; 32-query
+    # blocks at d = 32 are half a 1 KB load per wavefront
+    kv = {t: i for t, i in tiles.items() if i["pass"] == F.FBL_ATTN_BWD_KV}
+    for t, i in kv.items():
+        assert i["legal"] == (not (D == 128 and i["cols"] == 64) and not (D == 32 and i["cols"] == 32)), (D, t)
+    for Sq, Skv in ((4096, 4096), (200, 200), (1024, 1024), (448, 300), (128, 128), (64, 64)):
+        lq = fbl.fbl_layout_desc(BF16, 2, Sq, 4, D)
+        lk = fbl.fbl_layout_desc(BF16, 2, Skv, 2, D)
+        for p in (F.FBL_ATTN_FWD, F.FBL_ATTN_BWD_KV, F.FBL_ATTN_BWD_DQ):
+            legal = {t: _attn_c123(i, D, Sq, Skv) for t, i in tiles.items() if i["pass"] == p}
+            legal = {t: v for t, v in legal.items() if v[0]}
+            want = sorted(t for t, v in legal.items() if v[1])
+            if not want:  # C3 fallback: the least padded volume
+                least = min(v[2] for v in legal.values())
+                want = sorted(t for t, v in legal.items() if v[2] == least)
+            assert fbl.attn_candidates(p, lq, lk) == want, (D, Sq, Skv, p)
+        # the automatic choice (nothing tuned in this process) is a candidate of each pass
+        auto = fbl.attn_auto_tiles(lq, lk, 1)
+        for p, t in enumerate(auto):
+            assert t in fbl.attn_candidates(p, lq, lk), (D, Sq, Skv, p, t)
+
+
+def test_attn_tile_rejections():
+    lq, lk, lv, lo, p = _fwd_setup(D=128)
+    assert fbl.fbl_attn_fwd_raw(lq, p["q"], lk, p["k"], lv, p["v"], lo, p["o"], p["lse"], 0.1, F.Mask(0, 0, None),
+                                stream=0, tile=5) == F.FBL_ERR_ARG  # a kv tile for the forward
+    assert fbl.fbl_attn_fwd_raw(lq, p["q"], lk, p["k"], lv, p["v"], lo, p["o"], p["lse"], 0.1, F.Mask(0, 0, None),
+                                stream=0, tile=99) == F.FBL_ERR_ARG
+    lq, lk, lv, lo, p, ws = _bwd_setup(D=128)
+    call = lambda kt, qt, phases=F.FBL_BWD_ALL, lq_=lq, lk_=lk, lv_=lv, lo_=lo: fbl.fbl_attn_bwd_raw(
+        lq_, p["q"], lk_, p["k"], lv_, p["v"], lo_, p["o"], lo_, p["do"], p["lse"], 0.1, F.Mask(0, 0, None), lq_,
+        p["dq"], lk_, p["dk"], lv_, p["dv"], p["ws"], ws, stream=0, phases=phases, kv_tile=kt, dq_tile=qt)
+    assert call(6, -1) == F.FBL_ERR_UNSUPPORTED   # 64-query kv tiles exceed the registers at d = 128
+    assert call(0, -1) == F.FBL_ERR_ARG           # a forward tile as the kv tile
+    assert call(-1, 5) == F.FBL_ERR_ARG           # a kv tile as the dQ tile
+    assert call(5, 7, phases=0) == F.FBL_ERR_ARG
+    # fp32 storage: one configuration per pass, explicit ids refused
+    lq, lk, lv, lo, p, ws = _bwd_setup(D=64, dtype=F32)
+    assert call(5, -1, lq_=lq, lk_=lk, lv_=lv, lo_=lo) == F.FBL_ERR_ARG
+    assert fbl.fbl_attn_fwd_raw(lq, p["q"], lk, p["k"], lv, p["v"], lo, p["o"], p["lse"], 0.1, F.Mask(0, 0, None),
+                                stream=0, tile=0) == F.FBL_ERR_ARG
+    info = (ctypes.c_int32 * 8)()
+    assert F.LIB.fbl_attn_tile_info(0, 48, info) == F.FBL_ERR_UNSUPPORTED
+    assert F.LIB.fbl_attn_tile_info(-1, 64, info) == F.FBL_ERR_ARG
+    assert F.LIB.fbl_attn_tile_info(0, 64, None) == F.FBL_ERR_NULL
+    with pytest.raises(F.FblError):
+        fbl.attn_candidates(F.FBL_ATTN_FWD, fbl.fbl_layout_desc(F32, 1, 64, 2, 64), fbl.fbl_layout_desc(F32, 1, 64, 2, 64))
