@@ -8,6 +8,7 @@
 // except that the tuning calls wait for their own timing events.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdint>
 #include <cstring>
@@ -119,6 +120,9 @@ fbl_status check_qkv(const fbl_layout* lq, const void* q, const fbl_layout* lk, 
     // cross-attention (S_q != S_kv) takes no causal mask: its alignment is not defined here
     if ((mask.kind & FBL_MASK_CAUSAL) && lq->S != lk->S) return FBL_ERR_UNSUPPORTED;
     if (!std::isfinite(scale)) return FBL_ERR_ARG;
+    // launch grids count 32-row blocks of every (batch, head): keep them in range
+    for (const fbl_layout* l : {lq, lk})
+        if (l->B * l->H * ((l->S + 31) / 32) > INT32_MAX) return FBL_ERR_UNSUPPORTED;
     return FBL_OK;
 }
 
@@ -203,12 +207,12 @@ AttnKey attn_key(uint32_t pass, const fbl_layout* lq, const fbl_layout* lk, uint
 // 64-queries-per-wavefront tiles last.
 int32_t attn_default_tile(uint32_t pass, int64_t D, int64_t Sq, int64_t Skv) {
     static const int fwd[] = {0, 2, 3, 4, 1};
-    static const int kv[] = {5, 6};
+    static const int kv[] = {5, 6, 10};
     static const int dq[] = {7, 8, 9};
     const int* order;
     int n;
     if (pass == FBL_ATTN_FWD) order = fwd, n = 5;
-    else if (pass == FBL_ATTN_BWD_KV) order = kv, n = 2;
+    else if (pass == FBL_ATTN_BWD_KV) order = kv, n = 3;
     else order = dq, n = 3;
     const uint64_t cand = attn_candidate_set(pass, D, Sq, Skv);
     for (int i = 0; i < n; ++i)
@@ -264,36 +268,42 @@ size_t ws_ds_bytes(const fbl_layout* lq, const fbl_layout* lk) {
     return (size_t)(heads * per_head);
 }
 
-// Split of the key/value pass (bf16 with stored dS).  Its work items are key
-// blocks of 128 keys per (batch, kv head).  Under a causal mask the first key
-// blocks carry the most queries, and with fewer than two items per CU (512)
-// the pass waits on those few large items while other CUs idle; without a
-// mask the items are equal and only a grid of fewer items than workgroup
-// slots (256 CUs, two workgroups each at D = 64) leaves CUs idle.  Sharing each key block's query iterations among 2 (or 4) workgroups
-// gives the scheduler items of half (a quarter) the size; each writes fp32
-// partial dK and dV and a reduction adds them in a fixed order.  Causal: split
-// while below 512 items; otherwise while the split grid still fits the slots.
-// Only where the first key block has at least 16 iterations per share.
-// (Measured: splitting the 512 items of the GPT-2-medium-like causal shape,
-// or the Llama-3.2-1B-like GQA shape four ways, is slower.)  The causal
-// choice is never below the other, so it sizes the workspace.
-// bq: the kv tile's queries per iteration (0: the smallest a kv tile at this
-// head dim stages, which gives the largest split and so sizes the workspace).
-int kv_split_for(const fbl_layout* lq, const fbl_layout* lk, bool causal = true, int64_t bq = 0) {
+// Split of the key/value pass (bf16 with stored dS).  Its work items are the
+// kv tile's key blocks (`rows` keys) per (batch, kv head).  Under a causal
+// mask the first key blocks carry the most queries, and with few items (less
+// than 512 items of 128 keys: two per CU) the pass waits on those few large
+// items while other CUs idle; without a mask the items are equal and only a
+// grid of fewer items than half the resident workgroup slots (256 CUs times
+// the tile's workgroups per CU) leaves CUs idle.  Sharing each key block's
+// query iterations among 2 (or 4) workgroups gives the scheduler items of
+// half (a quarter) the size; each writes fp32 partial dK and dV and a
+// reduction adds them in a fixed order.  Only where the first key block has
+// at least 16 iterations per share.  (Measured with 128-key blocks: splitting
+// the 512 items of the GPT-2-medium-like causal shape, or the Llama-3.2-1B-like
+// GQA shape four ways, is slower.)
+int kv_split_for(const fbl_layout* lq, const fbl_layout* lk, bool causal, int tile) {
     if (lq->dtype != FBL_BF16 || lk->H <= 0 || lq->D <= 0) return 1;
-    const int64_t items = (lk->S + 127) / 128 * lk->H * lk->B;
-    if (bq == 0) bq = lq->D == 32 ? 64 : 32;
-    const int64_t slots = lq->D == 64 ? 512 : 256;  // workgroups resident at once (two per CU at D = 64)
-    const int64_t iters = lq->H / lk->H * ((lq->S + bq - 1) / bq);
+    const fbl::AttnTile& t = fbl::kAttnTiles[tile];
+    const int64_t rows = fbl::attn_rows(t);
+    const int64_t items = (lk->S + rows - 1) / rows * lk->H * lk->B;
+    const int64_t slots = 256 * (int64_t)fbl::attn_occ(t, (int)lq->D);
+    const int64_t iters = lq->H / lk->H * ((lq->S + t.cols - 1) / t.cols);
     int split = 1;
-    while (split < 4 && (causal ? items * split < 512 : items * split * 2 <= slots) && iters >= 16 * split) split *= 2;
+    while (split < 4 && (causal ? items * split * rows < 512 * 128 : items * split * 2 <= slots) &&
+           iters >= 16 * split)
+        split *= 2;
     return split;
 }
 
 // Workspace, part 3 (with part 2 only): the split key/value pass's fp32
 // partial dK and dV, [2][kv_split][B, S_kv, Hkv, D]; 0 without a split.
+// Sized for the largest split any kv tile that runs at this head dim takes,
+// with or without a causal mask.
 size_t ws_part_bytes(const fbl_layout* lq, const fbl_layout* lk) {
-    const int split = kv_split_for(lq, lk);
+    int split = 1;
+    for (int i = 0; i < fbl::kAttnTileCount; ++i)
+        if (attn_tile_legal(FBL_ATTN_BWD_KV, i, lq->D))
+            split = std::max(split, std::max(kv_split_for(lq, lk, true, i), kv_split_for(lq, lk, false, i)));
     if (split == 1 || ws_ds_bytes(lq, lk) == 0) return 0;
     return align256((size_t)2 * split * lk->B * lk->S * lk->H * lk->D * sizeof(float));
 }
@@ -528,7 +538,7 @@ fbl_status bwd_run(uint32_t phases, const fbl_layout* lq, const void* q, const f
     // and the split key/value pass when it also holds the partial sums
     const size_t part_bytes = ws_part_bytes(lq, lk);
     if (a.ds && part_bytes && ws_bytes >= ws_stats_bytes(lq) + ds_bytes + part_bytes) {
-        a.kv_split = kv_split_for(lq, lk, (mask.kind & FBL_MASK_CAUSAL) != 0, fbl::kAttnTiles[a.kv_tile].cols);
+        a.kv_split = kv_split_for(lq, lk, (mask.kind & FBL_MASK_CAUSAL) != 0, a.kv_tile);
         a.dkv_part = reinterpret_cast<float*>(static_cast<char*>(ws) + ws_stats_bytes(lq) + ds_bytes);
     }
     a.nq32 = (int)((lq->S + 31) / 32);

@@ -45,43 +45,62 @@ constexpr int kQBM = 32 * kWaves;   // queries per q-pass workgroup
 constexpr int kQBN = 64;            // keys per q-pass tile
 
 // ------------------------------------------------------------------ stats
-// Each (b, s, h) row of d elements is read by D*sizeof(T)/16 lanes (one
-// 16-byte chunk each); consecutive rows are consecutive heads of one token,
-// so a wavefront reads a contiguous run of the token-major tensors.
+// A workgroup covers kStatRows consecutive query tokens of one (batch, query
+// head): every row of d elements is read by D*sizeof(T)/16 lanes (one 16-byte
+// chunk each, a whole row per lane group), all of a thread's rows are in
+// flight at once, and the two statistics of the block's rows are written as
+// contiguous runs (the statistics rows are [B, Hq, 2, S]).
+constexpr int kStatRows = 64;
+
 template <typename T, int D>
 __global__ __launch_bounds__(256) void attn_bwd_stats(BwdArgs a) {
     constexpr int EPC = 16 / (int)sizeof(T);
-    constexpr int LPR = D / EPC;
-    constexpr int RPB = 256 / LPR;
-    const int64_t nrows = (int64_t)a.B * a.S * a.Hq;
-    const int64_t row = (int64_t)blockIdx.x * RPB + threadIdx.x / LPR;
+    constexpr int LPR = D / EPC;        // lanes per row
+    constexpr int RPP = 256 / LPR;      // rows per pass of the workgroup
+    constexpr int NP = kStatRows / RPP;  // passes (rows per thread)
+    __shared__ float dsum[kStatRows];
+    const int nsb = (a.S + kStatRows - 1) / kStatRows;
+    const int bhi = (int)(blockIdx.x / nsb);
+    const int h = bhi % a.Hq, b = bhi / a.Hq;
+    const int s0 = (int)(blockIdx.x % nsb) * kStatRows;
     const int part = threadIdx.x % LPR;
-    float acc = 0.f;
-    int b = 0, s = 0, h = 0;
-    if (row < nrows) {
-        h = (int)(row % a.Hq);
-        s = (int)((row / a.Hq) % a.S);
-        b = (int)(row / ((int64_t)a.Hq * a.S));
-        const T* o = static_cast<const T*>(a.o) + a.mo.offset(b, h, s, part * EPC);
-        const T* g = static_cast<const T*>(a.dout) + a.mdo.offset(b, h, s, part * EPC);
-        const uint4 xo = load16(o), xg = load16(g);
-        if constexpr (sizeof(T) == 2) {
-            const bf16x8 vo = __builtin_bit_cast(bf16x8, xo), vg = __builtin_bit_cast(bf16x8, xg);
+    const T* o = static_cast<const T*>(a.o) + a.mo.head_base(b, h) + part * EPC;
+    const T* g = static_cast<const T*>(a.dout) + a.mdo.head_base(b, h) + part * EPC;
+    uint4 xo[NP], xg[NP];
 #pragma unroll
-            for (int e = 0; e < 8; ++e) acc += (float)vo[e] * (float)vg[e];
-        } else {
-            const f32x4 vo = __builtin_bit_cast(f32x4, xo), vg = __builtin_bit_cast(f32x4, xg);
-#pragma unroll
-            for (int e = 0; e < 4; ++e) acc += vo[e] * vg[e];
+    for (int p = 0; p < NP; ++p) {
+        const int s = s0 + p * RPP + (int)threadIdx.x / LPR;
+        xo[p] = xg[p] = uint4{0u, 0u, 0u, 0u};
+        if (s < a.S) {
+            xo[p] = load16(o + (int64_t)s * a.mo.ss);
+            xg[p] = load16(g + (int64_t)s * a.mdo.ss);
         }
     }
 #pragma unroll
-    for (int off = LPR / 2; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
-    if (row < nrows && part == 0) {
-        const int64_t bh = (int64_t)b * a.Hq + h;
-        const float lse = a.lse[bh * a.S + s];
-        a.stats[2 * bh * a.S + s] = lse == -INFINITY ? INFINITY : lse * kLog2e;
-        a.stats[(2 * bh + 1) * a.S + s] = acc;
+    for (int p = 0; p < NP; ++p) {
+        float acc = 0.f;
+        if constexpr (sizeof(T) == 2) {
+            const bf16x8 vo = __builtin_bit_cast(bf16x8, xo[p]), vg = __builtin_bit_cast(bf16x8, xg[p]);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) acc += (float)vo[e] * (float)vg[e];
+        } else {
+            const f32x4 vo = __builtin_bit_cast(f32x4, xo[p]), vg = __builtin_bit_cast(f32x4, xg[p]);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) acc += vo[e] * vg[e];
+        }
+#pragma unroll
+        for (int off = LPR / 2; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
+        if (part == 0) dsum[p * RPP + threadIdx.x / LPR] = acc;
+    }
+    __syncthreads();
+    const int64_t bh = (int64_t)b * a.Hq + h;
+    if (threadIdx.x < kStatRows) {
+        const int s = s0 + (int)threadIdx.x;
+        if (s < a.S) {
+            const float lse = a.lse[bh * a.S + s];
+            a.stats[2 * bh * a.S + s] = lse == -INFINITY ? INFINITY : lse * kLog2e;
+            a.stats[(2 * bh + 1) * a.S + s] = dsum[threadIdx.x];
+        }
     }
 }
 
@@ -559,15 +578,13 @@ int padded8(int n) { return (n + 7) / 8 * 8; }
 
 template <typename T, int D>
 hipError_t launch_attn_bwd(const BwdArgs& a, unsigned phases, hipStream_t stream) {
-    constexpr int LPR = D / (16 / (int)sizeof(T));
-    constexpr int RPB = 256 / LPR;
     if constexpr (sizeof(T) == 4) {
         const hipError_t e = set_bwd_lds_f32<D>();
         if (e != hipSuccess) return e;
     }
     if (phases & 1u) {
-        const int64_t nrows = (int64_t)a.B * a.S * a.Hq;
-        hipLaunchKernelGGL((attn_bwd_stats<T, D>), dim3((unsigned)((nrows + RPB - 1) / RPB)), dim3(256), 0, stream, a);
+        const int64_t nblk = (int64_t)((a.S + kStatRows - 1) / kStatRows) * a.B * a.Hq;
+        hipLaunchKernelGGL((attn_bwd_stats<T, D>), dim3((unsigned)nblk), dim3(256), 0, stream, a);
     }
     if (phases & 2u) {
         if constexpr (sizeof(T) == 2) {

@@ -48,17 +48,18 @@ namespace fbl {
 
 namespace {
 
-constexpr int kPWaves = 4;
-constexpr int kPKeys = 32 * kPWaves;  // keys per workgroup
 constexpr int kLead = 4;              // product slots between an operand read and its use
 
-// BQ_ queries per block (the staged Q/dO tile rows of the tile table).  At
-// D = 64 with 32-query blocks the wavefront's state fits 256 registers, so
-// two workgroups share a CU (two waves per SIMD).
-template <int D, int BQ_>
+// BQ_ queries per block (the staged Q/dO tile rows of the tile table), NW_
+// wavefronts of 32 keys per workgroup.  At D = 64 with 32-query blocks the
+// wavefront's state fits 256 registers, so two wavefronts share a SIMD.
+// OCC workgroups per CU; WPS wavefronts per SIMD.
+template <int D, int BQ_, int NW_>
 struct KvPipe {
     static constexpr int BQ = BQ_;
-    static constexpr int OCC = (D == 64 && BQ == 32) ? 2 : 1;
+    static constexpr int NW = NW_;
+    static constexpr int WPS = (D == 64 && BQ == 32) ? 2 : 1;
+    static constexpr int OCC = WPS * 4 / NW;
     static constexpr int NQT = BQ / 32;
     static constexpr int TB = BQ * D * 2;  // bytes of one bf16 Q or dO tile
     static constexpr int NBUF = 4;
@@ -75,9 +76,11 @@ struct KvPipe {
     static_assert(BYTES <= 160 * 1024, "LDS of one workgroup");
 };
 
-template <int D, int BQ_, bool DS>
-__global__ __launch_bounds__(256, (KvPipe<D, BQ_>::OCC)) void attn_bwd_kv_bf16(BwdArgs a) {
-    using P = KvPipe<D, BQ_>;
+template <int D, int BQ_, int NW_, bool DS>
+__global__ __launch_bounds__(64 * NW_, (KvPipe<D, BQ_, NW_>::WPS)) void attn_bwd_kv_bf16(BwdArgs a) {
+    using P = KvPipe<D, BQ_, NW_>;
+    constexpr int kPWaves = NW_;
+    constexpr int kPKeys = 32 * kPWaves;  // keys per workgroup
     constexpr int NC = D / 16;
     constexpr int ND = D / 32;
     constexpr int BQ = P::BQ;
@@ -503,15 +506,15 @@ __global__ __launch_bounds__(256) void attn_bwd_kv_reduce(BwdArgs a) {
     store4(dst, acc[0], acc[1], acc[2], acc[3]);
 }
 
-template <int D, int BQ, bool DS>
+template <int D, int BQ, int NW, bool DS>
 hipError_t launch_kv(const BwdArgs& a, hipStream_t stream) {
-    using P = KvPipe<D, BQ>;
-    const hipError_t once = ensure_dynamic_lds<&attn_bwd_kv_bf16<D, BQ, DS>>(P::BYTES);
+    using P = KvPipe<D, BQ, NW>;
+    const hipError_t once = ensure_dynamic_lds<&attn_bwd_kv_bf16<D, BQ, NW, DS>>(P::BYTES);
     if (once != hipSuccess) return once;
     constexpr int lds = P::BYTES;
-    const int nkb = (a.Skv + kPKeys - 1) / kPKeys;
-    hipLaunchKernelGGL((attn_bwd_kv_bf16<D, BQ, DS>), dim3(rank_major_grid(nkb * a.kv_split, a.Hkv * a.B)),
-                       dim3(256), lds, stream, a);
+    const int nkb = (a.Skv + 32 * NW - 1) / (32 * NW);
+    hipLaunchKernelGGL((attn_bwd_kv_bf16<D, BQ, NW, DS>), dim3(rank_major_grid(nkb * a.kv_split, a.Hkv * a.B)),
+                       dim3(64 * NW), lds, stream, a);
     if (a.kv_split > 1) {
         const int64_t n = 2 * (int64_t)a.B * a.Skv * a.Hkv * (D / 4);
         hipLaunchKernelGGL((attn_bwd_kv_reduce<D>), dim3((unsigned)((n + 255) / 256)), dim3(256), 0, stream, a);
@@ -526,13 +529,14 @@ hipError_t launch_kv(const BwdArgs& a, hipStream_t stream) {
 template <int D, int TILE>
 hipError_t launch_kv_tile(const BwdArgs& a, hipStream_t stream) {
     constexpr AttnTile t = kAttnTiles[TILE];
-    static_assert(t.pass == kAttnKv && t.per_wave == 32 && t.waves == kPWaves && t.bufs == 4, "a kv-pass tile");
+    static_assert(t.pass == kAttnKv && t.per_wave == 32 && t.bufs == 4, "a kv-pass tile");
     if constexpr (!attn_c1(t, D) || !attn_c2(t, D)) {
         return hipErrorInvalidValue;  // not built at this head dim (the filters exclude it)
     } else {
-        static_assert(KvPipe<D, t.cols>::BYTES == attn_lds_bytes(t, D) && KvPipe<D, t.cols>::OCC == attn_occ(t, D),
+        using P = KvPipe<D, t.cols, t.waves>;
+        static_assert(P::BYTES == attn_lds_bytes(t, D) && P::OCC == attn_occ(t, D),
                       "the kernel's LDS layout and occupancy are the tile table's");
-        return a.ds ? launch_kv<D, t.cols, true>(a, stream) : launch_kv<D, t.cols, false>(a, stream);
+        return a.ds ? launch_kv<D, t.cols, t.waves, true>(a, stream) : launch_kv<D, t.cols, t.waves, false>(a, stream);
     }
 }
 
@@ -541,6 +545,7 @@ hipError_t launch_attn_bwd_kv_bf16(const BwdArgs& a, int tile, hipStream_t strea
     switch (tile) {
         case 5: return launch_kv_tile<D, 5>(a, stream);
         case 6: return launch_kv_tile<D, 6>(a, stream);
+        case 10: return launch_kv_tile<D, 10>(a, stream);
         default: return hipErrorInvalidValue;
     }
 }

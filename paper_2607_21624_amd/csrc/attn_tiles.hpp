@@ -44,6 +44,8 @@ constexpr AttnTile kAttnTiles[] = {
     {kAttnDq, 32, 32, 4, 0, 4},  // 7
     {kAttnDq, 32, 32, 8, 0, 4},  // 8
     {kAttnDq, 32, 32, 4, 0, 3},  // 9
+    // kv pass, 64 keys per workgroup: two independent workgroups per CU
+    {kAttnKv, 32, 32, 2, 0, 4},  // 10
 };
 constexpr int kAttnTileCount = (int)(sizeof(kAttnTiles) / sizeof(kAttnTiles[0]));
 
@@ -66,7 +68,8 @@ constexpr int kLdsPerCu = 160 * 1024;
 // Workgroups per CU the kernel is built for.
 constexpr int attn_occ(const AttnTile& t, int D) {
     if (t.occ) return t.occ;
-    if (t.pass == kAttnKv) return (D == 64 && t.cols == 32) ? 2 : 1;  // the D = 64 state fits 256 registers
+    if (t.pass == kAttnKv)  // one wavefront per SIMD (two at D = 64 with 32-query tiles: the state fits 256 registers)
+        return ((D == 64 && t.cols == 32) ? 2 : 1) * 4 / t.waves;
     return (2 * attn_lds_bytes(t, D) <= kLdsPerCu && t.waves == 4) ? 2 : 1;
 }
 
