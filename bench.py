@@ -61,36 +61,51 @@ def ds_blocks(w, kv_len) -> int:
 
 
 def algorithmic_bytes(w, es: int, kv_len=None) -> dict:
-    """Minimum HBM traffic per kernel launch (each tensor read or written once;
-    the dS blocks written once by the kv pass and read once by the dQ pass)."""
+    """Minimum HBM traffic per kernel launch, as the measured metric defines it:
+    each tensor of the step read or written once -- the forward reads Q, K, V
+    and writes O, LSE; the backward reads Q, K, V, O, dO, LSE and writes dQ,
+    dK, dV -- split over the backward's launches by which one touches each
+    tensor.  Intermediates of this design (the row statistics, the dS blocks
+    the kv pass writes and the dQ pass reads) are not algorithmic; they are
+    reported separately by design_bytes."""
     nq = w.B * w.S * w.Hq * w.d * es
     nk = w.B * w.Skv * w.Hkv * w.d * es
     lse = w.B * w.Hq * w.S * 4
-    stats = 2 * lse
-    ds = ds_blocks(w, kv_len) * 2048 if es == 2 else 0
     return {"attn_fwd": 2 * nq + 2 * nk + lse,              # read Q K V, write O LSE
-            "attn_bwd_stats": 2 * nq + lse + stats,         # read O dO LSE, write stats
-            "attn_bwd_kv": 2 * nq + 2 * nk + stats + 2 * nk + ds,  # read Q dO K V stats, write dK dV dS
-            "attn_bwd_dq": ds + nk + nq,                    # read dS K, write dQ
-            # the step as a whole: fwd reads Q K V, writes O LSE; bwd reads Q K V O dO LSE, writes dQ dK dV
+            "attn_bwd_stats": 2 * nq + lse,                 # read O dO LSE
+            "attn_bwd_kv": 2 * nq + 2 * nk + 2 * nk,        # read Q dO K V, write dK dV
+            "attn_bwd_dq": nk + nq,                         # read K, write dQ
             "total": (2 * nq + 2 * nk + lse) + (3 * nq + 2 * nk + lse + nq + 2 * nk)}
 
 
-KERNEL_SOURCES = ("attn_fwd.hip", "attn_bwd.hip", "attn_bwd_kv.hip", "attn_bwd_q.hip", "attn_bwd_dq.hip", "stage.hpp",
-                  "cdna4.hpp", "tokmap.hpp")
+def design_bytes(w, es: int, kv_len=None) -> dict:
+    """HBM bytes of this design's intermediates per launch: the statistics rows
+    (8 bytes per query row, written by the statistics pass and read by the kv
+    pass) and the bf16 dS blocks (written by the kv pass, read by the dQ pass)."""
+    stats = 2 * w.B * w.Hq * w.S * 4
+    ds = ds_blocks(w, kv_len) * 2048 if es == 2 else 0
+    return {"attn_bwd_stats": stats, "attn_bwd_kv": stats + ds, "attn_bwd_dq": ds}
+
+
+KERNEL_SOURCES = ("attn_fwd.hip", "attn_fwd_bf16.hip", "attn_bwd.hip", "attn_bwd_kv.hip", "attn_bwd_q.hip",
+                  "attn_bwd_dq.hip", "attn_tiles.hpp", "stage.hpp", "cdna4.hpp", "tokmap.hpp")
+
+
+def sources_sha() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, "paper_2607_21624_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
 
 
 def measured_traffic(workload: str):
     """HBM bytes per launch from the committed rocprofv3 FETCH_SIZE/WRITE_SIZE summary,
     only if it was taken on the kernel sources as they are now (else None)."""
-    import hashlib
     path = os.path.join(ROOT, "profiles", f"attn_{workload}_hbm_traffic.txt")
     if not os.path.exists(path):
         return None
-    h = hashlib.sha256()
-    for f in KERNEL_SOURCES:
-        with open(os.path.join(ROOT, "paper_2607_21624_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
     out, sha = {}, None
     for line in open(path):
         line = line.strip()
@@ -100,7 +115,25 @@ def measured_traffic(workload: str):
             name, *kv = line.split()
             d = dict(x.split("=") for x in kv)
             out[name] = int(d["fetch_bytes"]) + int(d["write_bytes"])
-    return out if sha == h.hexdigest()[:16] else None
+    return out if sha == sources_sha() else None
+
+
+def traced_launch_us(workload: str):
+    """Average launch duration (us) per kernel over the timed steps of the
+    committed rocprofv3 kernel trace of this workload, only if it was taken on
+    the kernel sources as they are now (else None)."""
+    path = os.path.join(ROOT, "profiles", f"attn_{workload}_kernel_trace.txt")
+    if not os.path.exists(path):
+        return None
+    out, sha = {}, None
+    for line in open(path):
+        line = line.strip()
+        if line.startswith("# kernel sources sha256[:16] = "):
+            sha = line.split("= ")[1].split()[0]
+        elif line.startswith("timed "):
+            _, name, us = line.split()[:3]
+            out[name] = float(us)
+    return out if sha == sources_sha() else None
 
 
 def cpu_baseline(w, inp, budget_s: float):
@@ -472,18 +505,27 @@ def main():
     t_dom, a_dom = per_kernel[dom]
     es = 2 if w.dtype == "bf16" else 4
     alg_bytes = algorithmic_bytes(w, es, inp["kv_len"])
+    des_bytes = design_bytes(w, es, inp["kv_len"])
     traffic = measured_traffic(w.name)
-    dom_traffic = None
-    if traffic is not None:
-        key = "attn_fwd_kernel" if dom == "attn_fwd" else dom
-        dom_traffic = traffic.get(key)
+    trace = traced_launch_us(w.name)
+    dom_traffic = None if traffic is None else traffic.get(dom)
+    dom_trace_us = None if trace is None else trace.get(dom)
+    flops_launch = a_dom * w.d * pairs
     roofline = {"bound": "mfma", "achieved": round(ktf[dom], 2), "peak": peak, "unit": "TFLOP/s",
                 "frac": round(ktf[dom] / peak, 4), "traffic": dom_traffic, "kernel": dom,
-                "avg_launch_ms": round(t_dom, 4), "flops_per_launch": a_dom * w.d * pairs,
+                # achieved = flops_per_launch / avg_launch_ms, the launch timed with HIP events on the
+                # stream it runs on, averaged over this run's timed steps
+                "frac_source": "HIP events around each launch over the timed steps of this run",
+                "avg_launch_ms": round(t_dom, 4), "flops_per_launch": flops_launch,
+                # the same figure from the committed rocprofv3 kernel trace (timed steps), when it was
+                # taken on the current sources
+                "trace_avg_launch_ms": None if dom_trace_us is None else round(dom_trace_us / 1e3, 4),
+                "trace_frac": None if dom_trace_us is None else round(flops_launch / (dom_trace_us * 1e-6) / 1e12 / peak, 4),
                 "algorithmic_bytes_per_launch": alg_bytes[dom],
-                # the paper's MemEfficiency (section 4.2): minimal over measured bytes
+                "design_bytes_per_launch": des_bytes.get(dom, 0),
+                # the paper's MemEfficiency (section 4.2): algorithmic over counted HBM bytes
+                # (FETCH_SIZE + WRITE_SIZE, calibrated), when the counters match the sources
                 "mem_efficiency": None if dom_traffic is None else round(alg_bytes[dom] / dom_traffic, 3),
-                # counted HBM bytes (FETCH_SIZE + WRITE_SIZE) over the launch time
                 "hbm_gbs_measured": None if dom_traffic is None else round(dom_traffic / (t_dom * 1e-3) / 1e9, 1)}
     stat = lambda x: {"median": round(float(np.median(x)), 4), "min": round(float(np.min(x)), 4),
                       "max": round(float(np.max(x)), 4)}

@@ -34,7 +34,14 @@ def test_llama7b_work_counts():
     assert bench.ds_blocks(w, None) == 32 * nb * (nb + 1) // 2          # 8256 blocks per head
     ab = bench.algorithmic_bytes(w, 2)
     assert ab["total"] == 403_701_760
-    assert ab["attn_bwd_dq"] == 32 * 8256 * 2048 + 2 * 4096 * 32 * 128 * 2
+    nq = 4096 * 32 * 128 * 2   # bytes of Q (and of K, V, O, dO, dQ, dK, dV) at this shape
+    # per launch, each tensor it must touch once: the kv pass reads Q, dO, K, V and writes dK, dV;
+    # the dQ pass reads K and writes dQ; the statistics pass reads O, dO and LSE
+    lse = 32 * 4096 * 4
+    assert ab["attn_bwd_kv"] == 6 * nq and ab["attn_bwd_dq"] == 2 * nq and ab["attn_bwd_stats"] == 2 * nq + lse
+    assert ab["attn_fwd"] == 4 * nq + lse and ab["total"] == ab["attn_fwd"] + 8 * nq + lse
+    db = bench.design_bytes(w, 2)
+    assert db["attn_bwd_dq"] == 32 * 8256 * 2048 and db["attn_bwd_kv"] == db["attn_bwd_dq"] + 2 * 32 * 4096 * 4
 
 
 @pytest.mark.parametrize("name", ["bert_base_keypad", "gpt2_medium_causal", "tiny_mha_f32",
