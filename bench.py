@@ -75,6 +75,8 @@ def algorithmic_bytes(w, es: int, kv_len=None) -> dict:
             "attn_bwd_stats": 2 * nq + lse,                 # read O dO LSE
             "attn_bwd_kv": 2 * nq + 2 * nk + 2 * nk,        # read Q dO K V, write dK dV
             "attn_bwd_dq": nk + nq,                         # read K, write dQ
+            "attn_bwd_q": nk + nq,                          # (fp32: the recomputing dQ pass, same split)
+            "attn_bwd_fused": 4 * nq + 4 * nk + lse,        # one launch: read Q O dO LSE K V, write dQ dK dV
             "total": (2 * nq + 2 * nk + lse) + (3 * nq + 2 * nk + lse + nq + 2 * nk)}
 
 
@@ -422,6 +424,15 @@ def main():
     lq_, lk_ = fbl.layout_of(q, w.Hq), fbl.layout_of(k, w.Hkv)
     auto = fbl.attn_auto_tiles(lq_, lk_, int(w.mask)) if w.dtype == "bf16" else None
     run_tiles = None if auto is None else [a if t == fbl.FBL_ATTN_TILE_AUTO else t for t, a in zip(tiles, auto)]
+    qname = "attn_bwd_dq" if w.dtype == "bf16" else "attn_bwd_q"
+    # the backward as the library runs it: one launch up to 128 keys with automatic
+    # tiles, else its three phases, each bracketed by events of its own
+    fused = fbl.attn_bwd_launches(lq_, lk_, int(w.mask), ws.numel(), kv_tile=tiles[1], dq_tile=tiles[2]) == 1
+    if fused:
+        bwd_phases = [("attn_bwd_fused", fbl.FBL_BWD_ALL)]
+    else:
+        bwd_phases = [("attn_bwd_stats", fbl.FBL_BWD_PREP), ("attn_bwd_kv", fbl.FBL_BWD_KV), (qname, fbl.FBL_BWD_Q)]
+    n_ev = 2 + len(bwd_phases)
 
     def bwd(phases):
         fbl.attn_bwd(q, k, v, o, do, lse, w.Hq, w.Hkv, scale, causal, kv_len, dq=dq, dk=dk, dv=dv, workspace=ws,
@@ -433,22 +444,17 @@ def main():
         fbl.attn_fwd(q, k, v, w.Hq, w.Hkv, scale, causal, kv_len, out=o, lse=lse, tile=tiles[0])
         if ev is not None:
             ev[1].record(stream)
-        bwd(fbl.FBL_BWD_PREP)
-        if ev is not None:
-            ev[2].record(stream)
-        bwd(fbl.FBL_BWD_KV)
-        if ev is not None:
-            ev[3].record(stream)
-        bwd(fbl.FBL_BWD_Q)
-        if ev is not None:
-            ev[4].record(stream)
+        for i, (_, ph) in enumerate(bwd_phases):
+            bwd(ph)
+            if ev is not None:
+                ev[2 + i].record(stream)
 
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
     mem_before = torch.cuda.memory_allocated()
 
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(n_ev)] for _ in range(args.steps)]
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     start.record(stream)
@@ -459,16 +465,16 @@ def main():
     total_ms = start.elapsed_time(stop)
     ms_per_step = total_ms / args.steps
     eager_ms_per_step = ms_per_step
-    k_fwd = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
-    k_stats = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
-    k_kv = float(np.mean([e[2].elapsed_time(e[3]) for e in evs]))
-    k_q = float(np.mean([e[3].elapsed_time(e[4]) for e in evs]))
-    step_each = np.array([e[0].elapsed_time(e[4]) for e in evs])   # each step, first to last launch
+    # average duration of each launch over the timed steps
+    k_ms = {"attn_fwd": float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))}
+    for i, (n, _) in enumerate(bwd_phases):
+        k_ms[n] = float(np.mean([e[1 + i].elapsed_time(e[2 + i]) for e in evs]))
+    step_each = np.array([e[0].elapsed_time(e[-1]) for e in evs])   # each step, first to last launch
     fwd_each = np.array([e[0].elapsed_time(e[1]) for e in evs])
     bwd_each = step_each - fwd_each
     assert torch.cuda.memory_allocated() == mem_before, "the timed steps allocated device memory"
     if args.graph:
-        # the step's four launches captured once and replayed: no host work per step
+        # the step's launches captured once and replayed: no host work per step
         # (capture and its memory pool come after the eager timing and its no-allocation check)
         side = torch.cuda.Stream()
         with torch.cuda.stream(side):
@@ -492,14 +498,15 @@ def main():
     tflops = flops / (ms_per_step * 1e-3) / 1e12
     peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
     # Algorithmic FLOPs per launch (2*d per allowed pair per matrix product):
-    #   attn_fwd     QK^T, PV                                    4*d
-    #   attn_bwd_kv  QK^T recompute, dO V^T, P^T dO, dS^T Q      8*d
-    #   attn_bwd_dq  dS K from the dS the kv pass stored         2*d
+    #   attn_fwd        QK^T, PV                                    4*d
+    #   attn_bwd_kv     QK^T recompute, dO V^T, P^T dO, dS^T Q      8*d
+    #   attn_bwd_dq     dS K from the dS the kv pass stored         2*d
+    #   attn_bwd_fused  the kv products and dS K in one launch     10*d
     #   (fp32 storage has no stored-dS path: attn_bwd_q recomputes QK^T and dO V^T, 6*d executed)
-    qname = "attn_bwd_dq" if w.dtype == "bf16" else "attn_bwd_q"
-    per_kernel = {"attn_fwd": (k_fwd, 4), "attn_bwd_kv": (k_kv, 8), qname: (k_q, 2)}
+    alg = {"attn_fwd": 4, "attn_bwd_kv": 8, "attn_bwd_dq": 2, "attn_bwd_q": 2, "attn_bwd_fused": 10}
+    executed = {**alg, "attn_bwd_q": 6}
+    per_kernel = {n: (t, alg[n]) for n, t in k_ms.items() if n in alg}
     ktf = {n: a * w.d * pairs / (t * 1e-3) / 1e12 for n, (t, a) in per_kernel.items()}
-    executed = {"attn_fwd": 4, "attn_bwd_kv": 8, qname: 2 if qname == "attn_bwd_dq" else 6}
     ktf_exec = {n: executed[n] * w.d * pairs / (per_kernel[n][0] * 1e-3) / 1e12 for n in per_kernel}
     dom = max(per_kernel, key=lambda n: per_kernel[n][0])
     t_dom, a_dom = per_kernel[dom]
@@ -563,11 +570,12 @@ def main():
         "ms": {"step": stat(step_each), "fwd": stat(fwd_each), "bwd": stat(bwd_each)},
         "layout_copy_bytes": 0 if foreign == [] else None,
         "dispatched_kernels": kernels,
-        "kernel_ms": {"attn_fwd": round(k_fwd, 4), "attn_bwd_stats": round(k_stats, 4), "attn_bwd_kv": round(k_kv, 4),
-                      qname: round(k_q, 4)},
+        "bwd_launches": len(bwd_phases),
+        "kernel_ms": {n: round(t, 4) for n, t in k_ms.items()},
         # the HBM-bound launches: algorithmic bytes over their time
-        "kernel_gbs_algorithmic": {"attn_bwd_stats": round(alg_bytes["attn_bwd_stats"] / (k_stats * 1e-3) / 1e9, 1),
-                                   qname: round(alg_bytes["attn_bwd_dq"] / (k_q * 1e-3) / 1e9, 1)},
+        "kernel_gbs_algorithmic": None if fused else {
+            "attn_bwd_stats": round(alg_bytes["attn_bwd_stats"] / (k_ms["attn_bwd_stats"] * 1e-3) / 1e9, 1),
+            qname: round(alg_bytes["attn_bwd_dq"] / (k_ms[qname] * 1e-3) / 1e9, 1)},
         "kernel_tflops_algorithmic": {n: round(v, 2) for n, v in ktf.items()},
         "kernel_tflops_executed": {n: round(v, 2) for n, v in ktf_exec.items()},
         "algorithmic_gflop": round(flops / 1e9, 3),

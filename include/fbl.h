@@ -244,6 +244,12 @@ fbl_status fbl_attn_bwd_workspace_min(const fbl_layout* lq, const fbl_layout* lk
  * the workspace, and the workspace does not overlap an input or lse (it is
  * written while they are read).  bf16 storage runs the kv and dQ tiles
  * FBL_ATTN_TILE_AUTO resolves to.
+ * Up to 128 keys (S_kv <= 128; fp32 storage only at D <= 64) the backward is
+ * one launch: a workgroup holds all keys of one (batch, key/value head) in
+ * LDS and, per block of queries of its group, forms D_i, the dK and dV
+ * contributions and the block's dS, and contracts that dS with K into dQ --
+ * no workspace is read or written.  Its results agree with the three-launch
+ * path of fbl_attn_bwd_phases up to rounding order, not bit for bit.
  */
 fbl_status fbl_attn_bwd(const fbl_layout* lq, const void* q, const fbl_layout* lk, const void* k,
                         const fbl_layout* lv, const void* v, const fbl_layout* lo, const void* o,
@@ -255,7 +261,11 @@ fbl_status fbl_attn_bwd(const fbl_layout* lq, const void* q, const fbl_layout* l
  * The three launches of fbl_attn_bwd, selectable one by one (same arguments
  * and checks as fbl_attn_bwd; `phases` is an OR of the bits below, enqueued
  * in the order listed).  fbl_attn_bwd(...) equals
- * fbl_attn_bwd_phases(FBL_BWD_ALL, ...).  FBL_BWD_KV and FBL_BWD_Q read what
+ * fbl_attn_bwd_phases(FBL_BWD_ALL, ...), which takes the one-launch backward
+ * where fbl_attn_bwd does; the three phases called separately (or
+ * fbl_attn_bwd_tiled with an explicit tile) always run the three launches
+ * below, and give the same bits on any streams they are ordered on.
+ * FBL_BWD_KV and FBL_BWD_Q read what
  * FBL_BWD_PREP left in the workspace, so the same workspace must be passed to
  * all phases.  With the full workspace (fbl_attn_bwd_workspace bytes, bf16)
  * FBL_BWD_Q reads the dS that FBL_BWD_KV stored, so KV must run before Q;
@@ -275,6 +285,19 @@ fbl_status fbl_attn_bwd_phases(uint32_t phases, const fbl_layout* lq, const void
                                const void* o, const fbl_layout* ldo, const void* dO, const float* lse, float scale,
                                fbl_mask mask, const fbl_layout* ldq, void* dq, const fbl_layout* ldk, void* dk,
                                const fbl_layout* ldv, void* dv, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * The number of kernel launches fbl_attn_bwd_tiled(phases, ...) enqueues for
+ * query/key descriptors lq and lk, mask bits mask_kind (FBL_MASK_*), a
+ * workspace of ws_bytes and the requested tiles: 1 for the one-launch
+ * backward (fbl_attn_bwd: FBL_BWD_ALL, automatic tiles, S_kv <= 128); else
+ * one per phase bit, plus one with FBL_BWD_KV when the key/value pass is
+ * split (its partial sums are then added by a reduction launch).  Checks the
+ * descriptors as fbl_attn_bwd does (FBL_ERR_* as there) and the tiles as
+ * fbl_attn_bwd_tiled.  Host only; reads no data pointer.
+ */
+fbl_status fbl_attn_bwd_launches(uint32_t phases, const fbl_layout* lq, const fbl_layout* lk, uint32_t mask_kind,
+                                 size_t ws_bytes, int32_t kv_tile, int32_t dq_tile, int32_t* launches);
 
 /*
  * Tile configurations of the attention kernels (bf16 storage).  Each pass

@@ -13,6 +13,6 @@ from .fbl import (  # noqa: F401
     FBL_TUNE_TIME, FBL_TUNE_GFLOPS_X_MEMEFF, gemm_tiles, proj_candidates, proj_tune, proj_tuned_tile, proj_auto_tile, proj_tune_reset,
     fbl_layout_desc_status, fbl_layout_map_device, fbl_layout_offset, layout_of, status_str,
     NOALLOC_SCRATCH_BYTES, attn_bwd_noalloc, fbl_attn_bwd_noalloc_raw,
-    FBL_ATTN_FWD, FBL_ATTN_BWD_KV, FBL_ATTN_BWD_DQ, FBL_ATTN_TILE_AUTO, attn_tiles, attn_candidates, attn_auto_tiles,
+    FBL_ATTN_FWD, FBL_ATTN_BWD_KV, FBL_ATTN_BWD_DQ, FBL_ATTN_TILE_AUTO, attn_tiles, attn_candidates, attn_auto_tiles, attn_bwd_launches,
     attn_tune, attn_tuned_tile, attn_tune_reset,
 )

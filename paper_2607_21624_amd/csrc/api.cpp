@@ -141,6 +141,24 @@ hipError_t dispatch_fwd(int32_t dtype, int D, int tile, const fbl::FwdArgs& a, h
     }
 }
 
+hipError_t dispatch_bwd_fused(int32_t dtype, int D, const fbl::BwdArgs& a, hipStream_t s) {
+    if (dtype == FBL_F32) return D == 32 ? fbl::launch_attn_bwd_fused<float, 32>(a, s)
+                                         : fbl::launch_attn_bwd_fused<float, 64>(a, s);
+    switch (D) {
+        case 32: return fbl::launch_attn_bwd_fused<bf16, 32>(a, s);
+        case 64: return fbl::launch_attn_bwd_fused<bf16, 64>(a, s);
+        default: return fbl::launch_attn_bwd_fused<bf16, 128>(a, s);
+    }
+}
+
+// Key/value sequences up to this length fit one kv workgroup (four
+// wavefronts of 32 keys), and the backward runs as one fused pass (fp32
+// storage up to d = 64: at d = 128 its fused state exceeds the registers).
+constexpr int64_t kFusedBwdMaxKeys = 128;
+bool bwd_fuses(const fbl_layout* lq, const fbl_layout* lk) {
+    return lk->S <= kFusedBwdMaxKeys && (lq->dtype == FBL_BF16 || lq->D <= 64);
+}
+
 template <typename T>
 hipError_t dispatch_bwd(int D, const fbl::BwdArgs& a, unsigned phases, hipStream_t s) {
     switch (D) {
@@ -470,6 +488,38 @@ fbl_status fbl_attn_bwd_workspace_min(const fbl_layout* lq, const fbl_layout* lk
 
 namespace {
 
+// What a backward call runs, from the shapes, the mask, the workspace size
+// and the requested tiles alone (no pointer is read).
+struct BwdPlan {
+    bool fused = false;      // the one-launch backward
+    bool stores_ds = false;  // the kv pass stores dS, the dQ pass reads it
+    int kv_split = 1;        // key/value pass split (partial sums + reduction)
+    int32_t kv_tile = 5, dq_tile = 7;
+};
+
+fbl_status bwd_plan(uint32_t phases, const fbl_layout* lq, const fbl_layout* lk, uint32_t mask_kind,
+                    size_t ws_bytes, int32_t kv_tile, int32_t dq_tile, BwdPlan* p) {
+    fbl_status st;
+    // tiles of the bf16 passes (fp32 storage has one configuration per pass)
+    if (lq->dtype == FBL_BF16) {
+        if ((st = attn_resolve(FBL_ATTN_BWD_KV, lq, lk, mask_kind, kv_tile, &p->kv_tile)) != FBL_OK) return st;
+        if ((st = attn_resolve(FBL_ATTN_BWD_DQ, lq, lk, mask_kind, dq_tile, &p->dq_tile)) != FBL_OK) return st;
+    } else if (kv_tile != FBL_ATTN_TILE_AUTO || dq_tile != FBL_ATTN_TILE_AUTO) {
+        return FBL_ERR_ARG;
+    }
+    // the whole backward with automatic tiles, keys within one kv workgroup: one fused launch
+    p->fused = phases == FBL_BWD_ALL && bwd_fuses(lq, lk) && kv_tile == FBL_ATTN_TILE_AUTO &&
+               dq_tile == FBL_ATTN_TILE_AUTO;
+    // stored-dS path when the workspace holds the dS blocks, else recompute
+    const size_t ds_bytes = ws_ds_bytes(lq, lk);
+    p->stores_ds = ds_bytes && ws_bytes >= ws_stats_bytes(lq) + ds_bytes;
+    // and the split key/value pass when it also holds the partial sums
+    const size_t part_bytes = ws_part_bytes(lq, lk);
+    if (p->stores_ds && part_bytes && ws_bytes >= ws_stats_bytes(lq) + ds_bytes + part_bytes)
+        p->kv_split = kv_split_for(lq, lk, (mask_kind & FBL_MASK_CAUSAL) != 0, p->kv_tile);
+    return FBL_OK;
+}
+
 fbl_status bwd_run(uint32_t phases, const fbl_layout* lq, const void* q, const fbl_layout* lk, const void* k,
                    const fbl_layout* lv, const void* v, const fbl_layout* lo, const void* o, const fbl_layout* ldo,
                    const void* dO, const float* lse, float scale, fbl_mask mask, const fbl_layout* ldq, void* dq,
@@ -513,6 +563,8 @@ fbl_status bwd_run(uint32_t phases, const fbl_layout* lq, const void* q, const f
             if (views_overlap(outs[i], out_l[i], outs[j], out_l[j])) return FBL_ERR_ARG;
     }
 
+    BwdPlan plan;
+    if ((st = bwd_plan(phases, lq, lk, mask.kind, ws_bytes, kv_tile, dq_tile, &plan)) != FBL_OK) return st;
     fbl::BwdArgs a;
     a.q = q;
     a.k = k;
@@ -524,23 +576,12 @@ fbl_status bwd_run(uint32_t phases, const fbl_layout* lq, const void* q, const f
     a.dk = dk;
     a.dv = dv;
     a.stats = static_cast<float*>(ws);
-    // stored-dS path when the workspace holds the dS blocks, else recompute
-    const size_t ds_bytes = ws_ds_bytes(lq, lk);
-    a.ds = ds_bytes && ws_bytes >= ws_stats_bytes(lq) + ds_bytes ? static_cast<char*>(ws) + ws_stats_bytes(lq)
-                                                                 : nullptr;
-    // tiles of the bf16 passes (fp32 storage has one configuration per pass)
-    if (lq->dtype == FBL_BF16) {
-        if ((st = attn_resolve(FBL_ATTN_BWD_KV, lq, lk, mask.kind, kv_tile, &a.kv_tile)) != FBL_OK) return st;
-        if ((st = attn_resolve(FBL_ATTN_BWD_DQ, lq, lk, mask.kind, dq_tile, &a.dq_tile)) != FBL_OK) return st;
-    } else if (kv_tile != FBL_ATTN_TILE_AUTO || dq_tile != FBL_ATTN_TILE_AUTO) {
-        return FBL_ERR_ARG;
-    }
-    // and the split key/value pass when it also holds the partial sums
-    const size_t part_bytes = ws_part_bytes(lq, lk);
-    if (a.ds && part_bytes && ws_bytes >= ws_stats_bytes(lq) + ds_bytes + part_bytes) {
-        a.kv_split = kv_split_for(lq, lk, (mask.kind & FBL_MASK_CAUSAL) != 0, a.kv_tile);
-        a.dkv_part = reinterpret_cast<float*>(static_cast<char*>(ws) + ws_stats_bytes(lq) + ds_bytes);
-    }
+    a.ds = plan.stores_ds ? static_cast<char*>(ws) + ws_stats_bytes(lq) : nullptr;
+    a.kv_tile = plan.kv_tile;
+    a.dq_tile = plan.dq_tile;
+    a.kv_split = plan.kv_split;
+    if (plan.kv_split > 1)
+        a.dkv_part = reinterpret_cast<float*>(static_cast<char*>(ws) + ws_stats_bytes(lq) + ws_ds_bytes(lq, lk));
     a.nq32 = (int)((lq->S + 31) / 32);
     a.nk32 = (int)((lk->S + 31) / 32);
     a.mq = tokmap(lq);
@@ -560,8 +601,12 @@ fbl_status bwd_run(uint32_t phases, const fbl_layout* lq, const void* q, const f
     a.scale_log2 = scale * 1.4426950408889634f;
     a.mask = mask_args(mask);
     const hipStream_t s = static_cast<hipStream_t>(stream);
-    const hipError_t e = lq->dtype == FBL_BF16 ? dispatch_bwd<bf16>((int)lq->D, a, phases, s)
-                                               : dispatch_bwd<float>((int)lq->D, a, phases, s);
+    hipError_t e;
+    if (plan.fused)
+        e = dispatch_bwd_fused(lq->dtype, (int)lq->D, a, s);
+    else
+        e = lq->dtype == FBL_BF16 ? dispatch_bwd<bf16>((int)lq->D, a, phases, s)
+                                  : dispatch_bwd<float>((int)lq->D, a, phases, s);
     return e == hipSuccess ? FBL_OK : FBL_ERR_HIP;
 }
 
@@ -585,6 +630,26 @@ fbl_status fbl_attn_bwd(const fbl_layout* lq, const void* q, const fbl_layout* l
                         void* dv, void* ws, size_t ws_bytes, void* stream) {
     return bwd_run(FBL_BWD_ALL, lq, q, lk, k, lv, v, lo, o, ldo, dO, lse, scale, mask, ldq, dq, ldk, dk, ldv, dv, ws,
                    ws_bytes, FBL_ATTN_TILE_AUTO, FBL_ATTN_TILE_AUTO, stream);
+}
+
+fbl_status fbl_attn_bwd_launches(uint32_t phases, const fbl_layout* lq, const fbl_layout* lk, uint32_t mask_kind,
+                                size_t ws_bytes, int32_t kv_tile, int32_t dq_tile, int32_t* launches) {
+    if (!launches) return FBL_ERR_NULL;
+    if (phases == 0 || (phases & ~FBL_BWD_ALL) || (mask_kind & ~(FBL_MASK_CAUSAL | FBL_MASK_KEY_PADDING)))
+        return FBL_ERR_ARG;
+    fbl_status st;
+    if ((st = check_layout(lq)) != FBL_OK || (st = check_layout(lk)) != FBL_OK) return st;
+    if (lq->dtype != lk->dtype) return FBL_ERR_DTYPE;
+    if (lq->B != lk->B || lq->D != lk->D || lq->H % lk->H != 0) return FBL_ERR_SHAPE;
+    if (lq->D != 32 && lq->D != 64 && lq->D != 128) return FBL_ERR_UNSUPPORTED;
+    BwdPlan plan;
+    if ((st = bwd_plan(phases, lq, lk, mask_kind, ws_bytes, kv_tile, dq_tile, &plan)) != FBL_OK) return st;
+    if (plan.fused) {
+        *launches = 1;
+        return FBL_OK;
+    }
+    *launches = (int32_t)__builtin_popcount(phases) + ((phases & FBL_BWD_KV) && plan.kv_split > 1 ? 1 : 0);
+    return FBL_OK;
 }
 
 fbl_status fbl_attn_bwd_tiled(uint32_t phases, const fbl_layout* lq, const void* q, const fbl_layout* lk,

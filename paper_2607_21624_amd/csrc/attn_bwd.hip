@@ -105,7 +105,12 @@ __global__ __launch_bounds__(256) void attn_bwd_stats(BwdArgs a) {
 }
 
 // ------------------------------------------------------------- kv pass
-template <typename T, int D>
+// FUSED: the whole backward in this one pass, for key/value sequences of at
+// most one key block (kKvBN keys): every workgroup then holds all the keys of
+// its (batch, kv head), so it also forms each query block's row statistics
+// (D from O and dO, LSE from the forward's output) and its dQ = scale dS K
+// completely -- no statistics pass, no stored dS, no dQ pass.
+template <typename T, int D, bool FUSED>
 struct KvCfg {
     static constexpr int BQ = D == 128 ? 32 : 64;  // queries per block (register budget)
     static constexpr int NQT = BQ / 32;
@@ -114,12 +119,21 @@ struct KvCfg {
     // LDS: Q0 Q1 dO0 dO1 tiles, then lse2 0/1 and D 0/1 (256 bytes each: one
     // 64-lane dword DMA; the first BQ floats are used)
     static constexpr int OFF_STATS = 4 * TB;
-    static constexpr int BYTES = 4 * TB + 4 * 256;
+    // FUSED: the block of kKvBN K rows (the dQ product's operand, staged once)
+    // and one block of dS, [BQ queries][DS_PITCH] of T (rows padded by 8
+    // elements: 16-byte aligned, and consecutive rows on other LDS banks)
+    static constexpr int OFF_K = OFF_STATS + 4 * 256;
+    static constexpr int KT_BYTES = kKvBN * D * (int)sizeof(T);
+    static constexpr int DS_PITCH = kKvBN + 8;
+    static constexpr int OFF_DS = OFF_K + KT_BYTES;
+    static constexpr int BYTES = FUSED ? OFF_DS + BQ * DS_PITCH * (int)sizeof(T) : OFF_STATS + 4 * 256;
+    static_assert(BYTES <= 160 * 1024, "LDS of one workgroup");
+    static_assert(OFF_K % 1024 == 0, "the K block starts on a 1 KB boundary");
 };
 
-template <typename T, int D>
-__global__ __launch_bounds__(256, 1) void attn_bwd_kv(BwdArgs a) {
-    using C = KvCfg<T, D>;
+template <typename T, int D, bool FUSED>
+__device__ __forceinline__ void kv_pass(const BwdArgs& a) {
+    using C = KvCfg<T, D, FUSED>;
     constexpr int NC = D / 16;
     constexpr int ND = D / 32;
     constexpr int BQ = C::BQ;
@@ -212,10 +226,48 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_kv(BwdArgs a) {
         const Rsrc ro = make_rsrc(static_cast<const T*>(a.dout) + a.mdo.head_base(b, h), ospan);
         pq.issue(lds + buf * TB, rq, (uint32_t)q0 * qbytes, wave);
         po.issue(lds + (2 + buf) * TB, ro, (uint32_t)q0 * obytes, wave);
-        if (wave < 2) {  // wave 0: lse2 of the block's queries, wave 1: D
+        if constexpr (FUSED) {  // wave 0: the forward's LSE of the block's queries (D is formed in the step)
+            if (wave == 0) {
+                const float* row = a.lse + ((int64_t)b * a.Hq + h) * S;
+                dma4(make_rsrc(row, (uint32_t)(S * 4)), lds + C::OFF_STATS + buf * 256, (uint32_t)lane * 4u,
+                     (uint32_t)q0 * 4u);
+            }
+        } else if (wave < 2) {  // wave 0: lse2 of the block's queries, wave 1: D
             const float* row = a.stats + (2 * ((int64_t)b * a.Hq + h) + wave) * S;
             dma4(make_rsrc(row, (uint32_t)(S * 4)), lds + C::OFF_STATS + (2 * wave + buf) * 256, (uint32_t)lane * 4u, (uint32_t)q0 * 4u);
         }
+    };
+    // FUSED: D_i = sum_k dO_ik O_ik of the block's BQ rows of query head h,
+    // TPR threads per row, into the block's D slot
+    auto form_d = [&](int buf, int h, int q0) {
+        constexpr int EPC = 16 / (int)sizeof(T);
+        constexpr int TPR = 256 / BQ;           // threads per row
+        constexpr int CPT = D / (TPR * EPC);    // 16-byte chunks per thread
+        static_assert(CPT >= 1 && D % (TPR * EPC) == 0, "whole chunks per thread");
+        const int r = (int)threadIdx.x / TPR, part = (int)threadIdx.x % TPR;
+        const int sq = q0 + r;
+        float acc = 0.f;
+        if (sq < S) {
+            const T* orow = static_cast<const T*>(a.o) + a.mo.head_base(b, h) + (int64_t)sq * a.mo.ss;
+            const T* grow = static_cast<const T*>(a.dout) + a.mdo.head_base(b, h) + (int64_t)sq * a.mdo.ss;
+#pragma unroll
+            for (int c = 0; c < CPT; ++c) {
+                const int col = (part * CPT + c) * EPC;
+                const uint4 xo = load16(orow + col), xg = load16(grow + col);
+                if constexpr (sizeof(T) == 2) {
+                    const bf16x8 vo = __builtin_bit_cast(bf16x8, xo), vg = __builtin_bit_cast(bf16x8, xg);
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) acc += (float)vo[e] * (float)vg[e];
+                } else {
+                    const f32x4 vo = __builtin_bit_cast(f32x4, xo), vg = __builtin_bit_cast(f32x4, xg);
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) acc += vo[e] * vg[e];
+                }
+            }
+        }
+#pragma unroll
+        for (int off = TPR / 2; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
+        if (part == 0) reinterpret_cast<float*>(kv_smem + C::OFF_STATS + (2 + buf) * 256)[r] = acc;
     };
 
     // per-lane LDS addresses into buffer 0; `flip` moves them to the other buffer
@@ -252,7 +304,11 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_kv(BwdArgs a) {
         for (int qt = 0; qt < NQT; ++qt) {
 #pragma unroll
             for (int rr = 0; rr < 4; ++rr) {
-                const f32x4 l4 = *(const FBL_LDS f32x4*)(uintptr_t)(st_addr + (qt * 32 + 8 * rr) * 4);
+                f32x4 l4 = *(const FBL_LDS f32x4*)(uintptr_t)(st_addr + (qt * 32 + 8 * rr) * 4);
+                if constexpr (FUSED) {  // the forward's natural-log LSE: to log2 units, +inf for an empty row
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) l4[j] = l4[j] == -INFINITY ? INFINITY : l4[j] * kLog2e;
+                }
                 const f32x4 d4 = *(const FBL_LDS f32x4*)(uintptr_t)(st_addr + 512 + (qt * 32 + 8 * rr) * 4);
 #pragma unroll
                 for (int j = 0; j < 4; ++j) {
@@ -300,6 +356,43 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_kv(BwdArgs a) {
                 }
             }
         }
+        if constexpr (FUSED) {  // dS of the wave's 32 keys into the block's dS rows: [query][key]
+            T* sds = reinterpret_cast<T*>(kv_smem + C::OFF_DS);
+#pragma unroll
+            for (int qt = 0; qt < NQT; ++qt)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) store_out(sds + (qt * 32 + acc_row(r, g)) * C::DS_PITCH + key - k0, dp[qt][r]);
+        }
+    };
+    // FUSED: dQ of the block, dQ^T(d x queries) = scale K^T dS^T over the
+    // workgroup's kKvBN keys -- A = K^T from the K block (transposed reads),
+    // B = dS^T from the dS rows (row reads); NQT x ND output tiles spread over
+    // the four wavefronts; query row q of head h at q0 + 32qt + lane % 32
+    auto dq_block = [&](int h, int q0) {
+        const T* sk = reinterpret_cast<const T*>(kv_smem + C::OFF_K);
+        const T* sds = reinterpret_cast<const T*>(kv_smem + C::OFF_DS);
+#pragma unroll
+        for (int o = wave; o < NQT * ND; o += kWaves) {
+            const int qt = o / ND, t = o % ND;
+            f32x16 acc = f32x16{};
+#pragma unroll
+            for (int kc = 0; kc < kKvBN / 16; ++kc) {
+                Frag<T> fk, fs;
+                tile_tr_frag<D>(fk, sk, 16 * kc + 8 * g, 16 * kc + 8 * g + 4, 32 * t, lane);
+                lds_row_frag(fs, sds + (qt * 32 + c32) * C::DS_PITCH + 16 * kc + 8 * g);
+                mma(acc, fk, fs);
+            }
+            const int qi = q0 + qt * 32 + c32;
+            if (qi < S) {
+                T* dqrow = static_cast<T*>(a.dq) + a.mdq.head_base(b, h) + (int64_t)qi * a.mdq.ss;
+#pragma unroll
+                for (int rr = 0; rr < 4; ++rr) {
+                    const int dcol = 32 * t + 8 * rr + 4 * g;
+                    store4(dqrow + dcol, acc[4 * rr] * a.scale, acc[4 * rr + 1] * a.scale, acc[4 * rr + 2] * a.scale,
+                           acc[4 * rr + 3] * a.scale);
+                }
+            }
+        }
     };
 
     auto step = [&](auto mask_c, int it) {
@@ -308,8 +401,25 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_kv(BwdArgs a) {
         __syncthreads();  // block `it` landed; block it-1's buffers are free
         if (it + 1 < n_iter) issue(it + 1);
         const int q0 = (qb_start + it % per_head) * BQ;
+        const int h = hk * G_ + it / per_head;
+        if constexpr (FUSED) {
+            form_d(buf, h, q0);
+            __syncthreads();  // the block's D row is in LDS
+        }
         // a wave whose keys all follow every query of the block has nothing to add
-        if (!(a.mask.causal && q0 + BQ - 1 < kw0) && kw0 < kv_end) compute(mask_c, buf, q0);
+        if (!(a.mask.causal && q0 + BQ - 1 < kw0) && kw0 < kv_end) {
+            compute(mask_c, buf, q0);
+        } else if constexpr (FUSED) {  // its dS columns are zero
+            T* sds = reinterpret_cast<T*>(kv_smem + C::OFF_DS);
+#pragma unroll
+            for (int qt = 0; qt < NQT; ++qt)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) store_out(sds + (qt * 32 + acc_row(r, g)) * C::DS_PITCH + key - k0, 0.f);
+        }
+        if constexpr (FUSED) {
+            __syncthreads();  // every wavefront's dS columns are in LDS
+            dq_block(h, q0);
+        }
         if constexpr (kBf16) {
 #pragma unroll
             for (int c = 0; c < NC; ++c) lo.row[c] += flip;
@@ -323,6 +433,22 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_kv(BwdArgs a) {
         flip = -flip;
     };
 
+    if constexpr (FUSED) {  // the workgroup's K rows for the dQ products (rows past S_kv read as zeros)
+        DmaPlan<T, D, kKvBN, kWaves> pk;
+        pk.init((uint32_t)(a.mk.ss * es), wave, lane);
+        pk.issue(lds + C::OFF_K, make_rsrc(kbase, (uint32_t)((int64_t)(Skv - 1) * a.mk.ss * es + D * es)), 0u, wave);
+    }
+    if constexpr (FUSED) {  // no allowed key (kv_len = 0): dQ of the whole group is zero
+        if (n_iter == 0) {
+            for (int64_t i = threadIdx.x; i < (int64_t)G_ * S * (D / 4); i += 256) {
+                const int c4 = (int)(i % (D / 4));
+                const int sq = (int)((i / (D / 4)) % S);
+                const int h = hk * G_ + (int)(i / ((int64_t)S * (D / 4)));
+                store4(static_cast<T*>(a.dq) + a.mdq.head_base(b, h) + (int64_t)sq * a.mdq.ss + 4 * c4, 0.f, 0.f, 0.f,
+                       0.f);
+            }
+        }
+    }
     if (n_iter > 0) issue(0);
     int it = 0;
     for (int hh = 0; hh < G_ && n_iter > 0; ++hh) {
@@ -345,6 +471,17 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_kv(BwdArgs a) {
             }
         }
     }
+}
+
+template <typename T, int D>
+__global__ __launch_bounds__(256, 1) void attn_bwd_kv(BwdArgs a) {
+    kv_pass<T, D, false>(a);
+}
+
+// the one-launch backward (keys within one block of kKvBN)
+template <typename T, int D>
+__global__ __launch_bounds__(256, 1) void attn_bwd_fused(BwdArgs a) {
+    kv_pass<T, D, true>(a);
 }
 
 // --------------------------------------------------------------- q pass
@@ -553,9 +690,9 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) void attn_bwd_q(BwdArg
 // Explicit instantiations: the host-side launch stubs of every kernel used
 // below.  bf16 storage runs the software-pipelined passes of attn_bwd_kv.hip,
 // attn_bwd_dq.hip and attn_bwd_q.hip; the two passes here serve fp32.
-#define FBL_BWD_KERNELS_F32(D)                                   \
-    template __global__ void attn_bwd_stats<float, D>(BwdArgs); \
-    template __global__ void attn_bwd_kv<float, D>(BwdArgs);    \
+#define FBL_BWD_KERNELS_F32(D)                                     \
+    template __global__ void attn_bwd_stats<float, D>(BwdArgs);   \
+    template __global__ void attn_bwd_kv<float, D>(BwdArgs);        \
     template __global__ void attn_bwd_q<float, D>(BwdArgs);
 FBL_BWD_KERNELS_F32(32)
 FBL_BWD_KERNELS_F32(64)
@@ -567,7 +704,7 @@ template __global__ void attn_bwd_stats<bf16, 128>(BwdArgs);
 
 template <int D>
 hipError_t set_bwd_lds_f32() {
-    const hipError_t e = ensure_dynamic_lds<&attn_bwd_kv<float, D>>(KvCfg<float, D>::BYTES);
+    const hipError_t e = ensure_dynamic_lds<&attn_bwd_kv<float, D>>(KvCfg<float, D, false>::BYTES);
     if (e != hipSuccess) return e;
     return ensure_dynamic_lds<&attn_bwd_q<float, D>>(QSmem<float, D>::BYTES);
 }
@@ -575,6 +712,21 @@ hipError_t set_bwd_lds_f32() {
 int padded8(int n) { return (n + 7) / 8 * 8; }
 
 }  // namespace
+
+template <typename T, int D>
+hipError_t launch_attn_bwd_fused(const BwdArgs& a, hipStream_t stream) {
+    constexpr int lds = KvCfg<T, D, true>::BYTES;
+    const hipError_t e = ensure_dynamic_lds<&attn_bwd_fused<T, D>>(lds);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((attn_bwd_fused<T, D>), dim3(padded8(a.Hkv * a.B)), dim3(256), lds, stream, a);
+    return hipGetLastError();
+}
+
+template hipError_t launch_attn_bwd_fused<float, 32>(const BwdArgs&, hipStream_t);
+template hipError_t launch_attn_bwd_fused<float, 64>(const BwdArgs&, hipStream_t);
+template hipError_t launch_attn_bwd_fused<bf16, 32>(const BwdArgs&, hipStream_t);
+template hipError_t launch_attn_bwd_fused<bf16, 64>(const BwdArgs&, hipStream_t);
+template hipError_t launch_attn_bwd_fused<bf16, 128>(const BwdArgs&, hipStream_t);
 
 template <typename T, int D>
 hipError_t launch_attn_bwd(const BwdArgs& a, unsigned phases, hipStream_t stream) {
@@ -592,7 +744,7 @@ hipError_t launch_attn_bwd(const BwdArgs& a, unsigned phases, hipStream_t stream
             if (ek != hipSuccess) return ek;
         } else {
             const int n = (a.Skv + kKvBN - 1) / kKvBN * a.Hkv * a.B;
-            constexpr int lds = KvCfg<T, D>::BYTES;
+            constexpr int lds = KvCfg<T, D, false>::BYTES;
             hipLaunchKernelGGL((attn_bwd_kv<T, D>), dim3(padded8(n)), dim3(256), lds, stream, a);
         }
     }

@@ -44,6 +44,11 @@ hipError_t launch_attn_fwd_bf16(const FwdArgs& a, int tile, hipStream_t stream);
 template <typename T, int D>
 hipError_t launch_attn_bwd(const BwdArgs& a, unsigned phases, hipStream_t stream);
 
+// The whole backward in one launch, for key/value sequences of at most 128
+// tokens (one key block per (batch, kv head)): row statistics, dK, dV and dQ.
+template <typename T, int D>
+hipError_t launch_attn_bwd_fused(const BwdArgs& a, hipStream_t stream);
+
 // Key/value-major backward pass for bf16 storage (software-pipelined kernel)
 // with kv tile `tile` of kAttnTiles (its split is a.kv_split).
 template <int D>

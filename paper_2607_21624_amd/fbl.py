@@ -54,7 +54,7 @@ FBL_ATTN_TILE_AUTO = -1
 
 EXPORTED = ("fbl_layout_desc", "fbl_layout_packed_qkv", "fbl_layout_offset", "fbl_layout_map_device", "fbl_attn_fwd",
             "fbl_attn_bwd_workspace", "fbl_attn_bwd_workspace_min", "fbl_attn_bwd", "fbl_attn_bwd_phases",
-            "fbl_attn_bwd_noalloc", "fbl_attn_fwd_tiled", "fbl_attn_bwd_tiled", "fbl_attn_tile_count",
+            "fbl_attn_bwd_noalloc", "fbl_attn_fwd_tiled", "fbl_attn_bwd_tiled", "fbl_attn_bwd_launches", "fbl_attn_tile_count",
             "fbl_attn_tile_info", "fbl_attn_candidates", "fbl_attn_auto_tiles", "fbl_attn_tune", "fbl_attn_tuned_tile",
             "fbl_attn_tune_reset", "fbl_proj", "fbl_proj_dt",
             "fbl_gemm_tile_count", "fbl_gemm_tile_info", "fbl_proj_candidates", "fbl_proj_tune", "fbl_proj_tuned_tile", "fbl_proj_auto_tile",
@@ -134,6 +134,9 @@ def _load() -> ctypes.CDLL:
     lib.fbl_attn_candidates.restype = ctypes.c_int
     lib.fbl_attn_auto_tiles.argtypes = [P(Layout), P(Layout), ctypes.c_uint32, P(ctypes.c_int32)]
     lib.fbl_attn_auto_tiles.restype = ctypes.c_int
+    lib.fbl_attn_bwd_launches.argtypes = [ctypes.c_uint32, P(Layout), P(Layout), ctypes.c_uint32, ctypes.c_size_t,
+                                          ctypes.c_int32, ctypes.c_int32, P(ctypes.c_int32)]
+    lib.fbl_attn_bwd_launches.restype = ctypes.c_int
     lib.fbl_attn_tune.argtypes = ([P(Layout), vp, P(Layout), vp, P(Layout), vp, P(Layout), vp, vp, P(Layout), vp,
                                    ctypes.c_float, Mask, P(Layout), vp, P(Layout), vp, P(Layout), vp, vp,
                                    ctypes.c_size_t, ctypes.c_uint32, ctypes.c_int32, P(ctypes.c_float),
@@ -437,6 +440,16 @@ def attn_auto_tiles(lq: Layout, lk: Layout, mask_kind: int):
     t = (ctypes.c_int32 * 3)()
     _check(LIB.fbl_attn_auto_tiles(ctypes.byref(lq), ctypes.byref(lk), mask_kind, t), "fbl_attn_auto_tiles")
     return tuple(t)
+
+
+def attn_bwd_launches(lq: Layout, lk: Layout, mask_kind: int, ws_bytes: int, phases: int = FBL_BWD_ALL,
+                      kv_tile: int = FBL_ATTN_TILE_AUTO, dq_tile: int = FBL_ATTN_TILE_AUTO) -> int:
+    """Kernel launches a backward call with these shapes, mask bits, workspace
+    size and tiles enqueues (1: the one-launch backward)."""
+    n = ctypes.c_int32()
+    _check(LIB.fbl_attn_bwd_launches(phases, ctypes.byref(lq), ctypes.byref(lk), mask_kind, ws_bytes, kv_tile,
+                                     dq_tile, ctypes.byref(n)), "fbl_attn_bwd_launches")
+    return n.value
 
 
 def attn_tune(q, k, v, do, Hq: int, Hkv: int, scale: Optional[float] = None, causal: bool = False, kv_len=None,

@@ -40,6 +40,8 @@ def test_llama7b_work_counts():
     lse = 32 * 4096 * 4
     assert ab["attn_bwd_kv"] == 6 * nq and ab["attn_bwd_dq"] == 2 * nq and ab["attn_bwd_stats"] == 2 * nq + lse
     assert ab["attn_fwd"] == 4 * nq + lse and ab["total"] == ab["attn_fwd"] + 8 * nq + lse
+    # the one-launch backward touches each backward tensor once: the whole backward's share of the total
+    assert ab["attn_bwd_fused"] == ab["total"] - ab["attn_fwd"]
     db = bench.design_bytes(w, 2)
     assert db["attn_bwd_dq"] == 32 * 8256 * 2048 and db["attn_bwd_kv"] == db["attn_bwd_dq"] + 2 * 32 * 4096 * 4
 

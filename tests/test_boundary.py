@@ -628,3 +628,40 @@ def test_attn_tile_rejections():
     assert F.LIB.fbl_attn_tile_info(0, 64, None) == F.FBL_ERR_NULL
     with pytest.raises(F.FblError):
         fbl.attn_candidates(F.FBL_ATTN_FWD, fbl.fbl_layout_desc(F32, 1, 64, 2, 64), fbl.fbl_layout_desc(F32, 1, 64, 2, 64))
+
+
+def test_bwd_launch_counts():
+    """fbl_attn_bwd_launches: the one-launch backward up to 128 keys with
+    automatic tiles (fp32 only at d <= 64), three launches otherwise, four
+    where the key/value pass is split (its partial sums reduced by a fourth),
+    one per phase bit when the phases are called one by one."""
+    ALL, KV = F.FBL_BWD_ALL, F.FBL_BWD_KV
+
+    def count(dt, B, Sq, Skv, Hq, Hkv, D, mask, ws="full", **kw):
+        lq = fbl.fbl_layout_desc(dt, B, Sq, Hq, D)
+        lk = fbl.fbl_layout_desc(dt, B, Skv, Hkv, D)
+        n = {"full": fbl.fbl_attn_bwd_workspace, "min": fbl.fbl_attn_bwd_workspace_min}[ws](lq, lk)
+        return fbl.attn_bwd_launches(lq, lk, mask, n, **kw)
+
+    assert count(BF16, 8, 128, 128, 12, 12, 64, 2) == 1             # BERT-base-like, key padding
+    assert count(BF16, 8, 128, 128, 12, 12, 64, 2, kv_tile=5) == 3  # a named tile: three launches
+    assert count(BF16, 8, 128, 128, 12, 12, 64, 2, phases=KV) == 1
+    assert count(BF16, 2, 300, 128, 4, 4, 128, 0) == 1              # cross attention, 128 keys
+    assert count(BF16, 2, 129, 129, 4, 4, 64, 1) == 3               # one key too many
+    assert count(F32, 1, 64, 64, 2, 2, 32, 0) == 1
+    assert count(F32, 1, 64, 64, 2, 2, 128, 0) == 3                 # fp32 at d = 128 does not fuse
+    assert count(BF16, 1, 4096, 4096, 32, 32, 128, 1) == 3          # Llama-7B-like causal
+    assert count(BF16, 2, 2048, 2048, 32, 8, 64, 1) == 4            # Llama-3.2-1B-like GQA: split kv pass
+    assert count(BF16, 2, 2048, 2048, 32, 8, 64, 1, ws="min") == 3  # no dS store, no split
+    assert count(BF16, 2, 2048, 2048, 32, 8, 64, 1, phases=KV) == 2
+    lq = fbl.fbl_layout_desc(F32, 1, 64, 2, 32)
+    n = ctypes.c_int32()
+    assert F.LIB.fbl_attn_bwd_launches(0, ctypes.byref(lq), ctypes.byref(lq), 0, 1 << 20, -1, -1,
+                                       ctypes.byref(n)) == F.FBL_ERR_ARG
+    assert F.LIB.fbl_attn_bwd_launches(ALL, ctypes.byref(lq), ctypes.byref(lq), 0, 1 << 20, 5, -1,
+                                       ctypes.byref(n)) == F.FBL_ERR_ARG    # fp32: automatic tiles only
+    assert F.LIB.fbl_attn_bwd_launches(ALL, ctypes.byref(lq), ctypes.byref(lq), 0, 1 << 20, -1, -1,
+                                       None) == F.FBL_ERR_NULL
+    l48 = fbl.fbl_layout_desc(BF16, 1, 64, 2, 48)
+    assert F.LIB.fbl_attn_bwd_launches(ALL, ctypes.byref(l48), ctypes.byref(l48), 0, 1 << 20, -1, -1,
+                                       ctypes.byref(n)) == F.FBL_ERR_UNSUPPORTED

@@ -329,8 +329,9 @@ def test_sequence_sliced_views(d, mask):
 def test_backward_phases_separately(name):
     """fbl_attn_bwd_phases: the preprocessing, key/value and dQ phases as three
     calls -- on one stream, then on two streams ordered by an event -- give the
-    bits of the single call (the Llama-3.2-1B-like shape with its split key/value
-    pass)."""
+    bits of the single three-kernel call (the Llama-3.2-1B-like shape with its
+    split key/value pass).  The single call names its tiles, which keeps it off
+    the one-launch backward that automatic tiles pick for up to 128 keys."""
     import torch
     fbl = _lib()
     w = synth.WORKLOADS[name]
@@ -344,10 +345,13 @@ def test_backward_phases_separately(name):
     ws = torch.empty(fbl.fbl_attn_bwd_workspace(fbl.layout_of(q, w.Hq), fbl.layout_of(k, w.Hkv)),
                      dtype=torch.uint8, device="cuda")
     outs = [torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)]
-    run = lambda ph, stream=None: fbl.attn_bwd(q, k, v, o, do, lse, w.Hq, w.Hkv, scale, causal, kv_len,
-                                               dq=outs[0], dk=outs[1], dv=outs[2], workspace=ws, phases=ph,
-                                               stream=stream)
-    run(fbl.FBL_BWD_ALL)
+    run = lambda ph, stream=None, tiles=(-1, -1): fbl.attn_bwd(q, k, v, o, do, lse, w.Hq, w.Hkv, scale, causal,
+                                                               kv_len, dq=outs[0], dk=outs[1], dv=outs[2],
+                                                               workspace=ws, phases=ph, stream=stream,
+                                                               kv_tile=tiles[0], dq_tile=tiles[1])
+    mask_kind = int(causal) | (2 if kv_len is not None else 0)
+    _, kv_tile, dq_tile = fbl.attn_auto_tiles(fbl.layout_of(q, w.Hq), fbl.layout_of(k, w.Hkv), mask_kind)
+    run(fbl.FBL_BWD_ALL, tiles=(kv_tile, dq_tile))
     torch.cuda.synchronize()
     ref = [t.clone() for t in outs]
     for t in outs:
