@@ -244,8 +244,10 @@ fbl_status fbl_attn_bwd_workspace_min(const fbl_layout* lq, const fbl_layout* lk
  * the workspace, and the workspace does not overlap an input or lse (it is
  * written while they are read).  bf16 storage runs the kv and dQ tiles
  * FBL_ATTN_TILE_AUTO resolves to.
- * Up to 128 keys (S_kv <= 128; fp32 storage only at D <= 64) the backward is
- * one launch: a workgroup holds all keys of one (batch, key/value head) in
+ * Up to 128 keys (S_kv <= 128; fp32 storage only at D <= 64), when there are
+ * at least 128 (batch, key/value head) pairs or each pair has at most 64
+ * query blocks (Hq/Hkv * ceil(S_q / 64), ceil(S_q / 32) at D = 128), the
+ * backward is one launch: a workgroup holds all keys of one (batch, key/value head) in
  * LDS and, per block of queries of its group, forms D_i, the dK and dV
  * contributions and the block's dS, and contracts that dS with K into dQ --
  * no workspace is read or written.  Its results agree with the three-launch
@@ -290,7 +292,8 @@ fbl_status fbl_attn_bwd_phases(uint32_t phases, const fbl_layout* lq, const void
  * The number of kernel launches fbl_attn_bwd_tiled(phases, ...) enqueues for
  * query/key descriptors lq and lk, mask bits mask_kind (FBL_MASK_*), a
  * workspace of ws_bytes and the requested tiles: 1 for the one-launch
- * backward (fbl_attn_bwd: FBL_BWD_ALL, automatic tiles, S_kv <= 128); else
+ * backward (fbl_attn_bwd: FBL_BWD_ALL, automatic tiles, the shapes given at
+ * fbl_attn_bwd); else
  * one per phase bit, plus one with FBL_BWD_KV when the key/value pass is
  * split (its partial sums are then added by a reduction launch).  Checks the
  * descriptors as fbl_attn_bwd does (FBL_ERR_* as there) and the tiles as

@@ -154,9 +154,18 @@ hipError_t dispatch_bwd_fused(int32_t dtype, int D, const fbl::BwdArgs& a, hipSt
 // Key/value sequences up to this length fit one kv workgroup (four
 // wavefronts of 32 keys), and the backward runs as one fused pass (fp32
 // storage up to d = 64: at d = 128 its fused state exceeds the registers).
+// The fused pass has one workgroup per (batch, kv head), each walking every
+// query block of its group; with few such workgroups and long query
+// sequences the three-launch path (its key/value pass split over up to four
+// workgroups, its dQ pass over query blocks) spreads the work wider, so the
+// fused pass is taken only when its grid holds at least 128 workgroups or
+// each workgroup has at most 64 query blocks.
 constexpr int64_t kFusedBwdMaxKeys = 128;
 bool bwd_fuses(const fbl_layout* lq, const fbl_layout* lk) {
-    return lk->S <= kFusedBwdMaxKeys && (lq->dtype == FBL_BF16 || lq->D <= 64);
+    if (lk->S > kFusedBwdMaxKeys || (lq->dtype != FBL_BF16 && lq->D > 64)) return false;
+    const int64_t bq = lq->D == 128 ? 32 : 64;  // query rows per block of the fused pass
+    const int64_t blocks = lq->H / lk->H * ((lq->S + bq - 1) / bq);
+    return lq->B * lk->H >= 128 || blocks <= 64;
 }
 
 template <typename T>

@@ -648,6 +648,10 @@ def test_bwd_launch_counts():
     assert count(BF16, 8, 128, 128, 12, 12, 64, 2, phases=KV) == 1
     assert count(BF16, 2, 300, 128, 4, 4, 128, 0) == 1              # cross attention, 128 keys
     assert count(BF16, 2, 129, 129, 4, 4, 64, 1) == 3               # one key too many
+    # 128 keys but two (batch, head) pairs of 128 query blocks: the split three-launch path
+    assert count(BF16, 1, 8192, 128, 2, 2, 64, 0) == 4
+    assert count(BF16, 128, 8192, 128, 2, 1, 64, 0) == 1            # 128 pairs: one launch
+    assert count(BF16, 1, 4096, 128, 2, 2, 64, 0) == 1              # 64 query blocks: one launch
     assert count(F32, 1, 64, 64, 2, 2, 32, 0) == 1
     assert count(F32, 1, 64, 64, 2, 2, 128, 0) == 3                 # fp32 at d = 128 does not fuse
     assert count(BF16, 1, 4096, 4096, 32, 32, 128, 1) == 3          # Llama-7B-like causal

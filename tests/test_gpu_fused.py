@@ -1,7 +1,8 @@
 """The one-launch backward for key/value sequences of at most 128 tokens (the
 statistics, dK, dV and dQ of a (batch, kv head) formed by one workgroup that
 holds all its keys), against the fp64 oracle and against the three-pass
-backward on the same inputs."""
+backward on the same inputs; and a 128-key shape with few, long (batch, head)
+pairs, which keeps the split three-launch path."""
 import math
 
 import numpy as np
@@ -21,6 +22,8 @@ CASES = [  # name, B, S_q, S_kv, Hq, Hkv, d, dtype, mask
     ("tiny_f32", 2, 64, 0, 2, 2, 32, "f32", synth.MASK_NONE),
     ("causal_f32_d64", 2, 90, 0, 4, 2, 64, "f32", synth.MASK_CAUSAL),
     ("cross_f32", 1, 200, 50, 2, 2, 64, "f32", synth.MASK_KEY_PADDING),
+    # 128 keys, but two (batch, head) pairs of 96 query blocks: the split three-launch path
+    ("long_q", 1, 6144, 128, 2, 2, 64, "bf16", synth.MASK_NONE),
 ]
 
 
@@ -39,6 +42,9 @@ def test_fused_backward(name, B, Sq, Skv, Hq, Hkv, d, dt, mask):
     causal = bool(mask & synth.MASK_CAUSAL)
     scale = 1.0 / math.sqrt(d)
     o, lse = fbl.attn_fwd(q, k, v, Hq, Hkv, scale, causal, kv_len)
+    ws_full = fbl.fbl_attn_bwd_workspace(fbl.layout_of(q, Hq), fbl.layout_of(k, Hkv))
+    n_launch = fbl.attn_bwd_launches(fbl.layout_of(q, Hq), fbl.layout_of(k, Hkv), mask, ws_full)
+    assert n_launch == (4 if name == "long_q" else 1), n_launch
     fused = fbl.attn_bwd(q, k, v, o, do, lse, Hq, Hkv, scale, causal, kv_len)
     again = fbl.attn_bwd(q, k, v, o, do, lse, Hq, Hkv, scale, causal, kv_len)
     # the same backward as three passes (statistics, key/value-major, dQ)
