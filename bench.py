@@ -290,6 +290,7 @@ def bench_block(args, fbl, torch, np):
         if ev is not None:
             ev[-1].record(stream)
 
+    spin = spin_up(step, args.spinup_s)
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
@@ -316,6 +317,7 @@ def bench_block(args, fbl, torch, np):
         "metric": "attention block fwd+bwd (QKV projection, attention, output projection) TFLOP/s at 1 GPU; "
                   "layout-copy bytes (=0)",
         "value": round(tflops, 2), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "spinup": {"seconds": args.spinup_s, "steps": spin},
         "ms_per_step": round(ms_per_step, 4), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16", "data": "synthetic (seeded N(0,1) activations and gradients, scaled N(0,1) weights)",
         "config": {"workload": f"attention block, {w.name} shape", "B": B, "S": S, "Hq": Hq, "Hkv": Hkv, "d": d,
@@ -327,6 +329,21 @@ def bench_block(args, fbl, torch, np):
         "layout_copy_bytes": 0 if foreign == [] else None,
         "dispatched_kernels": kernels,
     }), flush=True)
+
+
+def spin_up(step, seconds: float) -> int:
+    """Run `step` back to back for `seconds` (untimed, before the warmup steps):
+    under sustained load the chip's clocks and the first touches of the
+    buffers take some tens of milliseconds to settle, longer than a few warmup
+    steps of a sub-millisecond step.  Returns the number of steps run."""
+    import torch
+    n, t_end = 0, time.perf_counter() + seconds
+    while time.perf_counter() < t_end:
+        for _ in range(4):
+            step()
+        n += 4
+        torch.cuda.synchronize()
+    return n
 
 
 def dispatched_kernels(step):
@@ -348,6 +365,8 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--spinup-s", type=float, default=0.2,
+                    help="seconds of untimed steps before the warmup steps (clock and first-touch settling)")
     ap.add_argument("--workload", default="llama7b_causal")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-kernel-list", action="store_true",
@@ -449,6 +468,7 @@ def main():
             if ev is not None:
                 ev[2 + i].record(stream)
 
+    spin = spin_up(step, args.spinup_s)
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
@@ -483,6 +503,7 @@ def main():
         graph = torch.cuda.CUDAGraph()
         with torch.cuda.graph(graph):
             step()
+        spin_up(graph.replay, args.spinup_s)  # the capture left the GPU idle
         for _ in range(args.warmup):
             graph.replay()
         torch.cuda.synchronize()
@@ -553,6 +574,7 @@ def main():
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
+        "spinup": {"seconds": args.spinup_s, "steps": spin},
         "ms_per_step": round(ms_per_step, 4),
         "higher_is_better": True,
         "scaling": "weak",
