@@ -434,15 +434,7 @@ def main():
     tiles = [fbl.FBL_ATTN_TILE_AUTO] * 3
     if args.tiles:
         tiles = [int(x) for x in args.tiles.split(",")]
-    tune = None
-    if args.tune:
-        best, tms, _ = fbl.attn_tune(q, k, v, do, w.Hq, w.Hkv, scale, causal, kv_len, o=o, lse=lse, dq=dq, dk=dk,
-                                     dv=dv, workspace=ws, reps=5)
-        torch.cuda.synchronize()
-        tune = {"chosen": list(best), "ms": {str(t): round(x, 4) for t, x in tms.items()}}
     lq_, lk_ = fbl.layout_of(q, w.Hq), fbl.layout_of(k, w.Hkv)
-    auto = fbl.attn_auto_tiles(lq_, lk_, int(w.mask)) if w.dtype == "bf16" else None
-    run_tiles = None if auto is None else [a if t == fbl.FBL_ATTN_TILE_AUTO else t for t, a in zip(tiles, auto)]
     qname = "attn_bwd_dq" if w.dtype == "bf16" else "attn_bwd_q"
     # the backward as the library runs it: one launch up to 128 keys with automatic
     # tiles, else its three phases, each bracketed by events of its own
@@ -469,6 +461,14 @@ def main():
                 ev[2 + i].record(stream)
 
     spin = spin_up(step, args.spinup_s)
+    tune = None
+    if args.tune:  # measured at steady clocks (after the spin-up), then the chosen tiles run
+        best, tms, _ = fbl.attn_tune(q, k, v, do, w.Hq, w.Hkv, scale, causal, kv_len, o=o, lse=lse, dq=dq, dk=dk,
+                                     dv=dv, workspace=ws, reps=5)
+        torch.cuda.synchronize()
+        tune = {"chosen": list(best), "ms": {str(t): round(x, 4) for t, x in tms.items()}}
+    auto = fbl.attn_auto_tiles(lq_, lk_, int(w.mask)) if w.dtype == "bf16" else None
+    run_tiles = None if auto is None else [a if t == fbl.FBL_ATTN_TILE_AUTO else t for t, a in zip(tiles, auto)]
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()

@@ -228,19 +228,35 @@ AttnKey attn_key(uint32_t pass, const fbl_layout* lq, const fbl_layout* lk, uint
 }
 
 // Untuned choice: the first candidate in a preference order per pass, else
-// the first legal tile of the pass.  The forward's order is the measured one
-// on the Llama-7B-like, Llama-3.2-1B-like GQA and GPT-2-medium-like causal
-// shapes (the same at d = 128 and 64): 128 queries in 64-key tiles first, the
-// 64-queries-per-wavefront tiles last.
-int32_t attn_default_tile(uint32_t pass, int64_t D, int64_t Sq, int64_t Skv) {
+// the first legal tile of the pass.  The orders are the measured ones (tuned
+// at steady clocks on the Llama-7B-like, Llama-3.2-1B-like GQA, GPT-2-medium-
+// like and S = 512 shapes):
+//   forward  128 queries in 64-key tiles first, the 64-queries-per-wavefront
+//            tiles last (the same at d = 128 and 64);
+//   kv pass  at d = 64, the 32-query tiles with two workgroups per CU while
+//            the grid has at least 512 key blocks of 128 (two per CU), else
+//            the 64-query tiles, which halve the iterations of each of the
+//            fewer workgroups (GQA 2048: 120 -> 110 us; S = 512: -7..-25%;
+//            GPT-2-like 1024 with 512 blocks: +5%);
+//   dQ pass  the 8-wavefront tile (256 queries per workgroup) when it still
+//            gives 512 workgroups (Llama-7B-like -2%, GQA 2048 -10%), else
+//            the 4-wavefront one (GPT-2-like with 256: +30% for the wide tile).
+int32_t attn_default_tile(uint32_t pass, const fbl_layout* lq, const fbl_layout* lk) {
+    const int64_t D = lq->D, Sq = lq->S, Skv = lk->S;
     static const int fwd[] = {0, 2, 3, 4, 1};
-    static const int kv[] = {5, 6, 10};
-    static const int dq[] = {7, 8, 9};
+    static const int kv_many[] = {5, 6, 10}, kv_few[] = {6, 5, 10};
+    static const int dq_narrow[] = {7, 8, 9}, dq_wide[] = {8, 7, 9};
     const int* order;
-    int n;
-    if (pass == FBL_ATTN_FWD) order = fwd, n = 5;
-    else if (pass == FBL_ATTN_BWD_KV) order = kv, n = 3;
-    else order = dq, n = 3;
+    int n = 3;
+    if (pass == FBL_ATTN_FWD) {
+        order = fwd, n = 5;
+    } else if (pass == FBL_ATTN_BWD_KV) {
+        const int64_t blocks = lk->B * lk->H * ((Skv + 127) / 128);
+        order = (D == 64 && blocks < 512) ? kv_few : kv_many;
+    } else {
+        const int64_t wgs = lq->B * lq->H * ((Sq + 255) / 256);
+        order = wgs >= 512 ? dq_wide : dq_narrow;
+    }
     const uint64_t cand = attn_candidate_set(pass, D, Sq, Skv);
     for (int i = 0; i < n; ++i)
         if (cand >> order[i] & 1) return order[i];
@@ -268,7 +284,7 @@ fbl_status attn_resolve(uint32_t pass, const fbl_layout* lq, const fbl_layout* l
             return FBL_OK;
         }
     }
-    *out = attn_default_tile(pass, lq->D, lq->S, lk->S);
+    *out = attn_default_tile(pass, lq, lk);
     return *out >= 0 ? FBL_OK : FBL_ERR_UNSUPPORTED;
 }
 
