@@ -102,40 +102,50 @@ def sources_sha() -> str:
     return h.hexdigest()[:16]
 
 
-def measured_traffic(workload: str):
+def _tiles_str(tiles) -> str:
+    return "none" if tiles is None else ",".join(str(t) for t in tiles)
+
+
+def measured_traffic(workload: str, tiles=None):
     """HBM bytes per launch from the committed rocprofv3 FETCH_SIZE/WRITE_SIZE summary,
-    only if it was taken on the kernel sources as they are now (else None)."""
+    only if it was taken on the kernel sources as they are now and with the attention
+    tiles this run uses (else None)."""
     path = os.path.join(ROOT, "profiles", f"attn_{workload}_hbm_traffic.txt")
     if not os.path.exists(path):
         return None
-    out, sha = {}, None
+    out, sha, rec_tiles = {}, None, None
     for line in open(path):
         line = line.strip()
         if line.startswith("sha="):
             sha = line[4:]
+        elif line.startswith("tiles="):
+            rec_tiles = line[6:]
         elif line and not line.startswith("#"):
             name, *kv = line.split()
             d = dict(x.split("=") for x in kv)
             out[name] = int(d["fetch_bytes"]) + int(d["write_bytes"])
-    return out if sha == sources_sha() else None
+    return out if sha == sources_sha() and rec_tiles == _tiles_str(tiles) else None
 
 
-def traced_launch_us(workload: str):
+def traced_launch_us(workload: str, tiles=None):
     """Average launch duration (us) per kernel over the timed steps of the
     committed rocprofv3 kernel trace of this workload, only if it was taken on
-    the kernel sources as they are now (else None)."""
+    the kernel sources as they are now and with the attention tiles this run
+    uses (else None)."""
     path = os.path.join(ROOT, "profiles", f"attn_{workload}_kernel_trace.txt")
     if not os.path.exists(path):
         return None
-    out, sha = {}, None
+    out, sha, rec_tiles = {}, None, None
     for line in open(path):
         line = line.strip()
         if line.startswith("# kernel sources sha256[:16] = "):
             sha = line.split("= ")[1].split()[0]
+        elif line.startswith("# attention tiles (forward, kv, dQ) = "):
+            rec_tiles = line.split("= ")[1]
         elif line.startswith("timed "):
             _, name, us = line.split()[:3]
             out[name] = float(us)
-    return out if sha == sources_sha() else None
+    return out if sha == sources_sha() and rec_tiles == _tiles_str(tiles) else None
 
 
 def cpu_baseline(w, inp, budget_s: float):
@@ -534,8 +544,8 @@ def main():
     es = 2 if w.dtype == "bf16" else 4
     alg_bytes = algorithmic_bytes(w, es, inp["kv_len"])
     des_bytes = design_bytes(w, es, inp["kv_len"])
-    traffic = measured_traffic(w.name)
-    trace = traced_launch_us(w.name)
+    traffic = measured_traffic(w.name, run_tiles)
+    trace = traced_launch_us(w.name, run_tiles)
     dom_traffic = None if traffic is None else traffic.get(dom)
     dom_trace_us = None if trace is None else trace.get(dom)
     flops_launch = a_dom * w.d * pairs
