@@ -157,7 +157,8 @@ fbl_status fbl_layout_packed_qkv(fbl_layout* lq, fbl_layout* lk, fbl_layout* lv,
 int64_t fbl_layout_offset(const fbl_layout* l, int64_t b, int64_t h, int64_t s, int64_t i);
 
 /*
- * Diagnostic: evaluate the index map on the GPU with the same device code the
+ * Diagnostic: evaluate the index map (the tile-based index transformation of
+ * section 4.3, device side) on the GPU with the same device code the
  * attention kernels use to address tensors, writing out[((b*H + h)*S + s)*D + i]
  * = offset(b, h, s, i) as int64 into the device buffer `out` of
  * B*H*S*D elements.  Enqueued on `stream`.
@@ -214,7 +215,8 @@ fbl_status fbl_attn_fwd(const fbl_layout* lq, const void* q, const fbl_layout* l
 fbl_status fbl_attn_bwd_workspace(const fbl_layout* lq, const fbl_layout* lk, size_t* bytes);
 
 /*
- * Smallest workspace fbl_attn_bwd accepts: part 1 above only.  With any
+ * Smallest workspace fbl_attn_bwd accepts (section 4.1's backward with the
+ * dQ products recomputed): part 1 above only.  With any
  * workspace smaller than fbl_attn_bwd_workspace the dQ pass recomputes S and
  * dP from Q, K, V, dO and the row statistics instead of reading stored dS
  * (same results up to rounding order).
@@ -260,7 +262,10 @@ fbl_status fbl_attn_bwd(const fbl_layout* lq, const void* q, const fbl_layout* l
                         const fbl_layout* ldv, void* dv, void* ws, size_t ws_bytes, void* stream);
 
 /*
- * The three launches of fbl_attn_bwd, selectable one by one (same arguments
+ * The three launches of fbl_attn_bwd -- the backward's two reduction
+ * directions of sections 4.1 and 4.2 (the key/value pass reduces over
+ * queries, the dQ pass over keys) after the row statistics -- selectable one
+ * by one (same arguments
  * and checks as fbl_attn_bwd; `phases` is an OR of the bits below, enqueued
  * in the order listed).  fbl_attn_bwd(...) equals
  * fbl_attn_bwd_phases(FBL_BWD_ALL, ...), which takes the one-launch backward
@@ -289,7 +294,8 @@ fbl_status fbl_attn_bwd_phases(uint32_t phases, const fbl_layout* lq, const void
                                const fbl_layout* ldv, void* dv, void* ws, size_t ws_bytes, void* stream);
 
 /*
- * The number of kernel launches fbl_attn_bwd_tiled(phases, ...) enqueues for
+ * The number of kernel launches fbl_attn_bwd_tiled(phases, ...) enqueues (the
+ * passes of section 4.1's backward, or the one-launch form) for
  * query/key descriptors lq and lk, mask bits mask_kind (FBL_MASK_*), a
  * workspace of ws_bytes and the requested tiles: 1 for the one-launch
  * backward (fbl_attn_bwd: FBL_BWD_ALL, automatic tiles, the shapes given at
@@ -349,7 +355,9 @@ fbl_status fbl_attn_candidates(uint32_t pass, const fbl_layout* lq, const fbl_la
                                int32_t cap, int32_t* count);
 
 /*
- * The ids FBL_ATTN_TILE_AUTO resolves to for (lq, lk, mask kind): tiles[0]
+ * The R-Tile choice of section 4.2 for one shape, the per-shape lookup the
+ * paper's runtime makes (section 5.5): the ids FBL_ATTN_TILE_AUTO resolves to
+ * for (lq, lk, mask kind): tiles[0]
  * forward, tiles[1] kv pass, tiles[2] dQ pass -- the measured choice of
  * fbl_attn_tune for this shape when the process holds one, else the first
  * candidate in a preference order measured on MI355X.  Host only.
@@ -357,7 +365,8 @@ fbl_status fbl_attn_candidates(uint32_t pass, const fbl_layout* lq, const fbl_la
 fbl_status fbl_attn_auto_tiles(const fbl_layout* lq, const fbl_layout* lk, uint32_t mask_kind, int32_t* tiles);
 
 /*
- * fbl_attn_fwd and fbl_attn_bwd_phases with explicit tiles (fbl_attn_bwd is
+ * fbl_attn_fwd and fbl_attn_bwd_phases with explicit R-Tile shapes (section
+ * 4.2; fbl_attn_bwd is
  * fbl_attn_bwd_tiled(FBL_BWD_ALL, ..., FBL_ATTN_TILE_AUTO, FBL_ATTN_TILE_AUTO,
  * stream)): `tile`, `kv_tile`, `dq_tile` are ids of the right pass that pass
  * C1 and C2 at this head dim
@@ -481,7 +490,8 @@ fbl_status fbl_proj(uint32_t op, int64_t M, int64_t K, int64_t N, const void* a,
                     int64_t ldb, void* c, int64_t ldc, int32_t tile, void* stream);
 
 /*
- * fbl_proj for either storage type: dtype FBL_BF16 is fbl_proj exactly;
+ * fbl_proj (the projection products of section 2.2's LoRA example) for either
+ * storage type: dtype FBL_BF16 is fbl_proj exactly;
  * FBL_F32 runs the same three products on fp32 operands and result (fp32
  * MFMAs, fp32 accumulation) with one tile shape -- tile must be
  * FBL_GEMM_TILE_AUTO (else FBL_ERR_ARG) -- any extents and leading
@@ -492,7 +502,8 @@ fbl_status fbl_proj_dt(uint32_t op, int32_t dtype, int64_t M, int64_t K, int64_t
                        const void* b, int64_t ldb, void* c, int64_t ldc, int32_t tile, void* stream);
 
 /*
- * Tile configurations of the projection products.  fbl_gemm_tile_count gives
+ * Tile configurations of the projection products (their R-Tile shapes,
+ * section 4.2).  fbl_gemm_tile_count gives
  * the number of ids; fbl_gemm_tile_info writes 8 values for one id:
  *   info[0..1]  bm, bn   output tile rows x cols of one workgroup
  *   info[2]     bk       contraction elements staged per step
@@ -553,7 +564,8 @@ int32_t fbl_proj_tuned_tile(uint32_t op, int64_t M, int64_t K, int64_t N);
 void fbl_proj_tune_reset(void);
 
 /*
- * The tile id FBL_GEMM_TILE_AUTO resolves to for a bf16 product (op, M, K,
+ * The tile id FBL_GEMM_TILE_AUTO resolves to (section 4.2's selection) for a
+ * bf16 product (op, M, K,
  * N): the tuned choice when the table holds one, else the untuned preference
  * among the candidates -- by the number of 128 x 128 output tiles and the
  * contraction length, measured on MI355X.  The untuned choice depends on the
