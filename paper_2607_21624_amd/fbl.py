@@ -342,6 +342,33 @@ def _check_kv_len(kv_len, B: int, where: str) -> None:
         raise FblError(FBL_ERR_SHAPE, f"{where}: kv_len has {kv_len.numel()} entries, needs {B}")
 
 
+def _check_lse(lse, B: int, Hq: int, S: int, where: str) -> None:
+    """lse must be a contiguous float32 [B, Hq, S_q] tensor: the kernels read and
+    write it as B*Hq*S_q consecutive floats."""
+    if lse is None:
+        return
+    import torch
+    if not isinstance(lse, torch.Tensor):
+        raise FblError(FBL_ERR_ARG, f"{where}: lse must be a torch tensor")
+    if lse.dtype != torch.float32:
+        raise FblError(FBL_ERR_DTYPE, f"{where}: lse must be float32, got {lse.dtype}")
+    if tuple(lse.shape) != (B, Hq, S):
+        raise FblError(FBL_ERR_SHAPE, f"{where}: lse has shape {tuple(lse.shape)}, needs {(B, Hq, S)}")
+    if not lse.is_contiguous():
+        raise FblError(FBL_ERR_LAYOUT, f"{where}: lse must be contiguous")
+
+
+def _check_workspace(ws, where: str) -> None:
+    """The workspace is handed over as one span of numel * element_size bytes."""
+    if ws is None:
+        return
+    import torch
+    if not isinstance(ws, torch.Tensor):
+        raise FblError(FBL_ERR_ARG, f"{where}: workspace must be a torch tensor")
+    if not ws.is_contiguous():
+        raise FblError(FBL_ERR_LAYOUT, f"{where}: workspace must be contiguous")
+
+
 def _check_device(where: str, stream, **tensors) -> None:
     """Every tensor argument lives on one GPU, the device the launch stream
     belongs to: the kernels dereference each pointer on that device."""
@@ -370,6 +397,8 @@ def attn_fwd(q, k, v, Hq: int, Hkv: int, scale: Optional[float] = None, causal: 
     import torch
     _check_kv_len(kv_len, q.shape[0], "attn_fwd")
     _check_device("attn_fwd", stream, q=q, k=k, v=v, kv_len=kv_len, out=out, lse=lse)
+    if q.dim() == 3:
+        _check_lse(lse, q.shape[0], Hq, q.shape[1], "attn_fwd")
     lq, lk, lv = _layout(q, Hq), _layout(k, Hkv), _layout(v, Hkv)
     if scale is None:
         scale = 1.0 / math.sqrt(lq.D)
@@ -392,6 +421,9 @@ def attn_bwd(q, k, v, o, do, lse, Hq: int, Hkv: int, scale: Optional[float] = No
     _check_kv_len(kv_len, q.shape[0], "attn_bwd")
     _check_device("attn_bwd", stream, q=q, k=k, v=v, o=o, do=do, lse=lse, kv_len=kv_len, dq=dq, dk=dk, dv=dv,
                   workspace=workspace)
+    if q.dim() == 3:
+        _check_lse(lse, q.shape[0], Hq, q.shape[1], "attn_bwd")
+    _check_workspace(workspace, "attn_bwd")
     lq, lk, lv = _layout(q, Hq), _layout(k, Hkv), _layout(v, Hkv)
     lo, ldo = _layout(o, Hq), _layout(do, Hq)
     if scale is None:
@@ -462,6 +494,9 @@ def attn_tune(q, k, v, do, Hq: int, Hkv: int, scale: Optional[float] = None, cau
     _check_kv_len(kv_len, q.shape[0], "attn_tune")
     _check_device("attn_tune", stream, q=q, k=k, v=v, do=do, kv_len=kv_len, o=o, lse=lse, dq=dq, dk=dk, dv=dv,
                   workspace=workspace)
+    if q.dim() == 3:
+        _check_lse(lse, q.shape[0], Hq, q.shape[1], "attn_tune")
+    _check_workspace(workspace, "attn_tune")
     lq, lk, lv, ldo = _layout(q, Hq), _layout(k, Hkv), _layout(v, Hkv), _layout(do, Hq)
     if scale is None:
         scale = 1.0 / math.sqrt(lq.D)
@@ -515,6 +550,8 @@ def attn_bwd_noalloc(q, k, v, o, do, lse, Hq: int, Hkv: int, dq, dk, dv, scale: 
     _check_kv_len(kv_len, q.shape[0], "attn_bwd_noalloc")
     _check_device("attn_bwd_noalloc", stream, q=q, k=k, v=v, o=o, do=do, lse=lse, kv_len=kv_len, dq=dq, dk=dk,
                   dv=dv)
+    if q.dim() == 3:
+        _check_lse(lse, q.shape[0], Hq, q.shape[1], "attn_bwd_noalloc")
     lq, lk, lv = _layout(q, Hq), _layout(k, Hkv), _layout(v, Hkv)
     lo, ldo = _layout(o, Hq), _layout(do, Hq)
     ldq, ldk, ldv = _layout(dq, Hq), _layout(dk, Hkv), _layout(dv, Hkv)
@@ -549,6 +586,8 @@ def attn_fwd_packed(qkv, Hq: int, Hkv: int, scale: Optional[float] = None, causa
     import torch
     _check_kv_len(kv_len, qkv.shape[0], "attn_fwd_packed")
     _check_device("attn_fwd_packed", stream, qkv=qkv, kv_len=kv_len, out=out, lse=lse)
+    if qkv.dim() == 3:
+        _check_lse(lse, qkv.shape[0], Hq, qkv.shape[1], "attn_fwd_packed")
     lq, lk, lv, pq, pk, pv = _packed(qkv, Hq, Hkv)
     if scale is None:
         scale = 1.0 / math.sqrt(lq.D)
@@ -571,6 +610,9 @@ def attn_bwd_packed(qkv, o, do, lse, Hq: int, Hkv: int, scale: Optional[float] =
     _check_kv_len(kv_len, qkv.shape[0], "attn_bwd_packed")
     _check_device("attn_bwd_packed", stream, qkv=qkv, o=o, do=do, lse=lse, kv_len=kv_len, dqkv=dqkv,
                   workspace=workspace)
+    if qkv.dim() == 3:
+        _check_lse(lse, qkv.shape[0], Hq, qkv.shape[1], "attn_bwd_packed")
+    _check_workspace(workspace, "attn_bwd_packed")
     lq, lk, lv, pq, pk, pv = _packed(qkv, Hq, Hkv)
     if scale is None:
         scale = 1.0 / math.sqrt(lq.D)

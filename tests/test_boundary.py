@@ -530,6 +530,29 @@ def test_binding_rejects_kv_len_and_host_tensors():
         assert ei.value.status == F.FBL_ERR_ARG
 
 
+def test_binding_checks_lse_and_workspace():
+    """The saved log-sum-exp and the workspace reach the kernels as raw spans:
+    lse must be a contiguous float32 [B, Hq, S_q] tensor and the workspace
+    contiguous, else the binding raises (the kernels would read or write past
+    them)."""
+    import torch
+    B, Hq, S = 2, 4, 16
+    F._check_lse(None, B, Hq, S, "t")
+    F._check_lse(torch.zeros(B, Hq, S), B, Hq, S, "t")
+    for bad, status in ((torch.zeros(B, Hq, S, dtype=torch.bfloat16), F.FBL_ERR_DTYPE),
+                        (torch.zeros(B, Hq, S - 1), F.FBL_ERR_SHAPE),
+                        (torch.zeros(B * Hq * S), F.FBL_ERR_SHAPE),
+                        (torch.zeros(B, S, Hq).transpose(1, 2), F.FBL_ERR_LAYOUT),
+                        ([0.0] * (B * Hq * S), F.FBL_ERR_ARG)):
+        with pytest.raises(F.FblError) as ei:
+            F._check_lse(bad, B, Hq, S, "t")
+        assert ei.value.status == status
+    F._check_workspace(torch.zeros(1024, dtype=torch.uint8), "t")
+    with pytest.raises(F.FblError) as ei:
+        F._check_workspace(torch.zeros(2048, dtype=torch.uint8)[::2], "t")
+    assert ei.value.status == F.FBL_ERR_LAYOUT
+
+
 def test_autograd_rejects_broadcast_gradient():
     """The autograd wrappers read the incoming gradient in place; a broadcast
     view (inner stride 0) is refused instead of silently copied."""

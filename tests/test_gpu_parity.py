@@ -520,3 +520,24 @@ def test_unusual_scales(scale):
     assert not bad, bad
     if scale == 0.0:
         assert np.max(np.abs(got["dq"])) == 0.0 and np.max(np.abs(got["dk"])) == 0.0
+
+
+def test_binding_rejects_bad_lse_and_workspace():
+    """On the GPU too, a saved log-sum-exp of the wrong type or shape, or a
+    strided workspace, is refused by the binding before any launch."""
+    import torch
+    fbl = _lib()
+    B, S, H, d = 2, 64, 2, 64
+    q = torch.randn(B, S, H * d, device="cuda").to(torch.bfloat16)
+    o, lse = fbl.attn_fwd(q, q, q, H, H, 0.125, False)
+    note("binding rejects bad lse / workspace")
+    for bad in (lse.to(torch.bfloat16), lse[:, :, :-1], lse.transpose(1, 2).contiguous().transpose(1, 2)):
+        with pytest.raises(fbl.FblError):
+            fbl.attn_bwd(q, q, q, o, q, bad, H, H, 0.125, False)
+        with pytest.raises(fbl.FblError):
+            fbl.attn_fwd(q, q, q, H, H, 0.125, False, lse=bad)
+    ws = torch.empty(2 * fbl.fbl_attn_bwd_workspace(fbl.layout_of(q, H), fbl.layout_of(q, H)), dtype=torch.uint8,
+                     device="cuda")
+    with pytest.raises(fbl.FblError):
+        fbl.attn_bwd(q, q, q, o, q, lse, H, H, 0.125, False, workspace=ws[::2])
+    torch.cuda.synchronize()
