@@ -126,9 +126,16 @@ struct KvCfg {
     static constexpr int KT_BYTES = kKvBN * D * (int)sizeof(T);
     static constexpr int DS_PITCH = kKvBN + 8;
     static constexpr int OFF_DS = OFF_K + KT_BYTES;
-    static constexpr int BYTES = FUSED ? OFF_DS + BQ * DS_PITCH * (int)sizeof(T) : OFF_STATS + 4 * 256;
+    // FUSED with bf16 storage: the block's O rows too (staged with Q and dO, two
+    // buffers), so that D is formed from LDS; fp32 forms it from global memory
+    static constexpr bool O_TILE = FUSED && sizeof(T) == 2;
+    static constexpr int OFF_O = (OFF_DS + BQ * DS_PITCH * (int)sizeof(T) + 1023) / 1024 * 1024;
+    static constexpr int BYTES = !FUSED ? OFF_STATS + 4 * 256
+                                 : O_TILE ? OFF_O + 2 * TB
+                                          : OFF_DS + BQ * DS_PITCH * (int)sizeof(T);
     static_assert(BYTES <= 160 * 1024, "LDS of one workgroup");
     static_assert(OFF_K % 1024 == 0, "the K block starts on a 1 KB boundary");
+    static_assert(OFF_O % 1024 == 0 && TB % 1024 == 0, "the O tiles start on 1 KB boundaries");
 };
 
 template <typename T, int D, bool FUSED>
@@ -217,6 +224,10 @@ __device__ __forceinline__ void kv_pass(const BwdArgs& a) {
     const uint32_t qbytes = (uint32_t)(a.mq.ss * es), obytes = (uint32_t)(a.mdo.ss * es);
     const uint32_t qspan = (uint32_t)((int64_t)(S - 1) * a.mq.ss * es + D * es);
     const uint32_t ospan = (uint32_t)((int64_t)(S - 1) * a.mdo.ss * es + D * es);
+    DmaPlan<T, D, BQ, kWaves> pof;  // O rows (FUSED, bf16)
+    const uint32_t ofbytes = (uint32_t)(a.mo.ss * es);
+    const uint32_t ofspan = (uint32_t)((int64_t)(S - 1) * a.mo.ss * es + D * es);
+    if constexpr (C::O_TILE) pof.init(ofbytes, wave, lane);
 
     auto issue = [&](int it) {
         const int buf = it & 1;
@@ -226,6 +237,10 @@ __device__ __forceinline__ void kv_pass(const BwdArgs& a) {
         const Rsrc ro = make_rsrc(static_cast<const T*>(a.dout) + a.mdo.head_base(b, h), ospan);
         pq.issue(lds + buf * TB, rq, (uint32_t)q0 * qbytes, wave);
         po.issue(lds + (2 + buf) * TB, ro, (uint32_t)q0 * obytes, wave);
+        if constexpr (C::O_TILE) {
+            const Rsrc rof = make_rsrc(static_cast<const T*>(a.o) + a.mo.head_base(b, h), ofspan);
+            pof.issue(lds + C::OFF_O + buf * TB, rof, (uint32_t)q0 * ofbytes, wave);
+        }
         if constexpr (FUSED) {  // wave 0: the forward's LSE of the block's queries (D is formed in the step)
             if (wave == 0) {
                 const float* row = a.lse + ((int64_t)b * a.Hq + h) * S;
@@ -247,7 +262,17 @@ __device__ __forceinline__ void kv_pass(const BwdArgs& a) {
         const int r = (int)threadIdx.x / TPR, part = (int)threadIdx.x % TPR;
         const int sq = q0 + r;
         float acc = 0.f;
-        if (sq < S) {
+        if constexpr (C::O_TILE) {  // both rows from the staged tiles (rows past S are zeros)
+            using G = TileGeom<T, D>;
+#pragma unroll
+            for (int c = 0; c < CPT; ++c) {
+                const uint32_t eo = 2u * (uint32_t)G::off(r, (part * CPT + c) * EPC);
+                const bf16x8 vo = lds_b128(lds + C::OFF_O + buf * TB + eo, 0u);
+                const bf16x8 vg = lds_b128(lds + (2 + buf) * TB + eo, 0u);
+#pragma unroll
+                for (int e = 0; e < 8; ++e) acc += (float)vo[e] * (float)vg[e];
+            }
+        } else if (sq < S) {
             const T* orow = static_cast<const T*>(a.o) + a.mo.head_base(b, h) + (int64_t)sq * a.mo.ss;
             const T* grow = static_cast<const T*>(a.dout) + a.mdo.head_base(b, h) + (int64_t)sq * a.mdo.ss;
 #pragma unroll
@@ -368,12 +393,36 @@ __device__ __forceinline__ void kv_pass(const BwdArgs& a) {
     // workgroup's kKvBN keys -- A = K^T from the K block (transposed reads),
     // B = dS^T from the dS rows (row reads); NQT x ND output tiles spread over
     // the four wavefronts; query row q of head h at q0 + 32qt + lane % 32
+    // FUSED: dQ of a block is computed after its dS and (bf16) stored at the
+    // start of the next step, after that step's wait: its stores then have a
+    // whole step to retire before the next wait (which covers every
+    // outstanding memory operation of the wavefront).  One output tile per
+    // wavefront.
+    static_assert(!FUSED || NQT * ND <= kWaves, "at most one dQ tile per wavefront");
+    f32x16 dq_acc = f32x16{};
+    int dq_h = -1, dq_q0 = 0;  // the block whose dQ tile is held (dq_h < 0: none)
+    auto dq_flush_now = [&]() {
+        if (dq_h >= 0) {
+            const int qt = wave / ND, t = wave % ND;
+            const int qi = dq_q0 + qt * 32 + c32;
+            if (qi < S) {
+                T* dqrow = static_cast<T*>(a.dq) + a.mdq.head_base(b, dq_h) + (int64_t)qi * a.mdq.ss;
+#pragma unroll
+                for (int rr = 0; rr < 4; ++rr) {
+                    const int dcol = 32 * t + 8 * rr + 4 * g;
+                    store4(dqrow + dcol, dq_acc[4 * rr] * a.scale, dq_acc[4 * rr + 1] * a.scale,
+                           dq_acc[4 * rr + 2] * a.scale, dq_acc[4 * rr + 3] * a.scale);
+                }
+            }
+            dq_h = -1;
+        }
+    };
+
     auto dq_block = [&](int h, int q0) {
         const T* sk = reinterpret_cast<const T*>(kv_smem + C::OFF_K);
         const T* sds = reinterpret_cast<const T*>(kv_smem + C::OFF_DS);
-#pragma unroll
-        for (int o = wave; o < NQT * ND; o += kWaves) {
-            const int qt = o / ND, t = o % ND;
+        if (wave < NQT * ND) {
+            const int qt = wave / ND, t = wave % ND;
             f32x16 acc = f32x16{};
 #pragma unroll
             for (int kc = 0; kc < kKvBN / 16; ++kc) {
@@ -382,19 +431,24 @@ __device__ __forceinline__ void kv_pass(const BwdArgs& a) {
                 lds_row_frag(fs, sds + (qt * 32 + c32) * C::DS_PITCH + 16 * kc + 8 * g);
                 mma(acc, fk, fs);
             }
-            const int qi = q0 + qt * 32 + c32;
-            if (qi < S) {
-                T* dqrow = static_cast<T*>(a.dq) + a.mdq.head_base(b, h) + (int64_t)qi * a.mdq.ss;
+            if constexpr (kBf16) {
+                dq_acc = acc;
+                dq_h = h;
+                dq_q0 = q0;
+            } else {  // fp32: no registers to spare for holding it
+                const int qi = q0 + qt * 32 + c32;
+                if (qi < S) {
+                    T* dqrow = static_cast<T*>(a.dq) + a.mdq.head_base(b, h) + (int64_t)qi * a.mdq.ss;
 #pragma unroll
-                for (int rr = 0; rr < 4; ++rr) {
-                    const int dcol = 32 * t + 8 * rr + 4 * g;
-                    store4(dqrow + dcol, acc[4 * rr] * a.scale, acc[4 * rr + 1] * a.scale, acc[4 * rr + 2] * a.scale,
-                           acc[4 * rr + 3] * a.scale);
+                    for (int rr = 0; rr < 4; ++rr) {
+                        const int dcol = 32 * t + 8 * rr + 4 * g;
+                        store4(dqrow + dcol, acc[4 * rr] * a.scale, acc[4 * rr + 1] * a.scale,
+                               acc[4 * rr + 2] * a.scale, acc[4 * rr + 3] * a.scale);
+                    }
                 }
             }
         }
     };
-
     auto step = [&](auto mask_c, int it) {
         const int buf = it & 1;
         wait_vmcnt<0>();
@@ -403,6 +457,7 @@ __device__ __forceinline__ void kv_pass(const BwdArgs& a) {
         const int q0 = (qb_start + it % per_head) * BQ;
         const int h = hk * G_ + it / per_head;
         if constexpr (FUSED) {
+            if constexpr (kBf16) dq_flush_now();  // the previous block's dQ tile
             form_d(buf, h, q0);
             __syncthreads();  // the block's D row is in LDS
         }
@@ -455,6 +510,7 @@ __device__ __forceinline__ void kv_pass(const BwdArgs& a) {
         for (int j = 0; j < n_mask; ++j, ++it) step(std::true_type{}, it);
         for (int j = n_mask; j < per_head; ++j, ++it) step(std::false_type{}, it);
     }
+    if constexpr (FUSED && kBf16) dq_flush_now();
 
     // dK (times scale) and dV rows of this wave's keys: lane <-> key, 4 consecutive d per store
     if (key < Skv) {
