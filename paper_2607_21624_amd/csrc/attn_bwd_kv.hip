@@ -48,6 +48,41 @@ namespace fbl {
 
 namespace {
 
+// The LDS DMA of one kv block -- NPQ loads of 1 KB from each of the Q and dO
+// tiles and one 256-byte load of the statistics row -- in one statement, so
+// one set of wait states covers every scalar operand (a load issued on its
+// own needs them each time: the compiler may reload a spilled scalar operand
+// with a vector instruction just before it).  The LDS address of load i is
+// lq + i * kq (Q), lq + TB + i * kq (dO) and lst (statistics).
+template <int NPQ>
+FBL_DEV void kv_block_dma(Rsrc rq, Rsrc ro, Rsrc rst, uint32_t sq, uint32_t so, uint32_t sst, uint32_t lq, uint32_t lo,
+                          uint32_t lst, uint32_t kq, const uint32_t* vq, const uint32_t* vo, uint32_t vst) {
+    static_assert(NPQ == 1 || NPQ == 2, "one or two loads per tile");
+    if constexpr (NPQ == 2) {
+        asm volatile(
+            "s_nop 4\n\t"
+            "s_mov_b32 m0, %5\n\ts_nop 0\n\tbuffer_load_dwordx4 %0, %10, %13 offen lds\n\t"
+            "s_mov_b32 m0, %6\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %10, %13 offen lds\n\t"
+            "s_mov_b32 m0, %7\n\ts_nop 0\n\tbuffer_load_dwordx4 %2, %11, %14 offen lds\n\t"
+            "s_mov_b32 m0, %8\n\ts_nop 0\n\tbuffer_load_dwordx4 %3, %11, %14 offen lds\n\t"
+            "s_mov_b32 m0, %9\n\ts_nop 0\n\tbuffer_load_dword %4, %12, %15 offen lds"
+            :
+            : "v"(vq[0]), "v"(vq[1]), "v"(vo[0]), "v"(vo[1]), "v"(vst), "s"(lq), "s"(lq + kq), "s"(lo), "s"(lo + kq),
+              "s"(lst), "s"(rq), "s"(ro), "s"(rst), "s"(sq), "s"(so), "s"(sst)
+            : "memory", "m0");
+    } else {
+        asm volatile(
+            "s_nop 4\n\t"
+            "s_mov_b32 m0, %3\n\ts_nop 0\n\tbuffer_load_dwordx4 %0, %6, %9 offen lds\n\t"
+            "s_mov_b32 m0, %4\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %7, %10 offen lds\n\t"
+            "s_mov_b32 m0, %5\n\ts_nop 0\n\tbuffer_load_dword %2, %8, %11 offen lds"
+            :
+            : "v"(vq[0]), "v"(vo[0]), "v"(vst), "s"(lq), "s"(lo), "s"(lst), "s"(rq), "s"(ro), "s"(rst), "s"(sq),
+              "s"(so), "s"(sst)
+            : "memory", "m0");
+    }
+}
+
 constexpr int kLead = 4;              // product slots between an operand read and its use
 
 // BQ_ queries per block (the staged Q/dO tile rows of the tile table), NW_
@@ -206,9 +241,19 @@ __global__ __launch_bounds__(64 * NW_, (KvPipe<D, BQ_, NW_>::WPS)) void attn_bwd
             rst = make_rsrc(st_head, st_bytes);
         }
     };
-    auto issue = [&](auto buf_c) {
+    auto issue_all = [&](auto buf_c) {
+        constexpr int BB = decltype(buf_c)::value;
+        if constexpr (NPQ <= 2) {
+            const uint32_t lq = lds + BB * BUFB + wave * 1024;
+            kv_block_dma<NPQ>(rq, ro, rst, dma_q0 * qbytes, dma_q0 * obytes, dma_q0 * 4u, lq, lq + TB,
+                              st_lds0 + BB * st_step, kPWaves * 1024, pq.voff, po.voff, (uint32_t)lane * 4u);
+        } else {
 #pragma unroll
-        for (int part = 0; part < NPART; ++part) issue_part(buf_c, part);
+            for (int part = 0; part < NPART; ++part) issue_part(buf_c, part);
+        }
+    };
+    auto issue = [&](auto buf_c) {
+        issue_all(buf_c);
         advance_dma();
     };
     // (measured: spreading the loads over the products of phase Y, or moving
@@ -345,10 +390,7 @@ __global__ __launch_bounds__(64 * NW_, (KvPipe<D, BQ_, NW_>::WPS)) void attn_bwd
         wait_vmcnt<0>();
         __syncthreads();
         const bool stage = it + 3 < n_iter;  // block it+3 exists
-        if (stage) {
-#pragma unroll
-            for (int part = 0; part < NPART; ++part) issue_part(B3{}, part);
-        }
+        if (stage) issue_all(B3{});
         // dS of block it to the workspace; the stores retire during phase Y
         // and X(it+1), before the next vmcnt wait
         if constexpr (DS) {
