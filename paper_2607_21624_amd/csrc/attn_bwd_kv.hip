@@ -54,6 +54,22 @@ namespace {
 // own needs them each time: the compiler may reload a spilled scalar operand
 // with a vector instruction just before it).  The LDS address of load i is
 // lq + i * kq (Q), lq + TB + i * kq (dO) and lst (statistics).
+// S/dP product in the vector-register form, starting the sum from zero when
+// `first`.  Built-in MFMAs of a kernel that also needs accumulation registers
+// all take the accumulator form, whose results the elementwise step would have
+// to copy out (32 instructions per block); these are written out instead.
+// The destination is early-clobber so that it never shares registers with A or
+// B.  The compiler sees an opaque instruction: the wait states the hardware
+// needs around it (operands written by a vector instruction at least 2
+// instructions before; results read at least a product phase later) are
+// checked on the generated code by tests/test_isa_hazards.py.
+FBL_DEV void mma_vgpr(f32x16& acc, const Frag<bf16>& a, const Frag<bf16>& b, bool first) {
+    if (first)
+        asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, 0" : "=&v"(acc) : "v"(a.v), "v"(b.v));
+    else
+        asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+v"(acc) : "v"(a.v), "v"(b.v));
+}
+
 template <int NPQ>
 FBL_DEV void kv_block_dma(Rsrc rq, Rsrc ro, Rsrc rst, uint32_t sq, uint32_t so, uint32_t sst, uint32_t lq, uint32_t lo,
                           uint32_t lst, uint32_t kq, const uint32_t* vq, const uint32_t* vo, uint32_t vst) {
@@ -269,6 +285,13 @@ __global__ __launch_bounds__(64 * NW_, (KvPipe<D, BQ_, NW_>::WPS)) void attn_bwd
     // tile qt = k / (2 NC) over d-chunk c = (k / 2) % NC; its A operand is one
     // row fragment of the Q or dO tile.
     constexpr int NSDP = 2 * NQT * NC;
+    // At D = 128 with 32-query blocks the S and dP products run in the vector-
+    // register form (mma_vgpr) into two accumulator sets, one per block parity,
+    // which the elementwise step reads in place; the registers that takes come
+    // from reading a block's row operands kRowLead product slots ahead (the
+    // rest during the previous phase X) instead of all of them in phase Y.
+    constexpr bool kVgprSdp = D == 128 && NQT == 1;
+    constexpr int kRowLead = kVgprSdp ? 12 : NSDP;  // row operands of a block read before its phase X
     Frag<bf16> fa[NSDP];
     auto read_row = [&](auto buf_c, int k) {
         constexpr int BB = decltype(buf_c)::value;
@@ -276,18 +299,24 @@ __global__ __launch_bounds__(64 * NW_, (KvPipe<D, BQ_, NW_>::WPS)) void attn_bwd
         fa[k].v = lds_b128(lo.row[c], BB * BUFB + (k % 2 ? TB : 0) + qt * 32 * D * 2);
     };
     // S and dP accumulators of the block whose products are in flight: lane <->
-    // key, in-lane query 32qt + acc_row.  At the start of each phase X their
-    // values move to vector registers (the elementwise step reads them there)
-    // and the accumulators start the next block.
-    f32x16 s_acc[NQT], dp_acc[NQT];
-    auto sdp_one = [&](int k) {
+    // key, in-lane query 32qt + acc_row.  With one set, at the start of each
+    // phase X their values move to vector registers (the elementwise step reads
+    // them there) and the accumulators start the next block; with two, block
+    // it uses set it % 2.
+    constexpr int NSET = kVgprSdp ? 2 : 1;
+    f32x16 s_acc[NSET][NQT], dp_acc[NSET][NQT];  // [block parity when kVgprSdp]
+    auto sdp_one = [&](auto set_c, int k) {
+        constexpr int PS = decltype(set_c)::value;
         const int qt = k / (2 * NC), c = (k / 2) % NC;
-        if (k % 2 == 0) {
-            if (c == 0) s_acc[qt] = f32x16{};
-            mma(s_acc[qt], fa[k], kf[c]);
+        if constexpr (kVgprSdp) {
+            if (k % 2 == 0) mma_vgpr(s_acc[PS][qt], fa[k], kf[c], c == 0);
+            else mma_vgpr(dp_acc[PS][qt], fa[k], vf[c], c == 0);
+        } else if (k % 2 == 0) {
+            if (c == 0) s_acc[PS][qt] = f32x16{};
+            mma(s_acc[PS][qt], fa[k], kf[c]);
         } else {
-            if (c == 0) dp_acc[qt] = f32x16{};
-            mma(dp_acc[qt], fa[k], vf[c]);
+            if (c == 0) dp_acc[PS][qt] = f32x16{};
+            mma(dp_acc[PS][qt], fa[k], vf[c]);
         }
     };
     // dV/dK products of a block: product m is dV^T += dO^T P (m even) or
@@ -325,14 +354,17 @@ __global__ __launch_bounds__(64 * NW_, (KvPipe<D, BQ_, NW_>::WPS)) void attn_bwd
         constexpr int B = decltype(buf_c)::value;
         using B2 = std::integral_constant<int, (B + 2) % 4>;
         using B3 = std::integral_constant<int, (B + 3) % 4>;
+        using B1 = std::integral_constant<int, (B + 1) % 4>;
+        constexpr int PC = kVgprSdp ? B % 2 : 0;  // accumulator set of block it
+        using PN = std::integral_constant<int, kVgprSdp ? 1 - PC : 0>;  // ... and of block it+1
         // ---------------- phase X
         __builtin_amdgcn_sched_barrier(0);
         float sv[NEL], dpv[NEL];  // S and dP of block it, out of the accumulators
 #pragma unroll
         for (int e = 0; e < NEL; ++e) {
-            sv[e] = s_acc[e / 16][e % 16];
-            dpv[e] = dp_acc[e / 16][e % 16];
-            asm volatile("" : "+v"(sv[e]), "+v"(dpv[e]));
+            sv[e] = s_acc[PC][e / 16][e % 16];
+            dpv[e] = dp_acc[PC][e / 16][e % 16];
+            if constexpr (!kVgprSdp) asm volatile("" : "+v"(sv[e]), "+v"(dpv[e]));
         }
         // row statistics of block it (the first element needs them two slots later)
 #pragma unroll
@@ -342,7 +374,9 @@ __global__ __launch_bounds__(64 * NW_, (KvPipe<D, BQ_, NW_>::WPS)) void attn_bwd
 #pragma unroll
         for (int k = 0; k < NSDP; ++k) {
             // product k of block it+1 (stale operands past the last block: unused)
-            sdp_one(k);
+            sdp_one(PN{}, k);
+            // row operands of block it+1 not read in phase Y, kRowLead slots ahead of their product
+            if (k + kRowLead < NSDP) read_row(B1{}, k + kRowLead);
             // the first transposed operands of phase Y
             if (k >= NSDP - kLead) read_tr(buf_c, k - (NSDP - kLead));
 #pragma unroll
@@ -421,8 +455,8 @@ __global__ __launch_bounds__(64 * NW_, (KvPipe<D, BQ_, NW_>::WPS)) void attn_bwd
             if (m % 2 == 0) mma(dv[t], f, pb[qt][cc]);
             else mma(dk[t], f, dsb[qt][cc]);
             if (m + kLead < NCM) read_tr(buf_c, m + kLead);
-            // row operands of block it+2, for phase X(it+1) (stale past the last block: unused)
-            read_row(B2{}, m);
+            // the first kRowLead row operands of block it+2, for phase X(it+1) (stale past the last block: unused)
+            if (m >= NCM - kRowLead) read_row(B2{}, m - (NCM - kRowLead));
             // DMA of block it+3 into the buffer of block it-1
             __builtin_amdgcn_sched_barrier(0);
         }
@@ -442,9 +476,9 @@ __global__ __launch_bounds__(64 * NW_, (KvPipe<D, BQ_, NW_>::WPS)) void attn_bwd
 #pragma unroll
         for (int k = 0; k < NSDP; ++k) read_row(C0{}, k);
 #pragma unroll
-        for (int k = 0; k < NSDP; ++k) sdp_one(k);
+        for (int k = 0; k < NSDP; ++k) sdp_one(std::integral_constant<int, 0>{}, k);
 #pragma unroll
-        for (int k = 0; k < NSDP; ++k) read_row(C1{}, k);  // stale when there is no block 1
+        for (int k = 0; k < kRowLead; ++k) read_row(C1{}, k);  // stale when there is no block 1
     }
     // Blocks in order, four per trip (one per LDS buffer).
     int j = j_lo;  // index of block `it` within its head's blocks
