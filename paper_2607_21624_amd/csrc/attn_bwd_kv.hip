@@ -18,6 +18,9 @@
 //   barrier; DMA of block i+3
 //   phase Y(i): dV/dK products of block i   |  LDS reads of block i's
 //               transposed operands and block i+2's row operands
+// (at D = 128, 4 of block i+2's 16 row operands in phase Y(i) and the other
+// 12 during phase X(i+1), each 12 product slots ahead of its use, which frees
+// the registers for the S/dP accumulators of two blocks: see mma_vgpr)
 // Operands are read a few product slots ahead of their use (kLead).  Four
 // LDS buffers: while blocks i..i+2 are resident, block i+3 streams in by DMA
 // (global -> LDS, no registers) a full iteration before it is first read.  The
@@ -48,12 +51,6 @@ namespace fbl {
 
 namespace {
 
-// The LDS DMA of one kv block -- NPQ loads of 1 KB from each of the Q and dO
-// tiles and one 256-byte load of the statistics row -- in one statement, so
-// one set of wait states covers every scalar operand (a load issued on its
-// own needs them each time: the compiler may reload a spilled scalar operand
-// with a vector instruction just before it).  The LDS address of load i is
-// lq + i * kq (Q), lq + TB + i * kq (dO) and lst (statistics).
 // S/dP product in the vector-register form, starting the sum from zero when
 // `first`.  Built-in MFMAs of a kernel that also needs accumulation registers
 // all take the accumulator form, whose results the elementwise step would have
@@ -70,6 +67,12 @@ FBL_DEV void mma_vgpr(f32x16& acc, const Frag<bf16>& a, const Frag<bf16>& b, boo
         asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+v"(acc) : "v"(a.v), "v"(b.v));
 }
 
+// The LDS DMA of one kv block -- NPQ loads of 1 KB from each of the Q and dO
+// tiles and one 256-byte load of the statistics row -- in one statement, so
+// one set of wait states covers every scalar operand (a load issued on its
+// own needs them each time: the compiler may reload a spilled scalar operand
+// with a vector instruction just before it).  The LDS address of load i is
+// lq + i * kq (Q), lq + TB + i * kq (dO) and lst (statistics).
 template <int NPQ>
 FBL_DEV void kv_block_dma(Rsrc rq, Rsrc ro, Rsrc rst, uint32_t sq, uint32_t so, uint32_t sst, uint32_t lq, uint32_t lo,
                           uint32_t lst, uint32_t kq, const uint32_t* vq, const uint32_t* vo, uint32_t vst) {
