@@ -459,16 +459,24 @@ def main():
         fbl.attn_bwd(q, k, v, o, do, lse, w.Hq, w.Hkv, scale, causal, kv_len, dq=dq, dk=dk, dv=dv, workspace=ws,
                      phases=phases, kv_tile=tiles[1], dq_tile=tiles[2])
 
-    def step(ev=None):
-        if ev is not None:
-            ev[0].record(stream)
+    def step(ev=None, around=None):
+        # ev: events recorded between the launches (n_ev of them), or, with
+        # `around` naming a launch, only just before and after that one (2)
+        def mark(i, name, after):
+            if ev is None:
+                return
+            if around is None:
+                ev[i].record(stream)
+            elif around == name:
+                ev[1 if after else 0].record(stream)
+        mark(0, "attn_fwd", False)
         fbl.attn_fwd(q, k, v, w.Hq, w.Hkv, scale, causal, kv_len, out=o, lse=lse, tile=tiles[0])
-        if ev is not None:
-            ev[1].record(stream)
-        for i, (_, ph) in enumerate(bwd_phases):
+        mark(1, "attn_fwd", True)
+        for i, (n, ph) in enumerate(bwd_phases):
+            if around is not None:
+                mark(0, n, False)
             bwd(ph)
-            if ev is not None:
-                ev[2 + i].record(stream)
+            mark(2 + i, n, True)
 
     spin = spin_up(step, args.spinup_s)
     tune = None
@@ -479,30 +487,44 @@ def main():
         tune = {"chosen": list(best), "ms": {str(t): round(x, 4) for t, x in tms.items()}}
     auto = fbl.attn_auto_tiles(lq_, lk_, int(w.mask)) if w.dtype == "bf16" else None
     run_tiles = None if auto is None else [a if t == fbl.FBL_ATTN_TILE_AUTO else t for t, a in zip(tiles, auto)]
-    for _ in range(args.warmup):
-        step()
+    # The warmup steps time every launch (events between them), which names the
+    # dominant one; the timed steps carry events only around that launch (for
+    # the roofline), since each event between two launches adds a gap to the
+    # step; every launch is timed again in as many untimed steps after them.
+    def launch_ms(evs):
+        t = {"attn_fwd": float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))}
+        for i, (n, _) in enumerate(bwd_phases):
+            t[n] = float(np.mean([e[1 + i].elapsed_time(e[2 + i]) for e in evs]))
+        return t
+    warm_evs = [[torch.cuda.Event(enable_timing=True) for _ in range(n_ev)] for _ in range(max(args.warmup, 1))]
+    for i in range(args.warmup):
+        step(warm_evs[i])
     torch.cuda.synchronize()
+    dom = max(launch_ms(warm_evs[:args.warmup]).items(), key=lambda kv: kv[1])[0] if args.warmup else bwd_phases[0][0]
     mem_before = torch.cuda.memory_allocated()
 
+    dom_evs = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(n_ev)] for _ in range(args.steps)]
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     start.record(stream)
     for i in range(args.steps):
-        step(evs[i])
+        step(dom_evs[i], around=dom)
     stop.record(stream)
     torch.cuda.synchronize()
     total_ms = start.elapsed_time(stop)
     ms_per_step = total_ms / args.steps
     eager_ms_per_step = ms_per_step
-    # average duration of each launch over the timed steps
-    k_ms = {"attn_fwd": float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))}
-    for i, (n, _) in enumerate(bwd_phases):
-        k_ms[n] = float(np.mean([e[1 + i].elapsed_time(e[2 + i]) for e in evs]))
+    t_dom_timed = float(np.mean([e[0].elapsed_time(e[1]) for e in dom_evs]))
+    assert torch.cuda.memory_allocated() == mem_before, "the timed steps allocated device memory"
+    # every launch, over as many untimed steps
+    for i in range(args.steps):
+        step(evs[i])
+    torch.cuda.synchronize()
+    k_ms = launch_ms(evs)
     step_each = np.array([e[0].elapsed_time(e[-1]) for e in evs])   # each step, first to last launch
     fwd_each = np.array([e[0].elapsed_time(e[1]) for e in evs])
     bwd_each = step_each - fwd_each
-    assert torch.cuda.memory_allocated() == mem_before, "the timed steps allocated device memory"
     if args.graph:
         # the step's launches captured once and replayed: no host work per step
         # (capture and its memory pool come after the eager timing and its no-allocation check)
@@ -539,8 +561,8 @@ def main():
     per_kernel = {n: (t, alg[n]) for n, t in k_ms.items() if n in alg}
     ktf = {n: a * w.d * pairs / (t * 1e-3) / 1e12 for n, (t, a) in per_kernel.items()}
     ktf_exec = {n: executed[n] * w.d * pairs / (per_kernel[n][0] * 1e-3) / 1e12 for n in per_kernel}
-    dom = max(per_kernel, key=lambda n: per_kernel[n][0])
-    t_dom, a_dom = per_kernel[dom]
+    a_dom = alg[dom]
+    t_dom = t_dom_timed
     es = 2 if w.dtype == "bf16" else 4
     alg_bytes = algorithmic_bytes(w, es, inp["kv_len"])
     des_bytes = design_bytes(w, es, inp["kv_len"])
@@ -549,11 +571,12 @@ def main():
     dom_traffic = None if traffic is None else traffic.get(dom)
     dom_trace_us = None if trace is None else trace.get(dom)
     flops_launch = a_dom * w.d * pairs
-    roofline = {"bound": "mfma", "achieved": round(ktf[dom], 2), "peak": peak, "unit": "TFLOP/s",
-                "frac": round(ktf[dom] / peak, 4), "traffic": dom_traffic, "kernel": dom,
+    achieved = flops_launch / (t_dom * 1e-3) / 1e12
+    roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
+                "frac": round(achieved / peak, 4), "traffic": dom_traffic, "kernel": dom,
                 # achieved = flops_per_launch / avg_launch_ms, the launch timed with HIP events on the
                 # stream it runs on, averaged over this run's timed steps
-                "frac_source": "HIP events around each launch over the timed steps of this run",
+                "frac_source": "HIP events around this launch over the timed steps of this run",
                 "avg_launch_ms": round(t_dom, 4), "flops_per_launch": flops_launch,
                 # the same figure from the committed rocprofv3 kernel trace (timed steps), when it was
                 # taken on the current sources
@@ -603,6 +626,7 @@ def main():
         "layout_copy_bytes": 0 if foreign == [] else None,
         "dispatched_kernels": kernels,
         "bwd_launches": len(bwd_phases),
+        # every launch, timed with events between the launches in as many untimed steps after the timed ones
         "kernel_ms": {n: round(t, 4) for n, t in k_ms.items()},
         # the HBM-bound launches: algorithmic bytes over their time
         "kernel_gbs_algorithmic": None if fused else {
