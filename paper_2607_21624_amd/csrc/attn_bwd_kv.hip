@@ -18,9 +18,9 @@
 //   barrier; DMA of block i+3
 //   phase Y(i): dV/dK products of block i   |  LDS reads of block i's
 //               transposed operands and block i+2's row operands
-// (at D = 128, 4 of block i+2's 16 row operands in phase Y(i) and the other
-// 12 during phase X(i+1), each 12 product slots ahead of its use, which frees
-// the registers for the S/dP accumulators of two blocks: see mma_vgpr)
+// (with one wavefront per SIMD, only the first kRowLead of block i+2's row
+// operands in phase Y(i) and the rest during phase X(i+1), which frees the
+// registers for the S/dP accumulators of two blocks: see mma_vgpr)
 // Operands are read a few product slots ahead of their use (kLead).  Four
 // LDS buffers: while blocks i..i+2 are resident, block i+3 streams in by DMA
 // (global -> LDS, no registers) a full iteration before it is first read.  The
@@ -288,13 +288,14 @@ __global__ __launch_bounds__(64 * NW_, (KvPipe<D, BQ_, NW_>::WPS)) void attn_bwd
     // tile qt = k / (2 NC) over d-chunk c = (k / 2) % NC; its A operand is one
     // row fragment of the Q or dO tile.
     constexpr int NSDP = 2 * NQT * NC;
-    // At D = 128 with 32-query blocks the S and dP products run in the vector-
-    // register form (mma_vgpr) into two accumulator sets, one per block parity,
-    // which the elementwise step reads in place; the registers that takes come
-    // from reading a block's row operands kRowLead product slots ahead (the
-    // rest during the previous phase X) instead of all of them in phase Y.
-    constexpr bool kVgprSdp = D == 128 && NQT == 1;
-    constexpr int kRowLead = kVgprSdp ? 12 : NSDP;  // row operands of a block read before its phase X
+    // With one wavefront per SIMD (D = 128 with 32-query blocks, D = 64 with
+    // 64-query blocks) the S and dP products run in the vector-register form
+    // (mma_vgpr) into two accumulator sets, one per block parity, which the
+    // elementwise step reads in place; the registers that takes come from
+    // reading only a block's first kRowLead row operands in phase Y and the rest
+    // during the previous phase X, kRowLead product slots ahead of their use.
+    constexpr bool kVgprSdp = (D == 128 && NQT == 1) || (D == 64 && NQT == 2);
+    constexpr int kRowLead = kVgprSdp ? (D == 128 ? 12 : 4) : NSDP;  // row operands of a block read in phase Y
     Frag<bf16> fa[NSDP];
     auto read_row = [&](auto buf_c, int k) {
         constexpr int BB = decltype(buf_c)::value;
