@@ -487,20 +487,28 @@ def main():
         tune = {"chosen": list(best), "ms": {str(t): round(x, 4) for t, x in tms.items()}}
     auto = fbl.attn_auto_tiles(lq_, lk_, int(w.mask)) if w.dtype == "bf16" else None
     run_tiles = None if auto is None else [a if t == fbl.FBL_ATTN_TILE_AUTO else t for t, a in zip(tiles, auto)]
-    # The warmup steps time every launch (events between them), which names the
-    # dominant one; the timed steps carry events only around that launch (for
-    # the roofline), since each event between two launches adds a gap to the
-    # step; every launch is timed again in as many untimed steps after them.
+    # Algorithmic FLOPs per launch (2*d per allowed pair per matrix product):
+    #   attn_fwd        QK^T, PV                                    4*d
+    #   attn_bwd_kv     QK^T recompute, dO V^T, P^T dO, dS^T Q      8*d
+    #   attn_bwd_dq     dS K from the dS the kv pass stored         2*d
+    #   attn_bwd_fused  the kv products and dS K in one launch     10*d
+    #   (fp32 storage has no stored-dS path: attn_bwd_q recomputes QK^T and dO V^T, 6*d executed)
+    alg = {"attn_fwd": 4, "attn_bwd_kv": 8, "attn_bwd_dq": 2, "attn_bwd_q": 2, "attn_bwd_fused": 10}
+    executed = {**alg, "attn_bwd_q": 6}
+    # The dominant launch (most algorithmic FLOPs) is timed inside the timed
+    # steps with events just around it (for the roofline): each event recorded
+    # between two launches adds a gap to the step.  Every launch is timed in as
+    # many untimed steps after them.
+    dom = max((n for n in ["attn_fwd"] + [n for n, _ in bwd_phases] if n in alg), key=lambda n: alg[n])
+
     def launch_ms(evs):
         t = {"attn_fwd": float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))}
         for i, (n, _) in enumerate(bwd_phases):
             t[n] = float(np.mean([e[1 + i].elapsed_time(e[2 + i]) for e in evs]))
         return t
-    warm_evs = [[torch.cuda.Event(enable_timing=True) for _ in range(n_ev)] for _ in range(max(args.warmup, 1))]
-    for i in range(args.warmup):
-        step(warm_evs[i])
+    for _ in range(args.warmup):
+        step()
     torch.cuda.synchronize()
-    dom = max(launch_ms(warm_evs[:args.warmup]).items(), key=lambda kv: kv[1])[0] if args.warmup else bwd_phases[0][0]
     mem_before = torch.cuda.memory_allocated()
 
     dom_evs = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
@@ -550,14 +558,6 @@ def main():
     flops = 14 * w.d * pairs
     tflops = flops / (ms_per_step * 1e-3) / 1e12
     peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
-    # Algorithmic FLOPs per launch (2*d per allowed pair per matrix product):
-    #   attn_fwd        QK^T, PV                                    4*d
-    #   attn_bwd_kv     QK^T recompute, dO V^T, P^T dO, dS^T Q      8*d
-    #   attn_bwd_dq     dS K from the dS the kv pass stored         2*d
-    #   attn_bwd_fused  the kv products and dS K in one launch     10*d
-    #   (fp32 storage has no stored-dS path: attn_bwd_q recomputes QK^T and dO V^T, 6*d executed)
-    alg = {"attn_fwd": 4, "attn_bwd_kv": 8, "attn_bwd_dq": 2, "attn_bwd_q": 2, "attn_bwd_fused": 10}
-    executed = {**alg, "attn_bwd_q": 6}
     per_kernel = {n: (t, alg[n]) for n, t in k_ms.items() if n in alg}
     ktf = {n: a * w.d * pairs / (t * 1e-3) / 1e12 for n, (t, a) in per_kernel.items()}
     ktf_exec = {n: executed[n] * w.d * pairs / (per_kernel[n][0] * 1e-3) / 1e12 for n in per_kernel}
